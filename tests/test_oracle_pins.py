@@ -1,0 +1,390 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test is chosen so that a plausible slip in the oracle (dropped term, wrong
+sign or index, transposed operand, wrong padding) fails at least one of them.
+"""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import moara_oracle as O
+from tests.conftest import golden
+
+MODS = ["q", "k", "v", "o", "gate", "up", "down"]
+
+
+# ---------------------------------------------------------------- bf16 rounding
+
+def test_round_bf16_matches_torch_cast():
+    g = np.random.default_rng(0)
+    x = np.concatenate([g.standard_normal(20000) * 10.0 ** g.integers(-40, 38, 20000),
+                        [0.0, -0.0, 1.0, -1.0, 1.0 + 2 ** -8, 1.0 + 3 * 2 ** -8, 3.0e38, 1e-39, -1e-41]]).astype(np.float32)
+    ref = torch.from_numpy(x).to(torch.bfloat16).to(torch.float64).numpy()
+    got = O.round_bf16(x.astype(np.float64))
+    np.testing.assert_array_equal(got, ref)
+
+
+def test_round_bf16_ties_to_even():
+    # 1 + 2^-8 is halfway between 1 and 1 + 2^-7: ties to even -> 1.
+    assert O.round_bf16(np.array([1.0 + 2 ** -8]))[0] == 1.0
+    # 1 + 3*2^-8 is halfway between 1+2^-7 and 1+2^-6: even mantissa is 1+2^-6.
+    assert O.round_bf16(np.array([1.0 + 3 * 2 ** -8]))[0] == 1.0 + 2 ** -6
+
+
+# ---------------------------------------------------------------- Phase 3 ranks
+
+def test_final_rank_allocation_row():
+    gd = golden("rank_allocations.json")
+    types = list(range(7))
+    out = O.allocate_ranks(256, types, donors=[0, 1], receivers=[6], delta_r=128)
+    assert [out[t] for t in types] == gd["ours_r256"]
+    for rb in (256, 512, 1024):
+        out = O.allocate_ranks(rb, types, [0, 1], [6], rb // 2)
+        assert [out[t] for t in types] == [rb // 2, rb // 2, rb, rb, rb, rb, 2 * rb]
+        assert sum(out.values()) == 7 * rb
+
+
+def test_budget_is_preserved_like_the_random_allocations():
+    gd = golden("rank_allocations.json")
+    budget = sum(gd["ours_r256"])
+    assert budget == 7 * 256
+    for row in gd["random_runs"]:
+        assert sum(row) == budget
+    # the reallocation rule keeps the budget for any integer transfer
+    types = list(range(7))
+    for D, R, dr in [([0, 1], [6], 64), ([0], [5, 6], 64), ([0, 1, 2, 3], [6], 16), ([2], [4], 200)]:
+        out = O.allocate_ranks(256, types, D, R, dr)
+        assert sum(out.values()) == budget
+
+
+def test_non_integer_transfer_rejected():
+    with pytest.raises(ValueError):
+        O.allocate_ranks(256, list(range(7)), [0, 1, 2], [5, 6], 1)
+    with pytest.raises(ValueError):
+        O.allocate_ranks(256, list(range(7)), [0, 1], [0], 10)
+    with pytest.raises(ValueError):
+        O.allocate_ranks(100, list(range(7)), [0, 1], [6], 100)   # donors drop to 0
+
+
+# ---------------------------------------------------------------- memory model
+
+def _opt_state_mib(sc, vocab, ranks, decompose):
+    d, f, L, B = sc["hidden"], sc["intermediate"], sc["layers"], sc["B"]
+    shapes = [(d, d), (d, d), (d, d), (d, d), (f, d), (f, d), (d, f)] * L
+    rk = [ranks[i % 7] for i in range(7 * L)]
+    tgt = O.paper_state_bytes(shapes, rk, [B] * len(shapes), 2, 4, decompose)
+    non_target = 2 * 2 * (2 * vocab * d + (2 * L + 1) * d)    # Adam moments of embeddings/head/norms, 2 B each
+    return (tgt + non_target) / 2 ** 20
+
+
+def test_optimizer_state_table_reproduces():
+    gd = golden("table11_opt_state.json")
+    for name, sc in gd["scales"].items():
+        rb = sc["r_base"]
+        uni = [rb] * 7
+        moa = [rb // 2, rb // 2, rb, rb, rb, rb, 2 * rb]
+        got = {
+            "baseline": _opt_state_mib(sc, gd["vocab"], uni, False),
+            "decomp": _opt_state_mib(sc, gd["vocab"], uni, True),
+            "rank": _opt_state_mib(sc, gd["vocab"], moa, False),
+            "ours": _opt_state_mib(sc, gd["vocab"], moa, True),
+        }
+        for k, v in got.items():
+            assert round(v, 2) == sc[k], (name, k, v, sc[k])
+    sc = gd["scales"]["7B"]
+    split = gd["7B_split_MiB"]
+    assert round(_opt_state_mib(sc, 32000, [512, 512, 1024, 1024, 1024, 1024, 2048], False)
+                 - _opt_state_mib(sc, 32000, [1024] * 7, False)) == split["rank"]
+    assert round(_opt_state_mib(sc, 32000, [1024] * 7, True)
+                 - _opt_state_mib(sc, 32000, [1024] * 7, False)) == split["decomp"]
+
+
+def test_memory_model_rejects_transposed_blocking():
+    # blocking along rows instead of columns changes the 350M decomposition delta
+    gd = golden("table11_opt_state.json")
+    sc = gd["scales"]["350M"]
+    d, f, L, B = sc["hidden"], sc["intermediate"], sc["layers"], sc["B"]
+    shapes_t = [(d, d)] * 4 + [(d, f), (d, f), (f, d)]
+    mag_t = sum(2 * 4 * m * math.ceil(n / B) for m, n in shapes_t) * L / 2 ** 20
+    assert round(mag_t, 2) != round(sc["decomp"] - sc["baseline"], 2)
+
+
+# ---------------------------------------------------------------- decomposition
+
+def test_worked_example_decomposition_and_step():
+    gd = golden("worked_example.json")
+    G = np.array(gd["G"])
+    M, V = O.decompose(G, gd["B"], gd["decomp_eps"])
+    tol = gd["tolerance"]
+    np.testing.assert_allclose(M, gd["M"], atol=tol)
+    np.testing.assert_allclose(V, gd["V"], atol=tol)
+    s = np.linalg.svd(V, compute_uv=False)
+    np.testing.assert_allclose(s, gd["sigma"], atol=tol)
+    cfg = O.OracleConfig(block_size=gd["B"], rank=gd["r"], adam_eps=gd["adam_eps"], scale=gd["scale"],
+                         beta1=gd["beta1"], beta2=gd["beta2"], decomp_eps=gd["decomp_eps"])
+    st = O.init_state(2, 4, cfg)
+    assert st.side == gd["side"]
+    W = np.zeros((2, 4))
+    W1 = O.step(W, G, st, cfg, lr=1.0)
+    np.testing.assert_allclose(st.P, gd["P"], atol=tol)
+    # the paper's update is W <- W - lr * U
+    np.testing.assert_allclose(-W1, gd["U_step1"], atol=tol)
+    # same G again: constant-gradient invariance of the Adam step
+    W2 = O.step(W1, G, st, cfg, lr=1.0)
+    np.testing.assert_allclose(W1 - W2, gd["U_step1"], atol=tol)
+
+
+def test_partial_block_norm_over_real_columns():
+    g = np.random.default_rng(1)
+    G = g.standard_normal((5, 11))
+    M, V = O.decompose(G, 4)
+    assert M.shape == (5, 3)
+    np.testing.assert_allclose(M[:, 2], np.linalg.norm(G[:, 8:11], axis=1), rtol=1e-14)
+    np.testing.assert_allclose(M[:, 0], np.linalg.norm(G[:, 0:4], axis=1), rtol=1e-14)
+    np.testing.assert_allclose(V[:, 9], G[:, 9] / (M[:, 2] + 1e-12), rtol=1e-14)
+    assert V.shape == G.shape
+
+
+def test_block_size_one_gives_sign_and_abs():
+    G = np.array([[0.5, -2.0, 0.0, 3.0]])
+    M, V = O.decompose(G, 1)
+    np.testing.assert_allclose(M, np.abs(G))
+    np.testing.assert_allclose(V, np.sign(G), atol=1e-11)
+
+
+def test_block_at_least_n_is_row_normalisation():
+    g = np.random.default_rng(2)
+    G = g.standard_normal((4, 7))
+    for B in (7, 8, 1024):
+        M, V = O.decompose(G, B)
+        assert M.shape == (4, 1)
+        np.testing.assert_allclose(M[:, 0], np.linalg.norm(G, axis=1), rtol=1e-14)
+        np.testing.assert_allclose(np.linalg.norm(V, axis=1), 1.0, rtol=1e-12)
+
+
+def test_recomposition_identity_and_unit_blocks():
+    g = np.random.default_rng(3)
+    G = g.standard_normal((6, 20)) * 1e-3
+    G[2, 4:8] = 0.0                                  # a zero block
+    M, V = O.decompose(G, 4)
+    np.testing.assert_allclose(O.recompose(M, V, 4), G * O.rep_b(M / (M + 1e-12), 4, 20), rtol=1e-14, atol=0)
+    assert np.all(V[2, 4:8] == 0.0)
+    norms = np.sqrt((np.pad(V, ((0, 0), (0, 0))).reshape(6, 5, 4) ** 2).sum(2))
+    np.testing.assert_allclose(norms, M / (M + 1e-12), rtol=1e-13)
+
+
+def test_blockwise_scale_only_moves_magnitude():
+    g = np.random.default_rng(4)
+    G = g.standard_normal((3, 8))
+    M, V = O.decompose(G, 4)
+    G2 = G.copy()
+    G2[1, 4:8] *= 7.5
+    M2, V2 = O.decompose(G2, 4)
+    np.testing.assert_allclose(M2[1, 1], 7.5 * M[1, 1], rtol=1e-14)
+    np.testing.assert_allclose(V2, V, rtol=1e-12)
+
+
+def test_proposition1_magnitude_factor_cancels_in_cosine():
+    g = np.random.default_rng(5)
+    G = g.standard_normal((12, 16))
+    B = 4
+    M, V = O.decompose(G, B)
+    P = O.truncated_svd(V, 3, O.LEFT)
+    Vt = P @ (P.T @ V)
+    Gt = O.recompose(M, Vt, B)
+    for i in range(12):
+        for b in range(4):
+            sl = slice(b * B, (b + 1) * B)
+            c1 = G[i, sl] @ Gt[i, sl] / (np.linalg.norm(G[i, sl]) * np.linalg.norm(Gt[i, sl]))
+            c2 = V[i, sl] @ Vt[i, sl] / (np.linalg.norm(V[i, sl]) * np.linalg.norm(Vt[i, sl]))
+            assert abs(c1 - c2) < 1e-12
+
+
+# ---------------------------------------------------------------- truncated SVD
+
+def _jacobi_svd(A, sweeps=30):
+    """One-sided (Hestenes) Jacobi SVD, pure Python loops, for tiny matrices."""
+    U = np.array(A, dtype=np.float64, copy=True)
+    n = U.shape[1]
+    Vm = np.eye(n)
+    for _ in range(sweeps):
+        off = 0.0
+        for p in range(n - 1):
+            for q in range(p + 1, n):
+                a = float(U[:, p] @ U[:, p]); b = float(U[:, q] @ U[:, q]); c = float(U[:, p] @ U[:, q])
+                if abs(c) <= 1e-300:
+                    continue
+                off = max(off, abs(c) / math.sqrt(a * b))
+                zeta = (b - a) / (2 * c)
+                t = math.copysign(1.0, zeta) / (abs(zeta) + math.sqrt(1 + zeta * zeta))
+                cs = 1 / math.sqrt(1 + t * t); sn = cs * t
+                up = U[:, p].copy(); U[:, p] = cs * up - sn * U[:, q]; U[:, q] = sn * up + cs * U[:, q]
+                vp = Vm[:, p].copy(); Vm[:, p] = cs * vp - sn * Vm[:, q]; Vm[:, q] = sn * vp + cs * Vm[:, q]
+        if off < 1e-15:
+            break
+    s = np.linalg.norm(U, axis=0)
+    order = np.argsort(-s)
+    return U[:, order] / s[order], s[order], Vm[:, order]
+
+
+@pytest.mark.parametrize("m,n", [(6, 8), (8, 5), (7, 7)])
+def test_truncated_svd_against_hand_written_jacobi(m, n):
+    g = np.random.default_rng(m * 10 + n)
+    A = g.standard_normal((m, n)) * np.linspace(3.0, 0.2, n)
+    Uj, sj, Vj = _jacobi_svd(A if m >= n else A.T)
+    if m < n:
+        Uj, Vj = Vj, Uj
+    sl = np.linalg.svd(A, compute_uv=False)
+    np.testing.assert_allclose(sj[:len(sl)], sl, rtol=1e-12)
+    r = 3
+    side = O.projection_side(m, n)
+    P = O.truncated_svd(A, r, side)
+    ref = Uj[:, :r] if side == O.LEFT else Vj[:, :r]
+    assert O.max_principal_angle(P, ref) < 1e-10
+
+
+def test_projector_orthonormal_energy_and_full_rank_identity():
+    g = np.random.default_rng(7)
+    G = g.standard_normal((10, 24))
+    _, V = O.decompose(G, 8)
+    s = np.linalg.svd(V, compute_uv=False)
+    for r in (1, 4, 10):
+        P = O.truncated_svd(V, r, O.LEFT)
+        np.testing.assert_allclose(P.T @ P, np.eye(r), atol=1e-12)
+        np.testing.assert_allclose(np.linalg.norm(P.T @ V) ** 2, np.sum(s[:r] ** 2), rtol=1e-12)   # Eckart-Young
+    P = O.truncated_svd(V, 10, O.LEFT)
+    np.testing.assert_allclose(P @ P.T, np.eye(10), atol=1e-12)
+    M, V = O.decompose(G, 8)
+    np.testing.assert_allclose(O.recompose(M, P @ (P.T @ V), 8), G * O.rep_b(M / (M + 1e-12), 8, 24), atol=1e-12)
+    # right side: Q spans the top right singular vectors
+    Q = O.truncated_svd(V.T, 4, O.RIGHT)
+    np.testing.assert_allclose(Q.T @ Q, np.eye(4), atol=1e-12)
+    np.testing.assert_allclose(np.linalg.norm(V.T @ Q) ** 2, np.sum(s[:4] ** 2), rtol=1e-12)
+
+
+def test_canonical_signs():
+    P = np.array([[0.1, -0.9], [-0.8, 0.2], [0.3, 0.9]])
+    C = O.canonical_signs(P)
+    np.testing.assert_allclose(C[:, 0], -P[:, 0])      # largest |.| is -0.8 -> flip
+    np.testing.assert_allclose(C[:, 1], -P[:, 1])      # tie 0.9: lowest index (-0.9) decides -> flip
+
+
+def test_principal_angle_helper():
+    th = 0.3
+    A = np.array([[1.0], [0.0], [0.0]])
+    B = np.array([[math.cos(th)], [math.sin(th)], [0.0]])
+    assert abs(O.max_principal_angle(A, B) - th) < 1e-14
+    assert O.max_principal_angle(A, -A * 3) < 1e-14
+
+
+# ---------------------------------------------------------------- Adam and the step
+
+def test_identity_projection_without_decomposition_is_torch_adam():
+    """decompose=False with P = I (r = m, LEFT) must be exactly torch.optim.Adam."""
+    g = np.random.default_rng(8)
+    m, n = 4, 6
+    cfg = O.OracleConfig(block_size=2, rank=m, decompose=False, refresh_interval=0, scale=1.0,
+                         beta1=0.9, beta2=0.999, adam_eps=1e-8)
+    st = O.init_state(m, n, cfg)
+    st.P = np.eye(m)
+    W = g.standard_normal((m, n))
+    p = torch.nn.Parameter(torch.from_numpy(W.copy()))
+    opt = torch.optim.Adam([p], lr=0.01, betas=(0.9, 0.999), eps=1e-8)
+    for t in range(5):
+        G = g.standard_normal((m, n))
+        W = O.step(W, G, st, cfg, lr=0.01)
+        p.grad = torch.from_numpy(G.copy())
+        opt.step()
+    np.testing.assert_allclose(W, p.detach().numpy(), rtol=0, atol=1e-13)
+
+
+def test_first_step_closed_forms_and_constant_gradient():
+    g = np.random.default_rng(9)
+    G = g.standard_normal((8, 12))
+    cfg = O.OracleConfig(block_size=4, rank=3, scale=1.0)
+    st = O.init_state(8, 12, cfg)
+    M, V = O.decompose(G, 4)
+    P = O.truncated_svd(V, 3, O.LEFT)
+    R = P.T @ V
+    W0 = np.zeros((8, 12))
+    W1 = O.step(W0, G, st, cfg, lr=1.0)
+    N1 = R / (np.abs(R) + cfg.adam_eps)
+    dM1 = M / (M + cfg.adam_eps)
+    np.testing.assert_allclose(-W1, O.rep_b(dM1, 4, 12) * (P @ N1), rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(st.exp_avg, 0.1 * R, rtol=1e-14)
+    np.testing.assert_allclose(st.exp_avg_sq, 0.001 * R * R, rtol=1e-14)
+    W2 = O.step(W1, G, st, cfg, lr=1.0)
+    W3 = O.step(W2, G, st, cfg, lr=1.0)
+    np.testing.assert_allclose(W2 - W3, W0 - W1, rtol=1e-9, atol=1e-15)
+
+
+def test_zero_gradient_zero_moments_is_a_no_op():
+    cfg = O.OracleConfig(block_size=4, rank=2, refresh_interval=0)
+    st = O.init_state(6, 8, cfg)
+    st.P = np.linalg.qr(np.random.default_rng(0).standard_normal((6, 2)))[0]
+    W = np.random.default_rng(1).standard_normal((6, 8))
+    W1 = O.step(W, np.zeros((6, 8)), st, cfg, lr=0.1)
+    np.testing.assert_array_equal(W1, W)
+
+
+def test_right_side_uses_state_m_by_r():
+    g = np.random.default_rng(10)
+    m, n = 12, 5
+    cfg = O.OracleConfig(block_size=2, rank=2, scale=1.0)
+    st = O.init_state(m, n, cfg)
+    assert st.side == O.RIGHT and st.exp_avg.shape == (m, 2)
+    G = g.standard_normal((m, n))
+    W1 = O.step(np.zeros((m, n)), G, st, cfg, lr=1.0)
+    M, V = O.decompose(G, 2)
+    Q = O.truncated_svd(V, 2, O.RIGHT)
+    R = V @ Q
+    N1 = R / (np.abs(R) + cfg.adam_eps)
+    np.testing.assert_allclose(-W1, O.rep_b(M / (M + 1e-8), 2, n) * (N1 @ Q.T), rtol=1e-12, atol=1e-15)
+
+
+def test_refresh_schedule_and_moment_continuity():
+    g = np.random.default_rng(11)
+    cfg = O.OracleConfig(block_size=4, rank=2, refresh_interval=3)
+    st = O.init_state(6, 8, cfg)
+    Ps = []
+    for t in range(7):
+        O.step(np.zeros((6, 8)), g.standard_normal((6, 8)), st, cfg, lr=0.1)
+        Ps.append(st.P.copy())
+    # refreshes at t=0,3,6: P constant on [0,2], [3,5]
+    assert np.array_equal(Ps[0], Ps[1]) and np.array_equal(Ps[1], Ps[2])
+    assert not np.array_equal(Ps[2], Ps[3])
+    assert np.array_equal(Ps[3], Ps[5]) and not np.array_equal(Ps[5], Ps[6])
+    assert st.t == 7 and np.any(st.exp_avg != 0)
+
+
+def test_zero_direction_keeps_previous_projector():
+    cfg = O.OracleConfig(block_size=4, rank=2, refresh_interval=1)
+    st = O.init_state(6, 8, cfg)
+    O.step(np.zeros((6, 8)), np.zeros((6, 8)), st, cfg, lr=0.1)
+    np.testing.assert_array_equal(st.P, np.eye(6, 2))
+    G = np.random.default_rng(0).standard_normal((6, 8))
+    O.step(np.zeros((6, 8)), G, st, cfg, lr=0.1)
+    P1 = st.P.copy()
+    O.step(np.zeros((6, 8)), np.zeros((6, 8)), st, cfg, lr=0.1)
+    np.testing.assert_array_equal(st.P, P1)
+
+
+def test_bf16_weight_path_rounds_update_then_result():
+    cfg = O.OracleConfig(block_size=2, rank=1, refresh_interval=0, weight_dtype="bf16", scale=0.25)
+    st = O.init_state(1, 2, cfg)
+    st.P = np.array([[1.0]])
+    W = np.array([[1.0, -1.0]])
+    W1 = O.step(W, np.array([[3.0, -4.0]]), st, cfg, lr=2 ** -10)
+    # update magnitude 0.25 * 1 * dM(~1) * N(~1) = ~0.25, times lr 2^-10 is below half a bf16 ulp at 1.0
+    np.testing.assert_array_equal(W1, W)
+    W2 = O.step(W, np.array([[3.0, -4.0]]), st, cfg, lr=2 ** -5)
+    assert np.all(O.round_bf16(W2) == W2) and np.all(W2 != W)
+
+
+def test_floored_metric():
+    b = np.array([1.0, 0.0, -2.0])
+    assert O.floored_rel_err(b, b) == 0.0
+    a = b + np.array([0.0, 1e-3, 0.0])
+    assert abs(O.floored_rel_err(a, b) - 1e-3 / math.sqrt(5 / 3)) < 1e-15
