@@ -1,0 +1,264 @@
+"""Benchmark of the MoARa optimizer hot path on one MI355X.
+
+One "step" = one Algorithm 1 training-phase optimizer step over every projected
+matrix of the stack (decompose + Optimizer_M, projection + Optimizer_V,
+back-projection + update), inputs already resident in HBM. The projector refresh
+(TruncatedSVD of every matrix) is timed separately and reported as
+ms_per_refresh; the refresh interval of 200 steps gives the amortised figure.
+
+Prints ONE JSON line. Default workload: the Llama-2-7B-shaped stack (32 layers,
+d=4096, ffn=11008, bf16 weights, fp32 gradients, ranks q/k 512, v/o 1024, mlp
+768, B=128), synthetic seeded inputs.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_HBM = 8.0e12          # B/s
+PEAK_BF16 = 2.5e15         # dense MFMA flop/s
+PEAK_F32 = 157.3e12
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="llama2_7b")
+    ap.add_argument("--operand", default=None, help="GEMM operand dtype override: bf16 | f32")
+    ap.add_argument("--refresh-reps", type=int, default=1)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-sample-layers", type=int, default=1)
+    return ap.parse_args()
+
+
+def algorithmic_cost(wl, operand_bytes: int, weight_bytes: int):
+    """Per-step algorithmic bytes and flops per kernel (what the method must move or compute)."""
+    cost = {"decompose": [0, 0], "project": [0, 0], "backproject": [0, 0]}
+    for m in wl.matrices:
+        r = wl.rank_of(m)
+        M, N = m.rows, m.cols
+        s, L = (M, N) if M <= N else (N, M)
+        k = -(-N // wl.block_size)
+        # decompose + Optimizer_M: read G; write inv and dM; read+write two magnitude moments
+        cost["decompose"][0] += 4 * M * N + 4 * M * k * 6
+        # projection + Optimizer_V: read G and inv, read P, read+write two fp32 moments, write N
+        cost["project"][0] += 4 * M * N + 4 * M * k + operand_bytes * s * r + 16 * L * r + operand_bytes * L * r
+        cost["project"][1] += 2 * M * N * r
+        # back-projection + update: read N and P, read dM, read+write W
+        cost["backproject"][0] += operand_bytes * L * r + operand_bytes * s * r + 4 * M * k + 2 * weight_bytes * M * N
+        cost["backproject"][1] += 2 * M * N * r
+    return cost
+
+
+def refresh_flops(wl, p_over: int, q: int):
+    f = 0
+    for m in wl.matrices:
+        r = wl.rank_of(m)
+        s, L = min(m.rows, m.cols), max(m.rows, m.cols)
+        w = min(s, r + (r if p_over < 0 else p_over))
+        f += q * 2 * (2 * L * s * w)            # X Z and X^T Y
+        f += q * (2 * s * w * w)                 # Z Rinv
+        f += 2 * L * w * w                       # final Y Rinv
+    return f
+
+
+def cpu_baseline(wl, layers: int):
+    """The oracle (as it stands) on a bounded sample: the first `layers` layers' matrices,
+    with their projectors already set (steps only), timed on the host cores."""
+    import workloads as WL
+    from oracle import moara_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = ",".join(sorted({i.get("internal_api", "?") for i in threadpool_info()}))
+    except Exception:
+        threads, blas = os.cpu_count(), "?"
+    sub = WL.subset(wl, list(range(layers)))
+    mats = sub.matrices
+    Ws, Gs, sts, cfgs = [], [], [], []
+    for i, m in enumerate(mats):
+        G = WL.grad_np(sub, i, 0)
+        W = WL.weight_np(sub, i).astype(np.float64)
+        cfg = O.OracleConfig(block_size=sub.block_size, rank=sub.rank_of(m), adam_eps=sub.adam_eps, scale=sub.scale,
+                             refresh_interval=0, weight_dtype=sub.weight_dtype, operand_dtype=sub.operand_dtype)
+        st = O.init_state(m.rows, m.cols, cfg)
+        s = min(m.rows, m.cols)
+        st.P = np.linalg.qr(np.random.default_rng(i).standard_normal((s, cfg.rank)))[0]
+        Ws.append(W); Gs.append(G); sts.append(st); cfgs.append(cfg)
+    t0 = time.perf_counter()
+    for i in range(len(mats)):
+        Ws[i] = O.step(Ws[i], Gs[i], sts[i], cfgs[i], sub.lr)
+    dt = time.perf_counter() - t0
+    params = sum(m.rows * m.cols for m in mats)
+    cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
+    return {"value": params / dt, "unit": "params/s", "cores": int(min(cores, threads or cores)),
+            "kind": "oracle",
+            "sample": f"{len(mats)} matrices ({layers} layer(s)) of {wl.name}, one optimizer step each with the "
+                      f"projector set, float64 NumPy ({blas}, {threads} BLAS threads, {cores} host cores); "
+                      f"{params / 1e6:.1f}M params in {dt:.2f}s",
+            "seconds": dt}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1 "
+                                   "(the multi-GPU sharding is a design, not part of this build)"}))
+        return 2
+    import torch
+    import workloads as WL
+    from paper_2609_15037_amd import moara as M
+
+    wl = WL.WORKLOADS[a.workload]
+    operand = a.operand or wl.operand_dtype
+    ob = 2 if operand == "bf16" else 4
+    wb = 2 if wl.weight_dtype == "bf16" else 4
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    n = len(wl.matrices)
+    log(f"[bench] {wl.name}: {n} matrices, {wl.n_params / 1e9:.3f}G params, operand {operand}")
+
+    # ---- inputs resident in HBM
+    wdt = torch.bfloat16 if wl.weight_dtype == "bf16" else torch.float32
+    W, G = [], []
+    t0 = time.time()
+    for i, m in enumerate(wl.matrices):
+        W.append(WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=wdt, device=dev)))
+        g = torch.empty((m.rows, m.cols), dtype=torch.float32, device=dev)
+        WL.grad_device(wl, i, 0, g, active=True)
+        G.append(g)
+        if i % 32 == 31:
+            log(f"[bench] generated {i + 1}/{n} matrices ({time.time() - t0:.0f}s)")
+    torch.cuda.synchronize()
+
+    cfg = M.moara_default_config(
+        rank_table=list(wl.rank_table), block_size=wl.block_size, beta1=wl.beta1, beta2=wl.beta2,
+        adam_eps=wl.adam_eps, scale=wl.scale, refresh_interval=0,
+        weight_dtype=M.MOARA_BF16 if wl.weight_dtype == "bf16" else M.MOARA_F32,
+        operand_dtype=M.MOARA_BF16 if operand == "bf16" else M.MOARA_F32,
+        refresh_oversample=wl.refresh_oversample, refresh_iters=wl.refresh_iters)
+    descs = M.make_descs([(m.rows, m.cols, m.module) for m in wl.matrices])
+    stream = torch.cuda.current_stream()
+    st = M.moara_create_state(cfg, descs, stream=stream)
+    state_bytes, _ = M.moara_state_bytes(cfg, descs)
+    log(f"[bench] state {state_bytes / 2**30:.1f} GiB")
+
+    # ---- projector refresh (all matrices), timed with events on the library's stream
+    M.moara_set_timing(st, True)
+    ref_ms = []
+    for rep in range(max(1, a.refresh_reps)):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        M.moara_refresh_projector(st, G, stream=stream)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ref_ms.append(e0.elapsed_time(e1))
+        log(f"[bench] refresh {rep}: {ref_ms[-1]:.1f} ms")
+    M.moara_reset_kernel_stats(st, stream=stream)
+
+    # ---- steps
+    lr = wl.lr
+    for _ in range(a.warmup):
+        M.moara_step(st, W, G, lr, stream=stream)
+    torch.cuda.synchronize()
+    M.moara_reset_kernel_stats(st, stream=stream)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_host = time.perf_counter()
+    e0.record(stream)
+    for _ in range(a.steps):
+        M.moara_step(st, W, G, lr, stream=stream)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    host_s = time.perf_counter() - t_host
+    ms_total = e0.elapsed_time(e1)
+    ms_step = ms_total / a.steps
+    log(f"[bench] {a.steps} steps: {ms_step:.3f} ms/step (host clock {host_s / a.steps * 1e3:.3f})")
+
+    kern = {}
+    names = {M.MOARA_KERN_DECOMPOSE: "decompose", M.MOARA_KERN_PROJECT: "project",
+             M.MOARA_KERN_BACKPROJ: "backproject"}
+    for kid, name in names.items():
+        nl, ms = M.moara_kernel_stats(st, kid, stream=stream)
+        kern[name] = {"launches": nl, "ms_total": ms, "ms_per_step": ms / max(1, a.steps),
+                      "ms_per_launch": ms / max(1, nl)}
+    cost = algorithmic_cost(wl, ob, wb)
+    peak_mfma = PEAK_BF16 if operand == "bf16" else PEAK_F32
+    for name, (bytes_, flops) in cost.items():
+        t = kern[name]["ms_per_step"] / 1e3
+        kern[name]["alg_bytes_per_step"] = bytes_
+        kern[name]["alg_flops_per_step"] = flops
+        kern[name]["GBps"] = bytes_ / t / 1e9 if t > 0 else None
+        kern[name]["TFLOPs"] = flops / t / 1e12 if t > 0 else None
+        kern[name]["hbm_frac"] = bytes_ / t / PEAK_HBM if t > 0 else None
+        kern[name]["mfma_frac"] = flops / t / peak_mfma if t > 0 and flops else None
+    dom = max(kern, key=lambda k: kern[k]["ms_per_step"])
+    dk = kern[dom]
+    t_mem = dk["alg_bytes_per_step"] / PEAK_HBM
+    t_mfma = dk["alg_flops_per_step"] / peak_mfma
+    launches_per_step = max(1, dk["launches"] // max(1, a.steps))
+    if t_mfma > t_mem:
+        roof = {"bound": "mfma", "achieved": dk["TFLOPs"], "peak": peak_mfma / 1e12, "unit": "TFLOP/s",
+                "frac": dk["mfma_frac"]}
+    else:
+        roof = {"bound": "hbm", "achieved": dk["GBps"], "peak": PEAK_HBM / 1e9, "unit": "GB/s",
+                "frac": dk["hbm_frac"]}
+    roof.update({"kernel": dom, "launches_per_step": launches_per_step,
+                 "alg_bytes_per_launch": dk["alg_bytes_per_step"] / launches_per_step,
+                 "alg_flops_per_launch": dk["alg_flops_per_step"] / launches_per_step,
+                 "avg_launch_ms": dk["ms_total"] / max(1, dk["launches"]),
+                 "traffic": None})
+
+    rf = refresh_flops(wl, wl.refresh_oversample, wl.refresh_iters)
+    ref_med = float(np.median(ref_ms))
+    out = {
+        "metric": "params updated/sec per optimizer step at Llama-2-7B shapes; ms per projector refresh",
+        "value": wl.n_params / (ms_step / 1e3),
+        "unit": "params/s",
+        "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+        "dtype": operand, "data": "synthetic",
+        "config": {"workload": wl.name, "layers": wl.n_layers, "matrices": n, "params": wl.n_params,
+                   "rank_table": list(wl.rank_table[:7] if wl.moe_routed == 0 else wl.rank_table),
+                   "block_size": wl.block_size, "weights": wl.weight_dtype, "grads": "f32", "moments": "f32",
+                   "gemm_operands": operand, "refresh": {"oversample": wl.refresh_oversample,
+                                                         "iters": wl.refresh_iters}},
+        "ms_per_refresh": ref_med,
+        "refresh_tflops": rf / (ref_med / 1e3) / 1e12,
+        "refresh_frac_fp32_peak": rf / (ref_med / 1e3) / PEAK_F32,
+        "amortized_ms_per_step_T200": ms_step + ref_med / 200.0,
+        "step_roofline_ms": max(sum(c[0] for c in cost.values()) / PEAK_HBM,
+                                sum(c[1] for c in cost.values()) / peak_mfma) * 1e3,
+        "kernels": kern,
+        "roofline": roof,
+        "host_clock_ms_per_step": host_s / a.steps * 1e3,
+    }
+    if not a.no_cpu_baseline:
+        log("[bench] cpu baseline (oracle) ...")
+        cb = cpu_baseline(wl, a.cpu_sample_layers)
+        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+    else:
+        out["cpu_baseline"] = None
+    print(json.dumps(out), flush=True)
+    del st
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

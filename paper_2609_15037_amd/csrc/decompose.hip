@@ -1,0 +1,89 @@
+// Block-wise magnitude/direction decomposition (Section 3.1, Appendix B.1)
+// fused with Optimizer_M (Adam on the block magnitudes, Algorithm 1).
+//
+// For every row i and block j (columns [jB, min(jB+B, n)) -- the zero padding of
+// the last block contributes nothing to the norm):
+//   M[i,j]   = ||G[i, block j]||_2
+//   inv[i,j] = 1 / (M[i,j] + eps_d)        (V = G * inv is formed on the fly by the GEMMs)
+//   dM[i,j]  = Adam(M[i,j])                (when p.adam_m != 0)
+//
+// Memory-bound: reads G once (4 B/element), writes 4 (inv, dM, two moments)
+// and reads 2 fp32 values per block. One wave streams one row at a time with
+// 16-byte loads; a block of B <= 256 columns maps onto B/4 consecutive lanes and
+// is reduced with xor shuffles inside that lane group (fixed order, so results
+// are bit-reproducible). Other block sizes take a generic per-block path.
+#include "common.h"
+
+namespace {
+constexpr int DEC_ROWS = 16;   // rows per workgroup (4 waves x 4 rows)
+
+__device__ __forceinline__ void block_out(const MatDev& d, const StepParams& p, int64_t row, int j,
+                                          float ss, int adam_m) {
+  const float M = sqrtf(ss);
+  const int64_t idx = row * d.k + j;
+  d.inv[idx] = 1.0f / (M + p.decomp_eps);
+  if (adam_m) {
+    float e = d.mag1[idx], q = d.mag2[idx];
+    const float out = adam_out(M, e, q, p.beta1, p.beta2, p.adam_eps, d.bc1, d.bc2);
+    d.mag1[idx] = e;
+    d.mag2[idx] = q;
+    d.dM[idx] = out;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ mats, StepParams p, int adam_m) {
+  const uint32_t t = blockIdx.x;
+  const int mi = find_mat(mats, p.nmat, t, [](const MatDev& d) { return d.tile_dec; });
+  const MatDev d = mats[mi];
+  const int64_t row0 = (int64_t)(t - d.tile_dec) * DEC_ROWS;
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int B = p.B;
+  const int64_t n = d.n;
+  const bool fast = (B >= 4 && B <= 256 && (B & (B - 1)) == 0 && (n & 3) == 0 &&
+                     ((uintptr_t)d.G & 15) == 0);
+  for (int rr = wave; rr < DEC_ROWS; rr += 4) {
+    const int64_t row = row0 + rr;
+    if (row >= d.m) break;
+    const float* g = d.G + row * n;
+    if (fast) {
+      const int gl = B >> 2;   // lanes per block
+      for (int64_t c0 = 0; c0 < n; c0 += 256) {
+        const int64_t c = c0 + 4 * lane;
+        float ss = 0.f;
+        if (c < n) {
+          const float4 v = *reinterpret_cast<const float4*>(g + c);
+          ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
+        }
+        for (int o = 1; o < gl; o <<= 1) ss += __shfl_xor(ss, o, 64);
+        if ((lane & (gl - 1)) == 0 && c < n) block_out(d, p, row, (int)(c / B), ss, adam_m);
+      }
+    } else {
+      for (int j = 0; j < d.k; ++j) {
+        const int64_t cs = (int64_t)j * B;
+        const int64_t ce = (cs + B < n) ? cs + B : n;
+        float ss = 0.f;
+        for (int64_t c = cs + lane; c < ce; c += 64) {
+          const float v = g[c];
+          ss += v * v;
+        }
+        ss = wave_sum(ss);
+        if (lane == 0) block_out(d, p, row, j, ss, adam_m);
+      }
+    }
+  }
+}
+}  // namespace
+
+int decompose_tiles(int64_t m) { return (int)((m + DEC_ROWS - 1) / DEC_ROWS); }
+
+hipError_t launch_decompose(const MatDev* mats_dev, const StepParams& p, hipStream_t st) {
+  if (p.total_dec == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_decompose, dim3(p.total_dec), dim3(256), 0, st, mats_dev, p, 1);
+  return hipGetLastError();
+}
+
+hipError_t launch_decompose_inv_only(const MatDev* mats_dev, const StepParams& p, hipStream_t st) {
+  if (p.total_dec == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_decompose, dim3(p.total_dec), dim3(256), 0, st, mats_dev, p, 0);
+  return hipGetLastError();
+}

@@ -1,0 +1,65 @@
+// Grouped MFMA GEMM used by every dense contraction of the library.
+//
+//   C[M x N] = sum_k A[i][k] * B[j][k]     (i < M, j < N, k < K)
+//
+// One launch covers a list of independent problems (e.g. every matrix of a
+// layer stack); each workgroup finds its problem by binary search over the
+// problems' tile prefixes, then computes one BM x BN tile.
+#pragma once
+#include "common.h"
+
+enum { KIND_BF16 = 0, KIND_F32 = 1 };
+// A access modes:
+//   A_G_ROW   : A[i][k] = G[i*lda + k]   * inv[i*inv_ld + k/B]   (direction V, rows)
+//   A_G_TRANS : A[i][k] = G[k*lda + i]   * inv[k*inv_ld + i/B]   (direction V^T)
+//   A_KC      : A[i][k] = a[i*lda + k]   (operand dtype)
+// B access modes:
+//   B_KC      : B[j][k] = b[j*ldb + k]   (operand dtype)
+//   B_NC      : B[j][k] = b[k*ldb + j]   (fp32 kind only)
+enum { A_G_ROW = 0, A_G_TRANS = 1, A_KC = 2 };
+enum { B_KC = 0, B_NC = 1 };
+// Epilogues:
+//   EP_ADAM   : Optimizer_V on the projected tile; moments e1/e2 and output c are [M][N]
+//   EP_UPDATE : W[i][j] -= lr * scale * dM[i][j/B] * C[i][j] (bf16 or fp32 W in c)
+//   EP_STORE  : c[i*ldc + j] = C[i][j] (fp32)
+enum { EP_ADAM = 0, EP_UPDATE = 1, EP_STORE = 2 };
+
+struct GemmProb {
+  int64_t M, N, K;
+  const void* a;
+  int64_t lda;
+  const float* inv;   // A_G_* only; nullptr = no scaling (V = G)
+  int64_t inv_ld;
+  const void* b;
+  int64_t ldb;
+  void* c;
+  int64_t ldc;
+  float* e1;          // EP_ADAM moments
+  float* e2;
+  const float* dM;    // EP_UPDATE magnitudes (nullptr = 1)
+  int64_t dM_ld;
+  float bc1, bc2;     // EP_ADAM bias corrections
+  uint32_t tile_start;
+  uint32_t tiles_n;
+  int32_t vec;        // bit0: A may use 16-byte loads, bit1: B may
+  int32_t pad_;
+};
+
+struct GemmUniform {
+  int32_t B;            // decomposition block size (A_G_* scaling, EP_UPDATE)
+  int32_t nprob;
+  int32_t weight_bf16;  // EP_UPDATE
+  int32_t pad_;
+  float beta1, beta2, adam_eps;
+  float lr, scale;
+};
+
+template <int KIND> struct GemmTile;
+template <> struct GemmTile<KIND_BF16> { static constexpr int BM = 128, BN = 128, BK = 64; };
+template <> struct GemmTile<KIND_F32> { static constexpr int BM = 128, BN = 128, BK = 32; };
+
+// Host helpers (gemm.hip).
+uint32_t gemm_tiles_m(int kind, int64_t M);
+uint32_t gemm_tiles_n(int kind, int64_t N);
+hipError_t launch_gemm(int kind, int amode, int bmode, int ep, const GemmProb* probs_dev, int nprob,
+                       uint32_t total_tiles, const GemmUniform& u, hipStream_t st);

@@ -1,0 +1,999 @@
+// C ABI of the MoARa optimizer library: validation, state, scheduling.
+// Host code; every method step runs in the kernels of decompose.hip, gemm.hip
+// and refresh.hip.
+#include <math.h>
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <algorithm>
+#include <string>
+#include <vector>
+
+#include "../../include/moara.h"
+#include "common.h"
+#include "gemm.h"
+#include "refresh.h"
+
+hipError_t launch_decompose_inv_only(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
+int decompose_tiles(int64_t m);
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+#define HIP_TRY(expr)                                                                   \
+  do {                                                                                  \
+    hipError_t e_ = (expr);                                                             \
+    if (e_ != hipSuccess) return fail(MOARA_E_HIP, "%s: %s", #expr, hipGetErrorString(e_)); \
+  } while (0)
+
+constexpr size_t ALIGN = 256;
+size_t align_up(size_t x) { return (x + ALIGN - 1) & ~(ALIGN - 1); }
+
+struct MatHost {
+  int64_t m = 0, n = 0, L = 0, s = 0;
+  int32_t r = 0, side = 0, k = 0;
+  int64_t t = 0;
+  bool hasP = false;
+  float *inv = nullptr, *dM = nullptr, *mag1 = nullptr, *mag2 = nullptr;
+  float *exp1 = nullptr, *exp2 = nullptr, *P32 = nullptr;
+  void *N = nullptr, *Pop = nullptr, *Ptop = nullptr;
+};
+
+struct TimedLaunch {
+  int kind;
+  hipEvent_t a, b;
+};
+
+}  // namespace
+
+struct moara_state {
+  moara_config cfg;
+  int n = 0;
+  int device = 0;
+  std::vector<MatHost> mats;
+  char* block = nullptr;        // all persistent device memory
+  size_t block_bytes = 0;
+  // descriptor staging: pinned host ring + one device arena (stream ordered)
+  static constexpr int NSLOT = 8;
+  char* host_ring = nullptr;
+  char* dev_arena = nullptr;
+  size_t arena_bytes = 0;
+  hipEvent_t slot_ev[NSLOT] = {};
+  bool slot_used[NSLOT] = {};
+  int slot = 0;
+  // refresh workspace
+  char* ref_ws = nullptr;
+  size_t ref_ws_bytes = 0;
+  char* ref_arena = nullptr;      // device descriptors of the refresh (separate arena)
+  size_t ref_arena_bytes = 0;
+  char* ref_host = nullptr;
+  // timing
+  bool timing = false;
+  std::vector<TimedLaunch> pending;
+  std::vector<hipEvent_t> ev_pool;
+  int64_t launches[MOARA_NUM_KERNELS] = {};
+  double total_ms[MOARA_NUM_KERNELS] = {};
+};
+
+namespace {
+
+int elem_bytes(int dtype) { return dtype == MOARA_BF16 ? 2 : 4; }
+
+int validate_config(const moara_config* c) {
+  if (!c) return fail(MOARA_E_ARG, "config is NULL");
+  if (c->block_size < 1) return fail(MOARA_E_ARG, "block_size must be >= 1 (got %d)", c->block_size);
+  if (!(c->beta1 >= 0.f && c->beta1 < 1.f) || !(c->beta2 >= 0.f && c->beta2 < 1.f))
+    return fail(MOARA_E_ARG, "betas must lie in [0, 1)");
+  if (!(c->adam_eps > 0.f) || !isfinite(c->adam_eps)) return fail(MOARA_E_ARG, "adam_eps must be > 0");
+  if (!(c->decomp_eps >= 0.f) || !isfinite(c->decomp_eps)) return fail(MOARA_E_ARG, "decomp_eps must be >= 0");
+  if (!isfinite(c->scale)) return fail(MOARA_E_ARG, "scale must be finite");
+  if (c->weight_decay != 0.f) return fail(MOARA_E_UNSUPPORTED, "weight_decay != 0 is not supported (the method uses none)");
+  if (c->refresh_interval < 0) return fail(MOARA_E_ARG, "refresh_interval must be >= 0");
+  if (c->bias_correction != 0 && c->bias_correction != 1) return fail(MOARA_E_ARG, "bias_correction must be 0 or 1");
+  if (c->decompose != 0 && c->decompose != 1) return fail(MOARA_E_ARG, "decompose must be 0 or 1");
+  if (c->weight_dtype != MOARA_F32 && c->weight_dtype != MOARA_BF16) return fail(MOARA_E_ARG, "bad weight_dtype");
+  if (c->grad_dtype != MOARA_F32) return fail(MOARA_E_UNSUPPORTED, "only fp32 gradients are supported");
+  if (c->operand_dtype != MOARA_F32 && c->operand_dtype != MOARA_BF16) return fail(MOARA_E_ARG, "bad operand_dtype");
+  if (c->refresh_oversample < -1) return fail(MOARA_E_ARG, "refresh_oversample must be >= -1");
+  if (c->refresh_iters < 1 || c->refresh_iters > 1000) return fail(MOARA_E_ARG, "refresh_iters must be in [1, 1000]");
+  if (c->zero_grad_mode == 1) return fail(MOARA_E_UNSUPPORTED, "zero_grad_mode 1 is not implemented");
+  if (c->zero_grad_mode != 0) return fail(MOARA_E_ARG, "bad zero_grad_mode");
+  if (c->reserved != 0) return fail(MOARA_E_ARG, "reserved must be 0");
+  return MOARA_OK;
+}
+
+int resolve(const moara_config* cfg, const moara_matrix_desc* d, int32_t* rank, int32_t* side) {
+  if (!cfg || !d || !rank || !side) return fail(MOARA_E_ARG, "NULL argument");
+  if (d->rows < 1 || d->cols < 1) return fail(MOARA_E_SHAPE, "matrix shape %lldx%lld", (long long)d->rows, (long long)d->cols);
+  if (d->rows > (1LL << 31) - 1 || d->cols > (1LL << 31) - 1) return fail(MOARA_E_SHAPE, "matrix dimension too large");
+  if (d->module < 0 || d->module >= MOARA_NUM_MODULES) return fail(MOARA_E_ARG, "module id %d out of range", d->module);
+  if (d->side < MOARA_SIDE_AUTO || d->side > MOARA_SIDE_RIGHT) return fail(MOARA_E_ARG, "bad side %d", d->side);
+  if (d->rank_override < 0) return fail(MOARA_E_RANK, "rank_override must be >= 0");
+  if (d->reserved != 0) return fail(MOARA_E_ARG, "descriptor reserved field must be 0");
+  const int32_t r = d->rank_override > 0 ? d->rank_override : cfg->rank_table[d->module];
+  const int64_t mn = std::min(d->rows, d->cols);
+  if (r < 1 || r > mn) return fail(MOARA_E_RANK, "rank %d outside [1, min(m,n)=%lld] for module %d", r, (long long)mn, d->module);
+  int sd = d->side;
+  if (sd == MOARA_SIDE_AUTO) sd = (d->rows <= d->cols) ? MOARA_SIDE_LEFT : MOARA_SIDE_RIGHT;
+  *rank = r;
+  *side = sd;
+  return MOARA_OK;
+}
+
+struct Layout {
+  int64_t s, L, k;
+};
+Layout layout_of(const moara_matrix_desc& d, int side, int B) {
+  Layout l;
+  l.s = side == MOARA_SIDE_LEFT ? d.rows : d.cols;
+  l.L = side == MOARA_SIDE_LEFT ? d.cols : d.rows;
+  l.k = (d.cols + B - 1) / B;
+  return l;
+}
+
+int32_t subspace_width(const moara_config& c, int64_t s, int32_t r) {
+  const int64_t p = c.refresh_oversample < 0 ? r : c.refresh_oversample;
+  return (int32_t)std::min<int64_t>(s, r + p);
+}
+
+size_t mat_state_bytes(const moara_config& c, int64_t m, int64_t s, int64_t L, int64_t k, int32_t r) {
+  const int ob = elem_bytes(c.operand_dtype);
+  size_t b = 0;
+  b += align_up(4 * m * k) * 4;          // inv, dM, mag1, mag2
+  b += align_up(4 * L * r) * 2;          // exp1, exp2
+  b += align_up((size_t)ob * L * r);     // N
+  b += align_up(4 * s * r);              // P32
+  b += align_up((size_t)ob * s * r) * 2; // Pop, Ptop
+  return b;
+}
+
+size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w) {
+  const int64_t wpad = (w + 63) / 64 * 64;
+  size_t b = 0;
+  b += align_up(4 * s * w) * 2;            // Z, Z2
+  b += align_up(4 * L * w) * 2;            // Y, Y2
+  b += align_up(8 * (size_t)w * w);        // C
+  b += align_up(4 * (size_t)w * w);        // Rinv
+  b += align_up(8 * (size_t)wpad * s);     // Zc
+  b += align_up(4 * 64);                   // off
+  b += align_up(4 * wpad) + align_up(8 * wpad);
+  return b;
+}
+
+// ------------------------------------------------------------------ staging
+struct Stager {
+  moara_state* st;
+  char* host = nullptr;
+  size_t used = 0;
+  size_t cap = 0;
+  template <typename T>
+  size_t push(const T* p, size_t count) {
+    const size_t off = used;
+    const size_t bytes = sizeof(T) * count;
+    if (used + bytes > cap) return (size_t)-1;
+    memcpy(host + used, p, bytes);
+    used = align_up(used + bytes);
+    return off;
+  }
+};
+
+int begin_stage(moara_state* st, Stager& sg) {
+  const int s = st->slot;
+  if (st->slot_used[s]) HIP_TRY(hipEventSynchronize(st->slot_ev[s]));
+  sg.st = st;
+  sg.host = st->host_ring + (size_t)s * st->arena_bytes;
+  sg.used = 0;
+  sg.cap = st->arena_bytes;
+  return MOARA_OK;
+}
+
+int end_stage(moara_state* st, Stager& sg, hipStream_t stream) {
+  const int s = st->slot;
+  if (sg.used) HIP_TRY(hipMemcpyAsync(st->dev_arena, sg.host, sg.used, hipMemcpyHostToDevice, stream));
+  HIP_TRY(hipEventRecord(st->slot_ev[s], stream));
+  st->slot_used[s] = true;
+  st->slot = (s + 1) % moara_state::NSLOT;
+  return MOARA_OK;
+}
+
+// ------------------------------------------------------------------ timing
+hipEvent_t get_event(moara_state* st) {
+  if (!st->ev_pool.empty()) {
+    hipEvent_t e = st->ev_pool.back();
+    st->ev_pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+
+struct TimerScope {
+  moara_state* st;
+  int kind;
+  hipStream_t stream;
+  hipEvent_t a = nullptr;
+  TimerScope(moara_state* s, int k, hipStream_t str) : st(s), kind(k), stream(str) {
+    if (st->timing) {
+      a = get_event(st);
+      if (a) hipEventRecord(a, stream);
+    }
+  }
+  ~TimerScope() {
+    if (st->timing && a) {
+      hipEvent_t b = get_event(st);
+      if (b) {
+        hipEventRecord(b, stream);
+        st->pending.push_back({kind, a, b});
+      }
+    }
+  }
+};
+
+int collect_timing(moara_state* st, hipStream_t stream) {
+  if (st->pending.empty()) return MOARA_OK;
+  HIP_TRY(hipStreamSynchronize(stream));
+  for (auto& tl : st->pending) {
+    float ms = 0.f;
+    HIP_TRY(hipEventElapsedTime(&ms, tl.a, tl.b));
+    st->launches[tl.kind] += 1;
+    st->total_ms[tl.kind] += ms;
+    st->ev_pool.push_back(tl.a);
+    st->ev_pool.push_back(tl.b);
+  }
+  st->pending.clear();
+  return MOARA_OK;
+}
+
+// ------------------------------------------------------------------ step launch
+int vec_flags_g(const float* G, int64_t n) { return (((uintptr_t)G & 15) == 0 && (n & 3) == 0) ? 1 : 0; }
+int vec_flags_op(const void* p, int64_t ld, int operand_bf16) {
+  const int64_t q = operand_bf16 ? 8 : 4;
+  return (((uintptr_t)p & 15) == 0 && (ld % q) == 0) ? 1 : 0;
+}
+
+StepParams make_params(const moara_state* st, float lr) {
+  StepParams p{};
+  p.B = st->cfg.block_size;
+  p.decompose = st->cfg.decompose;
+  p.weight_bf16 = st->cfg.weight_dtype == MOARA_BF16;
+  p.beta1 = st->cfg.beta1;
+  p.beta2 = st->cfg.beta2;
+  p.adam_eps = st->cfg.adam_eps;
+  p.decomp_eps = st->cfg.decomp_eps;
+  p.lr = lr;
+  p.scale = st->cfg.scale;
+  return p;
+}
+
+GemmUniform make_uniform(const moara_state* st, float lr) {
+  GemmUniform u{};
+  u.B = st->cfg.block_size;
+  u.weight_bf16 = st->cfg.weight_dtype == MOARA_BF16;
+  u.beta1 = st->cfg.beta1;
+  u.beta2 = st->cfg.beta2;
+  u.adam_eps = st->cfg.adam_eps;
+  u.lr = lr;
+  u.scale = st->cfg.scale;
+  return u;
+}
+
+// Decompose (inv, and optionally Optimizer_M) for the listed matrices.
+int run_decompose(moara_state* st, const std::vector<int>& idx, const void* const* grads, bool adam_m,
+                  hipStream_t stream) {
+  if (idx.empty()) return MOARA_OK;
+  std::vector<MatDev> md;
+  uint32_t tiles = 0;
+  for (int i : idx) {
+    const MatHost& h = st->mats[i];
+    MatDev d{};
+    d.G = (const float*)grads[i];
+    d.m = h.m; d.n = h.n; d.k = h.k; d.r = h.r; d.side = h.side;
+    d.inv = h.inv; d.dM = h.dM; d.mag1 = h.mag1; d.mag2 = h.mag2;
+    const double t1 = (double)(h.t + 1);
+    d.bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
+    d.bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
+    d.tile_dec = tiles;
+    tiles += (uint32_t)decompose_tiles(h.m);
+    md.push_back(d);
+  }
+  Stager sg;
+  int rc = begin_stage(st, sg);
+  if (rc) return rc;
+  const size_t off = sg.push(md.data(), md.size());
+  if (off == (size_t)-1) return fail(MOARA_E_OOM, "descriptor arena too small");
+  rc = end_stage(st, sg, stream);
+  if (rc) return rc;
+  StepParams p = make_params(st, 0.f);
+  p.nmat = (int)md.size();
+  p.total_dec = tiles;
+  TimerScope ts(st, MOARA_KERN_DECOMPOSE, stream);
+  const MatDev* dev = (const MatDev*)(st->dev_arena + off);
+  HIP_TRY(adam_m ? launch_decompose(dev, p, stream) : launch_decompose_inv_only(dev, p, stream));
+  return MOARA_OK;
+}
+
+int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* weights, const void* const* grads,
+                     float lr, hipStream_t stream) {
+  const int ob = st->cfg.operand_dtype == MOARA_BF16;
+  const int kind = ob ? KIND_BF16 : KIND_F32;
+  std::vector<GemmProb> left, right, back;
+  uint32_t tl = 0, tr = 0, tb = 0;
+  for (int i : idx) {
+    const MatHost& h = st->mats[i];
+    const double t1 = (double)(h.t + 1);
+    GemmProb g{};
+    g.M = h.L; g.N = h.r; g.K = h.s;
+    g.a = grads[i]; g.lda = h.n;
+    g.inv = st->cfg.decompose ? h.inv : nullptr; g.inv_ld = h.k;
+    g.b = h.Ptop; g.ldb = h.s;
+    g.c = h.N; g.ldc = h.r;
+    g.e1 = h.exp1; g.e2 = h.exp2;
+    g.bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
+    g.bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
+    g.tiles_n = gemm_tiles_n(kind, g.N);
+    g.vec = vec_flags_g((const float*)grads[i], h.n) | (vec_flags_op(h.Ptop, h.s, ob) << 1);
+    const uint32_t nt = gemm_tiles_m(kind, g.M) * g.tiles_n;
+    if (h.side == MOARA_SIDE_LEFT) { g.tile_start = tl; tl += nt; left.push_back(g); }
+    else { g.tile_start = tr; tr += nt; right.push_back(g); }
+
+    GemmProb b{};
+    b.M = h.m; b.N = h.n; b.K = h.r;
+    if (h.side == MOARA_SIDE_LEFT) { b.a = h.Pop; b.b = h.N; }
+    else { b.a = h.N; b.b = h.Pop; }
+    b.lda = h.r; b.ldb = h.r;
+    b.c = weights[i]; b.ldc = h.n;
+    b.dM = st->cfg.decompose ? h.dM : nullptr; b.dM_ld = h.k;
+    b.tiles_n = gemm_tiles_n(kind, b.N);
+    b.vec = vec_flags_op(b.a, h.r, ob) | (vec_flags_op(b.b, h.r, ob) << 1);
+    b.tile_start = tb;
+    tb += gemm_tiles_m(kind, b.M) * b.tiles_n;
+    back.push_back(b);
+  }
+  Stager sg;
+  int rc = begin_stage(st, sg);
+  if (rc) return rc;
+  const size_t ol = left.empty() ? 0 : sg.push(left.data(), left.size());
+  const size_t orr = right.empty() ? 0 : sg.push(right.data(), right.size());
+  const size_t obk = back.empty() ? 0 : sg.push(back.data(), back.size());
+  if (ol == (size_t)-1 || orr == (size_t)-1 || obk == (size_t)-1) return fail(MOARA_E_OOM, "descriptor arena too small");
+  rc = end_stage(st, sg, stream);
+  if (rc) return rc;
+  const GemmUniform u = make_uniform(st, lr);
+  {
+    TimerScope ts(st, MOARA_KERN_PROJECT, stream);
+    if (!right.empty())
+      HIP_TRY(launch_gemm(kind, A_G_ROW, B_KC, EP_ADAM, (const GemmProb*)(st->dev_arena + orr), (int)right.size(), tr, u, stream));
+    if (!left.empty())
+      HIP_TRY(launch_gemm(kind, A_G_TRANS, B_KC, EP_ADAM, (const GemmProb*)(st->dev_arena + ol), (int)left.size(), tl, u, stream));
+  }
+  {
+    TimerScope ts(st, MOARA_KERN_BACKPROJ, stream);
+    HIP_TRY(launch_gemm(kind, A_KC, B_KC, EP_UPDATE, (const GemmProb*)(st->dev_arena + obk), (int)back.size(), tb, u, stream));
+  }
+  return MOARA_OK;
+}
+
+// ------------------------------------------------------------------ refresh driver
+struct RefMat {
+  int idx;
+  int64_t s, L;
+  int32_t w, wpad;
+  float *Z, *Z2, *Y, *Y2, *Rinv;
+  double *C, *Zc, *norms;
+  uint32_t* off;
+  int32_t* order;
+};
+
+int ensure_ref_ws(moara_state* st, size_t bytes) {
+  if (bytes <= st->ref_ws_bytes) return MOARA_OK;
+  if (st->ref_ws) {
+    HIP_TRY(hipDeviceSynchronize());
+    hipFree(st->ref_ws);
+    st->ref_ws = nullptr;
+    st->ref_ws_bytes = 0;
+  }
+  if (hipMalloc(&st->ref_ws, bytes) != hipSuccess) {
+    st->ref_ws = nullptr;
+    return fail(MOARA_E_OOM, "refresh workspace of %zu bytes", bytes);
+  }
+  st->ref_ws_bytes = bytes;
+  return MOARA_OK;
+}
+
+constexpr int MAX_SWEEPS = 14;
+
+// One refresh pass over a chunk of matrices. Buffer roles are fixed:
+//   Z2 <- Gaussian ; Z <- orth(Z2)
+//   repeat: Y <- X Z ; Z2 <- X^T Y ; Z <- orth(Z2)        (q - 1 times)
+//   last  : Y <- X Z ; Y2 <- orth(Y) ; Z2 <- X^T Y2 ; Jacobi on Z2 ; P <- top r
+int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream) {
+  const moara_config& c = st->cfg;
+  size_t need = 0;
+  std::vector<RefMat> rm;
+  for (int i : idx) {
+    const MatHost& h = st->mats[i];
+    RefMat x{};
+    x.idx = i; x.s = h.s; x.L = h.L;
+    x.w = subspace_width(c, h.s, h.r);
+    x.wpad = (x.w + 63) / 64 * 64;
+    need += mat_refresh_bytes(h.s, h.L, x.w);
+    rm.push_back(x);
+  }
+  int rc = ensure_ref_ws(st, need);
+  if (rc) return rc;
+  char* p = st->ref_ws;
+  auto take = [&](size_t b) { char* q = p; p += align_up(b); return q; };
+  for (auto& x : rm) {
+    x.Z = (float*)take(4 * x.s * x.w);
+    x.Z2 = (float*)take(4 * x.s * x.w);
+    x.Y = (float*)take(4 * x.L * x.w);
+    x.Y2 = (float*)take(4 * x.L * x.w);
+    x.C = (double*)take(8 * (size_t)x.w * x.w);
+    x.Rinv = (float*)take(4 * (size_t)x.w * x.w);
+    x.Zc = (double*)take(8 * (size_t)x.wpad * x.s);
+    x.off = (uint32_t*)take(4 * 64);
+    x.order = (int32_t*)take(4 * x.wpad);
+    x.norms = (double*)take(8 * x.wpad);
+  }
+  const int nm = (int)rm.size();
+  const int kind = KIND_F32;
+  const GemmUniform u = make_uniform(st, 0.f);
+
+  std::vector<RefDev> rd(nm);
+  uint32_t tg = 0, tj = 0, tc = 0;
+  int nb_max = 2;
+  for (int q = 0; q < nm; ++q) {
+    const RefMat& x = rm[q];
+    const MatHost& h = st->mats[x.idx];
+    RefDev& d = rd[q];
+    d.s = x.s; d.L = x.L; d.w = x.w; d.wpad = x.wpad; d.r = h.r;
+    d.operand_bf16 = c.operand_dtype == MOARA_BF16;
+    d.seed = c.refresh_seed * 0x9E3779B97F4A7C15ull + (uint64_t)(x.idx + 1) * 0xD1B54A32D192ED03ull;
+    d.Z = x.Z2; d.C = x.C; d.Rinv = x.Rinv; d.Zc = x.Zc;
+    d.P32 = h.P32; d.Pop = h.Pop; d.Ptop = h.Ptop;
+    d.off = x.off; d.order = x.order; d.norms = x.norms;
+    d.tile_gauss = tg; tg += gauss_tiles(x.s, x.w);
+    d.tile_jac = tj; tj += jacobi_tiles(x.wpad);
+    d.tile_cm = tc; tc += colmajor_tiles(x.s, x.wpad);
+    d.has_prev = h.hasP ? 1 : 0;
+    nb_max = std::max(nb_max, x.wpad / JB);
+  }
+  auto gram_list = [&](bool onY) {
+    std::vector<GramProb> g(nm);
+    uint32_t t = 0;
+    for (int q = 0; q < nm; ++q) {
+      const RefMat& x = rm[q];
+      GramProb& gp = g[q];
+      gp.A = onY ? x.Y : x.Z2;
+      gp.rows = onY ? x.L : x.s;
+      gp.lda = x.w; gp.C = x.C; gp.w = x.w;
+      gp.tiles = (x.w + 63) / 64;
+      gp.tile_start = t;
+      t += gram_tiles(x.w);
+    }
+    return std::make_pair(g, t);
+  };
+  auto apply_list = [&](bool onY) {   // Z = Z2 Rinv  or  Y2 = Y Rinv
+    std::vector<GemmProb> g(nm);
+    uint32_t t = 0;
+    for (int q = 0; q < nm; ++q) {
+      const RefMat& x = rm[q];
+      GemmProb& gp = g[q];
+      gp.M = onY ? x.L : x.s; gp.N = x.w; gp.K = x.w;
+      gp.a = onY ? (const void*)x.Y : (const void*)x.Z2;
+      gp.lda = x.w;
+      gp.b = x.Rinv; gp.ldb = x.w;
+      gp.c = onY ? (void*)x.Y2 : (void*)x.Z;
+      gp.ldc = x.w;
+      gp.tiles_n = gemm_tiles_n(kind, gp.N);
+      gp.vec = vec_flags_op(gp.a, x.w, 0) | (vec_flags_op(gp.b, x.w, 0) << 1);
+      gp.tile_start = t;
+      t += gemm_tiles_m(kind, gp.M) * gp.tiles_n;
+    }
+    return std::make_pair(g, t);
+  };
+  // Y = X Z  (tall: M = L, K = s)   or   Z2 = X^T Yin  (M = s, K = L)
+  auto big_list = [&](int side, bool xt, bool fromY2) {
+    std::vector<GemmProb> g;
+    uint32_t t = 0;
+    for (int q = 0; q < nm; ++q) {
+      const RefMat& x = rm[q];
+      const MatHost& h = st->mats[x.idx];
+      if (h.side != side) continue;
+      GemmProb gp{};
+      gp.M = xt ? x.s : x.L; gp.N = x.w; gp.K = xt ? x.L : x.s;
+      gp.a = grads[x.idx]; gp.lda = h.n;
+      gp.inv = c.decompose ? h.inv : nullptr; gp.inv_ld = h.k;
+      gp.b = xt ? (fromY2 ? x.Y2 : x.Y) : x.Z; gp.ldb = x.w;
+      gp.c = xt ? x.Z2 : x.Y; gp.ldc = x.w;
+      gp.tiles_n = gemm_tiles_n(kind, gp.N);
+      gp.vec = vec_flags_g((const float*)grads[x.idx], h.n) | (vec_flags_op(gp.b, x.w, 0) << 1);
+      gp.tile_start = t;
+      t += gemm_tiles_m(kind, gp.M) * gp.tiles_n;
+      g.push_back(gp);
+    }
+    return std::make_pair(g, t);
+  };
+  auto gZ2 = gram_list(false), gY = gram_list(true);
+  auto aZ = apply_list(false), aY = apply_list(true);
+  auto xzR = big_list(MOARA_SIDE_RIGHT, false, false), xzL = big_list(MOARA_SIDE_LEFT, false, false);
+  auto xtR = big_list(MOARA_SIDE_RIGHT, true, false), xtL = big_list(MOARA_SIDE_LEFT, true, false);
+  auto xt2R = big_list(MOARA_SIDE_RIGHT, true, true), xt2L = big_list(MOARA_SIDE_LEFT, true, true);
+
+  struct Part { const void* p; size_t b; };
+  std::vector<Part> parts = {
+      {rd.data(), sizeof(RefDev) * nm},                               // 0
+      {gZ2.first.data(), sizeof(GramProb) * nm},                      // 1
+      {gY.first.data(), sizeof(GramProb) * nm},                       // 2
+      {aZ.first.data(), sizeof(GemmProb) * nm},                       // 3
+      {aY.first.data(), sizeof(GemmProb) * nm},                       // 4
+      {xzR.first.data(), sizeof(GemmProb) * xzR.first.size()},       // 5
+      {xzL.first.data(), sizeof(GemmProb) * xzL.first.size()},       // 6
+      {xtR.first.data(), sizeof(GemmProb) * xtR.first.size()},       // 7
+      {xtL.first.data(), sizeof(GemmProb) * xtL.first.size()},       // 8
+      {xt2R.first.data(), sizeof(GemmProb) * xt2R.first.size()},     // 9
+      {xt2L.first.data(), sizeof(GemmProb) * xt2L.first.size()},     // 10
+  };
+  size_t total = 0;
+  std::vector<size_t> offs;
+  for (auto& pp : parts) { offs.push_back(total); total += align_up(pp.b ? pp.b : 1); }
+  if (total > st->ref_arena_bytes) {
+    HIP_TRY(hipStreamSynchronize(stream));
+    if (st->ref_arena) hipFree(st->ref_arena);
+    if (st->ref_host) hipHostFree(st->ref_host);
+    st->ref_arena = nullptr; st->ref_host = nullptr; st->ref_arena_bytes = 0;
+    if (hipMalloc(&st->ref_arena, total) != hipSuccess) return fail(MOARA_E_OOM, "refresh descriptor arena");
+    if (hipHostMalloc(&st->ref_host, total) != hipSuccess) return fail(MOARA_E_OOM, "refresh pinned arena");
+    st->ref_arena_bytes = total;
+  }
+  // the pinned buffer and arena are shared by all refresh chunks: wait for earlier users
+  HIP_TRY(hipStreamSynchronize(stream));
+  for (size_t q = 0; q < parts.size(); ++q)
+    if (parts[q].b) memcpy(st->ref_host + offs[q], parts[q].p, parts[q].b);
+  HIP_TRY(hipMemcpyAsync(st->ref_arena, st->ref_host, total, hipMemcpyHostToDevice, stream));
+  auto D = [&](int q) { return (const void*)(st->ref_arena + offs[q]); };
+  const RefDev* RD = (const RefDev*)D(0);
+
+  auto gemm = [&](int am, int q, const std::pair<std::vector<GemmProb>, uint32_t>& l) -> hipError_t {
+    if (l.first.empty()) return hipSuccess;
+    return launch_gemm(kind, am, B_NC, EP_STORE, (const GemmProb*)D(q), (int)l.first.size(), l.second, u, stream);
+  };
+  auto orth_Z = [&]() -> hipError_t {        // Z <- orth(Z2)
+    hipError_t e = launch_gram((const GramProb*)D(1), nm, gZ2.second, stream);
+    if (e == hipSuccess) e = launch_chol_inv(RD, nm, stream);
+    if (e == hipSuccess) e = gemm(A_KC, 3, aZ);
+    return e;
+  };
+  TimerScope ts(st, MOARA_KERN_REFRESH, stream);
+  HIP_TRY(launch_gauss(RD, nm, tg, stream));
+  HIP_TRY(orth_Z());
+  const int q_iters = c.refresh_iters;
+  for (int it = 0; it < q_iters; ++it) {
+    // Y = X Z : RIGHT X = V -> rows of G ; LEFT X = V^T -> columns of G
+    HIP_TRY(gemm(A_G_ROW, 5, xzR));
+    HIP_TRY(gemm(A_G_TRANS, 6, xzL));
+    if (it + 1 < q_iters) {
+      HIP_TRY(gemm(A_G_TRANS, 7, xtR));
+      HIP_TRY(gemm(A_G_ROW, 8, xtL));
+      HIP_TRY(orth_Z());
+    } else {
+      HIP_TRY(launch_gram((const GramProb*)D(2), nm, gY.second, stream));
+      HIP_TRY(launch_chol_inv(RD, nm, stream));
+      HIP_TRY(gemm(A_KC, 4, aY));
+      HIP_TRY(gemm(A_G_TRANS, 9, xt2R));
+      HIP_TRY(gemm(A_G_ROW, 10, xt2L));
+    }
+  }
+  HIP_TRY(launch_to_colmajor(RD, nm, tc, stream));
+  for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.off, 0, 4 * 64, stream));
+  for (int sw = 0; sw < MAX_SWEEPS; ++sw)
+    for (int rr = 0; rr < nb_max - 1; ++rr) HIP_TRY(launch_jacobi_round(RD, nm, tj, rr, sw, stream));
+  HIP_TRY(launch_finalize(RD, nm, stream));
+  for (auto& x : rm) st->mats[x.idx].hasP = true;
+  return MOARA_OK;
+}
+
+constexpr size_t REFRESH_BUDGET = (size_t)48 << 30;   // device bytes per refresh chunk
+
+int run_refresh(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream) {
+  if (idx.empty()) return MOARA_OK;
+  int rc = run_decompose(st, idx, grads, false, stream);
+  if (rc) return rc;
+  std::vector<int> chunk;
+  size_t bytes = 0;
+  for (int i : idx) {
+    const MatHost& h = st->mats[i];
+    const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r));
+    if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
+      if ((rc = refresh_chunk(st, chunk, grads, stream))) return rc;
+      chunk.clear();
+      bytes = 0;
+    }
+    chunk.push_back(i);
+    bytes += b;
+  }
+  return refresh_chunk(st, chunk, grads, stream);
+}
+
+}  // namespace
+
+// ============================================================================ ABI
+extern "C" {
+
+int moara_default_config(moara_config* out) {
+  if (!out) return fail(MOARA_E_ARG, "out is NULL");
+  memset(out, 0, sizeof *out);
+  out->block_size = 128;
+  out->beta1 = 0.9f;
+  out->beta2 = 0.999f;
+  out->adam_eps = 1e-6f;
+  out->decomp_eps = 1e-12f;
+  out->scale = 0.25f;
+  out->weight_decay = 0.f;
+  out->refresh_interval = 200;
+  out->bias_correction = 1;
+  out->decompose = 1;
+  out->weight_dtype = MOARA_BF16;
+  out->grad_dtype = MOARA_F32;
+  out->operand_dtype = MOARA_BF16;
+  out->refresh_oversample = -1;
+  out->refresh_iters = 20;
+  out->refresh_seed = 0;
+  out->zero_grad_mode = 0;
+  return MOARA_OK;
+}
+
+
+int moara_allocate_ranks(int32_t r_base, uint32_t types_mask, uint32_t donor_mask, uint32_t receiver_mask,
+                         int32_t delta_r, int32_t out_rank_table[MOARA_NUM_MODULES]) {
+  if (!out_rank_table) return fail(MOARA_E_ARG, "out_rank_table is NULL");
+  const uint32_t all = (1u << MOARA_NUM_MODULES) - 1u;
+  if (types_mask == 0 || (types_mask & ~all)) return fail(MOARA_E_ARG, "types_mask must be a non-empty set of module ids");
+  if ((donor_mask & ~types_mask) || (receiver_mask & ~types_mask))
+    return fail(MOARA_E_ARG, "donor and receiver sets must be subsets of the module types");
+  if (donor_mask & receiver_mask) return fail(MOARA_E_ARG, "donor and receiver sets overlap");
+  if ((donor_mask == 0) != (receiver_mask == 0)) return fail(MOARA_E_ARG, "donor and receiver sets must both be empty or both non-empty");
+  if (r_base < 1) return fail(MOARA_E_ARG, "r_base must be >= 1");
+  if (delta_r < 0) return fail(MOARA_E_ARG, "delta_r must be >= 0");
+  const int64_t nd = __builtin_popcount(donor_mask), nr = __builtin_popcount(receiver_mask);
+  int64_t gain = 0;
+  if (nr) {
+    if (((int64_t)delta_r * nd) % nr != 0)
+      return fail(MOARA_E_RANK, "receiver share delta_r*|D|/|R| = %d*%lld/%lld is not an integer", delta_r, (long long)nd, (long long)nr);
+    gain = (int64_t)delta_r * nd / nr;
+  }
+  int32_t tmp[MOARA_NUM_MODULES];
+  for (int t = 0; t < MOARA_NUM_MODULES; ++t) {
+    int64_t r = 0;
+    if (types_mask & (1u << t)) {
+      if (donor_mask & (1u << t)) r = (int64_t)r_base - delta_r;
+      else if (receiver_mask & (1u << t)) r = (int64_t)r_base + gain;
+      else r = r_base;
+      if (r < 1) return fail(MOARA_E_RANK, "rank of module %d falls below 1", t);
+      if (r > INT32_MAX) return fail(MOARA_E_RANK, "rank of module %d overflows", t);
+    }
+    tmp[t] = (int32_t)r;
+  }
+  memcpy(out_rank_table, tmp, sizeof tmp);
+  return MOARA_OK;
+}
+
+int moara_resolve_matrix(const moara_config* cfg, const moara_matrix_desc* desc, int32_t* out_rank, int32_t* out_side) {
+  return resolve(cfg, desc, out_rank, out_side);
+}
+
+static int validate_all(const moara_config* cfg, const moara_matrix_desc* descs, int32_t n,
+                        std::vector<int32_t>* ranks, std::vector<int32_t>* sides) {
+  int rc = validate_config(cfg);
+  if (rc) return rc;
+  if (n < 1) return fail(MOARA_E_ARG, "n must be >= 1");
+  if (!descs) return fail(MOARA_E_ARG, "descs is NULL");
+  ranks->resize(n);
+  sides->resize(n);
+  for (int i = 0; i < n; ++i) {
+    rc = resolve(cfg, &descs[i], &(*ranks)[i], &(*sides)[i]);
+    if (rc) {
+      g_err = "matrix " + std::to_string(i) + ": " + g_err;
+      return rc;
+    }
+  }
+  return MOARA_OK;
+}
+
+int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, int32_t n, int64_t* out_state_bytes,
+                      int64_t* out_refresh_workspace_bytes) {
+  std::vector<int32_t> ranks, sides;
+  int rc = validate_all(cfg, descs, n, &ranks, &sides);
+  if (rc) return rc;
+  if (!out_state_bytes) return fail(MOARA_E_ARG, "out_state_bytes is NULL");
+  size_t tot = 0, ref = 0;
+  for (int i = 0; i < n; ++i) {
+    const Layout l = layout_of(descs[i], sides[i], cfg->block_size);
+    tot += mat_state_bytes(*cfg, descs[i].rows, l.s, l.L, l.k, ranks[i]);
+    ref += mat_refresh_bytes(l.s, l.L, subspace_width(*cfg, l.s, ranks[i]));
+  }
+  *out_state_bytes = (int64_t)tot;
+  if (out_refresh_workspace_bytes) *out_refresh_workspace_bytes = (int64_t)std::min(ref, REFRESH_BUDGET + ref / (size_t)n);
+  return MOARA_OK;
+}
+
+static void free_state(moara_state* st) {
+  if (!st) return;
+  if (st->block) hipFree(st->block);
+  if (st->dev_arena) hipFree(st->dev_arena);
+  if (st->host_ring) hipHostFree(st->host_ring);
+  if (st->ref_ws) hipFree(st->ref_ws);
+  if (st->ref_arena) hipFree(st->ref_arena);
+  if (st->ref_host) hipHostFree(st->ref_host);
+  for (auto& e : st->slot_ev)
+    if (e) hipEventDestroy(e);
+  for (auto& tl : st->pending) { hipEventDestroy(tl.a); hipEventDestroy(tl.b); }
+  for (auto e : st->ev_pool) hipEventDestroy(e);
+  delete st;
+}
+
+int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, int32_t n, void* stream,
+                       moara_state** out) {
+  if (!out) return fail(MOARA_E_ARG, "out is NULL");
+  *out = nullptr;
+  std::vector<int32_t> ranks, sides;
+  int rc = validate_all(cfg, descs, n, &ranks, &sides);
+  if (rc) return rc;
+  hipStream_t hs = (hipStream_t)stream;
+  moara_state* st = new moara_state();
+  st->cfg = *cfg;
+  st->n = n;
+  if (hipGetDevice(&st->device) != hipSuccess) { free_state(st); return fail(MOARA_E_HIP, "hipGetDevice failed (no GPU?)"); }
+  st->mats.resize(n);
+  size_t tot = 0;
+  for (int i = 0; i < n; ++i) {
+    const Layout l = layout_of(descs[i], sides[i], cfg->block_size);
+    MatHost& h = st->mats[i];
+    h.m = descs[i].rows; h.n = descs[i].cols; h.r = ranks[i]; h.side = sides[i];
+    h.s = l.s; h.L = l.L; h.k = (int32_t)l.k;
+    tot += mat_state_bytes(*cfg, h.m, h.s, h.L, h.k, h.r);
+  }
+  if (hipMalloc(&st->block, tot) != hipSuccess) { free_state(st); return fail(MOARA_E_OOM, "state of %zu bytes", tot); }
+  st->block_bytes = tot;
+  const int ob = elem_bytes(cfg->operand_dtype);
+  char* p = st->block;
+  auto take = [&](size_t b) { char* q = p; p += align_up(b); return q; };
+  for (auto& h : st->mats) {
+    h.inv = (float*)take(4 * h.m * h.k);
+    h.dM = (float*)take(4 * h.m * h.k);
+    h.mag1 = (float*)take(4 * h.m * h.k);
+    h.mag2 = (float*)take(4 * h.m * h.k);
+    h.exp1 = (float*)take(4 * h.L * h.r);
+    h.exp2 = (float*)take(4 * h.L * h.r);
+    h.N = take((size_t)ob * h.L * h.r);
+    h.P32 = (float*)take(4 * h.s * h.r);
+    h.Pop = take((size_t)ob * h.s * h.r);
+    h.Ptop = take((size_t)ob * h.s * h.r);
+  }
+  st->arena_bytes = align_up(sizeof(MatDev) * n) + 3 * align_up(sizeof(GemmProb) * n) + 4 * ALIGN;
+  if (hipMalloc(&st->dev_arena, st->arena_bytes) != hipSuccess ||
+      hipHostMalloc(&st->host_ring, st->arena_bytes * moara_state::NSLOT) != hipSuccess) {
+    free_state(st);
+    return fail(MOARA_E_OOM, "descriptor arenas");
+  }
+  for (auto& e : st->slot_ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) { free_state(st); return fail(MOARA_E_HIP, "event create"); }
+  if (hipMemsetAsync(st->block, 0, tot, hs) != hipSuccess || hipStreamSynchronize(hs) != hipSuccess) {
+    free_state(st);
+    return fail(MOARA_E_HIP, "zero fill of the state failed");
+  }
+  *out = st;
+  return MOARA_OK;
+}
+
+static int collect_active(moara_state* st, const void* const* ptrs, const uint8_t* active, std::vector<int>* idx,
+                          const char* what) {
+  idx->clear();
+  for (int i = 0; i < st->n; ++i) {
+    if (active && !active[i]) continue;
+    if (!ptrs[i]) return fail(MOARA_E_ARG, "%s[%d] is NULL for an active matrix", what, i);
+    idx->push_back(i);
+  }
+  return MOARA_OK;
+}
+
+int moara_refresh_projector(moara_state* st, const void* const* grads, const uint8_t* active, void* stream) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  if (!grads) return fail(MOARA_E_ARG, "grads is NULL");
+  std::vector<int> idx;
+  int rc = collect_active(st, grads, active, &idx, "grads");
+  if (rc) return rc;
+  return run_refresh(st, idx, grads, (hipStream_t)stream);
+}
+
+int moara_step(moara_state* st, void* const* weights, const void* const* grads, const uint8_t* active, float lr,
+               void* stream) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  if (!weights || !grads) return fail(MOARA_E_ARG, "weights/grads is NULL");
+  if (!isfinite(lr)) return fail(MOARA_E_ARG, "lr must be finite");
+  std::vector<int> idx;
+  int rc = collect_active(st, grads, active, &idx, "grads");
+  if (rc) return rc;
+  for (int i : idx)
+    if (!weights[i]) return fail(MOARA_E_ARG, "weights[%d] is NULL for an active matrix", i);
+  const int T = st->cfg.refresh_interval;
+  std::vector<int> need;
+  for (int i : idx) {
+    const MatHost& h = st->mats[i];
+    if (T > 0 && h.t % T == 0) need.push_back(i);
+    else if (!h.hasP) return fail(MOARA_E_STATE, "matrix %d has no projector (set one, refresh, or use refresh_interval > 0)", i);
+  }
+  if (idx.empty()) return MOARA_OK;
+  hipStream_t hs = (hipStream_t)stream;
+  if (st->cfg.decompose) {
+    rc = run_decompose(st, idx, grads, true, hs);
+    if (rc) return rc;
+  }
+  if (!need.empty()) {
+    std::vector<int> chunk;
+    size_t bytes = 0;
+    for (int i : need) {
+      const MatHost& h = st->mats[i];
+      const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r));
+      if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
+        if ((rc = refresh_chunk(st, chunk, grads, hs))) return rc;
+        chunk.clear();
+        bytes = 0;
+      }
+      chunk.push_back(i);
+      bytes += b;
+    }
+    if ((rc = refresh_chunk(st, chunk, grads, hs))) return rc;
+  }
+  rc = run_project_back(st, idx, weights, grads, lr, hs);
+  if (rc) return rc;
+  for (int i : idx) st->mats[i].t += 1;
+  return MOARA_OK;
+}
+
+static int tensor_geometry(moara_state* st, int32_t mat, int32_t which, size_t* bytes) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  if (mat < 0 || mat >= st->n) return fail(MOARA_E_ARG, "matrix index %d out of range", mat);
+  const MatHost& h = st->mats[mat];
+  switch (which) {
+    case MOARA_T_P: *bytes = 4 * h.s * h.r; break;
+    case MOARA_T_EXP_AVG:
+    case MOARA_T_EXP_AVG_SQ: *bytes = 4 * h.L * h.r; break;
+    case MOARA_T_MAG_AVG:
+    case MOARA_T_MAG_AVG_SQ: *bytes = 4 * h.m * h.k; break;
+    case MOARA_T_STEP: *bytes = 8; break;
+    default: return fail(MOARA_E_ARG, "unknown tensor id %d", which);
+  }
+  return MOARA_OK;
+}
+
+int moara_get_tensor(moara_state* st, int32_t mat, int32_t which, void* host_dst, size_t bytes, void* stream) {
+  size_t need = 0;
+  int rc = tensor_geometry(st, mat, which, &need);
+  if (rc) return rc;
+  if (!host_dst) return fail(MOARA_E_ARG, "host_dst is NULL");
+  if (bytes != need) return fail(MOARA_E_SHAPE, "buffer is %zu bytes, tensor needs %zu", bytes, need);
+  const MatHost& h = st->mats[mat];
+  if (which == MOARA_T_STEP) { memcpy(host_dst, &h.t, 8); return MOARA_OK; }
+  if (which == MOARA_T_P && !h.hasP) return fail(MOARA_E_STATE, "matrix %d has no projector yet", mat);
+  hipStream_t hs = (hipStream_t)stream;
+  const void* src = which == MOARA_T_P ? (const void*)h.P32
+                  : which == MOARA_T_EXP_AVG ? (const void*)h.exp1
+                  : which == MOARA_T_EXP_AVG_SQ ? (const void*)h.exp2
+                  : which == MOARA_T_MAG_AVG ? (const void*)h.mag1 : (const void*)h.mag2;
+  const bool transpose = (which == MOARA_T_EXP_AVG || which == MOARA_T_EXP_AVG_SQ) && h.side == MOARA_SIDE_LEFT;
+  HIP_TRY(hipStreamSynchronize(hs));
+  if (!transpose) {
+    HIP_TRY(hipMemcpyAsync(host_dst, src, need, hipMemcpyDeviceToHost, hs));
+    HIP_TRY(hipStreamSynchronize(hs));
+    return MOARA_OK;
+  }
+  std::vector<float> tmp((size_t)h.L * h.r);
+  HIP_TRY(hipMemcpyAsync(tmp.data(), src, need, hipMemcpyDeviceToHost, hs));
+  HIP_TRY(hipStreamSynchronize(hs));
+  float* o = (float*)host_dst;   // paper orientation r x n from the stored n x r
+  for (int64_t l = 0; l < h.L; ++l)
+    for (int64_t j = 0; j < h.r; ++j) o[j * h.L + l] = tmp[l * h.r + j];
+  return MOARA_OK;
+}
+
+int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* host_src, size_t bytes, void* stream) {
+  size_t need = 0;
+  int rc = tensor_geometry(st, mat, which, &need);
+  if (rc) return rc;
+  if (!host_src) return fail(MOARA_E_ARG, "host_src is NULL");
+  if (bytes != need) return fail(MOARA_E_SHAPE, "buffer is %zu bytes, tensor needs %zu", bytes, need);
+  MatHost& h = st->mats[mat];
+  if (which == MOARA_T_STEP) {
+    int64_t t;
+    memcpy(&t, host_src, 8);
+    if (t < 0) return fail(MOARA_E_ARG, "step counter must be >= 0");
+    h.t = t;
+    return MOARA_OK;
+  }
+  hipStream_t hs = (hipStream_t)stream;
+  void* dst = which == MOARA_T_P ? (void*)h.P32
+            : which == MOARA_T_EXP_AVG ? (void*)h.exp1
+            : which == MOARA_T_EXP_AVG_SQ ? (void*)h.exp2
+            : which == MOARA_T_MAG_AVG ? (void*)h.mag1 : (void*)h.mag2;
+  const bool transpose = (which == MOARA_T_EXP_AVG || which == MOARA_T_EXP_AVG_SQ) && h.side == MOARA_SIDE_LEFT;
+  std::vector<float> tmp;
+  const void* src = host_src;
+  if (transpose) {
+    tmp.resize((size_t)h.L * h.r);
+    const float* in = (const float*)host_src;
+    for (int64_t l = 0; l < h.L; ++l)
+      for (int64_t j = 0; j < h.r; ++j) tmp[l * h.r + j] = in[j * h.L + l];
+    src = tmp.data();
+  }
+  HIP_TRY(hipStreamSynchronize(hs));
+  HIP_TRY(hipMemcpyAsync(dst, src, need, hipMemcpyHostToDevice, hs));
+  if (which == MOARA_T_P) {
+    HIP_TRY(launch_convert_projector(h.P32, h.Pop, h.Ptop, h.s, h.r, st->cfg.operand_dtype == MOARA_BF16, hs));
+    h.hasP = true;
+  }
+  HIP_TRY(hipStreamSynchronize(hs));
+  return MOARA_OK;
+}
+
+int moara_set_timing(moara_state* st, int32_t enable) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  st->timing = enable != 0;
+  return MOARA_OK;
+}
+
+int moara_kernel_stats(moara_state* st, int32_t kernel, int64_t* out_launches, double* out_total_ms, void* stream) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  if (kernel < 0 || kernel >= MOARA_NUM_KERNELS) return fail(MOARA_E_ARG, "kernel id %d out of range", kernel);
+  int rc = collect_timing(st, (hipStream_t)stream);
+  if (rc) return rc;
+  if (out_launches) *out_launches = st->launches[kernel];
+  if (out_total_ms) *out_total_ms = st->total_ms[kernel];
+  return MOARA_OK;
+}
+
+int moara_reset_kernel_stats(moara_state* st, void* stream) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  int rc = collect_timing(st, (hipStream_t)stream);
+  if (rc) return rc;
+  for (int k = 0; k < MOARA_NUM_KERNELS; ++k) { st->launches[k] = 0; st->total_ms[k] = 0.0; }
+  return MOARA_OK;
+}
+
+int moara_matrix_info(const moara_state* st, int32_t mat, int64_t* rows, int64_t* cols, int32_t* rank, int32_t* side,
+                      int32_t* n_blocks) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  if (mat < 0 || mat >= st->n) return fail(MOARA_E_ARG, "matrix index %d out of range", mat);
+  const MatHost& h = st->mats[mat];
+  if (rows) *rows = h.m;
+  if (cols) *cols = h.n;
+  if (rank) *rank = h.r;
+  if (side) *side = h.side;
+  if (n_blocks) *n_blocks = h.k;
+  return MOARA_OK;
+}
+
+void moara_destroy_state(moara_state* st) {
+  if (!st) return;
+  hipDeviceSynchronize();
+  free_state(st);
+}
+
+const char* moara_last_error(void) { return g_err.c_str(); }
+
+const char* moara_version(void) { return "moara-mi355x 0.1 (gfx950)"; }
+
+}  // extern "C"

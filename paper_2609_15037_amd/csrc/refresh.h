@@ -1,0 +1,50 @@
+// Projector refresh (Algorithm 1: P <- TruncatedSVD(V, r)) kernels.
+#pragma once
+#include "common.h"
+
+// Per-matrix refresh descriptor (device array, one entry per refreshed matrix).
+struct RefDev {
+  int64_t s;          // projected dimension (rows of P)
+  int64_t L;          // other dimension
+  int32_t w;          // subspace width r + p (<= s)
+  int32_t wpad;       // w rounded up to a multiple of JB (Jacobi block)
+  int32_t r;
+  int32_t operand_bf16;
+  uint64_t seed;      // Philox key for the Gaussian start block
+  float* Z;           // s x w fp32 (iterate, row-major)
+  double* C;          // w x w fp64 Gram / Cholesky workspace
+  float* Rinv;        // w x w fp32 inverse Cholesky factor
+  double* Zc;         // wpad x s fp64, column-major copy of X^T Y for the Jacobi sweeps
+  float* P32;         // s x r fp32 master projector
+  void* Pop;          // s x r operand dtype
+  void* Ptop;         // r x s operand dtype
+  uint32_t* off;      // per-sweep max off-diagonal (float bits), >= n_sweeps entries
+  int32_t* order;     // wpad scratch: column order by norm
+  double* norms;      // wpad scratch
+  uint32_t tile_gauss, tile_jac, tile_cm;   // per-launch workgroup prefixes
+  int32_t has_prev;   // 1: a projector exists (an all-zero V keeps it)
+};
+
+constexpr int JB = 32;   // Jacobi column block; a pair holds 2*JB columns
+
+// Gram problem: C = A^T A for A (rows x w, row stride lda), fp64 accumulation.
+struct GramProb {
+  const float* A;
+  int64_t rows, lda;
+  double* C;
+  int32_t w, tiles;     // tiles per dimension (64-wide)
+  uint32_t tile_start, pad_;
+};
+
+hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st);
+hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st);
+hipError_t launch_chol_inv(const RefDev* d, int n, hipStream_t st);
+hipError_t launch_to_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st);
+hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st);
+hipError_t launch_finalize(const RefDev* d, int n, hipStream_t st);
+hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
+                                    int operand_bf16, hipStream_t st);
+uint32_t gauss_tiles(int64_t s, int32_t w);
+uint32_t gram_tiles(int32_t w);
+uint32_t jacobi_tiles(int32_t wpad);
+uint32_t colmajor_tiles(int64_t s, int32_t wpad);

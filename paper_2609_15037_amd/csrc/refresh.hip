@@ -1,0 +1,584 @@
+// Projector refresh kernels: P <- TruncatedSVD(V, r) (Algorithm 1).
+//
+// Method (randomised subspace iteration with Rayleigh-Ritz, all on the device):
+//   Z0 = seeded Gaussian s x w block (w = r + p), Z = orth(Z0)
+//   repeat q times:  Y = X Z;  Zn = X^T Y;  Z = orth(Zn)      (last time: Y = orth(Y) first)
+//   Rayleigh-Ritz:   one-sided Jacobi on Zn = X^T Y (fp64) orthogonalises its columns
+//                    into (right singular vectors of X) x (singular values); the r
+//                    columns of largest norm, normalised, are P.
+// X is V (RIGHT, s = n) or V^T (LEFT, s = m); the big GEMMs live in gemm.hip.
+// orth() is CholeskyQR with an fp64 Gram and an fp64 Cholesky factor.
+//
+// Kernels here: Philox-4x32-10 Gaussian start (Salmon et al., SC'11, with the
+// Box-Muller transform), fp64 Gram, per-matrix Cholesky + triangular inverse,
+// the Jacobi sweep rounds and the final ordering / sign fixing.
+#include "refresh.h"
+
+namespace {
+
+// ------------------------------------------------------------------ Philox 4x32-10
+__device__ __forceinline__ void philox_round(uint32_t c[4], uint32_t k[2]) {
+  const uint32_t M0 = 0xD2511F53u, M1 = 0xCD9E8D57u;
+  const uint32_t lo0 = M0 * c[0], hi0 = __umulhi(M0, c[0]);
+  const uint32_t lo1 = M1 * c[2], hi1 = __umulhi(M1, c[2]);
+  const uint32_t n0 = hi1 ^ c[1] ^ k[0], n2 = hi0 ^ c[3] ^ k[1];
+  c[0] = n0; c[1] = lo1; c[2] = n2; c[3] = lo0;
+  k[0] += 0x9E3779B9u; k[1] += 0xBB67AE85u;
+}
+
+__device__ __forceinline__ void philox4x32_10(uint32_t c[4], uint64_t key) {
+  uint32_t k[2] = {(uint32_t)key, (uint32_t)(key >> 32)};
+#pragma unroll
+  for (int i = 0; i < 10; ++i) philox_round(c, k);
+}
+
+__device__ __forceinline__ float u01(uint32_t x) {   // (0, 1]
+  return ((float)(x >> 8) + 1.0f) * (1.0f / 16777216.0f);
+}
+
+constexpr int GAUSS_PER_WG = 1024;   // elements (4 per thread)
+
+__global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, int n) {
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_gauss <= t) lo = mid; else hi = mid - 1; }
+  const RefDev& d = ds[lo];
+  const int64_t total = d.s * d.w;
+  const int64_t e0 = ((int64_t)(t - d.tile_gauss) * GAUSS_PER_WG) + threadIdx.x * 4;
+  if (e0 >= total) return;
+  uint32_t c[4] = {(uint32_t)(e0 >> 2), (uint32_t)(e0 >> 34), 0x4D6F4152u, 0x52656672u};
+  philox4x32_10(c, d.seed);
+  const float r0 = sqrtf(-2.0f * logf(u01(c[0]))), r1 = sqrtf(-2.0f * logf(u01(c[2])));
+  const float a0 = 6.283185307179586f * u01(c[1]), a1 = 6.283185307179586f * u01(c[3]);
+  float v[4] = {r0 * cosf(a0), r0 * sinf(a0), r1 * cosf(a1), r1 * sinf(a1)};
+  for (int q = 0; q < 4 && e0 + q < total; ++q) d.Z[e0 + q] = v[q];
+}
+
+// ------------------------------------------------------------------ fp64 Gram C = A^T A
+__global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, int n) {
+  __shared__ double Ai[32][64 + 1];
+  __shared__ double Aj[32][64 + 1];
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (gs[mid].tile_start <= t) lo = mid; else hi = mid - 1; }
+  const GramProb& g = gs[lo];
+  // linear index over the upper triangle (ti <= tj) of T x T tiles
+  int rem = (int)(t - g.tile_start), ti = 0;
+  while (rem >= g.tiles - ti) { rem -= g.tiles - ti; ++ti; }
+  const int tj = ti + rem;
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  double acc[4][4] = {};
+  for (int64_t l0 = 0; l0 < g.rows; l0 += 32) {
+    for (int e = threadIdx.x; e < 32 * 64; e += 256) {
+      const int l = e >> 6, c = e & 63;
+      const int64_t row = l0 + l;
+      const int ci = ti * 64 + c, cj = tj * 64 + c;
+      Ai[l][c] = (row < g.rows && ci < g.w) ? (double)g.A[row * g.lda + ci] : 0.0;
+      Aj[l][c] = (row < g.rows && cj < g.w) ? (double)g.A[row * g.lda + cj] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int l = 0; l < 32; ++l) {
+      double a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { a[q] = Ai[l][ty * 4 + q]; b[q] = Aj[l][tx * 4 + q]; }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = ti * 64 + ty * 4 + q, j = tj * 64 + tx * 4 + u;
+      if (i < g.w && j < g.w) {
+        g.C[(int64_t)i * g.w + j] = acc[q][u];
+        g.C[(int64_t)j * g.w + i] = acc[q][u];
+      }
+    }
+}
+
+// ------------------------------------------------------------------ Cholesky + inverse
+// One workgroup per matrix. C (w x w, fp64, symmetric) -> upper R with C = R^T R
+// (right-looking, 32-wide blocks staged in LDS), then R^{-1} by block columns,
+// written as fp32 Rinv (zeros below the diagonal). A pivot that is not above
+// 1e-13 * max(diag C) is raised to that floor (rank-deficient iterates stay finite).
+constexpr int CB = 32;
+
+__global__ __launch_bounds__(256) void k_chol_inv(const RefDev* __restrict__ ds) {
+  const RefDev& d = ds[blockIdx.x];
+  const int w = d.w;
+  double* C = d.C;
+  const int tid = threadIdx.x;
+  __shared__ double D[CB][CB + 1];
+  __shared__ double Pa[CB][CB + 1];
+  __shared__ double Pc[CB][CB + 1];
+  __shared__ double red[256];
+
+  // floor for pivots
+  double mx = 0.0;
+  for (int i = tid; i < w; i += 256) mx = fmax(mx, C[(int64_t)i * w + i]);
+  red[tid] = mx;
+  __syncthreads();
+  for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
+  const double cmax = red[0];
+  const double floor_piv = cmax * 1e-13;
+  __syncthreads();
+  if (!(cmax > 0.0)) {   // all-zero iterate (V == 0): leave it unscaled
+    for (int64_t e = tid; e < (int64_t)w * w; e += 256) d.Rinv[e] = (e / w == e % w) ? 1.f : 0.f;
+    return;
+  }
+
+  // ---- Cholesky
+  for (int k0 = 0; k0 < w; k0 += CB) {
+    const int kb = min(CB, w - k0);
+    for (int e = tid; e < kb * kb; e += 256) {
+      const int i = e / kb, j = e % kb;
+      D[i][j] = C[(int64_t)(k0 + i) * w + k0 + j];
+    }
+    __syncthreads();
+    for (int j = 0; j < kb; ++j) {
+      if (tid == 0) {
+        double v = D[j][j];
+        if (!(v > floor_piv)) v = floor_piv;
+        D[j][j] = sqrt(v);
+      }
+      __syncthreads();
+      if (tid > j && tid < kb) D[j][tid] /= D[j][j];
+      __syncthreads();
+      for (int e = tid; e < kb * kb; e += 256) {
+        const int a = e / kb, c = e % kb;
+        if (a > j && c >= a) D[a][c] -= D[j][a] * D[j][c];
+      }
+      __syncthreads();
+    }
+    for (int e = tid; e < kb * kb; e += 256) {
+      const int i = e / kb, j = e % kb;
+      C[(int64_t)(k0 + i) * w + k0 + j] = (j >= i) ? D[i][j] : 0.0;
+    }
+    // panel: rows k0..k0+kb, columns >= k0+kb : solve R_kk^T X = C_panel
+    for (int c = k0 + kb + tid; c < w; c += 256) {
+      double x[CB];
+#pragma unroll
+      for (int i = 0; i < CB; ++i) {
+        if (i < kb) {
+          double v = C[(int64_t)(k0 + i) * w + c];
+#pragma unroll
+          for (int t = 0; t < CB; ++t)
+            if (t < i) v -= D[t][i] * x[t];
+          x[i] = v / D[i][i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < CB; ++i)
+        if (i < kb) C[(int64_t)(k0 + i) * w + c] = x[i];
+    }
+    __syncthreads();
+    // trailing update of the upper triangle
+    const int s0 = k0 + kb;
+    const int T = (w - s0 + CB - 1) / CB;
+    for (int ta = 0; ta < T; ++ta)
+      for (int tc = ta; tc < T; ++tc) {
+        const int a0 = s0 + ta * CB, c0 = s0 + tc * CB;
+        for (int e = tid; e < kb * CB; e += 256) {
+          const int t = e / CB, x = e % CB;
+          Pa[t][x] = (a0 + x < w) ? C[(int64_t)(k0 + t) * w + a0 + x] : 0.0;
+          Pc[t][x] = (c0 + x < w) ? C[(int64_t)(k0 + t) * w + c0 + x] : 0.0;
+        }
+        __syncthreads();
+        const int ya = tid >> 3, xc = (tid & 7) * 4;
+        double s4[4] = {0, 0, 0, 0};
+        for (int t = 0; t < kb; ++t) {
+          const double pa = Pa[t][ya];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) s4[q] += pa * Pc[t][xc + q];
+        }
+        const int a = a0 + ya;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int c = c0 + xc + q;
+          if (a < w && c < w && c >= a) C[(int64_t)a * w + c] -= s4[q];
+        }
+        __syncthreads();
+      }
+  }
+
+  // ---- inverse of the upper triangular R (in place, by 32-wide block columns)
+  for (int j0 = 0; j0 < w; j0 += CB) {
+    const int jb = min(CB, w - j0);
+    for (int e = tid; e < jb * jb; e += 256) {
+      const int i = e / jb, j = e % jb;
+      D[i][j] = (j >= i) ? C[(int64_t)(j0 + i) * w + j0 + j] : 0.0;
+    }
+    __syncthreads();
+    // Dinv into Pa (upper), one thread per column
+    if (tid < jb) {
+      // column j of the inverse of the upper triangular diagonal block (back substitution)
+      const int j = tid;
+      double x[CB];
+#pragma unroll
+      for (int i = CB - 1; i >= 0; --i) {
+        double v = (i == j) ? 1.0 : 0.0;
+#pragma unroll
+        for (int t = 0; t < CB; ++t)
+          if (t > i && t <= j) v -= D[i][t] * x[t];
+        x[i] = (i <= j) ? v / D[i][i] : 0.0;
+      }
+#pragma unroll
+      for (int i = 0; i < CB; ++i) Pa[i][j] = x[i];
+    }
+    __syncthreads();
+    // T = R[0:j0][J] * Dinv, in place in C[0:j0][J]
+    for (int i = tid; i < j0; i += 256) {
+      double rr[CB];
+#pragma unroll
+      for (int t = 0; t < CB; ++t) rr[t] = (t < jb) ? C[(int64_t)i * w + j0 + t] : 0.0;
+#pragma unroll
+      for (int c = 0; c < CB; ++c) {
+        if (c < jb) {
+          double v = 0.0;
+#pragma unroll
+          for (int t = 0; t < CB; ++t)
+            if (t <= c) v += rr[t] * Pa[t][c];
+          C[(int64_t)i * w + j0 + c] = v;
+        }
+      }
+    }
+    __syncthreads();
+    // X[0:j0][J] = -X[0:j0][0:j0] * T, row tiles top to bottom (rows below still hold T)
+    for (int i0 = 0; i0 < j0; i0 += CB) {
+      const int ib = min(CB, j0 - i0);
+      const int yi = tid >> 3, xc = (tid & 7) * 4;
+      double s4[4] = {0, 0, 0, 0};
+      for (int t0 = i0; t0 < j0; t0 += CB) {
+        const int tb = min(CB, j0 - t0);
+        for (int e = tid; e < CB * CB; e += 256) {
+          const int a = e / CB, b = e % CB;
+          Pc[a][b] = (a < ib && b < tb) ? C[(int64_t)(i0 + a) * w + t0 + b] : 0.0;     // X[I][t-chunk]
+          D[a][b] = (a < tb && b < jb) ? C[(int64_t)(t0 + a) * w + j0 + b] : 0.0;      // T[t-chunk][J]
+        }
+        __syncthreads();
+        for (int t = 0; t < tb; ++t) {
+          const double xv = Pc[yi][t];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) s4[q] += xv * D[t][xc + q];
+        }
+        __syncthreads();
+      }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (yi < ib && xc + q < jb) C[(int64_t)(i0 + yi) * w + j0 + xc + q] = -s4[q];
+      __syncthreads();
+    }
+    for (int e = tid; e < jb * jb; e += 256) {
+      const int i = e / jb, j = e % jb;
+      C[(int64_t)(j0 + i) * w + j0 + j] = Pa[i][j];
+    }
+    __syncthreads();
+  }
+  for (int64_t e = tid; e < (int64_t)w * w; e += 256) {
+    const int64_t i = e / w, j = e % w;
+    d.Rinv[e] = (j >= i) ? (float)C[e] : 0.f;
+  }
+}
+
+// ------------------------------------------------------------------ Zn (s x w fp32) -> Zc (wpad x s fp64)
+__global__ __launch_bounds__(256) void k_to_colmajor(const RefDev* __restrict__ ds, int n) {
+  __shared__ float tile[32][33];
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_cm <= t) lo = mid; else hi = mid - 1; }
+  const RefDev& d = ds[lo];
+  const int64_t tiles_s = (d.s + 31) / 32;
+  const int64_t lt = t - d.tile_cm;
+  const int64_t ts = lt % tiles_s, tc = lt / tiles_s;
+  const int x = threadIdx.x & 31, y = threadIdx.x >> 5;
+  for (int yy = y; yy < 32; yy += 8) {
+    const int64_t row = ts * 32 + yy, col = tc * 32 + x;
+    tile[yy][x] = (row < d.s && col < d.w) ? d.Z[row * d.w + col] : 0.f;
+  }
+  __syncthreads();
+  for (int yy = y; yy < 32; yy += 8) {
+    const int64_t col = tc * 32 + yy, row = ts * 32 + x;
+    if (col < d.wpad && row < d.s) d.Zc[col * d.s + row] = (double)tile[x][yy];
+  }
+}
+
+// ------------------------------------------------------------------ one Jacobi round
+// Workgroup = (matrix, block pair). Blocks of JB columns are paired by the
+// circle method: over nb-1 rounds every pair of the nb blocks meets once.
+__device__ __forceinline__ int circle(int pos, int round, int nb) {
+  return pos == 0 ? 0 : 1 + ((pos - 1 + round) % (nb - 1));
+}
+
+constexpr int PW = 2 * JB;   // 64 columns per pair
+
+__global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
+  __shared__ double T[32][PW + 1];
+  __shared__ double Gm[PW][PW + 1];
+  __shared__ double Jm[PW][PW + 1];
+  __shared__ double cs[PW / 2], sn[PW / 2];
+  __shared__ int pp[PW / 2], qq[PW / 2];
+  __shared__ double red[256];
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_jac <= t) lo = mid; else hi = mid - 1; }
+  const RefDev& d = ds[lo];
+  const int nb = d.wpad / JB;
+  const int pair = (int)(t - d.tile_jac);
+  if (round >= nb - 1) return;   // this matrix has fewer blocks than the widest one
+  if (sweep > 0 && __uint_as_float(d.off[sweep - 1]) < 1e-13f) return;   // converged
+  const int ba = circle(pair, round, nb), bb = circle(nb - 1 - pair, round, nb);
+  const int tid = threadIdx.x;
+  const int64_t s = d.s;
+  auto colp = [&](int x) -> double* { return d.Zc + (int64_t)((x < JB) ? ba * JB + x : bb * JB + (x - JB)) * s; };
+
+  // (1) Gram of the 64 columns
+  const int tx = tid & 15, ty = tid >> 4;
+  double acc[4][4] = {};
+  for (int64_t r0 = 0; r0 < s; r0 += 32) {
+    for (int e = tid; e < 32 * PW; e += 256) {
+      const int x = e >> 5, l = e & 31;
+      T[l][x] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int l = 0; l < 32; ++l) {
+      double a[4], b[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) { a[q] = T[l][ty * 4 + q]; b[q] = T[l][tx * 4 + q]; }
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) Gm[ty * 4 + q][tx * 4 + u] = acc[q][u];
+  for (int e = tid; e < PW * PW; e += 256) Jm[e / PW][e % PW] = (e / PW == e % PW) ? 1.0 : 0.0;
+  __syncthreads();
+  // convergence measure of this pair (before rotating): max |g_xy| / sqrt(g_xx g_yy)
+  {
+    double m = 0.0;
+    for (int e = tid; e < PW * PW; e += 256) {
+      const int x = e / PW, y = e % PW;
+      if (x < y) {
+        const double den = sqrt(Gm[x][x] * Gm[y][y]);
+        if (den > 0.0) m = fmax(m, fabs(Gm[x][y]) / den);
+      }
+    }
+    red[tid] = m;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
+    if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)red[0]));
+    if (red[0] < 1e-15) return;   // already orthogonal: nothing to rotate (uniform branch)
+  }
+
+  // (2) eigen-decomposition of the 64 x 64 Gram by parallel cyclic Jacobi
+  for (int isw = 0; isw < 16; ++isw) {
+    double mloc = 0.0;
+    for (int rr = 0; rr < PW - 1; ++rr) {
+      if (tid < PW / 2) {
+        int p = circle(tid, rr, PW), q = circle(PW - 1 - tid, rr, PW);
+        if (p > q) { const int tmp = p; p = q; q = tmp; }
+        const double app = Gm[p][p], aqq = Gm[q][q], apq = Gm[p][q];
+        double c = 1.0, sv = 0.0;
+        const double den = sqrt(app * aqq);
+        if (den > 0.0 && fabs(apq) > 1e-16 * den) {
+          mloc = fmax(mloc, fabs(apq) / den);
+          const double zeta = (aqq - app) / (2.0 * apq);
+          const double tt = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+          c = 1.0 / sqrt(1.0 + tt * tt);
+          sv = c * tt;
+        }
+        pp[tid] = p; qq[tid] = q; cs[tid] = c; sn[tid] = sv;
+      }
+      __syncthreads();
+      for (int e = tid; e < (PW / 2) * PW; e += 256) {   // rows: G <- J^T G
+        const int k = e / PW, col = e % PW;
+        const int p = pp[k], q = qq[k];
+        const double c = cs[k], sv = sn[k];
+        const double gp = Gm[p][col], gq = Gm[q][col];
+        Gm[p][col] = c * gp - sv * gq;
+        Gm[q][col] = sv * gp + c * gq;
+      }
+      __syncthreads();
+      for (int e = tid; e < (PW / 2) * PW; e += 256) {   // columns: G <- G J, J <- J J
+        const int k = e / PW, row = e % PW;
+        const int p = pp[k], q = qq[k];
+        const double c = cs[k], sv = sn[k];
+        const double gp = Gm[row][p], gq = Gm[row][q];
+        Gm[row][p] = c * gp - sv * gq;
+        Gm[row][q] = sv * gp + c * gq;
+        const double jp = Jm[row][p], jq = Jm[row][q];
+        Jm[row][p] = c * jp - sv * jq;
+        Jm[row][q] = sv * jp + c * jq;
+      }
+      __syncthreads();
+    }
+    red[tid] = (tid < PW / 2) ? mloc : 0.0;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
+    const bool done = red[0] < 1e-15;
+    __syncthreads();
+    if (done) break;
+  }
+
+  // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J
+  for (int64_t r0 = 0; r0 < s; r0 += 32) {
+    for (int e = tid; e < 32 * PW; e += 256) {
+      const int x = e >> 5, l = e & 31;
+      T[l][x] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
+    }
+    __syncthreads();
+    for (int e = tid; e < 32 * PW; e += 256) {
+      const int x = e >> 5, l = e & 31;
+      double v = 0.0;
+      for (int y = 0; y < PW; ++y) v = fma(T[l][y], Jm[y][x], v);
+      if (r0 + l < s) colp(x)[r0 + l] = v;
+    }
+    __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------ finalize
+// One workgroup per matrix: column norms, order by decreasing norm, normalise
+// the first r, make each column's largest-magnitude entry positive (lowest index
+// on ties), write P (fp32 master and both operand copies). An all-zero iterate
+// (V == 0) keeps the previous projector, or yields the first r canonical basis
+// vectors when there is none; numerically null directions also fall back to e_j.
+__global__ __launch_bounds__(256) void k_finalize(const RefDev* __restrict__ ds) {
+  const RefDev& d = ds[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int64_t s = d.s;
+  __shared__ double red[256];
+  __shared__ int redi[256];
+  for (int c = 0; c < d.wpad; ++c) {
+    const double* col = d.Zc + (int64_t)c * s;
+    double a = 0.0;
+    for (int64_t i = tid; i < s; i += 256) a = fma(col[i], col[i], a);
+    red[tid] = a;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] += red[tid + o]; __syncthreads(); }
+    if (tid == 0) d.norms[c] = sqrt(red[0]);
+    __syncthreads();
+  }
+  for (int c = tid; c < d.wpad; c += 256) {
+    const double nc = d.norms[c];
+    int rank = 0;
+    for (int c2 = 0; c2 < d.wpad; ++c2) {
+      const double n2 = d.norms[c2];
+      rank += (n2 > nc) || (n2 == nc && c2 < c);
+    }
+    d.order[rank] = c;
+  }
+  __syncthreads();
+  const double nmax = d.norms[d.order[0]];
+  if (!(nmax > 0.0) && d.has_prev) return;   // V == 0: keep the previous projector
+  for (int j = 0; j < d.r; ++j) {
+    const int src = d.order[j];
+    const double nrm = d.norms[src];
+    const double* col = d.Zc + (int64_t)src * s;
+    const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
+    // sign: entry of largest magnitude, lowest index on ties
+    double best = -1.0;
+    int bi = 0;
+    for (int64_t i = tid; i < s; i += 256) {
+      const double v = deg ? (i == (j % s) ? 1.0 : 0.0) : fabs(col[i]);
+      if (v > best) { best = v; bi = (int)i; }
+    }
+    red[tid] = best;
+    redi[tid] = bi;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) {
+      if (tid < o) {
+        if (red[tid + o] > red[tid] || (red[tid + o] == red[tid] && redi[tid + o] < redi[tid])) {
+          red[tid] = red[tid + o];
+          redi[tid] = redi[tid + o];
+        }
+      }
+      __syncthreads();
+    }
+    const double sgn = deg ? 1.0 : ((col[redi[0]] < 0.0) ? -1.0 : 1.0);
+    const double scale = deg ? 0.0 : sgn / nrm;
+    for (int64_t i = tid; i < s; i += 256) {
+      const float v = deg ? (i == (j % s) ? 1.f : 0.f) : (float)(col[i] * scale);
+      d.P32[i * d.r + j] = v;
+      if (d.operand_bf16) {
+        ((bf16*)d.Pop)[i * d.r + j] = f2bf(v);
+        ((bf16*)d.Ptop)[(int64_t)j * s + i] = f2bf(v);
+      } else {
+        ((float*)d.Pop)[i * d.r + j] = v;
+        ((float*)d.Ptop)[(int64_t)j * s + i] = v;
+      }
+    }
+    __syncthreads();
+  }
+}
+
+__global__ __launch_bounds__(256) void k_convert_projector(const float* __restrict__ P32, void* Pop, void* Ptop,
+                                                           int64_t s, int64_t r, int bf) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e >= s * r) return;
+  const int64_t i = e / r, j = e % r;
+  const float v = P32[e];
+  if (bf) {
+    ((bf16*)Pop)[e] = f2bf(v);
+    ((bf16*)Ptop)[j * s + i] = f2bf(v);
+  } else {
+    ((float*)Pop)[e] = v;
+    ((float*)Ptop)[j * s + i] = v;
+  }
+}
+
+}  // namespace
+
+uint32_t gauss_tiles(int64_t s, int32_t w) { return (uint32_t)((s * w + GAUSS_PER_WG - 1) / GAUSS_PER_WG); }
+uint32_t gram_tiles(int32_t w) { const int T = (w + 63) / 64; return (uint32_t)(T * (T + 1) / 2); }
+uint32_t jacobi_tiles(int32_t wpad) { return (uint32_t)(wpad / JB / 2); }
+uint32_t colmajor_tiles(int64_t s, int32_t wpad) { return (uint32_t)(((s + 31) / 32) * (wpad / 32)); }
+
+hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_gauss, dim3(total), dim3(256), 0, st, d, n);
+  return hipGetLastError();
+}
+hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_gram, dim3(total), dim3(256), 0, st, g, n);
+  return hipGetLastError();
+}
+hipError_t launch_chol_inv(const RefDev* d, int n, hipStream_t st) {
+  if (!n) return hipSuccess;
+  hipLaunchKernelGGL(k_chol_inv, dim3(n), dim3(256), 0, st, d);
+  return hipGetLastError();
+}
+hipError_t launch_to_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_to_colmajor, dim3(total), dim3(256), 0, st, d, n);
+  return hipGetLastError();
+}
+hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_jacobi_round, dim3(total), dim3(256), 0, st, d, n, round, sweep);
+  return hipGetLastError();
+}
+hipError_t launch_finalize(const RefDev* d, int n, hipStream_t st) {
+  if (!n) return hipSuccess;
+  hipLaunchKernelGGL(k_finalize, dim3(n), dim3(256), 0, st, d);
+  return hipGetLastError();
+}
+hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
+                                    int operand_bf16, hipStream_t st) {
+  const int64_t total = s * r;
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_convert_projector, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st, P32, Pop, Ptop,
+                     s, r, operand_bf16);
+  return hipGetLastError();
+}

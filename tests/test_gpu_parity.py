@@ -1,0 +1,301 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, element by element.
+
+Tolerances: max floored relative error 1e-4 when weights and GEMM operands are
+fp32; 2e-2 when bf16 operands or bf16 weights are used (the oracle then applies
+the same bf16 roundings of V, P, N and of the update). Projector refreshes are
+compared by principal angles (<= 1e-3 rad), since singular vectors are only
+defined up to sign and rotation within (near-)degenerate clusters.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import workloads as WL
+from oracle import moara_oracle as O
+from tests.harness import (TOL_BF16, TOL_F32, TOL_UPDATE_F32, Case, case_from_workload, compare, compare_update,
+                           gpu_state, have_gpu, adam_sensitivity, oracle_cfg, oracle_projector, rng, slices_of,
+                           to_dev, to_np)
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not have_gpu(), reason="needs an MI355X GPU")]
+
+
+def _M():
+    from paper_2609_15037_amd import moara as M
+    return M
+
+
+def _grad(c: Case, seed, step, i):
+    m, n, _ = c.shapes[i]
+    return (c.grad_std * rng(seed, 2, step, i).standard_normal((m, n))).astype(np.float32)
+
+
+def _weights(c: Case, seed):
+    return [(c.weight_std * rng(seed, 1, i).standard_normal((m, n))).astype(np.float32)
+            for i, (m, n, _) in enumerate(c.shapes)]
+
+
+def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=False):
+    import torch
+    M = _M()
+    tol = TOL_F32 if (c.weight_dtype == "f32" and c.operand_dtype == "f32") else TOL_BF16
+    n = len(c.shapes)
+    grad_fn = grad_fn or (lambda t, i: _grad(c, seed, t, i))
+    st = gpu_state(c)
+    Wd = [to_dev(w, c.weight_dtype) for w in _weights(c, seed)]
+    W0 = [to_np(w) for w in Wd]
+    Wo = [w.copy() for w in W0]
+    ocfg = [oracle_cfg(c, i) for i in range(n)]
+    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[i]) for i in range(n)]
+    report = {}
+    masks = [np.zeros(c.shapes[i][:2], dtype=bool) for i in range(n)]     # W check (dN > 0.1)
+    masks_u = [np.zeros(c.shapes[i][:2], dtype=bool) for i in range(n)]   # update check (dN > 0.01)
+    for t in range(steps):
+        Gs = [grad_fn(t, i) for i in range(n)]
+        if t == 0:
+            for i in range(n):
+                P = oracle_projector(Gs[i], c, i)
+                M.moara_set_tensor(st, i, M.MOARA_T_P, P)
+                ost[i].P = P
+        Gd = [to_dev(g, "f32") for g in Gs]
+        print(f"[parity] step {t} n={n} B={c.block_size} op={c.operand_dtype} w={c.weight_dtype}", flush=True)
+        M.moara_step(st, Wd, Gd, lr=c.lr)
+        for i in range(n):
+            Wo[i] = O.step(Wo[i], Gs[i], ost[i], ocfg[i], c.lr)
+            V = O.decompose(Gs[i], c.block_size)[1] if c.decompose else Gs[i].astype(np.float64)
+            dN = adam_sensitivity(V, ost[i].P, ost[i].side, ost[i].exp_avg_sq, ost[i].t, c.beta2, c.adam_eps)
+            masks[i] |= slices_of(dN > 0.1, ost[i].side, c.shapes[i][:2])
+            masks_u[i] |= slices_of(dN > 0.01, ost[i].side, c.shapes[i][:2])
+        torch.cuda.synchronize()
+        if check_every or t == steps - 1:
+            for i in range(n):
+                Wg = to_np(Wd[i])
+                compare(f"W[{i}]", Wg, Wo[i], tol, report, masks[i])
+                if c.weight_dtype == "f32":
+                    compare_update(f"dW[{i}]", Wg - W0[i], Wo[i] - W0[i], max(tol, TOL_UPDATE_F32), report, masks_u[i])
+                compare(f"exp_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG), ost[i].exp_avg, tol, report)
+                compare(f"exp_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG_SQ), ost[i].exp_avg_sq, tol, report)
+                if c.decompose:
+                    compare(f"mag_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG), ost[i].mag_avg, tol, report)
+                    compare(f"mag_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG_SQ), ost[i].mag_avg_sq, tol, report)
+                assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == t + 1
+    worst = max(v for k, v in report.items() if not k.endswith("masked_frac"))
+    masked = max([v for k, v in report.items() if k.endswith("masked_frac")] or [0.0])
+    print(f"[parity] worst floored rel err {worst:.3e} (tol {tol:.0e}); update elements masked as "
+          f"ill-conditioned {masked:.1e}", flush=True)
+    return report
+
+
+# ------------------------------------------------------------------ step parity
+
+def test_layer_d256_fp32_ten_steps():
+    c = case_from_workload(WL.WORKLOADS["layer_d256"], operand_dtype="f32")
+    step_parity(c, 10, check_every=True)
+
+
+def test_layer_d256_bf16_operands():
+    c = case_from_workload(WL.WORKLOADS["layer_d256"], operand_dtype="bf16")
+    rep = step_parity(c, 10)
+    # the oracle rounds the same operands to bf16, so the moments agree far below the bar
+    assert max(v for k, v in rep.items() if k.startswith("exp_avg")) < 1e-3
+
+
+def test_llama300m_layers_bf16():
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [0, 23])
+    c = case_from_workload(wl)
+    step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t))
+
+
+def test_llama300m_layer_fp32_operands():
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [5])
+    c = case_from_workload(wl, operand_dtype="f32")
+    c.weight_dtype = "f32"
+    c.weight_std = 0.02
+    step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t))
+
+
+@pytest.mark.parametrize("B", [48, 20, 1, 256, 1000])
+def test_ragged_shapes_and_block_sizes(B):
+    # several tiles in every dimension plus ragged tails; n % 4 != 0 forces scalar loads
+    c = Case(shapes=[(300, 452, WL.Q), (452, 300, WL.GATE), (129, 1000, WL.DOWN), (77, 130, WL.K), (5, 3, WL.V)],
+             ranks=[37, 50, 64, 9, 2], block_size=B)
+    step_parity(c, 3)
+
+
+@pytest.mark.parametrize("op", ["f32", "bf16"])
+def test_ragged_bf16_weights(op):
+    c = Case(shapes=[(300, 452, WL.Q), (452, 300, WL.GATE), (200, 136, WL.UP)], ranks=[40, 33, 136],
+             block_size=64, weight_dtype="bf16", operand_dtype=op, weight_std=0.02)
+    step_parity(c, 3)
+
+
+def test_decompose_off_is_galore_direction():
+    c = Case(shapes=[(256, 384, WL.Q), (384, 256, WL.UP)], ranks=[32, 48], block_size=64, decompose=False)
+    step_parity(c, 4)
+
+
+# ------------------------------------------------------------------ refresh
+
+def _angles_vs_oracle(c: Case, Gs, P_gpu_list, bar=1e-3):
+    worst = 0.0
+    for i, G in enumerate(Gs):
+        _, V = O.decompose(G, c.block_size)
+        side = O.projection_side(*G.shape)
+        ref = O.truncated_svd(V, c.ranks[i], side)
+        Pg = P_gpu_list[i].astype(np.float64)
+        assert Pg.shape == ref.shape
+        np.testing.assert_allclose(Pg.T @ Pg, np.eye(Pg.shape[1]), atol=2e-5)
+        ang = O.max_principal_angle(Pg, ref)
+        worst = max(worst, ang)
+        assert ang <= bar, f"matrix {i}: principal angle {ang:.2e} rad"
+        # ordering: the Ritz values follow the singular values
+        sv = np.linalg.svd(V, compute_uv=False)[: c.ranks[i]]
+        X = V if side == O.RIGHT else V.T
+        ritz = np.linalg.norm(X @ Pg, axis=0)
+        np.testing.assert_allclose(ritz, sv, rtol=1e-3)
+    return worst
+
+
+def test_refresh_layer_d256_principal_angles():
+    import torch
+    M = _M()
+    c = case_from_workload(WL.WORKLOADS["layer_d256"])
+    st = gpu_state(c)
+    Gs = [_grad(c, 3, 0, i) for i in range(len(c.shapes))]
+    print("[refresh] layer_d256", flush=True)
+    M.moara_refresh_projector(st, [to_dev(g, "f32") for g in Gs])
+    torch.cuda.synchronize()
+    Ps = [M.moara_get_tensor(st, i, M.MOARA_T_P) for i in range(len(Gs))]
+    worst = _angles_vs_oracle(c, Gs, Ps)
+    print(f"[refresh] worst principal angle {worst:.2e}", flush=True)
+
+
+def test_refresh_lowrank_llama300m_layer():
+    import torch
+    M = _M()
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [0])
+    c = case_from_workload(wl)
+    st = gpu_state(c)
+    Gs = [WL.grad_np(wl, i, 0) for i in range(len(wl.matrices))]
+    print("[refresh] llama_300m layer 0", flush=True)
+    M.moara_refresh_projector(st, [to_dev(g, "f32") for g in Gs])
+    torch.cuda.synchronize()
+    Ps = [M.moara_get_tensor(st, i, M.MOARA_T_P) for i in range(len(Gs))]
+    worst = _angles_vs_oracle(c, Gs, Ps)
+    print(f"[refresh] worst principal angle {worst:.2e}", flush=True)
+
+
+def test_refresh_inside_step_schedule():
+    import torch
+    M = _M()
+    c = Case(shapes=[(96, 160, WL.Q), (160, 96, WL.GATE)], ranks=[16, 24], block_size=32)
+    st = gpu_state(c, refresh_interval=2)
+    Wd = [to_dev(w, "f32") for w in _weights(c, 0)]
+    seen = []
+    for t in range(4):
+        Gs = [_grad(c, 5, t, i) for i in range(2)]
+        M.moara_step(st, Wd, [to_dev(g, "f32") for g in Gs], lr=1e-3)
+        torch.cuda.synchronize()
+        Ps = [M.moara_get_tensor(st, i, M.MOARA_T_P) for i in range(2)]
+        if t in (0, 2):
+            _angles_vs_oracle(c, Gs, Ps)
+        seen.append(Ps)
+    for i in range(2):
+        assert np.array_equal(seen[0][i], seen[1][i]) and np.array_equal(seen[2][i], seen[3][i])
+        assert not np.array_equal(seen[1][i], seen[2][i])
+
+
+def test_zero_gradient_refresh_keeps_previous_projector():
+    import torch
+    M = _M()
+    c = Case(shapes=[(64, 96, WL.Q)], ranks=[8], block_size=32)
+    st = gpu_state(c)
+    with pytest.raises(M.MoaraError):
+        M.moara_get_tensor(st, 0, M.MOARA_T_P)
+    Z = torch.zeros(64, 96, device="cuda")
+    M.moara_refresh_projector(st, [Z])
+    P0 = M.moara_get_tensor(st, 0, M.MOARA_T_P)
+    np.testing.assert_array_equal(P0, np.eye(64, 8, dtype=np.float32))
+    G = to_dev(_grad(c, 1, 0, 0), "f32")
+    M.moara_refresh_projector(st, [G])
+    P1 = M.moara_get_tensor(st, 0, M.MOARA_T_P)
+    M.moara_refresh_projector(st, [Z])
+    np.testing.assert_array_equal(M.moara_get_tensor(st, 0, M.MOARA_T_P), P1)
+
+
+# ------------------------------------------------------------------ state handling
+
+def test_inactive_matrices_are_untouched():
+    import torch
+    M = _M()
+    c = Case(shapes=[(128, 192, WL.EXP_GATE), (128, 192, WL.EXP_UP), (192, 128, WL.EXP_DOWN)], ranks=[16] * 3,
+             block_size=64)
+    st = gpu_state(c, refresh_interval=3)
+    Wd = [to_dev(w, "f32") for w in _weights(c, 0)]
+    act = np.array([1, 0, 1], dtype=np.uint8)
+    before = to_np(Wd[1]).copy()
+    for t in range(4):
+        Gs = [to_dev(_grad(c, 2, t, i), "f32") for i in range(3)]
+        M.moara_step(st, Wd, Gs, lr=1e-3, active=act)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(to_np(Wd[1]), before)
+    assert M.moara_get_tensor(st, 1, M.MOARA_T_STEP) == 0
+    assert M.moara_get_tensor(st, 0, M.MOARA_T_STEP) == 4
+    assert not np.any(M.moara_get_tensor(st, 1, M.MOARA_T_EXP_AVG))
+
+
+def test_checkpoint_roundtrip_is_bit_identical():
+    import torch
+    M = _M()
+    c = Case(shapes=[(160, 224, WL.Q), (224, 160, WL.UP)], ranks=[24, 32], block_size=32, weight_dtype="bf16",
+             operand_dtype="bf16", weight_std=0.02)
+    grads = [[to_dev(_grad(c, 9, t, i), "f32") for i in range(2)] for t in range(6)]
+    st = gpu_state(c, refresh_interval=4)
+    Wa = [to_dev(w, "bf16") for w in _weights(c, 0)]
+    for t in range(6):
+        M.moara_step(st, Wa, grads[t], lr=1e-3)
+    st1 = gpu_state(c, refresh_interval=4)
+    Wb = [to_dev(w, "bf16") for w in _weights(c, 0)]
+    for t in range(3):
+        M.moara_step(st1, Wb, grads[t], lr=1e-3)
+    saved = {(i, k): M.moara_get_tensor(st1, i, k) for i in range(2)
+             for k in (M.MOARA_T_P, M.MOARA_T_EXP_AVG, M.MOARA_T_EXP_AVG_SQ, M.MOARA_T_MAG_AVG,
+                       M.MOARA_T_MAG_AVG_SQ, M.MOARA_T_STEP)}
+    M.moara_destroy_state(st1)
+    st2 = gpu_state(c, refresh_interval=4)
+    for (i, k), v in saved.items():
+        M.moara_set_tensor(st2, i, k, v)
+    for t in range(3, 6):
+        M.moara_step(st2, Wb, grads[t], lr=1e-3)
+    torch.cuda.synchronize()
+    for i in range(2):
+        assert torch.equal(Wa[i], Wb[i])
+
+
+def test_runs_are_deterministic():
+    import torch
+    M = _M()
+    c = Case(shapes=[(256, 384, WL.Q), (384, 256, WL.GATE)], ranks=[32, 48], block_size=64)
+    outs = []
+    for _ in range(2):
+        st = gpu_state(c, refresh_interval=2)
+        Wd = [to_dev(w, "f32") for w in _weights(c, 0)]
+        for t in range(3):
+            M.moara_step(st, Wd, [to_dev(_grad(c, 4, t, i), "f32") for i in range(2)], lr=1e-3)
+        torch.cuda.synchronize()
+        outs.append([w.clone() for w in Wd])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
+def test_step_without_projector_is_rejected_before_launch():
+    import torch
+    M = _M()
+    c = Case(shapes=[(64, 64, WL.Q)], ranks=[8], block_size=32)
+    st = gpu_state(c, refresh_interval=0)
+    W = to_dev(_weights(c, 0)[0], "f32")
+    with pytest.raises(M.MoaraError) as e:
+        M.moara_step(st, [W], [to_dev(_grad(c, 0, 0, 0), "f32")], lr=1e-3)
+    assert e.value.status == M.MOARA_E_STATE
+    with pytest.raises(ValueError):
+        M.moara_step(st, [W.t()], [to_dev(_grad(c, 0, 0, 0), "f32")], lr=1e-3)

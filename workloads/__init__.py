@@ -72,6 +72,8 @@ class Workload:
     moe_routed: int = 0
     moe_active: int = 0
     n_layers: int = 1
+    refresh_oversample: int = -1           # subspace-iteration oversampling p (-1: p = r)
+    refresh_iters: int = 20                # subspace-iteration sweeps q
 
     @property
     def n_params(self) -> int:
@@ -131,7 +133,8 @@ def build_workloads() -> dict:
         matrices=_stack(1, _dense_layer, 256, 688),
         rank_table=_ranks(q=64, k=64, v=64, o=64, gate=32, up=32, down=32),
         block_size=64, weight_dtype="f32", operand_dtype="f32",
-        weight_std=1e-3, grad_recipe="iid", grad_std=1e-3, steps=10, n_layers=1)
+        weight_std=1e-3, grad_recipe="iid", grad_std=1e-3, steps=10, n_layers=1,
+        refresh_oversample=96, refresh_iters=20)
     w["llama_300m"] = Workload(
         name="llama_300m",
         description="Llama-300M-shaped stack: 24 layers d=1024 ffn=2736, bf16 weights, rank-64 1/i gradients",
