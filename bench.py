@@ -43,6 +43,9 @@ def parse():
     ap.add_argument("--refresh-reps", type=int, default=1)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-layers", type=int, default=1)
+    ap.add_argument("--layers", type=int, default=None, help="use only the first N layers (profiling runs)")
+    ap.add_argument("--refresh-iters", type=int, default=None,
+                    help="override the subspace-iteration count (the default is the workload's)")
     return ap.parse_args()
 
 
@@ -125,6 +128,8 @@ def main():
     from paper_2609_15037_amd import moara as M
 
     wl = WL.WORKLOADS[a.workload]
+    if a.layers:
+        wl = WL.subset(wl, list(range(a.layers)))
     operand = a.operand or wl.operand_dtype
     ob = 2 if operand == "bf16" else 4
     wb = 2 if wl.weight_dtype == "bf16" else 4
@@ -151,7 +156,8 @@ def main():
         adam_eps=wl.adam_eps, scale=wl.scale, refresh_interval=0,
         weight_dtype=M.MOARA_BF16 if wl.weight_dtype == "bf16" else M.MOARA_F32,
         operand_dtype=M.MOARA_BF16 if operand == "bf16" else M.MOARA_F32,
-        refresh_oversample=wl.refresh_oversample, refresh_iters=wl.refresh_iters)
+        refresh_oversample=wl.refresh_oversample,
+        refresh_iters=a.refresh_iters if a.refresh_iters else wl.refresh_iters)
     descs = M.make_descs([(m.rows, m.cols, m.module) for m in wl.matrices])
     stream = torch.cuda.current_stream()
     st = M.moara_create_state(cfg, descs, stream=stream)
@@ -224,7 +230,8 @@ def main():
                  "avg_launch_ms": dk["ms_total"] / max(1, dk["launches"]),
                  "traffic": None})
 
-    rf = refresh_flops(wl, wl.refresh_oversample, wl.refresh_iters)
+    q_used = a.refresh_iters if a.refresh_iters else wl.refresh_iters
+    rf = refresh_flops(wl, wl.refresh_oversample, q_used)
     ref_med = float(np.median(ref_ms))
     out = {
         "metric": "params updated/sec per optimizer step at Llama-2-7B shapes; ms per projector refresh",
@@ -238,7 +245,7 @@ def main():
                    "rank_table": list(wl.rank_table[:7] if wl.moe_routed == 0 else wl.rank_table),
                    "block_size": wl.block_size, "weights": wl.weight_dtype, "grads": "f32", "moments": "f32",
                    "gemm_operands": operand, "refresh": {"oversample": wl.refresh_oversample,
-                                                         "iters": wl.refresh_iters}},
+                                                         "iters": q_used}},
         "ms_per_refresh": ref_med,
         "refresh_tflops": rf / (ref_med / 1e3) / 1e12,
         "refresh_frac_fp32_peak": rf / (ref_med / 1e3) / PEAK_F32,

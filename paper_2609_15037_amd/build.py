@@ -18,7 +18,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libmoara.so")
-SOURCES = ["decompose.hip", "gemm.hip", "refresh.hip", "moara_api.hip"]
+SOURCES = ["decompose.hip", "gemm.hip", "refresh.hip", "chol.hip", "moara_api.hip"]
 
 
 def hipcc() -> str:

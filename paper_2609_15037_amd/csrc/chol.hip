@@ -1,0 +1,248 @@
+// Blocked Cholesky factorisation and triangular inverse of the fp64 Gram
+// matrices of a refresh batch (CholeskyQR: Z = Q R with R^T R = Z^T Z, then
+// Q = Z R^{-1}). 64 x 64 blocks; every launch covers all matrices of the batch:
+//   for each panel k:  diag(k)   factor C_kk = R_kk^T R_kk and invert R_kk (one WG per matrix)
+//                      panel(k)  R_kj = R_kk^{-T} C_kj for j > k           (one WG per block)
+//                      update(k) C_ac -= R_ka^T R_kc for k < a <= c        (one WG per block)
+//   for each block column J:  X_IJ = -(sum_{I<=t<J} X_It R_tJ) X_JJ for I < J  (one WG per block)
+// with X = R^{-1}. Pivots not above 1e-13 * max(diag C) are raised to that floor
+// so rank-deficient iterates stay finite; an all-zero Gram gives R = I.
+#include "refresh.h"
+
+namespace {
+
+constexpr int NB = 64;
+constexpr int LDB = NB + 1;
+
+__device__ __forceinline__ int find_pref(const uint32_t* pref, int n, uint32_t t) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (pref[mid] <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+__device__ __forceinline__ int nblk(int w) { return (w + NB - 1) / NB; }
+__device__ __forceinline__ int bsz(int w, int b) { return min(NB, w - b * NB); }
+
+// load a kb_r x kb_c block (zero padded to 64 x 64) of a w x w row-major matrix into LDS
+__device__ __forceinline__ void load_blk(double (*dst)[LDB], const double* M, int w, int br, int bc) {
+  const int r0 = br * NB, c0 = bc * NB;
+  for (int e = threadIdx.x; e < NB * NB; e += 256) {
+    const int i = e >> 6, j = e & 63;
+    dst[i][j] = (r0 + i < w && c0 + j < w) ? M[(int64_t)(r0 + i) * w + c0 + j] : 0.0;
+  }
+}
+
+// out[x][y] += sum_t A[t][x] * B[t][y]   (A, B in LDS, 64 x 64); thread owns a 4 x 4 block
+__device__ __forceinline__ void atb_acc(const double (*A)[LDB], const double (*Bm)[LDB], double (&acc)[4][4]) {
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+#pragma unroll 4
+  for (int t = 0; t < NB; ++t) {
+    double a[4], b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) { a[q] = A[t][ty * 4 + q]; b[q] = Bm[t][tx * 4 + q]; }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
+  }
+}
+
+// out[x][y] += sum_t A[x][t] * B[t][y]
+__device__ __forceinline__ void ab_acc(const double (*A)[LDB], const double (*Bm)[LDB], double (&acc)[4][4]) {
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+#pragma unroll 4
+  for (int t = 0; t < NB; ++t) {
+    double a[4], b[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) { a[q] = A[ty * 4 + q][t]; b[q] = Bm[t][tx * 4 + q]; }
+#pragma unroll
+    for (int q = 0; q < 4; ++q)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds, int k) {
+  const RefDev& d = ds[blockIdx.x];
+  const int w = d.w;
+  if (k >= nblk(w)) return;
+  __shared__ double D[NB][LDB];
+  __shared__ double Xi[NB][LDB];
+  __shared__ double red[256];
+  const int tid = threadIdx.x;
+  if (k == 0) {   // pivot floor from the diagonal of the untouched Gram
+    double mx = 0.0;
+    for (int i = tid; i < w; i += 256) mx = fmax(mx, d.C[(int64_t)i * w + i]);
+    red[tid] = mx;
+    __syncthreads();
+    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
+    if (tid == 0) d.cmax[0] = red[0];
+    __syncthreads();
+  }
+  const double cmax = (k == 0) ? red[0] : d.cmax[0];
+  const bool zero = !(cmax > 0.0);
+  const double floor_piv = cmax * 1e-13;
+  const int kb = bsz(w, k);
+  load_blk(D, d.C, w, k, k);
+  __syncthreads();
+  if (zero) {
+    for (int e = tid; e < NB * NB; e += 256) { const int i = e >> 6, j = e & 63; D[i][j] = (i == j) ? 1.0 : 0.0; }
+    __syncthreads();
+  } else {
+    for (int j = 0; j < kb; ++j) {
+      if (tid == 0) {
+        double v = D[j][j];
+        if (!(v > floor_piv)) v = floor_piv;
+        D[j][j] = sqrt(v);
+      }
+      __syncthreads();
+      if (tid > j && tid < kb) D[j][tid] /= D[j][j];
+      __syncthreads();
+      for (int e = tid; e < kb * kb; e += 256) {
+        const int a = e / kb, c = e % kb;
+        if (a > j && c >= a) D[a][c] -= D[j][a] * D[j][c];
+      }
+      __syncthreads();
+    }
+  }
+  // inverse of the upper triangular D (back substitution, one thread per column)
+  if (tid < kb) {
+    const int j = tid;
+    for (int i = NB - 1; i >= 0; --i) Xi[i][j] = 0.0;
+    Xi[j][j] = 1.0 / D[j][j];
+    for (int i = j - 1; i >= 0; --i) {
+      double v = 0.0;
+      for (int t = i + 1; t <= j; ++t) v += D[i][t] * Xi[t][j];
+      Xi[i][j] = -v / D[i][i];
+    }
+  }
+  __syncthreads();
+  const int r0 = k * NB;
+  for (int e = tid; e < kb * kb; e += 256) {
+    const int i = e / kb, j = e % kb;
+    const int64_t g = (int64_t)(r0 + i) * w + r0 + j;
+    const bool up = j >= i;
+    d.C[g] = up ? D[i][j] : 0.0;
+    d.X[g] = up ? Xi[i][j] : 0.0;
+    d.Rinv[g] = up ? (float)Xi[i][j] : 0.f;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_chol_panel(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
+                                                    int n, int k) {
+  const uint32_t t = blockIdx.x;
+  const int mi = find_pref(pref, n, t);
+  const RefDev& d = ds[mi];
+  const int w = d.w;
+  const int j = k + 1 + (int)(t - pref[mi]);
+  __shared__ double Xk[NB][LDB];
+  __shared__ double Cb[NB][LDB];
+  load_blk(Xk, d.X, w, k, k);
+  load_blk(Cb, d.C, w, k, j);
+  __syncthreads();
+  double acc[4][4] = {};
+  atb_acc(Xk, Cb, acc);   // (X_kk)^T C_kj
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  const bool zero = !(d.cmax[0] > 0.0);
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = k * NB + ty * 4 + q, c = j * NB + tx * 4 + u;
+      if (r < w && c < w) d.C[(int64_t)r * w + c] = zero ? 0.0 : acc[q][u];
+    }
+}
+
+__global__ __launch_bounds__(256) void k_chol_update(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
+                                                     int n, int k) {
+  const uint32_t t = blockIdx.x;
+  const int mi = find_pref(pref, n, t);
+  const RefDev& d = ds[mi];
+  const int w = d.w;
+  const int T = nblk(w) - k - 1;
+  int rem = (int)(t - pref[mi]), ta = 0;
+  while (rem >= T - ta) { rem -= T - ta; ++ta; }
+  const int a = k + 1 + ta, c = a + rem;
+  __shared__ double Ra[NB][LDB];
+  __shared__ double Rc[NB][LDB];
+  load_blk(Ra, d.C, w, k, a);
+  load_blk(Rc, d.C, w, k, c);
+  __syncthreads();
+  double acc[4][4] = {};
+  atb_acc(Ra, Rc, acc);
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = a * NB + ty * 4 + q, cc = c * NB + tx * 4 + u;
+      if (r < w && cc < w) d.C[(int64_t)r * w + cc] -= acc[q][u];
+    }
+}
+
+__global__ __launch_bounds__(256) void k_inv_col(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
+                                                 int n, int J) {
+  const uint32_t t = blockIdx.x;
+  const int mi = find_pref(pref, n, t);
+  const RefDev& d = ds[mi];
+  const int w = d.w;
+  const int I = (int)(t - pref[mi]);
+  __shared__ double Ab[NB][LDB];
+  __shared__ double Bb[NB][LDB];
+  double acc[4][4] = {};
+  for (int tb = I; tb < J; ++tb) {
+    load_blk(Ab, d.X, w, I, tb);
+    load_blk(Bb, d.C, w, tb, J);
+    __syncthreads();
+    ab_acc(Ab, Bb, acc);
+    __syncthreads();
+  }
+  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) Ab[ty * 4 + q][tx * 4 + u] = acc[q][u];
+  load_blk(Bb, d.X, w, J, J);
+  __syncthreads();
+  double out[4][4] = {};
+  ab_acc(Ab, Bb, out);
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int r = I * NB + ty * 4 + q, c = J * NB + tx * 4 + u;
+      if (r < w && c < w) {
+        const int64_t g = (int64_t)r * w + c;
+        d.X[g] = -out[q][u];
+        d.Rinv[g] = (float)(-out[q][u]);
+      }
+    }
+}
+
+}  // namespace
+
+int chol_blocks(int32_t w) { return (w + NB - 1) / NB; }
+
+hipError_t launch_chol_diag(const RefDev* d, int n, int k, hipStream_t st) {
+  if (!n) return hipSuccess;
+  hipLaunchKernelGGL(k_chol_diag, dim3(n), dim3(256), 0, st, d, k);
+  return hipGetLastError();
+}
+hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_chol_panel, dim3(total), dim3(256), 0, st, d, pref, n, k);
+  return hipGetLastError();
+}
+hipError_t launch_chol_update(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_chol_update, dim3(total), dim3(256), 0, st, d, pref, n, k);
+  return hipGetLastError();
+}
+hipError_t launch_inv_col(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int J, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_inv_col, dim3(total), dim3(256), 0, st, d, pref, n, J);
+  return hipGetLastError();
+}

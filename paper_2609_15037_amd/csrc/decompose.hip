@@ -8,10 +8,10 @@
 //   dM[i,j]  = Adam(M[i,j])                (when p.adam_m != 0)
 //
 // Memory-bound: reads G once (4 B/element), writes 4 (inv, dM, two moments)
-// and reads 2 fp32 values per block. One wave streams one row at a time with
-// 16-byte loads; a block of B <= 256 columns maps onto B/4 consecutive lanes and
-// is reduced with xor shuffles inside that lane group (fixed order, so results
-// are bit-reproducible). Other block sizes take a generic per-block path.
+// and reads 2 fp32 values per block. A block of B <= 256 columns maps onto B/4
+// consecutive lanes and is reduced with xor shuffles inside that lane group
+// (fixed order, so results are bit-reproducible). Other block sizes take a
+// generic per-block path.
 #include "common.h"
 
 namespace {
@@ -31,45 +31,79 @@ __device__ __forceinline__ void block_out(const MatDev& d, const StepParams& p, 
   }
 }
 
+// Phase 1: the block sums of squares of the workgroup's DEC_ROWS rows go to LDS
+// (each wave streams one row at a time with UNR 16-byte loads in flight).
+// Phase 2: all threads run Optimizer_M over those DEC_ROWS * k blocks, which are
+// contiguous in the m x k layout, so the moment/inv/dM traffic is coalesced.
+constexpr int DEC_LDS = 8192;   // floats of LDS for block sums (phase 1 -> 2)
+
 __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ mats, StepParams p, int adam_m) {
+  __shared__ float sums[DEC_LDS];
   const uint32_t t = blockIdx.x;
   const int mi = find_mat(mats, p.nmat, t, [](const MatDev& d) { return d.tile_dec; });
   const MatDev d = mats[mi];
   const int64_t row0 = (int64_t)(t - d.tile_dec) * DEC_ROWS;
+  const int rows = (int)((d.m - row0 < DEC_ROWS) ? d.m - row0 : DEC_ROWS);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int B = p.B;
   const int64_t n = d.n;
-  const bool fast = (B >= 4 && B <= 256 && (B & (B - 1)) == 0 && (n & 3) == 0 &&
-                     ((uintptr_t)d.G & 15) == 0);
-  for (int rr = wave; rr < DEC_ROWS; rr += 4) {
-    const int64_t row = row0 + rr;
-    if (row >= d.m) break;
-    const float* g = d.G + row * n;
-    if (fast) {
-      const int gl = B >> 2;   // lanes per block
-      for (int64_t c0 = 0; c0 < n; c0 += 256) {
-        const int64_t c = c0 + 4 * lane;
-        float ss = 0.f;
-        if (c < n) {
-          const float4 v = *reinterpret_cast<const float4*>(g + c);
-          ss = v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w;
-        }
-        for (int o = 1; o < gl; o <<= 1) ss += __shfl_xor(ss, o, 64);
-        if ((lane & (gl - 1)) == 0 && c < n) block_out(d, p, row, (int)(c / B), ss, adam_m);
-      }
-    } else {
-      for (int j = 0; j < d.k; ++j) {
+  const int k = d.k;
+  const bool staged = (int64_t)rows * k <= DEC_LDS;
+  const bool fast = staged && B >= 4 && B <= 256 && (B & (B - 1)) == 0 && (n & 3) == 0 &&
+                    ((uintptr_t)d.G & 15) == 0;
+  if (!staged) {
+    // generic path (very many blocks per row): one block at a time, Optimizer_M inline
+    for (int rr = wave; rr < rows; rr += 4) {
+      const int64_t row = row0 + rr;
+      const float* g = d.G + row * n;
+      for (int j = 0; j < k; ++j) {
         const int64_t cs = (int64_t)j * B;
         const int64_t ce = (cs + B < n) ? cs + B : n;
         float ss = 0.f;
-        for (int64_t c = cs + lane; c < ce; c += 64) {
-          const float v = g[c];
-          ss += v * v;
-        }
+        for (int64_t c = cs + lane; c < ce; c += 64) { const float v = g[c]; ss += v * v; }
         ss = wave_sum(ss);
         if (lane == 0) block_out(d, p, row, j, ss, adam_m);
       }
     }
+    return;
+  }
+  for (int rr = wave; rr < rows; rr += 4) {
+    const int64_t row = row0 + rr;
+    const float* g = d.G + row * n;
+    if (fast) {
+      constexpr int UNR = 8;
+      const int gl = B >> 2;   // lanes per block
+      for (int64_t c00 = 0; c00 < n; c00 += 256 * UNR) {
+        float4 v[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int64_t c = c00 + 256 * u + 4 * lane;
+          v[u] = (c < n) ? *reinterpret_cast<const float4*>(g + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int64_t c = c00 + 256 * u + 4 * lane;
+          float ss = v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
+          for (int o = 1; o < gl; o <<= 1) ss += __shfl_xor(ss, o, 64);
+          if ((lane & (gl - 1)) == 0 && c < n) sums[rr * k + (int)(c / B)] = ss;
+        }
+      }
+    } else {
+      for (int j = 0; j < k; ++j) {
+        const int64_t cs = (int64_t)j * B;
+        const int64_t ce = (cs + B < n) ? cs + B : n;
+        float ss = 0.f;
+        for (int64_t c = cs + lane; c < ce; c += 64) { const float v = g[c]; ss += v * v; }
+        ss = wave_sum(ss);
+        if (lane == 0) sums[rr * k + j] = ss;
+      }
+    }
+  }
+  __syncthreads();
+  const int total = rows * k;
+  for (int e = threadIdx.x; e < total; e += 256) {
+    const int rr = e / k, j = e - (e / k) * k;
+    block_out(d, p, row0 + rr, j, sums[e], adam_m);
   }
 }
 }  // namespace

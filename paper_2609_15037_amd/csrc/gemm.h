@@ -43,6 +43,10 @@ struct GemmProb {
   uint32_t tiles_n;
   int32_t vec;        // bit0: A may use 16-byte loads, bit1: B may
   int32_t pad_;
+  uint32_t a_bytes;   // extent of the A array (buffer loads past it return 0); 0 = unknown
+  uint32_t b_bytes;   // extent of the B array
+  uint32_t inv_bytes; // extent of the inv array
+  uint32_t pad2_;
 };
 
 struct GemmUniform {

@@ -164,7 +164,8 @@ size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w) {
   size_t b = 0;
   b += align_up(4 * s * w) * 2;            // Z, Z2
   b += align_up(4 * L * w) * 2;            // Y, Y2
-  b += align_up(8 * (size_t)w * w);        // C
+  b += align_up(8 * (size_t)w * w) * 2;    // C, X
+  b += align_up(8);                        // cmax
   b += align_up(4 * (size_t)w * w);        // Rinv
   b += align_up(8 * (size_t)wpad * s);     // Zc
   b += align_up(4 * 64);                   // off
@@ -264,6 +265,20 @@ int vec_flags_op(const void* p, int64_t ld, int operand_bf16) {
   return (((uintptr_t)p & 15) == 0 && (ld % q) == 0) ? 1 : 0;
 }
 
+// Enable the buffer-load fast path (vec bit 2) when both operands allow 16-byte
+// loads and every offset a tile can form (extent plus a 256-row overhang) fits
+// in the 32-bit buffer offset.
+void set_extents(GemmProb& g, size_t a_bytes, size_t a_row_bytes, size_t b_bytes, size_t b_row_bytes,
+                 size_t inv_bytes, size_t inv_row_bytes) {
+  const size_t lim = (size_t)0xFFFFFFFFu;
+  const bool ok = a_bytes + 256 * a_row_bytes < lim && b_bytes + 256 * b_row_bytes < lim &&
+                  inv_bytes + 256 * inv_row_bytes < lim;
+  g.a_bytes = ok ? (uint32_t)a_bytes : 0u;
+  g.b_bytes = ok ? (uint32_t)b_bytes : 0u;
+  g.inv_bytes = ok ? (uint32_t)inv_bytes : 0u;
+  if (ok && (g.vec & 3) == 3) g.vec |= 4;
+}
+
 StepParams make_params(const moara_state* st, float lr) {
   StepParams p{};
   p.B = st->cfg.block_size;
@@ -345,6 +360,8 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
     g.bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
     g.tiles_n = gemm_tiles_n(kind, g.N);
     g.vec = vec_flags_g((const float*)grads[i], h.n) | (vec_flags_op(h.Ptop, h.s, ob) << 1);
+    set_extents(g, 4 * (size_t)h.m * h.n, 4 * (size_t)h.n, (size_t)(ob ? 2 : 4) * h.r * h.s, (size_t)(ob ? 2 : 4) * h.s,
+                g.inv ? 4 * (size_t)h.m * h.k : 0, 4 * (size_t)h.k);
     const uint32_t nt = gemm_tiles_m(kind, g.M) * g.tiles_n;
     if (h.side == MOARA_SIDE_LEFT) { g.tile_start = tl; tl += nt; left.push_back(g); }
     else { g.tile_start = tr; tr += nt; right.push_back(g); }
@@ -358,6 +375,11 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
     b.dM = st->cfg.decompose ? h.dM : nullptr; b.dM_ld = h.k;
     b.tiles_n = gemm_tiles_n(kind, b.N);
     b.vec = vec_flags_op(b.a, h.r, ob) | (vec_flags_op(b.b, h.r, ob) << 1);
+    {
+      const size_t e = ob ? 2 : 4;
+      const size_t rows_a = h.side == MOARA_SIDE_LEFT ? h.s : h.L, rows_b = h.side == MOARA_SIDE_LEFT ? h.L : h.s;
+      set_extents(b, e * rows_a * h.r, e * h.r, e * rows_b * h.r, e * h.r, 0, 0);
+    }
     b.tile_start = tb;
     tb += gemm_tiles_m(kind, b.M) * b.tiles_n;
     back.push_back(b);
@@ -392,7 +414,7 @@ struct RefMat {
   int64_t s, L;
   int32_t w, wpad;
   float *Z, *Z2, *Y, *Y2, *Rinv;
-  double *C, *Zc, *norms;
+  double *C, *X, *cmax, *Zc, *norms;
   uint32_t* off;
   int32_t* order;
 };
@@ -442,6 +464,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.Y = (float*)take(4 * x.L * x.w);
     x.Y2 = (float*)take(4 * x.L * x.w);
     x.C = (double*)take(8 * (size_t)x.w * x.w);
+    x.X = (double*)take(8 * (size_t)x.w * x.w);
+    x.cmax = (double*)take(8);
     x.Rinv = (float*)take(4 * (size_t)x.w * x.w);
     x.Zc = (double*)take(8 * (size_t)x.wpad * x.s);
     x.off = (uint32_t*)take(4 * 64);
@@ -462,7 +486,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     d.s = x.s; d.L = x.L; d.w = x.w; d.wpad = x.wpad; d.r = h.r;
     d.operand_bf16 = c.operand_dtype == MOARA_BF16;
     d.seed = c.refresh_seed * 0x9E3779B97F4A7C15ull + (uint64_t)(x.idx + 1) * 0xD1B54A32D192ED03ull;
-    d.Z = x.Z2; d.C = x.C; d.Rinv = x.Rinv; d.Zc = x.Zc;
+    d.Z = x.Z2; d.C = x.C; d.X = x.X; d.cmax = x.cmax; d.Rinv = x.Rinv; d.Zc = x.Zc;
     d.P32 = h.P32; d.Pop = h.Pop; d.Ptop = h.Ptop;
     d.off = x.off; d.order = x.order; d.norms = x.norms;
     d.tile_gauss = tg; tg += gauss_tiles(x.s, x.w);
@@ -500,6 +524,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       gp.ldc = x.w;
       gp.tiles_n = gemm_tiles_n(kind, gp.N);
       gp.vec = vec_flags_op(gp.a, x.w, 0) | (vec_flags_op(gp.b, x.w, 0) << 1);
+      set_extents(gp, 4 * (size_t)gp.M * x.w, 4 * (size_t)x.w, 4 * (size_t)x.w * x.w, 4 * (size_t)x.w, 0, 0);
       gp.tile_start = t;
       t += gemm_tiles_m(kind, gp.M) * gp.tiles_n;
     }
@@ -521,12 +546,30 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       gp.c = xt ? x.Z2 : x.Y; gp.ldc = x.w;
       gp.tiles_n = gemm_tiles_n(kind, gp.N);
       gp.vec = vec_flags_g((const float*)grads[x.idx], h.n) | (vec_flags_op(gp.b, x.w, 0) << 1);
+      set_extents(gp, 4 * (size_t)h.m * h.n, 4 * (size_t)h.n, 4 * (size_t)gp.K * x.w, 4 * (size_t)x.w,
+                  gp.inv ? 4 * (size_t)h.m * h.k : 0, 4 * (size_t)h.k);
       gp.tile_start = t;
       t += gemm_tiles_m(kind, gp.M) * gp.tiles_n;
       g.push_back(gp);
     }
     return std::make_pair(g, t);
   };
+  // workgroup prefixes of the blocked Cholesky / inverse launches (same for every orth of the chunk)
+  int nbmax = 1;
+  for (auto& x : rm) nbmax = std::max(nbmax, chol_blocks(x.w));
+  std::vector<uint32_t> pan_pref((size_t)nbmax * nm), upd_pref((size_t)nbmax * nm), inv_pref((size_t)nbmax * nm);
+  std::vector<uint32_t> pan_tot(nbmax), upd_tot(nbmax), inv_tot(nbmax);
+  for (int k = 0; k < nbmax; ++k) {
+    uint32_t tp = 0, tu = 0, ti = 0;
+    for (int q = 0; q < nm; ++q) {
+      const int nb = chol_blocks(rm[q].w);
+      const int T = std::max(0, nb - k - 1);
+      pan_pref[(size_t)k * nm + q] = tp; tp += (uint32_t)T;
+      upd_pref[(size_t)k * nm + q] = tu; tu += (uint32_t)(T * (T + 1) / 2);
+      inv_pref[(size_t)k * nm + q] = ti; ti += (uint32_t)(k < nb ? k : 0);
+    }
+    pan_tot[k] = tp; upd_tot[k] = tu; inv_tot[k] = ti;
+  }
   auto gZ2 = gram_list(false), gY = gram_list(true);
   auto aZ = apply_list(false), aY = apply_list(true);
   auto xzR = big_list(MOARA_SIDE_RIGHT, false, false), xzL = big_list(MOARA_SIDE_LEFT, false, false);
@@ -546,6 +589,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       {xtL.first.data(), sizeof(GemmProb) * xtL.first.size()},       // 8
       {xt2R.first.data(), sizeof(GemmProb) * xt2R.first.size()},     // 9
       {xt2L.first.data(), sizeof(GemmProb) * xt2L.first.size()},     // 10
+      {pan_pref.data(), sizeof(uint32_t) * pan_pref.size()},          // 11
+      {upd_pref.data(), sizeof(uint32_t) * upd_pref.size()},          // 12
+      {inv_pref.data(), sizeof(uint32_t) * inv_pref.size()},          // 13
   };
   size_t total = 0;
   std::vector<size_t> offs;
@@ -571,13 +617,29 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     if (l.first.empty()) return hipSuccess;
     return launch_gemm(kind, am, B_NC, EP_STORE, (const GemmProb*)D(q), (int)l.first.size(), l.second, u, stream);
   };
+  const uint32_t* PAN = (const uint32_t*)D(11);
+  const uint32_t* UPD = (const uint32_t*)D(12);
+  const uint32_t* INV = (const uint32_t*)D(13);
+  auto chol_inv = [&]() -> hipError_t {      // C -> R (in place), X = R^{-1}, Rinv = fp32(X)
+    hipError_t e = hipSuccess;
+    for (int k = 0; k < nbmax && e == hipSuccess; ++k) {
+      e = launch_chol_diag(RD, nm, k, stream);
+      if (e == hipSuccess) e = launch_chol_panel(RD, PAN + (size_t)k * nm, nm, pan_tot[k], k, stream);
+      if (e == hipSuccess) e = launch_chol_update(RD, UPD + (size_t)k * nm, nm, upd_tot[k], k, stream);
+    }
+    for (int J = 1; J < nbmax && e == hipSuccess; ++J)
+      e = launch_inv_col(RD, INV + (size_t)J * nm, nm, inv_tot[J], J, stream);
+    return e;
+  };
   auto orth_Z = [&]() -> hipError_t {        // Z <- orth(Z2)
     hipError_t e = launch_gram((const GramProb*)D(1), nm, gZ2.second, stream);
-    if (e == hipSuccess) e = launch_chol_inv(RD, nm, stream);
+    if (e == hipSuccess) e = chol_inv();
     if (e == hipSuccess) e = gemm(A_KC, 3, aZ);
     return e;
   };
   TimerScope ts(st, MOARA_KERN_REFRESH, stream);
+  // blocks below the diagonal of Rinv are never written by the factorisation kernels
+  for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.Rinv, 0, 4 * (size_t)x.w * x.w, stream));
   HIP_TRY(launch_gauss(RD, nm, tg, stream));
   HIP_TRY(orth_Z());
   const int q_iters = c.refresh_iters;
@@ -591,7 +653,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       HIP_TRY(orth_Z());
     } else {
       HIP_TRY(launch_gram((const GramProb*)D(2), nm, gY.second, stream));
-      HIP_TRY(launch_chol_inv(RD, nm, stream));
+      HIP_TRY(chol_inv());
       HIP_TRY(gemm(A_KC, 4, aY));
       HIP_TRY(gemm(A_G_TRANS, 9, xt2R));
       HIP_TRY(gemm(A_G_ROW, 10, xt2L));

@@ -12,7 +12,9 @@ struct RefDev {
   int32_t operand_bf16;
   uint64_t seed;      // Philox key for the Gaussian start block
   float* Z;           // s x w fp32 (iterate, row-major)
-  double* C;          // w x w fp64 Gram / Cholesky workspace
+  double* C;          // w x w fp64 Gram, factorised in place into R (upper)
+  double* X;          // w x w fp64 R^{-1} (upper)
+  double* cmax;       // max diagonal of the Gram (pivot floor), one value
   float* Rinv;        // w x w fp32 inverse Cholesky factor
   double* Zc;         // wpad x s fp64, column-major copy of X^T Y for the Jacobi sweeps
   float* P32;         // s x r fp32 master projector
@@ -38,7 +40,11 @@ struct GramProb {
 
 hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st);
 hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st);
-hipError_t launch_chol_inv(const RefDev* d, int n, hipStream_t st);
+int chol_blocks(int32_t w);
+hipError_t launch_chol_diag(const RefDev* d, int n, int k, hipStream_t st);
+hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
+hipError_t launch_chol_update(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
+hipError_t launch_inv_col(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int J, hipStream_t st);
 hipError_t launch_to_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st);
 hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st);
 hipError_t launch_finalize(const RefDev* d, int n, hipStream_t st);

@@ -10,8 +10,8 @@
 // orth() is CholeskyQR with an fp64 Gram and an fp64 Cholesky factor.
 //
 // Kernels here: Philox-4x32-10 Gaussian start (Salmon et al., SC'11, with the
-// Box-Muller transform), fp64 Gram, per-matrix Cholesky + triangular inverse,
-// the Jacobi sweep rounds and the final ordering / sign fixing.
+// Box-Muller transform), fp64 Gram, the Jacobi sweep rounds and the final
+// ordering / sign fixing; the blocked Cholesky and inverse live in chol.hip.
 #include "refresh.h"
 
 namespace {
@@ -99,190 +99,6 @@ __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, i
         g.C[(int64_t)j * g.w + i] = acc[q][u];
       }
     }
-}
-
-// ------------------------------------------------------------------ Cholesky + inverse
-// One workgroup per matrix. C (w x w, fp64, symmetric) -> upper R with C = R^T R
-// (right-looking, 32-wide blocks staged in LDS), then R^{-1} by block columns,
-// written as fp32 Rinv (zeros below the diagonal). A pivot that is not above
-// 1e-13 * max(diag C) is raised to that floor (rank-deficient iterates stay finite).
-constexpr int CB = 32;
-
-__global__ __launch_bounds__(256) void k_chol_inv(const RefDev* __restrict__ ds) {
-  const RefDev& d = ds[blockIdx.x];
-  const int w = d.w;
-  double* C = d.C;
-  const int tid = threadIdx.x;
-  __shared__ double D[CB][CB + 1];
-  __shared__ double Pa[CB][CB + 1];
-  __shared__ double Pc[CB][CB + 1];
-  __shared__ double red[256];
-
-  // floor for pivots
-  double mx = 0.0;
-  for (int i = tid; i < w; i += 256) mx = fmax(mx, C[(int64_t)i * w + i]);
-  red[tid] = mx;
-  __syncthreads();
-  for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
-  const double cmax = red[0];
-  const double floor_piv = cmax * 1e-13;
-  __syncthreads();
-  if (!(cmax > 0.0)) {   // all-zero iterate (V == 0): leave it unscaled
-    for (int64_t e = tid; e < (int64_t)w * w; e += 256) d.Rinv[e] = (e / w == e % w) ? 1.f : 0.f;
-    return;
-  }
-
-  // ---- Cholesky
-  for (int k0 = 0; k0 < w; k0 += CB) {
-    const int kb = min(CB, w - k0);
-    for (int e = tid; e < kb * kb; e += 256) {
-      const int i = e / kb, j = e % kb;
-      D[i][j] = C[(int64_t)(k0 + i) * w + k0 + j];
-    }
-    __syncthreads();
-    for (int j = 0; j < kb; ++j) {
-      if (tid == 0) {
-        double v = D[j][j];
-        if (!(v > floor_piv)) v = floor_piv;
-        D[j][j] = sqrt(v);
-      }
-      __syncthreads();
-      if (tid > j && tid < kb) D[j][tid] /= D[j][j];
-      __syncthreads();
-      for (int e = tid; e < kb * kb; e += 256) {
-        const int a = e / kb, c = e % kb;
-        if (a > j && c >= a) D[a][c] -= D[j][a] * D[j][c];
-      }
-      __syncthreads();
-    }
-    for (int e = tid; e < kb * kb; e += 256) {
-      const int i = e / kb, j = e % kb;
-      C[(int64_t)(k0 + i) * w + k0 + j] = (j >= i) ? D[i][j] : 0.0;
-    }
-    // panel: rows k0..k0+kb, columns >= k0+kb : solve R_kk^T X = C_panel
-    for (int c = k0 + kb + tid; c < w; c += 256) {
-      double x[CB];
-#pragma unroll
-      for (int i = 0; i < CB; ++i) {
-        if (i < kb) {
-          double v = C[(int64_t)(k0 + i) * w + c];
-#pragma unroll
-          for (int t = 0; t < CB; ++t)
-            if (t < i) v -= D[t][i] * x[t];
-          x[i] = v / D[i][i];
-        }
-      }
-#pragma unroll
-      for (int i = 0; i < CB; ++i)
-        if (i < kb) C[(int64_t)(k0 + i) * w + c] = x[i];
-    }
-    __syncthreads();
-    // trailing update of the upper triangle
-    const int s0 = k0 + kb;
-    const int T = (w - s0 + CB - 1) / CB;
-    for (int ta = 0; ta < T; ++ta)
-      for (int tc = ta; tc < T; ++tc) {
-        const int a0 = s0 + ta * CB, c0 = s0 + tc * CB;
-        for (int e = tid; e < kb * CB; e += 256) {
-          const int t = e / CB, x = e % CB;
-          Pa[t][x] = (a0 + x < w) ? C[(int64_t)(k0 + t) * w + a0 + x] : 0.0;
-          Pc[t][x] = (c0 + x < w) ? C[(int64_t)(k0 + t) * w + c0 + x] : 0.0;
-        }
-        __syncthreads();
-        const int ya = tid >> 3, xc = (tid & 7) * 4;
-        double s4[4] = {0, 0, 0, 0};
-        for (int t = 0; t < kb; ++t) {
-          const double pa = Pa[t][ya];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) s4[q] += pa * Pc[t][xc + q];
-        }
-        const int a = a0 + ya;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int c = c0 + xc + q;
-          if (a < w && c < w && c >= a) C[(int64_t)a * w + c] -= s4[q];
-        }
-        __syncthreads();
-      }
-  }
-
-  // ---- inverse of the upper triangular R (in place, by 32-wide block columns)
-  for (int j0 = 0; j0 < w; j0 += CB) {
-    const int jb = min(CB, w - j0);
-    for (int e = tid; e < jb * jb; e += 256) {
-      const int i = e / jb, j = e % jb;
-      D[i][j] = (j >= i) ? C[(int64_t)(j0 + i) * w + j0 + j] : 0.0;
-    }
-    __syncthreads();
-    // Dinv into Pa (upper), one thread per column
-    if (tid < jb) {
-      // column j of the inverse of the upper triangular diagonal block (back substitution)
-      const int j = tid;
-      double x[CB];
-#pragma unroll
-      for (int i = CB - 1; i >= 0; --i) {
-        double v = (i == j) ? 1.0 : 0.0;
-#pragma unroll
-        for (int t = 0; t < CB; ++t)
-          if (t > i && t <= j) v -= D[i][t] * x[t];
-        x[i] = (i <= j) ? v / D[i][i] : 0.0;
-      }
-#pragma unroll
-      for (int i = 0; i < CB; ++i) Pa[i][j] = x[i];
-    }
-    __syncthreads();
-    // T = R[0:j0][J] * Dinv, in place in C[0:j0][J]
-    for (int i = tid; i < j0; i += 256) {
-      double rr[CB];
-#pragma unroll
-      for (int t = 0; t < CB; ++t) rr[t] = (t < jb) ? C[(int64_t)i * w + j0 + t] : 0.0;
-#pragma unroll
-      for (int c = 0; c < CB; ++c) {
-        if (c < jb) {
-          double v = 0.0;
-#pragma unroll
-          for (int t = 0; t < CB; ++t)
-            if (t <= c) v += rr[t] * Pa[t][c];
-          C[(int64_t)i * w + j0 + c] = v;
-        }
-      }
-    }
-    __syncthreads();
-    // X[0:j0][J] = -X[0:j0][0:j0] * T, row tiles top to bottom (rows below still hold T)
-    for (int i0 = 0; i0 < j0; i0 += CB) {
-      const int ib = min(CB, j0 - i0);
-      const int yi = tid >> 3, xc = (tid & 7) * 4;
-      double s4[4] = {0, 0, 0, 0};
-      for (int t0 = i0; t0 < j0; t0 += CB) {
-        const int tb = min(CB, j0 - t0);
-        for (int e = tid; e < CB * CB; e += 256) {
-          const int a = e / CB, b = e % CB;
-          Pc[a][b] = (a < ib && b < tb) ? C[(int64_t)(i0 + a) * w + t0 + b] : 0.0;     // X[I][t-chunk]
-          D[a][b] = (a < tb && b < jb) ? C[(int64_t)(t0 + a) * w + j0 + b] : 0.0;      // T[t-chunk][J]
-        }
-        __syncthreads();
-        for (int t = 0; t < tb; ++t) {
-          const double xv = Pc[yi][t];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) s4[q] += xv * D[t][xc + q];
-        }
-        __syncthreads();
-      }
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        if (yi < ib && xc + q < jb) C[(int64_t)(i0 + yi) * w + j0 + xc + q] = -s4[q];
-      __syncthreads();
-    }
-    for (int e = tid; e < jb * jb; e += 256) {
-      const int i = e / jb, j = e % jb;
-      C[(int64_t)(j0 + i) * w + j0 + j] = Pa[i][j];
-    }
-    __syncthreads();
-  }
-  for (int64_t e = tid; e < (int64_t)w * w; e += 256) {
-    const int64_t i = e / w, j = e % w;
-    d.Rinv[e] = (j >= i) ? (float)C[e] : 0.f;
-  }
 }
 
 // ------------------------------------------------------------------ Zn (s x w fp32) -> Zc (wpad x s fp64)
@@ -552,11 +368,6 @@ hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st) 
 hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st) {
   if (!total) return hipSuccess;
   hipLaunchKernelGGL(k_gram, dim3(total), dim3(256), 0, st, g, n);
-  return hipGetLastError();
-}
-hipError_t launch_chol_inv(const RefDev* d, int n, hipStream_t st) {
-  if (!n) return hipSuccess;
-  hipLaunchKernelGGL(k_chol_inv, dim3(n), dim3(256), 0, st, d);
   return hipGetLastError();
 }
 hipError_t launch_to_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st) {
