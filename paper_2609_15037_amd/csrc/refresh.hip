@@ -55,48 +55,71 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
 }
 
 // ------------------------------------------------------------------ fp64 Gram C = A^T A
+// One workgroup per 64 x 64 tile of the upper triangle. fp32 rows are staged in
+// LDS as fp64 (32 rows per chunk, two buffers, next chunk prefetched into
+// registers) and multiplied on v_mfma_f64_16x16x4; wave w owns tile rows
+// [16w, 16w+16).
+typedef double f64x4 __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, int n) {
-  __shared__ double Ai[32][64 + 1];
-  __shared__ double Aj[32][64 + 1];
+  __shared__ double Ai[2][32][64 + 1];
+  __shared__ double Aj[2][32][64 + 1];
   const uint32_t t = blockIdx.x;
   int lo = 0, hi = n - 1;
   while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (gs[mid].tile_start <= t) lo = mid; else hi = mid - 1; }
   const GramProb& g = gs[lo];
-  // linear index over the upper triangle (ti <= tj) of T x T tiles
   int rem = (int)(t - g.tile_start), ti = 0;
   while (rem >= g.tiles - ti) { rem -= g.tiles - ti; ++ti; }
   const int tj = ti + rem;
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-  double acc[4][4] = {};
-  for (int64_t l0 = 0; l0 < g.rows; l0 += 32) {
-    for (int e = threadIdx.x; e < 32 * 64; e += 256) {
-      const int l = e >> 6, c = e & 63;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int nch = (int)((g.rows + 31) / 32);
+  float pi[8], pj[8];
+  auto load_chunk = [&](int c) {
+    const int64_t l0 = (int64_t)c * 32;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q, l = e >> 6, cc = e & 63;
       const int64_t row = l0 + l;
-      const int ci = ti * 64 + c, cj = tj * 64 + c;
-      Ai[l][c] = (row < g.rows && ci < g.w) ? (double)g.A[row * g.lda + ci] : 0.0;
-      Aj[l][c] = (row < g.rows && cj < g.w) ? (double)g.A[row * g.lda + cj] : 0.0;
+      const int ci = ti * 64 + cc, cj = tj * 64 + cc;
+      pi[q] = (row < g.rows && ci < g.w) ? g.A[row * g.lda + ci] : 0.f;
+      pj[q] = (row < g.rows && cj < g.w) ? g.A[row * g.lda + cj] : 0.f;
     }
-    __syncthreads();
-#pragma unroll 4
-    for (int l = 0; l < 32; ++l) {
-      double a[4], b[4];
+  };
+  auto store_chunk = [&](int b) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) { a[q] = Ai[l][ty * 4 + q]; b[q] = Aj[l][tx * 4 + q]; }
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q;
+      Ai[b][e >> 6][e & 63] = (double)pi[q];
+      Aj[b][e >> 6][e & 63] = (double)pj[q];
     }
+  };
+  f64x4 acc[4];
+#pragma unroll
+  for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+  load_chunk(0);
+  store_chunk(0);
+  __syncthreads();
+  for (int c = 0; c < nch; ++c) {
+    if (c + 1 < nch) load_chunk(c + 1);
+    const int b = c & 1;
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+      const int kr = 4 * ks + (lane >> 4);
+      const double a = Ai[b][kr][16 * wave + (lane & 15)];
+#pragma unroll
+      for (int jt = 0; jt < 4; ++jt)
+        acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Aj[b][kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+    }
+    if (c + 1 < nch) store_chunk(b ^ 1);
     __syncthreads();
   }
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
+  for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = ti * 64 + ty * 4 + q, j = tj * 64 + tx * 4 + u;
-      if (i < g.w && j < g.w) {
-        g.C[(int64_t)i * g.w + j] = acc[q][u];
-        g.C[(int64_t)j * g.w + i] = acc[q][u];
+    for (int r = 0; r < 4; ++r) {
+      const int i = ti * 64 + 16 * wave + 4 * r + (lane >> 4), j = tj * 64 + 16 * jt + (lane & 15);
+      if (i < g.w && j < g.w && (ti != tj || i <= j)) {   // diagonal tiles: one writer per pair
+        g.C[(int64_t)i * g.w + j] = acc[jt][r];
+        g.C[(int64_t)j * g.w + i] = acc[jt][r];
       }
     }
 }
@@ -133,7 +156,8 @@ __device__ __forceinline__ int circle(int pos, int round, int nb) {
 constexpr int PW = 2 * JB;   // 64 columns per pair
 
 __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
-  __shared__ double T[32][PW + 1];
+  __shared__ double T[2][32][PW + 1];
+  __shared__ double O[32][PW + 1];
   __shared__ double Gm[PW][PW + 1];
   __shared__ double Jm[PW][PW + 1];
   __shared__ double cs[PW / 2], sn[PW / 2];
@@ -152,31 +176,55 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   const int64_t s = d.s;
   auto colp = [&](int x) -> double* { return d.Zc + (int64_t)((x < JB) ? ba * JB + x : bb * JB + (x - JB)) * s; };
 
-  // (1) Gram of the 64 columns
-  const int tx = tid & 15, ty = tid >> 4;
-  double acc[4][4] = {};
-  for (int64_t r0 = 0; r0 < s; r0 += 32) {
-    for (int e = tid; e < 32 * PW; e += 256) {
-      const int x = e >> 5, l = e & 31;
-      T[l][x] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
+  // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
+  // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
+  // Wave w owns Gram rows [16w, 16w+16) and all 64 columns (four 16 x 16 tiles).
+  // 32-row chunks alternate between two LDS buffers; the next chunk's global
+  // loads are in flight while the current one is multiplied.
+  const int lane = tid & 63, wave = tid >> 6;
+  const int nch = (int)((s + 31) / 32);
+  double pre[8];
+  auto load_chunk = [&](int c) {
+    const int64_t r0 = (int64_t)c * 32;
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q, x = e >> 5, l = e & 31;
+      pre[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
     }
-    __syncthreads();
-#pragma unroll 4
-    for (int l = 0; l < 32; ++l) {
-      double a[4], b[4];
+  };
+  auto store_chunk = [&](double (*Tb)[PW + 1]) {
 #pragma unroll
-      for (int q = 0; q < 4; ++q) { a[q] = T[l][ty * 4 + q]; b[q] = T[l][tx * 4 + q]; }
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-#pragma unroll
-        for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q;
+      Tb[e & 31][e >> 5] = pre[q];
     }
+  };
+  {
+    f64x4 acc[4];
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+    load_chunk(0);
+    store_chunk(T[0]);
     __syncthreads();
+    for (int c = 0; c < nch; ++c) {
+      if (c + 1 < nch) load_chunk(c + 1);
+      double (*Tc)[PW + 1] = T[c & 1];
+#pragma unroll
+      for (int ks = 0; ks < 8; ++ks) {
+        const int kr = 4 * ks + (lane >> 4);
+        const double a = Tc[kr][16 * wave + (lane & 15)];
+#pragma unroll
+        for (int jt = 0; jt < 4; ++jt)
+          acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Tc[kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+      }
+      if (c + 1 < nch) store_chunk(T[(c + 1) & 1]);
+      __syncthreads();
+    }
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) Gm[16 * wave + 4 * r + (lane >> 4)][16 * jt + (lane & 15)] = acc[jt][r];
   }
-#pragma unroll
-  for (int q = 0; q < 4; ++q)
-#pragma unroll
-    for (int u = 0; u < 4; ++u) Gm[ty * 4 + q][tx * 4 + u] = acc[q][u];
   for (int e = tid; e < PW * PW; e += 256) Jm[e / PW][e % PW] = (e / PW == e % PW) ? 1.0 : 0.0;
   __syncthreads();
   // convergence measure of this pair (before rotating): max |g_xy| / sqrt(g_xx g_yy)
@@ -193,7 +241,7 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
     if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)red[0]));
-    if (red[0] < 1e-15) return;   // already orthogonal: nothing to rotate (uniform branch)
+    if (red[0] < 1e-13) return;   // already orthogonal: nothing to rotate (uniform branch)
   }
 
   // (2) eigen-decomposition of the 64 x 64 Gram by parallel cyclic Jacobi
@@ -241,23 +289,40 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
     red[tid] = (tid < PW / 2) ? mloc : 0.0;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
-    const bool done = red[0] < 1e-15;
+    const bool done = red[0] < 1e-13;   // fp64 dots of 64 terms leave ~1e-14 relative noise
     __syncthreads();
     if (done) break;
   }
 
-  // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J
-  for (int64_t r0 = 0; r0 < s; r0 += 32) {
-    for (int e = tid; e < 32 * PW; e += 256) {
-      const int x = e >> 5, l = e & 31;
-      T[l][x] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
+  // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, 32 rows at a time on
+  // fp64 MFMA; wave w computes rows [16 (w&1), +16) x columns [32 (w>>1), +32).
+  // Results go through LDS so the write-back is column-contiguous.
+  load_chunk(0);
+  store_chunk(T[0]);
+  __syncthreads();
+  const int rt = wave & 1, cb = 2 * (wave >> 1);
+  for (int c = 0; c < nch; ++c) {
+    const int64_t r0 = (int64_t)c * 32;
+    if (c + 1 < nch) load_chunk(c + 1);
+    double (*Tc)[PW + 1] = T[c & 1];
+    f64x4 o0 = {0.0, 0.0, 0.0, 0.0}, o1 = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+    for (int ks = 0; ks < PW / 4; ++ks) {
+      const int y = 4 * ks + (lane >> 4);
+      const double a = Tc[16 * rt + (lane & 15)][y];
+      o0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Jm[y][16 * cb + (lane & 15)], o0, 0, 0, 0);
+      o1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Jm[y][16 * (cb + 1) + (lane & 15)], o1, 0, 0, 0);
     }
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      O[16 * rt + 4 * r + (lane >> 4)][16 * cb + (lane & 15)] = o0[r];
+      O[16 * rt + 4 * r + (lane >> 4)][16 * (cb + 1) + (lane & 15)] = o1[r];
+    }
+    if (c + 1 < nch) store_chunk(T[(c + 1) & 1]);
     __syncthreads();
     for (int e = tid; e < 32 * PW; e += 256) {
       const int x = e >> 5, l = e & 31;
-      double v = 0.0;
-      for (int y = 0; y < PW; ++y) v = fma(T[l][y], Jm[y][x], v);
-      if (r0 + l < s) colp(x)[r0 + l] = v;
+      if (r0 + l < s) colp(x)[r0 + l] = O[l][x];
     }
     __syncthreads();
   }
