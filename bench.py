@@ -46,6 +46,9 @@ def parse():
     ap.add_argument("--layers", type=int, default=None, help="use only the first N layers (profiling runs)")
     ap.add_argument("--refresh-iters", type=int, default=None,
                     help="override the subspace-iteration count (the default is the workload's)")
+    ap.add_argument("--copy-calibration-mib", type=int, default=0,
+                    help="run one plain elementwise copy kernel (y = -x) over this many MiB before the steps: the "
+                         "reference dispatch for scaling the FETCH_SIZE / WRITE_SIZE counters of a profiling run")
     return ap.parse_args()
 
 
@@ -66,6 +69,21 @@ def algorithmic_cost(wl, operand_bytes: int, weight_bytes: int):
         cost["backproject"][0] += operand_bytes * L * r + operand_bytes * s * r + 4 * M * k + 2 * weight_bytes * M * N
         cost["backproject"][1] += 2 * M * N * r
     return cost
+
+
+def method_cost(wl, operand_bytes: int, weight_bytes: int):
+    """What the method itself must move and compute per step, whatever the kernel split:
+    read G, read+write W, read+write the two direction moments, read+write the two
+    magnitude moments, read P; two GEMMs of 2mnr flops each."""
+    by, fl = 0, 0
+    for m in wl.matrices:
+        r = wl.rank_of(m)
+        M, N = m.rows, m.cols
+        s, L = min(M, N), max(M, N)
+        k = -(-N // wl.block_size)
+        by += 4 * M * N + 2 * weight_bytes * M * N + 16 * r * L + 16 * M * k + operand_bytes * s * r
+        fl += 4 * M * N * r
+    return by, fl
 
 
 def refresh_flops(wl, p_over: int, q: int):
@@ -177,6 +195,16 @@ def main():
         log(f"[bench] refresh {rep}: {ref_ms[-1]:.1f} ms")
     M.moara_reset_kernel_stats(st, stream=stream)
 
+    if a.copy_calibration_mib:
+        nb = a.copy_calibration_mib << 20
+        src = torch.ones(nb // 4, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        torch.neg(src, out=dst)   # one elementwise kernel: reads nb bytes, writes nb bytes
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy: {nb} bytes read, {nb} bytes written")
+        del src, dst
+
     # ---- steps
     lr = wl.lr
     for _ in range(a.warmup):
@@ -230,6 +258,8 @@ def main():
                  "avg_launch_ms": dk["ms_total"] / max(1, dk["launches"]),
                  "traffic": None})
 
+    mb, mf = method_cost(wl, ob, wb)
+    step_roof_ms = max(mb / PEAK_HBM, mf / peak_mfma) * 1e3
     q_used = a.refresh_iters if a.refresh_iters else wl.refresh_iters
     rf = refresh_flops(wl, wl.refresh_oversample, q_used)
     ref_med = float(np.median(ref_ms))
@@ -250,8 +280,8 @@ def main():
         "refresh_tflops": rf / (ref_med / 1e3) / 1e12,
         "refresh_frac_fp32_peak": rf / (ref_med / 1e3) / PEAK_F32,
         "amortized_ms_per_step_T200": ms_step + ref_med / 200.0,
-        "step_roofline_ms": max(sum(c[0] for c in cost.values()) / PEAK_HBM,
-                                sum(c[1] for c in cost.values()) / peak_mfma) * 1e3,
+        "step_roofline_ms": step_roof_ms,
+        "step_roofline_frac": step_roof_ms / ms_step,
         "kernels": kern,
         "roofline": roof,
         "host_clock_ms_per_step": host_s / a.steps * 1e3,
