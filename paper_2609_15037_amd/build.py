@@ -18,7 +18,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libmoara.so")
-SOURCES = ["decompose.hip", "gemm.hip", "refresh.hip", "chol.hip", "moara_api.hip"]
+SOURCES = ["decompose.hip", "gemm.hip", "gemm_nt.hip", "refresh.hip", "chol.hip", "moara_api.hip"]
 
 
 def hipcc() -> str:
@@ -49,7 +49,7 @@ def build(verbose: bool = False) -> str:
     with cf.ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
         objs = list(ex.map(lambda s: _compile(s, build_dir), SOURCES))
     tmp = OUT + ".tmp"
-    cmd = [hipcc(), "-shared", "--offload-arch=gfx950", "-o", tmp, *objs]
+    cmd = [hipcc(), "-shared", "--offload-arch=gfx950", "-Wl,-z,defs", "-o", tmp, *objs]
     r = subprocess.run(cmd, capture_output=True, text=True)
     if r.returncode != 0:
         raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")

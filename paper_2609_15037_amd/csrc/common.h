@@ -35,7 +35,8 @@ struct MatDev {
   uint32_t tile_dec;   // first WG index of this matrix in the decompose launch
   uint32_t tile_proj;  // ... in the projection launch
   uint32_t tile_back;  // ... in the back-projection launch
-  uint32_t pad_;
+  int32_t vt;          // V output layout: 0 row-major m x n, 1 transposed n x m
+  bf16* Vb;            // bf16 direction tensor V written by the decomposition (nullptr: none)
 };
 
 struct StepParams {
@@ -93,5 +94,12 @@ __device__ __forceinline__ float adam_out(float x, float& e, float& q, float b1,
 // All launchers return hipError_t from hipGetLastError after the launch.
 struct GemmProb;
 hipError_t launch_decompose(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
+hipError_t launch_decompose_inv_only(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
+hipError_t launch_decompose_vt(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
+int decompose_tiles(int64_t m);
+int decompose_vt_tiles(int64_t m);
+// limits of the V-writing decomposition paths (blocks per row)
+constexpr int DEC_VT_MAX_K = 160;    // transposed path, 64 rows per workgroup
+constexpr int DEC_ROW_MAX_K = 512;   // row-major path, 16 rows per workgroup
 hipError_t launch_project(const MatDev* mats_dev, const StepParams& p, int operand_bf16, hipStream_t st);
 hipError_t launch_backproject(const MatDev* mats_dev, const StepParams& p, int operand_bf16, hipStream_t st);

@@ -10,11 +10,21 @@
 // Memory-bound: reads G once (4 B/element), writes 4 (inv, dM, two moments)
 // and reads 2 fp32 values per block. A block of B <= 256 columns maps onto B/4
 // consecutive lanes and is reduced with xor shuffles inside that lane group
-// (fixed order, so results are bit-reproducible). Other block sizes take a
-// generic per-block path.
+// (fixed order, so results are bit-reproducible; the butterfly leaves the same
+// sum in every lane of the group). Other block sizes take a generic per-block
+// path.
+//
+// When the step's GEMMs take bf16 operands, the same pass also writes the
+// direction tensor V = G * inv in bf16 (2 B/element), in the layout in which
+// the projection reads it contiguously along its reduction index: row-major
+// m x n for a RIGHT projection (V Q), transposed n x m for a LEFT one (P^T V,
+// k_decompose_vt, which stages a 64-row x 256-column slab in LDS so that each
+// transposed row segment is written as 128 contiguous bytes).
 #include "common.h"
 
 namespace {
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int DEC_ROWS = 16;   // rows per workgroup (4 waves x 4 rows)
 
 __device__ __forceinline__ void block_out(const MatDev& d, const StepParams& p, int64_t row, int j,
@@ -86,6 +96,12 @@ __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ ma
           float ss = v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
           for (int o = 1; o < gl; o <<= 1) ss += __shfl_xor(ss, o, 64);
           if ((lane & (gl - 1)) == 0 && c < n) sums[rr * k + (int)(c / B)] = ss;
+          if (d.Vb && c < n) {
+            const float inv = 1.0f / (sqrtf(ss) + p.decomp_eps);
+            bf16x4 o;
+            o[0] = f2bf(v[u].x * inv); o[1] = f2bf(v[u].y * inv); o[2] = f2bf(v[u].z * inv); o[3] = f2bf(v[u].w * inv);
+            *reinterpret_cast<bf16x4*>(d.Vb + row * n + c) = o;
+          }
         }
       }
     } else {
@@ -106,9 +122,82 @@ __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ ma
     block_out(d, p, row0 + rr, j, sums[e], adam_m);
   }
 }
+
+// Transposed-V variant (LEFT projections): one workgroup per 64 rows. For each
+// 256-column slab every wave loads 16 of the rows (float4 per lane, 16 loads in
+// flight), reduces the block sums, writes V in bf16 into an LDS slab
+// T[64][256] (row-major, conflict-free 4-byte stores) and records the sums; the
+// slab is then written out transposed, 8 lanes per output row (16 bytes each),
+// i.e. 128-byte segments of Vt. The odd 4-byte pitch of T keeps the 8 row groups
+// read by one instruction on distinct banks. Optimizer_M then runs over the
+// 64 x k sums as in k_decompose. Preconditions (checked by the host): B a power
+// of two in [4, 256], n % 4 == 0, m % 8 == 0, k <= DEC_VT_MAX_K, G 16-byte aligned.
+constexpr int VT_ROWS = 64, VT_COLS = 256, VT_PITCH = VT_COLS + 2;   // bf16 elements
+
+__global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__ mats, StepParams p, int adam_m) {
+  __shared__ float sums[VT_ROWS * DEC_VT_MAX_K];
+  __shared__ __attribute__((aligned(16))) bf16 T[VT_ROWS * VT_PITCH];
+  const uint32_t t = blockIdx.x;
+  const int mi = find_mat(mats, p.nmat, t, [](const MatDev& d) { return d.tile_dec; });
+  const MatDev d = mats[mi];
+  const int64_t row0 = (int64_t)(t - d.tile_dec) * VT_ROWS;
+  const int rows = (int)((d.m - row0 < VT_ROWS) ? d.m - row0 : VT_ROWS);
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int B = p.B, gl = B >> 2, k = d.k;
+  const int64_t n = d.n, m = d.m;
+  for (int64_t c0 = 0; c0 < n; c0 += VT_COLS) {
+    const int64_t c = c0 + 4 * lane;
+    float4 v[16];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int rr = wave + 4 * i;
+      v[i] = (rr < rows && c < n) ? *reinterpret_cast<const float4*>(d.G + (row0 + rr) * n + c)
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      const int rr = wave + 4 * i;
+      float ss = v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
+      for (int o = 1; o < gl; o <<= 1) ss += __shfl_xor(ss, o, 64);
+      if (rr < rows && c < n && (lane & (gl - 1)) == 0) sums[rr * k + (int)(c / B)] = ss;
+      const float inv = 1.0f / (sqrtf(ss) + p.decomp_eps);
+      bf16x2 a, b;
+      a[0] = f2bf(v[i].x * inv); a[1] = f2bf(v[i].y * inv);
+      b[0] = f2bf(v[i].z * inv); b[1] = f2bf(v[i].w * inv);
+      *reinterpret_cast<bf16x2*>(T + rr * VT_PITCH + 4 * lane) = a;
+      *reinterpret_cast<bf16x2*>(T + rr * VT_PITCH + 4 * lane + 2) = b;
+    }
+    __syncthreads();
+#pragma unroll 2
+    for (int it = 0; it < 8; ++it) {
+      const int q = it * 256 + (int)threadIdx.x;
+      const int cl = q >> 3, g = q & 7;
+      const int64_t col = c0 + cl;
+      if (col < n && 8 * g < rows) {
+        bf16x8 o;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) o[e] = T[(8 * g + e) * VT_PITCH + cl];
+        *reinterpret_cast<bf16x8*>(d.Vb + col * m + row0 + 8 * g) = o;
+      }
+    }
+    __syncthreads();
+  }
+  const int total = rows * k;
+  for (int e = threadIdx.x; e < total; e += 256) {
+    const int rr = e / k, j = e - (e / k) * k;
+    block_out(d, p, row0 + rr, j, sums[e], adam_m);
+  }
+}
 }  // namespace
 
 int decompose_tiles(int64_t m) { return (int)((m + DEC_ROWS - 1) / DEC_ROWS); }
+int decompose_vt_tiles(int64_t m) { return (int)((m + VT_ROWS - 1) / VT_ROWS); }
+
+hipError_t launch_decompose_vt(const MatDev* mats_dev, const StepParams& p, hipStream_t st) {
+  if (p.total_dec == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_decompose_vt, dim3(p.total_dec), dim3(256), 0, st, mats_dev, p, 1);
+  return hipGetLastError();
+}
 
 hipError_t launch_decompose(const MatDev* mats_dev, const StepParams& p, hipStream_t st) {
   if (p.total_dec == 0) return hipSuccess;

@@ -62,8 +62,32 @@ template <int KIND> struct GemmTile;
 template <> struct GemmTile<KIND_BF16> { static constexpr int BM = 128, BN = 128, BK = 64; };
 template <> struct GemmTile<KIND_F32> { static constexpr int BM = 128, BN = 128, BK = 32; };
 
+// GROUP_M swizzle: consecutive tiles walk GM tile-rows for one tile-column before
+// moving on, so the workgroups resident on one XCD share B tiles in its L2 while
+// the GM A tile-rows stay resident too.
+constexpr int GM = 8;
+__device__ __forceinline__ void tile_coords(uint32_t lt, uint32_t tiles_m, uint32_t tiles_n, uint32_t& tm,
+                                            uint32_t& tn) {
+  const uint32_t per_group = GM * tiles_n;
+  const uint32_t group = lt / per_group;
+  const uint32_t first = group * GM;
+  const uint32_t gsz = (tiles_m - first < (uint32_t)GM) ? tiles_m - first : (uint32_t)GM;
+  const uint32_t idx = lt - group * per_group;
+  tm = first + idx % gsz;
+  tn = idx / gsz;
+}
+
 // Host helpers (gemm.hip).
 uint32_t gemm_tiles_m(int kind, int64_t M);
 uint32_t gemm_tiles_n(int kind, int64_t N);
 hipError_t launch_gemm(int kind, int amode, int bmode, int ep, const GemmProb* probs_dev, int nprob,
                        uint32_t total_tiles, const GemmUniform& u, hipStream_t st);
+
+// Large-tile bf16 path (gemm_nt.hip): A (M x K) and B (N x K) bf16, K-contiguous,
+// EP_ADAM or EP_UPDATE; 256-row tiles.
+uint32_t gemm_nt_tiles_m(int64_t M);
+uint32_t gemm_nt_tiles_n(int64_t N);
+bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,
+                      const void* a, const void* b, const void* c, int weight_bf16);
+hipError_t launch_gemm_nt(int ep, const GemmProb* probs_dev, int nprob, uint32_t total_tiles, const GemmUniform& u,
+                          hipStream_t st);

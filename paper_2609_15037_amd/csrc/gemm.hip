@@ -492,21 +492,6 @@ __device__ __forceinline__ void zero_acc(f32x16 (&acc)[2][2]) {
       for (int j = 0; j < 16; ++j) acc[mi][ni][j] = 0.f;
 }
 
-// GROUP_M swizzle: consecutive tiles walk GM tile-rows for one tile-column before
-// moving on, so the workgroups resident on one XCD share B tiles in its L2 while
-// the GM A tile-rows stay resident too.
-constexpr int GM = 8;
-__device__ __forceinline__ void tile_coords(uint32_t lt, uint32_t tiles_m, uint32_t tiles_n, uint32_t& tm,
-                                            uint32_t& tn) {
-  const uint32_t per_group = GM * tiles_n;
-  const uint32_t group = lt / per_group;
-  const uint32_t first = group * GM;
-  const uint32_t gsz = (tiles_m - first < (uint32_t)GM) ? tiles_m - first : (uint32_t)GM;
-  const uint32_t idx = lt - group * per_group;
-  tm = first + idx % gsz;
-  tn = idx / gsz;
-}
-
 // ------------------------------------------------------------------ kernels
 template <int AM, int BWM, int BWN, bool PD2, bool FAST>
 __device__ __forceinline__ void mainloop_bf16(const GemmProb& P, const GemmUniform& U, int64_t row0, int64_t col0,

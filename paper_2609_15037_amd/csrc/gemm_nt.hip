@@ -1,0 +1,441 @@
+// Large-tile bf16 GEMM for the step's projection and back-projection, used when
+// both operands are bf16, contiguous along the reduction index and K is a
+// multiple of 32:
+//
+//   C[M x N] = sum_k A[i][k] * B[j][k]     (A: M x K, B: N x K, both row-major)
+//
+// Workgroup tile 256 x 256, eight waves (2 along M x 4 along N), each wave a
+// 128 x 64 sub-tile of 4 x 2 v_mfma_f32_32x32x16_bf16 blocks (128 fp32
+// accumulators per lane). K advances in steps of 32 through a ring of four LDS
+// stages (32 KB each) filled by direct global->LDS buffer loads (no register
+// staging), three stages in flight ahead of the one being multiplied, one
+// barrier per step. Each 64-byte tile row holds four 16-byte chunks stored at
+// chunk ^ f(row), f(row) = ((row >> 1) & 3) ^ ((row >> 3) & 1), so that the
+// 16-byte fragment reads of 8- and 16-lane groups hit distinct banks; the
+// lane -> global address map of the DMA loads applies the same permutation.
+// Rows past M (N) re-read the last valid row and are never stored.
+//
+// The MFMA is issued as C^T = B A^T: lane l of block (mb, nb), register j holds
+//   row = 32 mb + (l & 31), col = 32 nb + 8 (j / 4) + 4 (l / 32) + (j % 4)
+// of the wave's sub-tile. The epilogues stage each 32-row slab of the wave's
+// accumulators through LDS and then walk it row-contiguously, so that moments,
+// N and W move as full 128-byte row segments.
+//   EP_ADAM  : Optimizer_V on the projected tile (moments e1/e2, output N bf16).
+//   EP_UPDATE: W[i][j] -= lr * bf16(scale * dM[i][j/B] * C[i][j]) (bf16 or fp32 W).
+#include "gemm.h"
+
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void lds_void;
+
+constexpr int TBM = 256, TBK = 32;
+constexpr int ROWB = TBK * 2;          // bytes per tile row per stage
+constexpr int TILEA = TBM * ROWB;      // 16 KB of A per stage
+constexpr int EPLD = 64 + 4;           // fp32 row stride of the epilogue staging slab
+constexpr int EPWAVE = 32 * EPLD;      // floats per wave slab
+
+__device__ __forceinline__ int swz(int R) { return ((R >> 1) & 3) ^ ((R >> 3) & 1); }
+
+// s_waitcnt vmcnt(n), n in [0, 15] (larger n waits for 15); expcnt and lgkmcnt are
+// left at their maxima (vmcnt occupies bits 3:0 of the immediate)
+__device__ __forceinline__ void wait_vm(int n) {
+#define WVM(k) case k: __builtin_amdgcn_s_waitcnt(0x0F70 | k); break;
+  switch (n) {
+    WVM(0) WVM(1) WVM(2) WVM(3) WVM(4) WVM(5) WVM(6) WVM(7)
+    WVM(8) WVM(9) WVM(10) WVM(11) WVM(12) WVM(13) WVM(14)
+    default: __builtin_amdgcn_s_waitcnt(0x0F7F); break;
+  }
+#undef WVM
+}
+
+// Workgroup barrier for the stage ring: each wave has already waited (vmcnt) for its
+// own DMA loads of the stage about to be read, so the barrier needs no fence; the
+// empty asm keeps the compiler from moving LDS accesses across it.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+__device__ __forceinline__ int find_prob(const GemmProb* probs, int n, uint32_t t) {
+  int lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int mid = (lo + hi + 1) >> 1;
+    if (probs[mid].tile_start <= t) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// WN waves along N (BN = 64 WN columns), 2 along M; NS LDS stages.
+template <int EP, int WN, int NS>
+__global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict__ probs, GemmUniform U) {
+  constexpr int NW = 2 * WN, TBN = 64 * WN;
+  constexpr int TILEB = TBN * ROWB, STAGEB = TILEA + TILEB;
+  constexpr int SA = 16 / NW, SB = (TBN / 16) / NW;   // 1 KB DMA slots per wave per stage
+  constexpr int OPS = SA + SB;                        // DMA instructions per wave per stage
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGEB + NW * 1024];
+  const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
+  const GemmProb& P = probs[find_prob(probs, U.nprob, t)];
+  uint32_t tm, tn;
+  tile_coords(t - P.tile_start, (uint32_t)((P.M + TBM - 1) / TBM), P.tiles_n, tm, tn);
+  const int64_t row0 = (int64_t)tm * TBM, col0 = (int64_t)tn * TBN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave & 1, wn = wave >> 1;
+
+  // ---- DMA address map: wave w fills 1 KB slots [SA w, SA w + SA) of the A tile and
+  // [SB w, SB w + SB) of the B tile (16 rows per slot)
+  const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)P.a, (short)0, (int)P.a_bytes, 0x00020000);
+  const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)P.b, (short)0, (int)P.b_bytes, 0x00020000);
+  static_assert(SA <= 4 && SB <= 4, "DMA slot arrays");
+  uint32_t va[4], vb[4];   // (fixed extent: a template-dependent array bound here drops the host launch stub)
+#pragma unroll
+  for (int j = 0; j < SA; ++j) {
+    const int R = 16 * (SA * wave + j) + (lane >> 2);
+    const int c = (lane & 3) ^ swz(R);
+    const int64_t ga = (row0 + R < P.M) ? row0 + R : P.M - 1;
+    va[j] = (uint32_t)(ga * P.lda * 2 + c * 16);
+  }
+#pragma unroll
+  for (int j = 0; j < SB; ++j) {
+    const int R = 16 * (SB * wave + j) + (lane >> 2);
+    const int c = (lane & 3) ^ swz(R);
+    const int64_t gb = (col0 + R < P.N) ? col0 + R : P.N - 1;
+    vb[j] = (uint32_t)(gb * P.ldb * 2 + c * 16);
+  }
+  auto issue = [&](int kt, int slot) {
+    char* base = smem + slot * STAGEB;
+    const int so = kt * TBK * 2;
+#pragma unroll
+    for (int j = 0; j < SA; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(base + (SA * wave + j) * 1024), 16, va[j], so, 0, 0);
+#pragma unroll
+    for (int j = 0; j < SB; ++j)
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(base + TILEA + (SB * wave + j) * 1024), 16, vb[j], so, 0, 0);
+  };
+
+  // ---- cache warm-up for the epilogue: during the last PFN steps of the main loop each
+  // wave DMAs one 1 KB piece of the tile's epilogue operand (bf16 W; the code also
+  // covers the two fp32 moment arrays) into a private LDS sink that is never read, so
+  // that the epilogue's loads find it in L2 / the memory-side cache instead of HBM.
+  constexpr int RW = 256 / NW;                      // tile rows per wave
+  const bool pf_w = EP == EP_UPDATE && U.weight_bf16;
+  const int rbytes = EP == EP_ADAM ? TBN * 4 : TBN * 2;   // bytes of one tile row of the operand
+  const int rpi = 1024 / rbytes, lpr = rbytes / 16;       // rows per DMA, lanes per row
+  // (measured: the warm-up pays off for the back-projection, whose K is short and whose
+  // epilogue moves W; for the projection the extra DMA traffic costs more than it saves)
+  const int PFN = (EP == EP_ADAM) ? 0 : (pf_w ? RW / rpi : 0);
+  const __amdgpu_buffer_rsrc_t rp0 = __builtin_amdgcn_make_buffer_rsrc(
+      EP == EP_ADAM ? (void*)P.e1 : P.c, (short)0, (int)(P.M * P.ldc * (EP == EP_ADAM ? 4 : 2)), 0x00020000);
+  const __amdgpu_buffer_rsrc_t rp1 = __builtin_amdgcn_make_buffer_rsrc(
+      EP == EP_ADAM ? (void*)P.e2 : P.c, (short)0, (int)(P.M * P.ldc * (EP == EP_ADAM ? 4 : 2)), 0x00020000);
+  const int nk0 = (int)(P.K / TBK);
+  const int kt0 = (nk0 - 1 - PFN > 0) ? nk0 - 1 - PFN : 0;    // first step that prefetches
+  auto pf_count = [&](int i) { return (i >= kt0 && i < kt0 + PFN && i < nk0 - 1) ? 1 : 0; };
+  auto prefetch = [&](int i) {
+    if (!pf_count(i)) return;
+    const int j = i - kt0;
+    const int half = (EP == EP_ADAM) ? (j >= RW / rpi) : 0;
+    const int jj = j - half * (RW / rpi);
+    const int64_t row = row0 + RW * wave + rpi * jj + lane / lpr;
+    const int64_t r2 = row < P.M ? row : P.M - 1;
+    const int ew = EP == EP_ADAM ? 4 : 8;             // elements per 16 bytes
+    const int64_t col = col0 + ew * (lane % lpr);
+    const int64_t c2 = col < P.N ? col : P.N - ew;
+    const uint32_t off = (uint32_t)((r2 * P.ldc + c2) * (EP == EP_ADAM ? 4 : 2));
+    lds_void* sink = (lds_void*)(smem + NS * STAGEB + wave * 1024);
+    if (half) __builtin_amdgcn_raw_ptr_buffer_load_lds(rp1, sink, 16, off, 0, 0, 0);
+    else __builtin_amdgcn_raw_ptr_buffer_load_lds(rp0, sink, 16, off, 0, 0, 0);
+  };
+
+  f32x16 acc[4][2];
+#pragma unroll
+  for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) acc[mb][nb][j] = 0.f;
+
+  // fragment byte offsets inside a stage (the two K halves of a step differ by chunk 2)
+  int offa[4][2], offb[2][2];
+#pragma unroll
+  for (int ks = 0; ks < 2; ++ks) {
+    const int c = 2 * ks + (lane >> 5);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      const int R = 128 * wm + 32 * mb + (lane & 31);
+      offa[mb][ks] = R * ROWB + ((c ^ swz(R)) << 4);
+    }
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) {
+      const int R = 64 * wn + 32 * nb + (lane & 31);
+      offb[nb][ks] = TILEA + R * ROWB + ((c ^ swz(R)) << 4);
+    }
+  }
+
+  // Main loop. Fragments are double-buffered in registers: F0 holds the first K half
+  // of the current stage, F1 the second. The stage barrier sits between the two
+  // MFMA groups, so that the LDS reads of one half always overlap the MFMAs of the
+  // other:
+  //   read F1 <- stage kt (2nd half); MFMA(F0)
+  //   wait for stage kt+1; barrier; DMA stage kt+NS-1 into the slot of stage kt-1
+  //   read F0 <- stage kt+1 (1st half); MFMA(F1)
+  // A slot is refilled only after every wave has passed the barrier that follows
+  // its last MFMA on that slot's data, and each wave waits (vmcnt) for its own DMA
+  // loads of a stage before the barrier that publishes it.
+  const int nk = (int)(P.K / TBK);
+  bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
+  auto read_frags = [&](int stage, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[2]) {
+    const char* st = smem + stage * STAGEB;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) fa[mb] = *reinterpret_cast<const bf16x8*>(st + offa[mb][ks]);
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb) fb[nb] = *reinterpret_cast<const bf16x8*>(st + offb[nb][ks]);
+  };
+  auto mfma_all = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[2]) {
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+      for (int nb = 0; nb < 2; ++nb)
+        acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[nb], fa[mb], acc[mb][nb], 0, 0, 0);
+  };
+#pragma unroll
+  for (int s = 0; s < NS - 1; ++s)
+    if (s < nk) issue(s, s);
+  wait_vm(OPS * (NS - 2 < nk - 1 ? NS - 2 : nk - 1));   // stages issued after stage 0 may stay in flight
+  stage_barrier();
+  read_frags(0, 0, fa0, fb0);
+  // The last step is peeled so that no fragment read sits behind a branch (the
+  // compiler then counts outstanding LDS reads exactly and waits only for the half
+  // it uses); sched_barrier(0) keeps the scheduler from interleaving the groups
+  // differently: every fragment read is issued before the MFMAs it overlaps.
+  int kt = 0;
+  for (; kt + 1 < nk; ++kt) {
+    read_frags(kt % NS, 1, fa1, fb1);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_all(fa0, fb0);
+    __builtin_amdgcn_sched_barrier(0);
+    // stage kt+1 was issued in step kt+2-NS; what may stay in flight is everything
+    // issued after it: that step's prefetch and the later steps' stages and prefetches
+    {
+      int newer = 0;
+      for (int i = kt + 2 - NS; i < kt; ++i) {
+        newer += pf_count(i);
+        if (i > kt + 2 - NS && i + NS - 1 < nk) newer += OPS;
+      }
+      wait_vm(newer);
+    }
+    stage_barrier();
+    if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
+    prefetch(kt);
+    read_frags((kt + 1) % NS, 0, fa0, fb0);
+    __builtin_amdgcn_sched_barrier(0);
+    mfma_all(fa1, fb1);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+  read_frags(kt % NS, 1, fa1, fb1);
+  mfma_all(fa0, fb0);
+  mfma_all(fa1, fb1);
+  __syncthreads();   // every wave is done with the stages: LDS becomes the epilogue slab
+
+  // ---- epilogue, one 32-row slab (block row mb) of the wave's sub-tile at a time.
+  // The global operands of the epilogue (moments, or W and the block magnitudes)
+  // are loaded before they are needed, many per lane at once, so that their
+  // latency is paid once per slab (moments) or once per tile (W) rather than once
+  // per row group.
+  float* slab = reinterpret_cast<float*>(smem) + wave * EPWAVE;
+  const int64_t wrow0 = row0 + 128 * wm, wcol0 = col0 + 64 * wn;
+  auto stage_slab = [&](int mb) {
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int c = 32 * nb + 8 * g + 4 * (lane >> 5);
+        *reinterpret_cast<float4*>(slab + (lane & 31) * EPLD + c) =
+            make_float4(acc[mb][nb][4 * g], acc[mb][nb][4 * g + 1], acc[mb][nb][4 * g + 2], acc[mb][nb][4 * g + 3]);
+      }
+  };
+  if constexpr (EP == EP_ADAM) {
+    // 16 lanes x 4 columns per row, 4 rows per pass, 8 passes per slab
+    const int cc = 4 * (lane & 15);
+    const int64_t col = wcol0 + cc;
+    float4 ev[8], qv[8];
+    auto load_slab = [&](int mb) {
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        const int64_t row = wrow0 + 32 * mb + 4 * p + (lane >> 4);
+        if (row < P.M && col < P.N) {
+          const int64_t idx = row * P.ldc + col;
+          ev[p] = *reinterpret_cast<const float4*>(P.e1 + idx);
+          qv[p] = *reinterpret_cast<const float4*>(P.e2 + idx);
+        }
+      }
+    };
+    load_slab(0);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      stage_slab(mb);
+      __syncthreads();
+#pragma unroll
+      for (int p = 0; p < 8; ++p) {
+        const int rr = 4 * p + (lane >> 4);
+        const int64_t row = wrow0 + 32 * mb + rr;
+        if (row < P.M && col < P.N) {
+          const float4 v = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
+          const int64_t idx = row * P.ldc + col;
+          float4 e = ev[p], q = qv[p];
+          bf16x4 o;
+          o[0] = f2bf(adam_out(v.x, e.x, q.x, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
+          o[1] = f2bf(adam_out(v.y, e.y, q.y, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
+          o[2] = f2bf(adam_out(v.z, e.z, q.z, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
+          o[3] = f2bf(adam_out(v.w, e.w, q.w, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
+          *reinterpret_cast<float4*>(P.e1 + idx) = e;
+          *reinterpret_cast<float4*>(P.e2 + idx) = q;
+          *reinterpret_cast<bf16x4*>((bf16*)P.c + idx) = o;
+        }
+      }
+      __syncthreads();
+      if (mb < 3) load_slab(mb + 1);
+    }
+  } else {
+    // 8 lanes x 8 columns per row, 8 rows per pass, 4 passes per slab
+    const int cc = 8 * (lane & 7);
+    const int64_t col = wcol0 + cc;
+    const bool one_mag = (U.B & 7) == 0;   // 8 aligned columns never straddle a block
+    if (U.weight_bf16 && one_mag) {
+      // W and magnitudes two slabs ahead (register double buffer)
+      bf16x8 wv[2][4];
+      float mg[2][4];
+      auto load_w = [&](int mb) {
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int64_t row = wrow0 + 32 * mb + 8 * p + (lane >> 3);
+          mg[mb & 1][p] = 1.f;
+          if (row < P.M && col < P.N) {
+            wv[mb & 1][p] = *reinterpret_cast<const bf16x8*>((const bf16*)P.c + row * P.ldc + col);
+            if (P.dM) mg[mb & 1][p] = P.dM[row * P.dM_ld + col / U.B];
+          }
+        }
+      };
+      load_w(0);
+      load_w(1);
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        stage_slab(mb);
+        __syncthreads();
+#pragma unroll
+        for (int p = 0; p < 4; ++p) {
+          const int rr = 8 * p + (lane >> 3);
+          const int64_t row = wrow0 + 32 * mb + rr;
+          if (row < P.M && col < P.N) {
+            const float4 v0 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
+            const float4 v1 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc + 4);
+            const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            const float m = mg[mb & 1][p];
+            bf16x8 o;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) o[q] = f2bf(bf2f(wv[mb & 1][p][q]) - U.lr * bf2f(f2bf(U.scale * (m * v[q]))));
+            *reinterpret_cast<bf16x8*>((bf16*)P.c + row * P.ldc + col) = o;
+          }
+        }
+        __syncthreads();
+        if (mb + 2 < 4) load_w(mb + 2);
+      }
+    } else {
+      // general form: fp32 W, or block sizes that split an 8-column group
+#pragma unroll
+      for (int mb = 0; mb < 4; ++mb) {
+        stage_slab(mb);
+        __syncthreads();
+#pragma unroll 2
+        for (int p = 0; p < 4; ++p) {
+          const int rr = 8 * p + (lane >> 3);
+          const int64_t row = wrow0 + 32 * mb + rr;
+          if (row < P.M && col < P.N) {
+            const float4 v0 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
+            const float4 v1 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc + 4);
+            const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+            float mag[8];
+            if (P.dM) {
+              const float* dmr = P.dM + row * P.dM_ld;
+#pragma unroll
+              for (int q = 0; q < 8; ++q) mag[q] = dmr[(col + q) / U.B];
+            } else {
+#pragma unroll
+              for (int q = 0; q < 8; ++q) mag[q] = 1.f;
+            }
+            const int64_t idx = row * P.ldc + col;
+            if (U.weight_bf16) {
+              bf16* W = (bf16*)P.c + idx;
+              const bf16x8 w = *reinterpret_cast<const bf16x8*>(W);
+              bf16x8 o;
+#pragma unroll
+              for (int q = 0; q < 8; ++q) o[q] = f2bf(bf2f(w[q]) - U.lr * bf2f(f2bf(U.scale * (mag[q] * v[q]))));
+              *reinterpret_cast<bf16x8*>(W) = o;
+            } else {
+              float* W = (float*)P.c + idx;
+              float4 w0 = *reinterpret_cast<const float4*>(W);
+              float4 w1 = *reinterpret_cast<const float4*>(W + 4);
+              w0.x -= U.lr * (U.scale * (mag[0] * v[0])); w0.y -= U.lr * (U.scale * (mag[1] * v[1]));
+              w0.z -= U.lr * (U.scale * (mag[2] * v[2])); w0.w -= U.lr * (U.scale * (mag[3] * v[3]));
+              w1.x -= U.lr * (U.scale * (mag[4] * v[4])); w1.y -= U.lr * (U.scale * (mag[5] * v[5]));
+              w1.z -= U.lr * (U.scale * (mag[6] * v[6])); w1.w -= U.lr * (U.scale * (mag[7] * v[7]));
+              *reinterpret_cast<float4*>(W) = w0;
+              *reinterpret_cast<float4*>(W + 4) = w1;
+            }
+          }
+        }
+        __syncthreads();
+      }
+    }
+  }
+}
+
+}  // namespace
+
+// Tile width along N: 256 (eight waves, four LDS stages, one workgroup per CU) or
+// 128 (four waves, three stages, two workgroups per CU).
+#ifndef GEMM_NT_BN
+#define GEMM_NT_BN 256
+#endif
+uint32_t gemm_nt_tiles_m(int64_t M) { return (uint32_t)((M + TBM - 1) / TBM); }
+uint32_t gemm_nt_tiles_n(int64_t N) { return (uint32_t)((N + GEMM_NT_BN - 1) / GEMM_NT_BN); }
+
+bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,
+                      const void* a, const void* b, const void* c, int weight_bf16) {
+  if (M <= 0 || N <= 0 || K <= 0 || K % TBK) return false;
+  if (lda % 8 || ldb % 8 || lda < K || ldb < K) return false;
+  if (((uintptr_t)a & 15) || ((uintptr_t)b & 15)) return false;
+  // byte extents must fit the 32-bit buffer offsets
+  if ((M - 1) * lda * 2 + K * 2 > 0x7FFFFFFFLL || (N - 1) * ldb * 2 + K * 2 > 0x7FFFFFFFLL) return false;
+  // the epilogue operands are addressed through 32-bit buffer offsets as well
+  if (M * ldc * (ep == EP_ADAM ? 4 : 2) > 0x7FFFFFFFLL) return false;
+  if (ep == EP_ADAM) {          // moments and N: 4-column groups (library memory, aligned)
+    if (N % 4 || ldc % 4) return false;
+  } else {                      // W: 8-column groups, 16-byte aligned rows
+    const int esz = weight_bf16 ? 2 : 4;
+    if (N % 8 || ldc % 8 || ((uintptr_t)c & 15) || (ldc * esz) % 16) return false;
+  }
+  return true;
+}
+
+namespace {
+template <int WN, int NS>
+hipError_t launch_nt(int ep, const GemmProb* probs_dev, uint32_t total_tiles, const GemmUniform& u, hipStream_t st) {
+  const dim3 grid(total_tiles), block(128 * WN);
+  if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, WN, NS>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, WN, NS>), grid, block, 0, st, probs_dev, u);
+  else return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+}  // namespace
+
+hipError_t launch_gemm_nt(int ep, const GemmProb* probs_dev, int nprob, uint32_t total_tiles, const GemmUniform& u0,
+                          hipStream_t st) {
+  if (total_tiles == 0 || nprob == 0) return hipSuccess;
+  GemmUniform u = u0;
+  u.nprob = nprob;
+  return launch_nt<GEMM_NT_BN / 64, GEMM_NT_BN == 256 ? 4 : 3>(ep, probs_dev, total_tiles, u, st);
+}

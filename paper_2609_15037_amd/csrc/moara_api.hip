@@ -15,8 +15,6 @@
 #include "gemm.h"
 #include "refresh.h"
 
-hipError_t launch_decompose_inv_only(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
-int decompose_tiles(int64_t m);
 
 namespace {
 
@@ -49,6 +47,8 @@ struct MatHost {
   float *inv = nullptr, *dM = nullptr, *mag1 = nullptr, *mag2 = nullptr;
   float *exp1 = nullptr, *exp2 = nullptr, *P32 = nullptr;
   void *N = nullptr, *Pop = nullptr, *Ptop = nullptr;
+  bool vpath = false;    // the decomposition writes V in bf16 for the large-tile projection
+  void* V = nullptr;     // m x n (RIGHT) or n x m (LEFT) bf16 direction workspace
 };
 
 struct TimedLaunch {
@@ -148,9 +148,24 @@ int32_t subspace_width(const moara_config& c, int64_t s, int32_t r) {
   return (int32_t)std::min<int64_t>(s, r + p);
 }
 
-size_t mat_state_bytes(const moara_config& c, int64_t m, int64_t s, int64_t L, int64_t k, int32_t r) {
+// Shapes for which the decomposition materialises V in bf16 and the projection runs
+// on the large-tile bf16 GEMM (see decompose.hip / gemm_nt.hip for the limits).
+bool vpath_shape_ok(const moara_config& c, int64_t m, int64_t n, int side, int32_t r) {
+  if (c.operand_dtype != MOARA_BF16 || !c.decompose) return false;
+  const int B = c.block_size;
+  if (B < 4 || B > 256 || (B & (B - 1))) return false;
+  if (n % 4 || r % 4) return false;
+  const int64_t k = (n + B - 1) / B;
+  if (2 * m * n > 0x7FFFFFFFLL) return false;
+  if (side == MOARA_SIDE_LEFT) return k <= DEC_VT_MAX_K && m % 32 == 0;
+  return k <= DEC_ROW_MAX_K && n % 32 == 0;
+}
+
+size_t mat_state_bytes(const moara_config& c, int64_t m, int64_t n, int side, int64_t s, int64_t L, int64_t k,
+                       int32_t r) {
   const int ob = elem_bytes(c.operand_dtype);
   size_t b = 0;
+  if (vpath_shape_ok(c, m, n, side, r)) b += align_up(2 * (size_t)m * n);   // V workspace
   b += align_up(4 * m * k) * 4;          // inv, dM, mag1, mag2
   b += align_up(4 * L * r) * 2;          // exp1, exp2
   b += align_up((size_t)ob * L * r);     // N
@@ -306,11 +321,12 @@ GemmUniform make_uniform(const moara_state* st, float lr) {
 }
 
 // Decompose (inv, and optionally Optimizer_M) for the listed matrices.
+// usev (indexed by matrix, may be null): write the bf16 V for that matrix as well.
 int run_decompose(moara_state* st, const std::vector<int>& idx, const void* const* grads, bool adam_m,
-                  hipStream_t stream) {
+                  hipStream_t stream, const std::vector<char>* usev = nullptr) {
   if (idx.empty()) return MOARA_OK;
-  std::vector<MatDev> md;
-  uint32_t tiles = 0;
+  std::vector<MatDev> md, mvt;
+  uint32_t tiles = 0, tiles_vt = 0;
   for (int i : idx) {
     const MatHost& h = st->mats[i];
     MatDev d{};
@@ -320,35 +336,109 @@ int run_decompose(moara_state* st, const std::vector<int>& idx, const void* cons
     const double t1 = (double)(h.t + 1);
     d.bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
     d.bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
-    d.tile_dec = tiles;
-    tiles += (uint32_t)decompose_tiles(h.m);
-    md.push_back(d);
+    const bool wv = adam_m && usev && (*usev)[i];
+    if (wv && h.side == MOARA_SIDE_LEFT) {
+      d.Vb = (bf16*)h.V; d.vt = 1;
+      d.tile_dec = tiles_vt;
+      tiles_vt += (uint32_t)decompose_vt_tiles(h.m);
+      mvt.push_back(d);
+    } else {
+      d.Vb = wv ? (bf16*)h.V : nullptr; d.vt = 0;
+      d.tile_dec = tiles;
+      tiles += (uint32_t)decompose_tiles(h.m);
+      md.push_back(d);
+    }
   }
   Stager sg;
   int rc = begin_stage(st, sg);
   if (rc) return rc;
-  const size_t off = sg.push(md.data(), md.size());
-  if (off == (size_t)-1) return fail(MOARA_E_OOM, "descriptor arena too small");
+  const size_t off = md.empty() ? 0 : sg.push(md.data(), md.size());
+  const size_t offv = mvt.empty() ? 0 : sg.push(mvt.data(), mvt.size());
+  if (off == (size_t)-1 || offv == (size_t)-1) return fail(MOARA_E_OOM, "descriptor arena too small");
   rc = end_stage(st, sg, stream);
   if (rc) return rc;
-  StepParams p = make_params(st, 0.f);
-  p.nmat = (int)md.size();
-  p.total_dec = tiles;
   TimerScope ts(st, MOARA_KERN_DECOMPOSE, stream);
-  const MatDev* dev = (const MatDev*)(st->dev_arena + off);
-  HIP_TRY(adam_m ? launch_decompose(dev, p, stream) : launch_decompose_inv_only(dev, p, stream));
+  if (!mvt.empty()) {
+    StepParams p = make_params(st, 0.f);
+    p.nmat = (int)mvt.size();
+    p.total_dec = tiles_vt;
+    HIP_TRY(launch_decompose_vt((const MatDev*)(st->dev_arena + offv), p, stream));
+  }
+  if (!md.empty()) {
+    StepParams p = make_params(st, 0.f);
+    p.nmat = (int)md.size();
+    p.total_dec = tiles;
+    const MatDev* dev = (const MatDev*)(st->dev_arena + off);
+    HIP_TRY(adam_m ? launch_decompose(dev, p, stream) : launch_decompose_inv_only(dev, p, stream));
+  }
   return MOARA_OK;
 }
 
 int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* weights, const void* const* grads,
-                     float lr, hipStream_t stream) {
+                     float lr, hipStream_t stream, const std::vector<char>* usev = nullptr) {
   const int ob = st->cfg.operand_dtype == MOARA_BF16;
   const int kind = ob ? KIND_BF16 : KIND_F32;
-  std::vector<GemmProb> left, right, back;
-  uint32_t tl = 0, tr = 0, tb = 0;
+  const int wbf = st->cfg.weight_dtype == MOARA_BF16;
+  std::vector<GemmProb> left, right, back, pnt, bnt;
+  uint32_t tl = 0, tr = 0, tb = 0, tpn = 0, tbn = 0;
   for (int i : idx) {
     const MatHost& h = st->mats[i];
     const double t1 = (double)(h.t + 1);
+    const float bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
+    const float bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
+    bool proj_done = false;
+    if (usev && (*usev)[i] &&
+        gemm_nt_eligible(EP_ADAM, h.L, h.r, h.s, h.s, h.s, h.r, h.V, h.Ptop, h.N, wbf)) {
+      // V was written by this step's decomposition: R^(T) (L x r) = V' (L x s) * Ptop^T
+      GemmProb g{};
+      g.M = h.L; g.N = h.r; g.K = h.s;
+      g.a = h.V; g.lda = h.s;
+      g.b = h.Ptop; g.ldb = h.s;
+      g.c = h.N; g.ldc = h.r;
+      g.e1 = h.exp1; g.e2 = h.exp2;
+      g.bc1 = bc1; g.bc2 = bc2;
+      g.a_bytes = (uint32_t)(2 * (size_t)h.L * h.s);
+      g.b_bytes = (uint32_t)(2 * (size_t)h.r * h.s);
+      g.tiles_n = gemm_nt_tiles_n(g.N);
+      g.tile_start = tpn;
+      tpn += gemm_nt_tiles_m(g.M) * g.tiles_n;
+      pnt.push_back(g);
+      proj_done = true;
+    }
+    {
+      const size_t rows_a = h.side == MOARA_SIDE_LEFT ? h.s : h.L, rows_b = h.side == MOARA_SIDE_LEFT ? h.L : h.s;
+      const void* ba = h.side == MOARA_SIDE_LEFT ? h.Pop : h.N;
+      const void* bb = h.side == MOARA_SIDE_LEFT ? h.N : h.Pop;
+      if (ob && gemm_nt_eligible(EP_UPDATE, h.m, h.n, h.r, h.r, h.r, h.n, ba, bb, weights[i], wbf)) {
+        GemmProb b{};
+        b.M = h.m; b.N = h.n; b.K = h.r;
+        b.a = ba; b.b = bb;
+        b.lda = h.r; b.ldb = h.r;
+        b.c = weights[i]; b.ldc = h.n;
+        b.dM = st->cfg.decompose ? h.dM : nullptr; b.dM_ld = h.k;
+        b.a_bytes = (uint32_t)(2 * rows_a * h.r);
+        b.b_bytes = (uint32_t)(2 * rows_b * h.r);
+        b.tiles_n = gemm_nt_tiles_n(b.N);
+        b.tile_start = tbn;
+        tbn += gemm_nt_tiles_m(b.M) * b.tiles_n;
+        bnt.push_back(b);
+      } else {
+        GemmProb b{};
+        b.M = h.m; b.N = h.n; b.K = h.r;
+        b.a = ba; b.b = bb;
+        b.lda = h.r; b.ldb = h.r;
+        b.c = weights[i]; b.ldc = h.n;
+        b.dM = st->cfg.decompose ? h.dM : nullptr; b.dM_ld = h.k;
+        b.tiles_n = gemm_tiles_n(kind, b.N);
+        b.vec = vec_flags_op(b.a, h.r, ob) | (vec_flags_op(b.b, h.r, ob) << 1);
+        const size_t e = ob ? 2 : 4;
+        set_extents(b, e * rows_a * h.r, e * h.r, e * rows_b * h.r, e * h.r, 0, 0);
+        b.tile_start = tb;
+        tb += gemm_tiles_m(kind, b.M) * b.tiles_n;
+        back.push_back(b);
+      }
+    }
+    if (proj_done) continue;
     GemmProb g{};
     g.M = h.L; g.N = h.r; g.K = h.s;
     g.a = grads[i]; g.lda = h.n;
@@ -356,8 +446,8 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
     g.b = h.Ptop; g.ldb = h.s;
     g.c = h.N; g.ldc = h.r;
     g.e1 = h.exp1; g.e2 = h.exp2;
-    g.bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
-    g.bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
+    g.bc1 = bc1;
+    g.bc2 = bc2;
     g.tiles_n = gemm_tiles_n(kind, g.N);
     g.vec = vec_flags_g((const float*)grads[i], h.n) | (vec_flags_op(h.Ptop, h.s, ob) << 1);
     set_extents(g, 4 * (size_t)h.m * h.n, 4 * (size_t)h.n, (size_t)(ob ? 2 : 4) * h.r * h.s, (size_t)(ob ? 2 : 4) * h.s,
@@ -365,24 +455,6 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
     const uint32_t nt = gemm_tiles_m(kind, g.M) * g.tiles_n;
     if (h.side == MOARA_SIDE_LEFT) { g.tile_start = tl; tl += nt; left.push_back(g); }
     else { g.tile_start = tr; tr += nt; right.push_back(g); }
-
-    GemmProb b{};
-    b.M = h.m; b.N = h.n; b.K = h.r;
-    if (h.side == MOARA_SIDE_LEFT) { b.a = h.Pop; b.b = h.N; }
-    else { b.a = h.N; b.b = h.Pop; }
-    b.lda = h.r; b.ldb = h.r;
-    b.c = weights[i]; b.ldc = h.n;
-    b.dM = st->cfg.decompose ? h.dM : nullptr; b.dM_ld = h.k;
-    b.tiles_n = gemm_tiles_n(kind, b.N);
-    b.vec = vec_flags_op(b.a, h.r, ob) | (vec_flags_op(b.b, h.r, ob) << 1);
-    {
-      const size_t e = ob ? 2 : 4;
-      const size_t rows_a = h.side == MOARA_SIDE_LEFT ? h.s : h.L, rows_b = h.side == MOARA_SIDE_LEFT ? h.L : h.s;
-      set_extents(b, e * rows_a * h.r, e * h.r, e * rows_b * h.r, e * h.r, 0, 0);
-    }
-    b.tile_start = tb;
-    tb += gemm_tiles_m(kind, b.M) * b.tiles_n;
-    back.push_back(b);
   }
   Stager sg;
   int rc = begin_stage(st, sg);
@@ -390,12 +462,17 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
   const size_t ol = left.empty() ? 0 : sg.push(left.data(), left.size());
   const size_t orr = right.empty() ? 0 : sg.push(right.data(), right.size());
   const size_t obk = back.empty() ? 0 : sg.push(back.data(), back.size());
-  if (ol == (size_t)-1 || orr == (size_t)-1 || obk == (size_t)-1) return fail(MOARA_E_OOM, "descriptor arena too small");
+  const size_t opn = pnt.empty() ? 0 : sg.push(pnt.data(), pnt.size());
+  const size_t obn = bnt.empty() ? 0 : sg.push(bnt.data(), bnt.size());
+  if (ol == (size_t)-1 || orr == (size_t)-1 || obk == (size_t)-1 || opn == (size_t)-1 || obn == (size_t)-1)
+    return fail(MOARA_E_OOM, "descriptor arena too small");
   rc = end_stage(st, sg, stream);
   if (rc) return rc;
   const GemmUniform u = make_uniform(st, lr);
   {
     TimerScope ts(st, MOARA_KERN_PROJECT, stream);
+    if (!pnt.empty())
+      HIP_TRY(launch_gemm_nt(EP_ADAM, (const GemmProb*)(st->dev_arena + opn), (int)pnt.size(), tpn, u, stream));
     if (!right.empty())
       HIP_TRY(launch_gemm(kind, A_G_ROW, B_KC, EP_ADAM, (const GemmProb*)(st->dev_arena + orr), (int)right.size(), tr, u, stream));
     if (!left.empty())
@@ -403,7 +480,10 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
   }
   {
     TimerScope ts(st, MOARA_KERN_BACKPROJ, stream);
-    HIP_TRY(launch_gemm(kind, A_KC, B_KC, EP_UPDATE, (const GemmProb*)(st->dev_arena + obk), (int)back.size(), tb, u, stream));
+    if (!bnt.empty())
+      HIP_TRY(launch_gemm_nt(EP_UPDATE, (const GemmProb*)(st->dev_arena + obn), (int)bnt.size(), tbn, u, stream));
+    if (!back.empty())
+      HIP_TRY(launch_gemm(kind, A_KC, B_KC, EP_UPDATE, (const GemmProb*)(st->dev_arena + obk), (int)back.size(), tb, u, stream));
   }
   return MOARA_OK;
 }
@@ -784,7 +864,7 @@ int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, i
   size_t tot = 0, ref = 0;
   for (int i = 0; i < n; ++i) {
     const Layout l = layout_of(descs[i], sides[i], cfg->block_size);
-    tot += mat_state_bytes(*cfg, descs[i].rows, l.s, l.L, l.k, ranks[i]);
+    tot += mat_state_bytes(*cfg, descs[i].rows, descs[i].cols, sides[i], l.s, l.L, l.k, ranks[i]);
     ref += mat_refresh_bytes(l.s, l.L, subspace_width(*cfg, l.s, ranks[i]));
   }
   *out_state_bytes = (int64_t)tot;
@@ -826,7 +906,8 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
     MatHost& h = st->mats[i];
     h.m = descs[i].rows; h.n = descs[i].cols; h.r = ranks[i]; h.side = sides[i];
     h.s = l.s; h.L = l.L; h.k = (int32_t)l.k;
-    tot += mat_state_bytes(*cfg, h.m, h.s, h.L, h.k, h.r);
+    h.vpath = vpath_shape_ok(*cfg, h.m, h.n, h.side, h.r);
+    tot += mat_state_bytes(*cfg, h.m, h.n, h.side, h.s, h.L, h.k, h.r);
   }
   if (hipMalloc(&st->block, tot) != hipSuccess) { free_state(st); return fail(MOARA_E_OOM, "state of %zu bytes", tot); }
   st->block_bytes = tot;
@@ -844,8 +925,9 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
     h.P32 = (float*)take(4 * h.s * h.r);
     h.Pop = take((size_t)ob * h.s * h.r);
     h.Ptop = take((size_t)ob * h.s * h.r);
+    if (h.vpath) h.V = take(2 * (size_t)h.m * h.n);
   }
-  st->arena_bytes = align_up(sizeof(MatDev) * n) + 3 * align_up(sizeof(GemmProb) * n) + 4 * ALIGN;
+  st->arena_bytes = 2 * align_up(sizeof(MatDev) * n) + 5 * align_up(sizeof(GemmProb) * n) + 8 * ALIGN;
   if (hipMalloc(&st->dev_arena, st->arena_bytes) != hipSuccess ||
       hipHostMalloc(&st->host_ring, st->arena_bytes * moara_state::NSLOT) != hipSuccess) {
     free_state(st);
@@ -900,8 +982,10 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
   }
   if (idx.empty()) return MOARA_OK;
   hipStream_t hs = (hipStream_t)stream;
+  std::vector<char> usev(st->n, 0);
+  for (int i : idx) usev[i] = st->mats[i].vpath && (((uintptr_t)grads[i] & 15) == 0);
   if (st->cfg.decompose) {
-    rc = run_decompose(st, idx, grads, true, hs);
+    rc = run_decompose(st, idx, grads, true, hs, &usev);
     if (rc) return rc;
   }
   if (!need.empty()) {
@@ -920,7 +1004,7 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
     }
     if ((rc = refresh_chunk(st, chunk, grads, hs))) return rc;
   }
-  rc = run_project_back(st, idx, weights, grads, lr, hs);
+  rc = run_project_back(st, idx, weights, grads, lr, hs, &usev);
   if (rc) return rc;
   for (int i : idx) st->mats[i].t += 1;
   return MOARA_OK;

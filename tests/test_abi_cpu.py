@@ -113,14 +113,29 @@ def test_create_state_validates_before_touching_the_gpu(field, value, code):
     assert e.value.status == code
 
 
-def test_state_bytes_counts_fp32_moments_and_projector_copies():
+def test_state_bytes_counts_fp32_moments_projector_copies_and_v_workspace():
     _lib()
     cfg = M.moara_default_config(rank_table=[64] * 10, block_size=64, operand_dtype=M.MOARA_BF16)
-    descs = M.make_descs([(256, 688, 4), (688, 256, 4)])
+    shapes = [(256, 688), (688, 256), (250, 688)]
+    descs = M.make_descs([(m, n, 4) for m, n in shapes])
     sb, rb = M.moara_state_bytes(cfg, descs)
     al = lambda x: (x + 255) // 256 * 256
     exp = 0
-    for m, n in [(256, 688), (688, 256)]:
+    for m, n in shapes:
         s, L, k, r = min(m, n), max(m, n), -(-n // 64), 64
         exp += 4 * al(4 * m * k) + 2 * al(4 * L * r) + al(2 * L * r) + al(4 * s * r) + 2 * al(2 * s * r)
+        # bf16 direction workspace of the large-tile projection: LEFT needs m % 32 == 0 and
+        # k <= 160, RIGHT n % 32 == 0 and k <= 512 (both: n % 4 == 0, r % 4 == 0)
+        left = m <= n
+        if n % 4 == 0 and r % 4 == 0 and ((left and m % 32 == 0 and k <= 160) or
+                                          (not left and n % 32 == 0 and k <= 512)):
+            exp += al(2 * m * n)
     assert sb == exp and rb > 0
+    # fp32 operands never materialise V
+    cfg32 = M.moara_default_config(rank_table=[64] * 10, block_size=64, operand_dtype=M.MOARA_F32)
+    sb32, _ = M.moara_state_bytes(cfg32, descs)
+    exp32 = 0
+    for m, n in shapes:
+        s, L, k, r = min(m, n), max(m, n), -(-n // 64), 64
+        exp32 += 4 * al(4 * m * k) + 2 * al(4 * L * r) + al(4 * L * r) + al(4 * s * r) + 2 * al(4 * s * r)
+    assert sb32 == exp32
