@@ -145,15 +145,20 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int B = p.B, gl = B >> 2, k = d.k;
   const int64_t n = d.n, m = d.m;
-  for (int64_t c0 = 0; c0 < n; c0 += VT_COLS) {
+  // the slab loop is software-pipelined: the 16 loads of the next slab are issued
+  // before the current slab is reduced, transposed and written out
+  float4 va[16], vb[16];
+  auto load = [&](int64_t c0, float4 (&v)[16]) {
     const int64_t c = c0 + 4 * lane;
-    float4 v[16];
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int rr = wave + 4 * i;
       v[i] = (rr < rows && c < n) ? *reinterpret_cast<const float4*>(d.G + (row0 + rr) * n + c)
                                   : make_float4(0.f, 0.f, 0.f, 0.f);
     }
+  };
+  auto process = [&](int64_t c0, const float4 (&v)[16]) {
+    const int64_t c = c0 + 4 * lane;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int rr = wave + 4 * i;
@@ -181,6 +186,14 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
       }
     }
     __syncthreads();
+  };
+  load(0, va);
+  for (int64_t c0 = 0; c0 < n; c0 += 2 * VT_COLS) {
+    if (c0 + VT_COLS < n) load(c0 + VT_COLS, vb);
+    process(c0, va);
+    if (c0 + VT_COLS >= n) break;
+    if (c0 + 2 * VT_COLS < n) load(c0 + 2 * VT_COLS, va);
+    process(c0 + VT_COLS, vb);
   }
   const int total = rows * k;
   for (int e = threadIdx.x; e < total; e += 256) {

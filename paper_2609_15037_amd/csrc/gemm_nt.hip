@@ -258,34 +258,32 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
       }
   };
   if constexpr (EP == EP_ADAM) {
-    // 16 lanes x 4 columns per row, 4 rows per pass, 8 passes per slab
+    // 16 lanes x 4 columns per row, 4 rows per pass, 8 passes per slab. The moments
+    // move in half-slabs (4 passes) through a register double buffer: the loads of
+    // the next half are in flight while the current one is computed.
     const int cc = 4 * (lane & 15);
     const int64_t col = wcol0 + cc;
-    float4 ev[8], qv[8];
-    auto load_slab = [&](int mb) {
+    float4 ev[2][4], qv[2][4];
+    auto load_half = [&](int h) {   // h = 2 mb + half
 #pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        const int64_t row = wrow0 + 32 * mb + 4 * p + (lane >> 4);
+      for (int p = 0; p < 4; ++p) {
+        const int64_t row = wrow0 + 16 * h + 4 * p + (lane >> 4);
         if (row < P.M && col < P.N) {
           const int64_t idx = row * P.ldc + col;
-          ev[p] = *reinterpret_cast<const float4*>(P.e1 + idx);
-          qv[p] = *reinterpret_cast<const float4*>(P.e2 + idx);
+          ev[h & 1][p] = *reinterpret_cast<const float4*>(P.e1 + idx);
+          qv[h & 1][p] = *reinterpret_cast<const float4*>(P.e2 + idx);
         }
       }
     };
-    load_slab(0);
+    auto compute_half = [&](int h) {
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      stage_slab(mb);
-      __syncthreads();
-#pragma unroll
-      for (int p = 0; p < 8; ++p) {
-        const int rr = 4 * p + (lane >> 4);
-        const int64_t row = wrow0 + 32 * mb + rr;
+      for (int p = 0; p < 4; ++p) {
+        const int rr = 16 * (h & 1) + 4 * p + (lane >> 4);
+        const int64_t row = wrow0 + 16 * h + 4 * p + (lane >> 4);
         if (row < P.M && col < P.N) {
           const float4 v = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
           const int64_t idx = row * P.ldc + col;
-          float4 e = ev[p], q = qv[p];
+          float4 e = ev[h & 1][p], q = qv[h & 1][p];
           bf16x4 o;
           o[0] = f2bf(adam_out(v.x, e.x, q.x, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
           o[1] = f2bf(adam_out(v.y, e.y, q.y, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
@@ -296,8 +294,17 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
           *reinterpret_cast<bf16x4*>((bf16*)P.c + idx) = o;
         }
       }
+    };
+    load_half(0);
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      load_half(2 * mb + 1);
+      stage_slab(mb);
       __syncthreads();
-      if (mb < 3) load_slab(mb + 1);
+      compute_half(2 * mb);
+      if (mb < 3) load_half(2 * mb + 2);
+      compute_half(2 * mb + 1);
+      __syncthreads();
     }
   } else {
     // 8 lanes x 8 columns per row, 8 rows per pass, 4 passes per slab
