@@ -27,6 +27,27 @@ typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 constexpr int DEC_ROWS = 16;   // rows per workgroup (4 waves x 4 rows)
 
+// Sum over aligned groups of gl lanes (gl a power of two <= 64). The first four
+// levels use DPP lane permutations (pairs within a quad, then the two quads of an
+// 8-lane half-row, then the two halves of a 16-lane row: mirror permutations pair
+// lanes whose values are already equal to their group's partial sum), the fifth a
+// ds_swizzle xor 16, the sixth a cross-half shuffle. Each level adds two equal
+// partial sums in either order, so every lane of a group ends with the same,
+// bit-identical total.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, true));
+}
+__device__ __forceinline__ float group_sum(float v, int gl) {
+  if (gl >= 2) v += dpp_f<0xB1>(v);    // quad_perm [1,0,3,2]
+  if (gl >= 4) v += dpp_f<0x4E>(v);    // quad_perm [2,3,0,1]
+  if (gl >= 8) v += dpp_f<0x141>(v);   // row_half_mirror
+  if (gl >= 16) v += dpp_f<0x140>(v);  // row_mirror
+  if (gl >= 32) v += __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F));   // lane ^ 16
+  if (gl >= 64) v += __shfl_xor(v, 32, 64);
+  return v;
+}
+
 __device__ __forceinline__ void block_out(const MatDev& d, const StepParams& p, int64_t row, int j,
                                           float ss, int adam_m) {
   const float M = sqrtf(ss);
@@ -83,6 +104,7 @@ __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ ma
     if (fast) {
       constexpr int UNR = 8;
       const int gl = B >> 2;   // lanes per block
+      const int lgB = __builtin_ctz(B);
       for (int64_t c00 = 0; c00 < n; c00 += 256 * UNR) {
         float4 v[UNR];
 #pragma unroll
@@ -94,8 +116,8 @@ __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ ma
         for (int u = 0; u < UNR; ++u) {
           const int64_t c = c00 + 256 * u + 4 * lane;
           float ss = v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
-          for (int o = 1; o < gl; o <<= 1) ss += __shfl_xor(ss, o, 64);
-          if ((lane & (gl - 1)) == 0 && c < n) sums[rr * k + (int)(c / B)] = ss;
+          ss = group_sum(ss, gl);
+          if ((lane & (gl - 1)) == 0 && c < n) sums[rr * k + (int)(c >> lgB)] = ss;
           if (d.Vb && c < n) {
             const float inv = 1.0f / (sqrtf(ss) + p.decomp_eps);
             bf16x4 o;
@@ -143,7 +165,7 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
   const int64_t row0 = (int64_t)(t - d.tile_dec) * VT_ROWS;
   const int rows = (int)((d.m - row0 < VT_ROWS) ? d.m - row0 : VT_ROWS);
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int B = p.B, gl = B >> 2, k = d.k;
+  const int B = p.B, gl = B >> 2, k = d.k, lgB = __builtin_ctz(B);
   const int64_t n = d.n, m = d.m;
   // the slab loop is software-pipelined: the 16 loads of the next slab are issued
   // before the current slab is reduced, transposed and written out
@@ -163,8 +185,8 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
     for (int i = 0; i < 16; ++i) {
       const int rr = wave + 4 * i;
       float ss = v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
-      for (int o = 1; o < gl; o <<= 1) ss += __shfl_xor(ss, o, 64);
-      if (rr < rows && c < n && (lane & (gl - 1)) == 0) sums[rr * k + (int)(c / B)] = ss;
+      ss = group_sum(ss, gl);
+      if (rr < rows && c < n && (lane & (gl - 1)) == 0) sums[rr * k + (int)(c >> lgB)] = ss;
       const float inv = 1.0f / (sqrtf(ss) + p.decomp_eps);
       bf16x2 a, b;
       a[0] = f2bf(v[i].x * inv); a[1] = f2bf(v[i].y * inv);
