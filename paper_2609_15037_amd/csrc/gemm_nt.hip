@@ -34,8 +34,6 @@ typedef __attribute__((address_space(3))) void lds_void;
 constexpr int TBM = 256, TBK = 32;
 constexpr int ROWB = TBK * 2;          // bytes per tile row per stage
 constexpr int TILEA = TBM * ROWB;      // 16 KB of A per stage
-constexpr int EPLD = 64 + 4;           // fp32 row stride of the epilogue staging slab
-constexpr int EPWAVE = 32 * EPLD;      // floats per wave slab
 
 __device__ __forceinline__ int swz(int R) { return ((R >> 1) & 3) ^ ((R >> 3) & 1); }
 
@@ -69,10 +67,13 @@ __device__ __forceinline__ int find_prob(const GemmProb* probs, int n, uint32_t 
   return lo;
 }
 
-// WN waves along N (BN = 64 WN columns), 2 along M; NS LDS stages.
-template <int EP, int WN, int NS>
-__global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict__ probs, GemmUniform U) {
-  constexpr int NW = 2 * WN, TBN = 64 * WN;
+// 2 x NWN waves, each owning a 128 x WTN sub-tile (4 x WTN/32 MFMA blocks); the tile
+// is 256 x (NWN WTN); NS LDS stages.
+template <int EP, int NWN, int WTN, int NS>
+__global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_nt(const GemmProb* __restrict__ probs, GemmUniform U) {
+  constexpr int NW = 2 * NWN, TBN = NWN * WTN, NB = WTN / 32;
+  constexpr int EPLD = WTN + 4;                      // fp32 row stride of the epilogue staging slab
+  constexpr int EPWAVE = 32 * EPLD;                  // floats per wave slab
   constexpr int TILEB = TBN * ROWB, STAGEB = TILEA + TILEB;
   constexpr int SA = 16 / NW, SB = (TBN / 16) / NW;   // 1 KB DMA slots per wave per stage
   constexpr int OPS = SA + SB;                        // DMA instructions per wave per stage
@@ -150,16 +151,16 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
     else __builtin_amdgcn_raw_ptr_buffer_load_lds(rp0, sink, 16, off, 0, 0, 0);
   };
 
-  f32x16 acc[4][2];
+  f32x16 acc[4][NB];
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) acc[mb][nb][j] = 0.f;
 
   // fragment byte offsets inside a stage (the two K halves of a step differ by chunk 2)
-  int offa[4][2], offb[2][2];
+  int offa[4][2], offb[4][2];
 #pragma unroll
   for (int ks = 0; ks < 2; ++ks) {
     const int c = 2 * ks + (lane >> 5);
@@ -169,8 +170,8 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
       offa[mb][ks] = R * ROWB + ((c ^ swz(R)) << 4);
     }
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) {
-      const int R = 64 * wn + 32 * nb + (lane & 31);
+    for (int nb = 0; nb < NB; ++nb) {
+      const int R = WTN * wn + 32 * nb + (lane & 31);
       offb[nb][ks] = TILEA + R * ROWB + ((c ^ swz(R)) << 4);
     }
   }
@@ -186,19 +187,19 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
   // its last MFMA on that slot's data, and each wave waits (vmcnt) for its own DMA
   // loads of a stage before the barrier that publishes it.
   const int nk = (int)(P.K / TBK);
-  bf16x8 fa0[4], fb0[2], fa1[4], fb1[2];
-  auto read_frags = [&](int stage, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[2]) {
+  bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
+  auto read_frags = [&](int stage, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
     const char* st = smem + stage * STAGEB;
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb) fa[mb] = *reinterpret_cast<const bf16x8*>(st + offa[mb][ks]);
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb) fb[nb] = *reinterpret_cast<const bf16x8*>(st + offb[nb][ks]);
+    for (int nb = 0; nb < NB; ++nb) fb[nb] = *reinterpret_cast<const bf16x8*>(st + offb[nb][ks]);
   };
-  auto mfma_all = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[2]) {
+  auto mfma_all = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4]) {
 #pragma unroll
     for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-      for (int nb = 0; nb < 2; ++nb)
+      for (int nb = 0; nb < NB; ++nb)
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[nb], fa[mb], acc[mb][nb], 0, 0, 0);
   };
 #pragma unroll
@@ -246,10 +247,10 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
   // latency is paid once per slab (moments) or once per tile (W) rather than once
   // per row group.
   float* slab = reinterpret_cast<float*>(smem) + wave * EPWAVE;
-  const int64_t wrow0 = row0 + 128 * wm, wcol0 = col0 + 64 * wn;
+  const int64_t wrow0 = row0 + 128 * wm, wcol0 = col0 + WTN * wn;
   auto stage_slab = [&](int mb) {
 #pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
       for (int g = 0; g < 4; ++g) {
         const int c = 32 * nb + 8 * g + 4 * (lane >> 5);
@@ -258,16 +259,17 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
       }
   };
   if constexpr (EP == EP_ADAM) {
-    // 16 lanes x 4 columns per row, 4 rows per pass, 8 passes per slab. The moments
-    // move in half-slabs (4 passes) through a register double buffer: the loads of
-    // the next half are in flight while the current one is computed.
-    const int cc = 4 * (lane & 15);
+    // LPR lanes x 4 columns per row, RPP rows per pass, 32 / RPP passes per slab. The
+    // moments move in half-slabs through a register double buffer: the loads of the
+    // next half are in flight while the current one is computed.
+    constexpr int LPR = WTN / 4, RPP = 64 / LPR, HP = 16 / RPP;   // HP passes per half-slab
+    const int cc = 4 * (lane % LPR);
     const int64_t col = wcol0 + cc;
-    float4 ev[2][4], qv[2][4];
+    float4 ev[2][HP], qv[2][HP];
     auto load_half = [&](int h) {   // h = 2 mb + half
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int64_t row = wrow0 + 16 * h + 4 * p + (lane >> 4);
+      for (int p = 0; p < HP; ++p) {
+        const int64_t row = wrow0 + 16 * h + RPP * p + lane / LPR;
         if (row < P.M && col < P.N) {
           const int64_t idx = row * P.ldc + col;
           ev[h & 1][p] = *reinterpret_cast<const float4*>(P.e1 + idx);
@@ -277,9 +279,9 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
     };
     auto compute_half = [&](int h) {
 #pragma unroll
-      for (int p = 0; p < 4; ++p) {
-        const int rr = 16 * (h & 1) + 4 * p + (lane >> 4);
-        const int64_t row = wrow0 + 16 * h + 4 * p + (lane >> 4);
+      for (int p = 0; p < HP; ++p) {
+        const int rr = 16 * (h & 1) + RPP * p + lane / LPR;
+        const int64_t row = wrow0 + 16 * h + RPP * p + lane / LPR;
         if (row < P.M && col < P.N) {
           const float4 v = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
           const int64_t idx = row * P.ldc + col;
@@ -307,18 +309,19 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
       __syncthreads();
     }
   } else {
-    // 8 lanes x 8 columns per row, 8 rows per pass, 4 passes per slab
-    const int cc = 8 * (lane & 7);
+    // LPR lanes x 8 columns per row, RPP rows per pass, PPS passes per slab
+    constexpr int LPR = WTN / 8, RPP = 64 / LPR, PPS = 32 / RPP;
+    const int cc = 8 * (lane % LPR);
     const int64_t col = wcol0 + cc;
     const bool one_mag = (U.B & 7) == 0;   // 8 aligned columns never straddle a block
     if (U.weight_bf16 && one_mag) {
       // W and magnitudes two slabs ahead (register double buffer)
-      bf16x8 wv[2][4];
-      float mg[2][4];
+      bf16x8 wv[2][PPS];
+      float mg[2][PPS];
       auto load_w = [&](int mb) {
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const int64_t row = wrow0 + 32 * mb + 8 * p + (lane >> 3);
+        for (int p = 0; p < PPS; ++p) {
+          const int64_t row = wrow0 + 32 * mb + RPP * p + lane / LPR;
           mg[mb & 1][p] = 1.f;
           if (row < P.M && col < P.N) {
             wv[mb & 1][p] = *reinterpret_cast<const bf16x8*>((const bf16*)P.c + row * P.ldc + col);
@@ -333,8 +336,8 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
         stage_slab(mb);
         __syncthreads();
 #pragma unroll
-        for (int p = 0; p < 4; ++p) {
-          const int rr = 8 * p + (lane >> 3);
+        for (int p = 0; p < PPS; ++p) {
+          const int rr = RPP * p + lane / LPR;
           const int64_t row = wrow0 + 32 * mb + rr;
           if (row < P.M && col < P.N) {
             const float4 v0 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
@@ -357,8 +360,8 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
         stage_slab(mb);
         __syncthreads();
 #pragma unroll 2
-        for (int p = 0; p < 4; ++p) {
-          const int rr = 8 * p + (lane >> 3);
+        for (int p = 0; p < PPS; ++p) {
+          const int rr = RPP * p + lane / LPR;
           const int64_t row = wrow0 + 32 * mb + rr;
           if (row < P.M && col < P.N) {
             const float4 v0 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
@@ -402,11 +405,22 @@ __global__ __launch_bounds__(128 * WN) void k_gemm_nt(const GemmProb* __restrict
 
 }  // namespace
 
-// Tile width along N: 256 (eight waves, four LDS stages, one workgroup per CU) or
-// 128 (four waves, three stages, two workgroups per CU).
-#ifndef GEMM_NT_BN
-#define GEMM_NT_BN 256
+// Variants (measured on the 7B-shaped step, the first is the fastest):
+//   1: 256 x 256 tiles, eight waves of 128 x 64, four LDS stages, one workgroup per CU;
+//   2: 256 x 256 tiles, four waves of 128 x 128 (accumulators in AGPRs), four stages
+//      (faster main loop, but half the waves to hide the epilogue's memory latency);
+//   3: 256 x 128 tiles, four waves of 128 x 64, three stages, two workgroups per CU.
+#ifndef GEMM_NT_VARIANT
+#define GEMM_NT_VARIANT 1
 #endif
+#if GEMM_NT_VARIANT == 1
+constexpr int V_NWN = 4, V_WTN = 64, V_NS = 4;
+#elif GEMM_NT_VARIANT == 2
+constexpr int V_NWN = 2, V_WTN = 128, V_NS = 4;
+#else
+constexpr int V_NWN = 2, V_WTN = 64, V_NS = 3;
+#endif
+constexpr int GEMM_NT_BN = V_NWN * V_WTN;
 uint32_t gemm_nt_tiles_m(int64_t M) { return (uint32_t)((M + TBM - 1) / TBM); }
 uint32_t gemm_nt_tiles_n(int64_t N) { return (uint32_t)((N + GEMM_NT_BN - 1) / GEMM_NT_BN); }
 
@@ -429,11 +443,11 @@ bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int6
 }
 
 namespace {
-template <int WN, int NS>
+template <int NWN, int WTN, int NS>
 hipError_t launch_nt(int ep, const GemmProb* probs_dev, uint32_t total_tiles, const GemmUniform& u, hipStream_t st) {
-  const dim3 grid(total_tiles), block(128 * WN);
-  if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, WN, NS>), grid, block, 0, st, probs_dev, u);
-  else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, WN, NS>), grid, block, 0, st, probs_dev, u);
+  const dim3 grid(total_tiles), block(128 * NWN);
+  if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -444,5 +458,5 @@ hipError_t launch_gemm_nt(int ep, const GemmProb* probs_dev, int nprob, uint32_t
   if (total_tiles == 0 || nprob == 0) return hipSuccess;
   GemmUniform u = u0;
   u.nprob = nprob;
-  return launch_nt<GEMM_NT_BN / 64, GEMM_NT_BN == 256 ? 4 : 3>(ep, probs_dev, total_tiles, u, st);
+  return launch_nt<V_NWN, V_WTN, V_NS>(ep, probs_dev, total_tiles, u, st);
 }
