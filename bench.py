@@ -52,23 +52,69 @@ def parse():
     return ap.parse_args()
 
 
-def algorithmic_cost(wl, operand_bytes: int, weight_bytes: int):
-    """Per-step algorithmic bytes and flops per kernel (what the method must move or compute)."""
+def v_path(wl, m, operand: str) -> bool:
+    """Whether the library materialises V in bf16 for this matrix (the large-tile projection
+    path): the shape rule of the library's state layout."""
+    if operand != "bf16":
+        return False
+    B = wl.block_size
+    if B < 4 or B > 256 or (B & (B - 1)):
+        return False
+    r = wl.rank_of(m)
+    if m.cols % 4 or r % 4:
+        return False
+    k = -(-m.cols // B)
+    if m.rows <= m.cols:
+        return k <= 160 and m.rows % 32 == 0
+    return k <= 512 and m.cols % 32 == 0
+
+
+def algorithmic_cost(wl, operand: str, weight_bytes: int):
+    """Per-step algorithmic bytes and flops per kernel (what each kernel of this split must
+    move or compute, given its inputs and outputs)."""
+    ob = 2 if operand == "bf16" else 4
     cost = {"decompose": [0, 0], "project": [0, 0], "backproject": [0, 0]}
     for m in wl.matrices:
         r = wl.rank_of(m)
         M, N = m.rows, m.cols
         s, L = (M, N) if M <= N else (N, M)
         k = -(-N // wl.block_size)
-        # decompose + Optimizer_M: read G; write inv and dM; read+write two magnitude moments
-        cost["decompose"][0] += 4 * M * N + 4 * M * k * 6
-        # projection + Optimizer_V: read G and inv, read P, read+write two fp32 moments, write N
-        cost["project"][0] += 4 * M * N + 4 * M * k + operand_bytes * s * r + 16 * L * r + operand_bytes * L * r
+        vp = v_path(wl, m, operand)
+        # decompose + Optimizer_M: read G; write inv and dM; read+write two magnitude moments;
+        # write V in bf16 on the large-tile path
+        cost["decompose"][0] += 4 * M * N + 4 * M * k * 6 + (2 * M * N if vp else 0)
+        # projection + Optimizer_V: read V (or G and inv), read P, read+write two fp32 moments, write N
+        cost["project"][0] += (2 * M * N if vp else 4 * M * N + 4 * M * k) + ob * s * r + 16 * L * r + ob * L * r
         cost["project"][1] += 2 * M * N * r
         # back-projection + update: read N and P, read dM, read+write W
-        cost["backproject"][0] += operand_bytes * L * r + operand_bytes * s * r + 4 * M * k + 2 * weight_bytes * M * N
+        cost["backproject"][0] += ob * L * r + ob * s * r + 4 * M * k + 2 * weight_bytes * M * N
         cost["backproject"][1] += 2 * M * N * r
     return cost
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "llama2_7b_step_pmc_traffic.txt")
+TRAFFIC_SOURCES = ["paper_2609_15037_amd/csrc/common.h", "paper_2609_15037_amd/csrc/gemm.h",
+                   "paper_2609_15037_amd/csrc/gemm_nt.hip", "paper_2609_15037_amd/csrc/decompose.hip"]
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed rocprofv3 FETCH_SIZE / WRITE_SIZE
+    summary, if it was taken on this workload with the kernel sources as they are now."""
+    import hashlib
+    if workload != "llama2_7b" or not os.path.exists(TRAFFIC_FILE):
+        return None
+    h = hashlib.sha256()
+    for src in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    rec, val = None, None
+    for line in open(TRAFFIC_FILE):
+        parts = line.split()
+        if len(parts) == 2 and parts[0] == "sources-sha256":
+            rec = parts[1]
+        if len(parts) == 3 and parts[0] == "traffic-bytes-per-launch" and parts[1] == kernel:
+            val = float(parts[2])
+    return val if rec == h.hexdigest() else None
 
 
 def method_cost(wl, operand_bytes: int, weight_bytes: int):
@@ -231,7 +277,7 @@ def main():
         nl, ms = M.moara_kernel_stats(st, kid, stream=stream)
         kern[name] = {"launches": nl, "ms_total": ms, "ms_per_step": ms / max(1, a.steps),
                       "ms_per_launch": ms / max(1, nl)}
-    cost = algorithmic_cost(wl, ob, wb)
+    cost = algorithmic_cost(wl, operand, wb)
     peak_mfma = PEAK_BF16 if operand == "bf16" else PEAK_F32
     for name, (bytes_, flops) in cost.items():
         t = kern[name]["ms_per_step"] / 1e3
@@ -256,7 +302,7 @@ def main():
                  "alg_bytes_per_launch": dk["alg_bytes_per_step"] / launches_per_step,
                  "alg_flops_per_launch": dk["alg_flops_per_step"] / launches_per_step,
                  "avg_launch_ms": dk["ms_total"] / max(1, dk["launches"]),
-                 "traffic": None})
+                 "traffic": measured_traffic(dom, wl.name) if not a.layers else None})
 
     mb, mf = method_cost(wl, ob, wb)
     step_roof_ms = max(mb / PEAK_HBM, mf / peak_mfma) * 1e3
