@@ -95,7 +95,7 @@ __device__ __forceinline__ float adam_out(float x, float& e, float& q, float b1,
 struct GemmProb;
 hipError_t launch_decompose(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
 hipError_t launch_decompose_inv_only(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
-hipError_t launch_decompose_vt(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
+hipError_t launch_decompose_vt(const MatDev* mats_dev, const StepParams& p, int adam_m, hipStream_t st);
 int decompose_tiles(int64_t m);
 int decompose_vt_tiles(int64_t m);
 // limits of the V-writing decomposition paths (blocks per row)

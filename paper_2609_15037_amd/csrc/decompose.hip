@@ -228,9 +228,9 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
 int decompose_tiles(int64_t m) { return (int)((m + DEC_ROWS - 1) / DEC_ROWS); }
 int decompose_vt_tiles(int64_t m) { return (int)((m + VT_ROWS - 1) / VT_ROWS); }
 
-hipError_t launch_decompose_vt(const MatDev* mats_dev, const StepParams& p, hipStream_t st) {
+hipError_t launch_decompose_vt(const MatDev* mats_dev, const StepParams& p, int adam_m, hipStream_t st) {
   if (p.total_dec == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_decompose_vt, dim3(p.total_dec), dim3(256), 0, st, mats_dev, p, 1);
+  hipLaunchKernelGGL(k_decompose_vt, dim3(p.total_dec), dim3(256), 0, st, mats_dev, p, adam_m);
   return hipGetLastError();
 }
 

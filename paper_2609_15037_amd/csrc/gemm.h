@@ -22,7 +22,8 @@ enum { B_KC = 0, B_NC = 1 };
 //   EP_ADAM   : Optimizer_V on the projected tile; moments e1/e2 and output c are [M][N]
 //   EP_UPDATE : W[i][j] -= lr * scale * dM[i][j/B] * C[i][j] (bf16 or fp32 W in c)
 //   EP_STORE  : c[i*ldc + j] = C[i][j] (fp32)
-enum { EP_ADAM = 0, EP_UPDATE = 1, EP_STORE = 2 };
+//   EP_STORE_BF16: c[i*ldc + j] = bf16(C[i][j])   (large-tile path only)
+enum { EP_ADAM = 0, EP_UPDATE = 1, EP_STORE = 2, EP_STORE_BF16 = 3 };
 
 struct GemmProb {
   int64_t M, N, K;
@@ -84,7 +85,7 @@ hipError_t launch_gemm(int kind, int amode, int bmode, int ep, const GemmProb* p
                        uint32_t total_tiles, const GemmUniform& u, hipStream_t st);
 
 // Large-tile bf16 path (gemm_nt.hip): A (M x K) and B (N x K) bf16, K-contiguous,
-// EP_ADAM or EP_UPDATE; 256-row tiles.
+// EP_ADAM, EP_UPDATE, EP_STORE or EP_STORE_BF16; 256-row tiles.
 uint32_t gemm_nt_tiles_m(int64_t M);
 uint32_t gemm_nt_tiles_n(int64_t N);
 bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int64_t ldb, int64_t ldc,

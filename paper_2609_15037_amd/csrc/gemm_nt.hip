@@ -22,6 +22,7 @@
 // N and W move as full 128-byte row segments.
 //   EP_ADAM  : Optimizer_V on the projected tile (moments e1/e2, output N bf16).
 //   EP_UPDATE: W[i][j] -= lr * bf16(scale * dM[i][j/B] * C[i][j]) (bf16 or fp32 W).
+//   EP_STORE / EP_STORE_BF16: C stored as fp32 / bf16 (the refresh's subspace products).
 #include "gemm.h"
 
 namespace {
@@ -258,7 +259,34 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
             make_float4(acc[mb][nb][4 * g], acc[mb][nb][4 * g + 1], acc[mb][nb][4 * g + 2], acc[mb][nb][4 * g + 3]);
       }
   };
-  if constexpr (EP == EP_ADAM) {
+  if constexpr (EP == EP_STORE || EP == EP_STORE_BF16) {
+    // LPR lanes x 4 columns per row, RPP rows per pass, 32 / RPP passes per slab
+    constexpr int LPR = WTN / 4, RPP = 64 / LPR, PPS = 32 / RPP;
+    const int cc = 4 * (lane % LPR);
+    const int64_t col = wcol0 + cc;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+      stage_slab(mb);
+      __syncthreads();
+#pragma unroll
+      for (int p = 0; p < PPS; ++p) {
+        const int rr = RPP * p + lane / LPR;
+        const int64_t row = wrow0 + 32 * mb + rr;
+        if (row < P.M && col < P.N) {
+          const float4 v = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
+          const int64_t idx = row * P.ldc + col;
+          if constexpr (EP == EP_STORE) {
+            *reinterpret_cast<float4*>((float*)P.c + idx) = v;
+          } else {
+            bf16x4 o;
+            o[0] = f2bf(v.x); o[1] = f2bf(v.y); o[2] = f2bf(v.z); o[3] = f2bf(v.w);
+            *reinterpret_cast<bf16x4*>((bf16*)P.c + idx) = o;
+          }
+        }
+      }
+      __syncthreads();
+    }
+  } else if constexpr (EP == EP_ADAM) {
     // LPR lanes x 4 columns per row, RPP rows per pass, 32 / RPP passes per slab. The
     // moments move in half-slabs through a register double buffer: the loads of the
     // next half are in flight while the current one is computed.
@@ -433,7 +461,10 @@ bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int6
   if ((M - 1) * lda * 2 + K * 2 > 0x7FFFFFFFLL || (N - 1) * ldb * 2 + K * 2 > 0x7FFFFFFFLL) return false;
   // the epilogue operands are addressed through 32-bit buffer offsets as well
   if (M * ldc * (ep == EP_ADAM ? 4 : 2) > 0x7FFFFFFFLL) return false;
-  if (ep == EP_ADAM) {          // moments and N: 4-column groups (library memory, aligned)
+  if (ep == EP_STORE || ep == EP_STORE_BF16) {   // 4-column groups, 16- (8-) byte aligned
+    const int esz = ep == EP_STORE ? 4 : 2;
+    if (N % 4 || ldc % 4 || ((uintptr_t)c & (4 * esz - 1))) return false;
+  } else if (ep == EP_ADAM) {   // moments and N: 4-column groups (library memory, aligned)
     if (N % 4 || ldc % 4) return false;
   } else {                      // W: 8-column groups, 16-byte aligned rows
     const int esz = weight_bf16 ? 2 : 4;
@@ -448,6 +479,8 @@ hipError_t launch_nt(int ep, const GemmProb* probs_dev, uint32_t total_tiles, co
   const dim3 grid(total_tiles), block(128 * NWN);
   if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_STORE) hipLaunchKernelGGL((k_gemm_nt<EP_STORE, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_STORE_BF16) hipLaunchKernelGGL((k_gemm_nt<EP_STORE_BF16, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }

@@ -174,9 +174,12 @@ size_t mat_state_bytes(const moara_config& c, int64_t m, int64_t n, int side, in
   return b;
 }
 
-size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w) {
+// bf: the matrix runs its early subspace iterations on the bf16 V (other orientation
+// of V and bf16 copies of the iterates)
+size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w, bool bf) {
   const int64_t wpad = (w + 63) / 64 * 64;
   size_t b = 0;
+  if (bf) b += align_up(2 * (size_t)s * L) + align_up(2 * (size_t)w * s) + align_up(2 * (size_t)w * L);
   b += align_up(4 * s * w) * 2;            // Z, Z2
   b += align_up(4 * L * w) * 2;            // Y, Y2
   b += align_up(8 * (size_t)w * w) * 2;    // C, X
@@ -336,7 +339,7 @@ int run_decompose(moara_state* st, const std::vector<int>& idx, const void* cons
     const double t1 = (double)(h.t + 1);
     d.bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
     d.bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
-    const bool wv = adam_m && usev && (*usev)[i];
+    const bool wv = usev && (*usev)[i];
     if (wv && h.side == MOARA_SIDE_LEFT) {
       d.Vb = (bf16*)h.V; d.vt = 1;
       d.tile_dec = tiles_vt;
@@ -362,7 +365,7 @@ int run_decompose(moara_state* st, const std::vector<int>& idx, const void* cons
     StepParams p = make_params(st, 0.f);
     p.nmat = (int)mvt.size();
     p.total_dec = tiles_vt;
-    HIP_TRY(launch_decompose_vt((const MatDev*)(st->dev_arena + offv), p, stream));
+    HIP_TRY(launch_decompose_vt((const MatDev*)(st->dev_arena + offv), p, adam_m ? 1 : 0, stream));
   }
   if (!md.empty()) {
     StepParams p = make_params(st, 0.f);
@@ -491,6 +494,8 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
 // ------------------------------------------------------------------ refresh driver
 struct RefMat {
   int idx;
+  bool bf;               // early iterations on the bf16 V (large-tile GEMMs)
+  void *XL, *Zt, *Yt;    // bf16: V as s x L; iterates Z^T (w x s) and Y^T (w x L)
   int64_t s, L;
   int32_t w, wpad;
   float *Z, *Z2, *Y, *Y2, *Rinv;
@@ -521,7 +526,12 @@ constexpr int MAX_SWEEPS = 14;
 //   Z2 <- Gaussian ; Z <- orth(Z2)
 //   repeat: Y <- X Z ; Z2 <- X^T Y ; Z <- orth(Z2)        (q - 1 times)
 //   last  : Y <- X Z ; Y2 <- orth(Y) ; Z2 <- X^T Y2 ; Jacobi on Z2 ; P <- top r
-int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream) {
+// usev (indexed by matrix, may be null): the bf16 V of that matrix was written by this
+// step's decomposition, so its early subspace iterations can run on bf16 MFMA.
+constexpr int REFRESH_F32_ITERS = 3;   // the last iterations always run in fp32 on G and inv
+
+int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream,
+                  const std::vector<char>* usev) {
   const moara_config& c = st->cfg;
   size_t need = 0;
   std::vector<RefMat> rm;
@@ -531,7 +541,10 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.idx = i; x.s = h.s; x.L = h.L;
     x.w = subspace_width(c, h.s, h.r);
     x.wpad = (x.w + 63) / 64 * 64;
-    need += mat_refresh_bytes(h.s, h.L, x.w);
+    x.bf = usev && (*usev)[i] && c.refresh_iters > REFRESH_F32_ITERS && x.w % 8 == 0 &&
+           gemm_nt_eligible(EP_STORE_BF16, x.w, h.L, h.s, h.s, h.s, h.L, h.V, h.V, h.V, 0) &&
+           gemm_nt_eligible(EP_STORE, h.s, x.w, h.L, h.L, h.L, x.w, h.V, h.V, h.V, 0);
+    need += mat_refresh_bytes(h.s, h.L, x.w, x.bf);
     rm.push_back(x);
   }
   int rc = ensure_ref_ws(st, need);
@@ -539,6 +552,11 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   char* p = st->ref_ws;
   auto take = [&](size_t b) { char* q = p; p += align_up(b); return q; };
   for (auto& x : rm) {
+    if (x.bf) {
+      x.XL = take(2 * (size_t)x.s * x.L);
+      x.Zt = take(2 * (size_t)x.w * x.s);
+      x.Yt = take(2 * (size_t)x.w * x.L);
+    }
     x.Z = (float*)take(4 * x.s * x.w);
     x.Z2 = (float*)take(4 * x.s * x.w);
     x.Y = (float*)take(4 * x.L * x.w);
@@ -611,13 +629,13 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     return std::make_pair(g, t);
   };
   // Y = X Z  (tall: M = L, K = s)   or   Z2 = X^T Yin  (M = s, K = L)
-  auto big_list = [&](int side, bool xt, bool fromY2) {
+  auto big_list = [&](int side, bool xt, bool fromY2, bool only_f32 = false) {
     std::vector<GemmProb> g;
     uint32_t t = 0;
     for (int q = 0; q < nm; ++q) {
       const RefMat& x = rm[q];
       const MatHost& h = st->mats[x.idx];
-      if (h.side != side) continue;
+      if (h.side != side || (only_f32 && x.bf)) continue;
       GemmProb gp{};
       gp.M = xt ? x.s : x.L; gp.N = x.w; gp.K = xt ? x.L : x.s;
       gp.a = grads[x.idx]; gp.lda = h.n;
@@ -655,6 +673,39 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   auto xzR = big_list(MOARA_SIDE_RIGHT, false, false), xzL = big_list(MOARA_SIDE_LEFT, false, false);
   auto xtR = big_list(MOARA_SIDE_RIGHT, true, false), xtL = big_list(MOARA_SIDE_LEFT, true, false);
   auto xt2R = big_list(MOARA_SIDE_RIGHT, true, true), xt2L = big_list(MOARA_SIDE_LEFT, true, true);
+  // early (bf16) iterations: the fp32 products of the matrices without a bf16 V ...
+  auto fxzR = big_list(MOARA_SIDE_RIGHT, false, false, true), fxzL = big_list(MOARA_SIDE_LEFT, false, false, true);
+  auto fxtR = big_list(MOARA_SIDE_RIGHT, true, false, true), fxtL = big_list(MOARA_SIDE_LEFT, true, false, true);
+  // ... and, for the others, Z^T (bf16) = transpose(Z), Y^T = Z^T X_K^T, Z2 = X_L Y  (X_K: L x s = the
+  // step's V workspace, X_L: s x L = its transpose)
+  std::vector<TransProb> tZ, tX;
+  std::vector<GemmProb> nY, nZ;
+  uint32_t ttz = 0, ttx = 0, tny = 0, tnz = 0;
+  for (int q = 0; q < nm; ++q) {
+    const RefMat& x = rm[q];
+    if (!x.bf) continue;
+    const MatHost& h = st->mats[x.idx];
+    TransProb a{};
+    a.in = x.Z; a.out = x.Zt; a.rows = x.s; a.cols = x.w; a.ldi = x.w; a.ldo = x.s; a.in_f32 = 1;
+    a.tiles_c = (int32_t)((x.w + 63) / 64); a.tile_start = ttz; ttz += transpose_tiles(x.s, x.w);
+    tZ.push_back(a);
+    TransProb b{};
+    b.in = h.V; b.out = x.XL; b.rows = x.L; b.cols = x.s; b.ldi = x.s; b.ldo = x.L; b.in_f32 = 0;
+    b.tiles_c = (int32_t)((x.s + 63) / 64); b.tile_start = ttx; ttx += transpose_tiles(x.L, x.s);
+    tX.push_back(b);
+    GemmProb y{};
+    y.M = x.w; y.N = x.L; y.K = x.s;
+    y.a = x.Zt; y.lda = x.s; y.b = h.V; y.ldb = x.s; y.c = x.Yt; y.ldc = x.L;
+    y.a_bytes = (uint32_t)(2 * (size_t)x.w * x.s); y.b_bytes = (uint32_t)(2 * (size_t)x.L * x.s);
+    y.tiles_n = gemm_nt_tiles_n(y.N); y.tile_start = tny; tny += gemm_nt_tiles_m(y.M) * y.tiles_n;
+    nY.push_back(y);
+    GemmProb z{};
+    z.M = x.s; z.N = x.w; z.K = x.L;
+    z.a = x.XL; z.lda = x.L; z.b = x.Yt; z.ldb = x.L; z.c = x.Z2; z.ldc = x.w;
+    z.a_bytes = (uint32_t)(2 * (size_t)x.s * x.L); z.b_bytes = (uint32_t)(2 * (size_t)x.w * x.L);
+    z.tiles_n = gemm_nt_tiles_n(z.N); z.tile_start = tnz; tnz += gemm_nt_tiles_m(z.M) * z.tiles_n;
+    nZ.push_back(z);
+  }
 
   struct Part { const void* p; size_t b; };
   std::vector<Part> parts = {
@@ -672,6 +723,14 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       {pan_pref.data(), sizeof(uint32_t) * pan_pref.size()},          // 11
       {upd_pref.data(), sizeof(uint32_t) * upd_pref.size()},          // 12
       {inv_pref.data(), sizeof(uint32_t) * inv_pref.size()},          // 13
+      {fxzR.first.data(), sizeof(GemmProb) * fxzR.first.size()},     // 14
+      {fxzL.first.data(), sizeof(GemmProb) * fxzL.first.size()},     // 15
+      {fxtR.first.data(), sizeof(GemmProb) * fxtR.first.size()},     // 16
+      {fxtL.first.data(), sizeof(GemmProb) * fxtL.first.size()},     // 17
+      {tZ.data(), sizeof(TransProb) * tZ.size()},                     // 18
+      {tX.data(), sizeof(TransProb) * tX.size()},                     // 19
+      {nY.data(), sizeof(GemmProb) * nY.size()},                      // 20
+      {nZ.data(), sizeof(GemmProb) * nZ.size()},                      // 21
   };
   size_t total = 0;
   std::vector<size_t> offs;
@@ -723,7 +782,21 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   HIP_TRY(launch_gauss(RD, nm, tg, stream));
   HIP_TRY(orth_Z());
   const int q_iters = c.refresh_iters;
+  const int q_bf = q_iters > REFRESH_F32_ITERS ? q_iters - REFRESH_F32_ITERS : 0;
+  if (!nY.empty() && q_bf > 0) HIP_TRY(launch_transpose((const TransProb*)D(19), (int)tX.size(), ttx, stream));
   for (int it = 0; it < q_iters; ++it) {
+    if (it < q_bf && !nY.empty()) {
+      // early iteration: bf16 MFMA products for the matrices with a bf16 V, fp32 for the rest
+      HIP_TRY(gemm(A_G_ROW, 14, fxzR));
+      HIP_TRY(gemm(A_G_TRANS, 15, fxzL));
+      HIP_TRY(gemm(A_G_TRANS, 16, fxtR));
+      HIP_TRY(gemm(A_G_ROW, 17, fxtL));
+      HIP_TRY(launch_transpose((const TransProb*)D(18), (int)tZ.size(), ttz, stream));
+      HIP_TRY(launch_gemm_nt(EP_STORE_BF16, (const GemmProb*)D(20), (int)nY.size(), tny, u, stream));
+      HIP_TRY(launch_gemm_nt(EP_STORE, (const GemmProb*)D(21), (int)nZ.size(), tnz, u, stream));
+      HIP_TRY(orth_Z());
+      continue;
+    }
     // Y = X Z : RIGHT X = V -> rows of G ; LEFT X = V^T -> columns of G
     HIP_TRY(gemm(A_G_ROW, 5, xzR));
     HIP_TRY(gemm(A_G_TRANS, 6, xzL));
@@ -752,22 +825,24 @@ constexpr size_t REFRESH_BUDGET = (size_t)48 << 30;   // device bytes per refres
 
 int run_refresh(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream) {
   if (idx.empty()) return MOARA_OK;
-  int rc = run_decompose(st, idx, grads, false, stream);
+  std::vector<char> usev(st->n, 0);
+  for (int i : idx) usev[i] = st->mats[i].vpath && (((uintptr_t)grads[i] & 15) == 0);
+  int rc = run_decompose(st, idx, grads, false, stream, &usev);
   if (rc) return rc;
   std::vector<int> chunk;
   size_t bytes = 0;
   for (int i : idx) {
     const MatHost& h = st->mats[i];
-    const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r));
+    const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), usev[i]);
     if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
-      if ((rc = refresh_chunk(st, chunk, grads, stream))) return rc;
+      if ((rc = refresh_chunk(st, chunk, grads, stream, &usev))) return rc;
       chunk.clear();
       bytes = 0;
     }
     chunk.push_back(i);
     bytes += b;
   }
-  return refresh_chunk(st, chunk, grads, stream);
+  return refresh_chunk(st, chunk, grads, stream, &usev);
 }
 
 }  // namespace
@@ -865,7 +940,8 @@ int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, i
   for (int i = 0; i < n; ++i) {
     const Layout l = layout_of(descs[i], sides[i], cfg->block_size);
     tot += mat_state_bytes(*cfg, descs[i].rows, descs[i].cols, sides[i], l.s, l.L, l.k, ranks[i]);
-    ref += mat_refresh_bytes(l.s, l.L, subspace_width(*cfg, l.s, ranks[i]));
+    ref += mat_refresh_bytes(l.s, l.L, subspace_width(*cfg, l.s, ranks[i]),
+                             vpath_shape_ok(*cfg, descs[i].rows, descs[i].cols, sides[i], ranks[i]));
   }
   *out_state_bytes = (int64_t)tot;
   if (out_refresh_workspace_bytes) *out_refresh_workspace_bytes = (int64_t)std::min(ref, REFRESH_BUDGET + ref / (size_t)n);
@@ -993,16 +1069,16 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
     size_t bytes = 0;
     for (int i : need) {
       const MatHost& h = st->mats[i];
-      const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r));
+      const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), usev[i]);
       if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
-        if ((rc = refresh_chunk(st, chunk, grads, hs))) return rc;
+        if ((rc = refresh_chunk(st, chunk, grads, hs, &usev))) return rc;
         chunk.clear();
         bytes = 0;
       }
       chunk.push_back(i);
       bytes += b;
     }
-    if ((rc = refresh_chunk(st, chunk, grads, hs))) return rc;
+    if ((rc = refresh_chunk(st, chunk, grads, hs, &usev))) return rc;
   }
   rc = run_project_back(st, idx, weights, grads, lr, hs, &usev);
   if (rc) return rc;

@@ -38,6 +38,17 @@ struct GramProb {
   uint32_t tile_start, pad_;
 };
 
+// Transpose (and convert to bf16): out[c][r] = bf16(in[r][c]) for r < rows, c < cols.
+struct TransProb {
+  const void* in;       // rows x cols, row stride ldi, fp32 (in_f32) or bf16
+  void* out;            // cols x rows bf16, row stride ldo
+  int64_t rows, cols, ldi, ldo;
+  int32_t in_f32, tiles_c;   // tiles_c: 64-wide tiles along cols
+  uint32_t tile_start, pad_;
+};
+uint32_t transpose_tiles(int64_t rows, int64_t cols);
+hipError_t launch_transpose(const TransProb* t, int n, uint32_t total, hipStream_t st);
+
 hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st);
 hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st);
 int chol_blocks(int32_t w);

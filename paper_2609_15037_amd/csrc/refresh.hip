@@ -328,6 +328,33 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   }
 }
 
+// ------------------------------------------------------------------ transpose
+// One workgroup per 64 x 64 tile: coalesced row reads into LDS, coalesced row
+// writes of the transposed tile (bf16 output).
+__global__ __launch_bounds__(256) void k_transpose(const TransProb* __restrict__ ts, int n) {
+  __shared__ float T[64][65];
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ts[mid].tile_start <= t) lo = mid; else hi = mid - 1; }
+  const TransProb& P = ts[lo];
+  const int rel = (int)(t - P.tile_start);
+  const int64_t r0 = (int64_t)(rel / P.tiles_c) * 64, c0 = (int64_t)(rel % P.tiles_c) * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int r = e >> 6, c = e & 63;
+    float v = 0.f;
+    if (r0 + r < P.rows && c0 + c < P.cols) {
+      const int64_t i = (r0 + r) * P.ldi + c0 + c;
+      v = P.in_f32 ? ((const float*)P.in)[i] : (float)((const bf16*)P.in)[i];
+    }
+    T[r][c] = v;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int c = e >> 6, r = e & 63;
+    if (r0 + r < P.rows && c0 + c < P.cols) ((bf16*)P.out)[(c0 + c) * P.ldo + r0 + r] = (bf16)T[r][c];
+  }
+}
+
 // ------------------------------------------------------------------ finalize
 // One workgroup per matrix: column norms, order by decreasing norm, normalise
 // the first r, make each column's largest-magnitude entry positive (lowest index
@@ -443,6 +470,12 @@ hipError_t launch_to_colmajor(const RefDev* d, int n, uint32_t total, hipStream_
 hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st) {
   if (!total) return hipSuccess;
   hipLaunchKernelGGL(k_jacobi_round, dim3(total), dim3(256), 0, st, d, n, round, sweep);
+  return hipGetLastError();
+}
+uint32_t transpose_tiles(int64_t rows, int64_t cols) { return (uint32_t)(((rows + 63) / 64) * ((cols + 63) / 64)); }
+hipError_t launch_transpose(const TransProb* t, int n, uint32_t total, hipStream_t st) {
+  if (!n || !total) return hipSuccess;
+  hipLaunchKernelGGL(k_transpose, dim3(total), dim3(256), 0, st, t, n);
   return hipGetLastError();
 }
 hipError_t launch_finalize(const RefDev* d, int n, hipStream_t st) {
