@@ -154,14 +154,18 @@ __device__ __forceinline__ int circle(int pos, int round, int nb) {
 }
 
 constexpr int PW = 2 * JB;   // 64 columns per pair
+// Inner Jacobi sweeps per pair visit. The pair's Gram need not be diagonalised
+// exactly on every visit: the outer sweeps converge just as fast with two inner
+// sweeps per visit, and the visits of one round then take about the same time.
+#ifndef JAC_INNER_SWEEPS
+#define JAC_INNER_SWEEPS 2
+#endif
 
 __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
-  __shared__ double T[2][32][PW + 1];
+  __shared__ double T[2][32][PW + 1];   // (also the second 64 x 64 G buffer of the inner solve)
   __shared__ double O[32][PW + 1];
   __shared__ double Gm[PW][PW + 1];
   __shared__ double Jm[PW][PW + 1];
-  __shared__ double cs[PW / 2], sn[PW / 2];
-  __shared__ int pp[PW / 2], qq[PW / 2];
   __shared__ double red[256];
   const uint32_t t = blockIdx.x;
   int lo = 0, hi = n - 1;
@@ -244,54 +248,57 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
     if (red[0] < 1e-13) return;   // already orthogonal: nothing to rotate (uniform branch)
   }
 
-  // (2) eigen-decomposition of the 64 x 64 Gram by parallel cyclic Jacobi
-  for (int isw = 0; isw < 16; ++isw) {
-    double mloc = 0.0;
-    for (int rr = 0; rr < PW - 1; ++rr) {
-      if (tid < PW / 2) {
-        int p = circle(tid, rr, PW), q = circle(PW - 1 - tid, rr, PW);
-        if (p > q) { const int tmp = p; p = q; q = tmp; }
-        const double app = Gm[p][p], aqq = Gm[q][q], apq = Gm[p][q];
-        double c = 1.0, sv = 0.0;
-        const double den = sqrt(app * aqq);
-        if (den > 0.0 && fabs(apq) > 1e-16 * den) {
-          mloc = fmax(mloc, fabs(apq) / den);
-          const double zeta = (aqq - app) / (2.0 * apq);
-          const double tt = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
-          c = 1.0 / sqrt(1.0 + tt * tt);
-          sv = c * tt;
+  // (2) JAC_INNER_SWEEPS sweeps of parallel cyclic Jacobi on the 64 x 64 Gram. One round
+  // rotates 32 disjoint pairs (circle method) on both sides at once, G' = R^T G R,
+  // double-buffered so that a round needs a single barrier: lane l computes the
+  // rotation of pair beta = l % 32 from the current G, fetches the rotations of its
+  // row pairs alpha from lanes alpha by shuffles, writes four 2 x 2 blocks of G', and
+  // applies rotation beta to eight rows of the accumulated J. The second G buffer
+  // aliases the row-chunk buffers, which are idle during this phase.
+  {
+    double (*Ga)[PW + 1] = Gm;
+    double (*Gb)[PW + 1] = reinterpret_cast<double (*)[PW + 1]>(&T[0][0][0]);
+    const int beta = lane & 31, half = lane >> 5;
+    for (int isw = 0; isw < JAC_INNER_SWEEPS; ++isw) {
+      for (int rr = 0; rr < PW - 1; ++rr) {
+        int pb = circle(beta, rr, PW), qb = circle(PW - 1 - beta, rr, PW);
+        if (pb > qb) { const int tmp = pb; pb = qb; qb = tmp; }
+        double cb = 1.0, sb = 0.0;
+        {
+          const double app = Ga[pb][pb], aqq = Ga[qb][qb], apq = Ga[pb][qb];
+          const double den = sqrt(app * aqq);
+          if (den > 0.0 && fabs(apq) > 1e-16 * den) {
+            const double zeta = (aqq - app) / (2.0 * apq);
+            const double tt = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
+            cb = 1.0 / sqrt(1.0 + tt * tt);
+            sb = cb * tt;
+          }
         }
-        pp[tid] = p; qq[tid] = q; cs[tid] = c; sn[tid] = sv;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int alpha = 2 * (4 * wave + i) + half;
+          int pa = circle(alpha, rr, PW), qa = circle(PW - 1 - alpha, rr, PW);
+          if (pa > qa) { const int tmp = pa; pa = qa; qa = tmp; }
+          const double ca = __shfl(cb, alpha, 64), sa = __shfl(sb, alpha, 64);
+          const double g_pp = Ga[pa][pb], g_pq = Ga[pa][qb], g_qp = Ga[qa][pb], g_qq = Ga[qa][qb];
+          const double r_pp = ca * g_pp - sa * g_qp, r_pq = ca * g_pq - sa * g_qq;   // rows
+          const double r_qp = sa * g_pp + ca * g_qp, r_qq = sa * g_pq + ca * g_qq;
+          Gb[pa][pb] = cb * r_pp - sb * r_pq;                                          // columns
+          Gb[pa][qb] = sb * r_pp + cb * r_pq;
+          Gb[qa][pb] = cb * r_qp - sb * r_qq;
+          Gb[qa][qb] = sb * r_qp + cb * r_qq;
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int a = half + 2 * (wave + 4 * i);
+          const double jp = Jm[a][pb], jq = Jm[a][qb];
+          Jm[a][pb] = cb * jp - sb * jq;
+          Jm[a][qb] = sb * jp + cb * jq;
+        }
+        __syncthreads();
+        double (*tmp)[PW + 1] = Ga; Ga = Gb; Gb = tmp;
       }
-      __syncthreads();
-      for (int e = tid; e < (PW / 2) * PW; e += 256) {   // rows: G <- J^T G
-        const int k = e / PW, col = e % PW;
-        const int p = pp[k], q = qq[k];
-        const double c = cs[k], sv = sn[k];
-        const double gp = Gm[p][col], gq = Gm[q][col];
-        Gm[p][col] = c * gp - sv * gq;
-        Gm[q][col] = sv * gp + c * gq;
-      }
-      __syncthreads();
-      for (int e = tid; e < (PW / 2) * PW; e += 256) {   // columns: G <- G J, J <- J J
-        const int k = e / PW, row = e % PW;
-        const int p = pp[k], q = qq[k];
-        const double c = cs[k], sv = sn[k];
-        const double gp = Gm[row][p], gq = Gm[row][q];
-        Gm[row][p] = c * gp - sv * gq;
-        Gm[row][q] = sv * gp + c * gq;
-        const double jp = Jm[row][p], jq = Jm[row][q];
-        Jm[row][p] = c * jp - sv * jq;
-        Jm[row][q] = sv * jp + c * jq;
-      }
-      __syncthreads();
     }
-    red[tid] = (tid < PW / 2) ? mloc : 0.0;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
-    const bool done = red[0] < 1e-13;   // fp64 dots of 64 terms leave ~1e-14 relative noise
-    __syncthreads();
-    if (done) break;
   }
 
   // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, 32 rows at a time on
