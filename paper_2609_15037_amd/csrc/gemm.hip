@@ -686,6 +686,7 @@ hipError_t launch_gemm(int kind, int amode, int bmode, int ep, const GemmProb* p
     GEMM_F(A_G_ROW, B_KC, EP_ADAM)
     GEMM_F(A_G_TRANS, B_KC, EP_ADAM)
     GEMM_F(A_KC, B_KC, EP_UPDATE)
+    GEMM_F(A_KC, B_KC, EP_STORE)
     GEMM_F(A_G_ROW, B_NC, EP_STORE)
     GEMM_F(A_G_TRANS, B_NC, EP_STORE)
     GEMM_F(A_KC, B_NC, EP_STORE)

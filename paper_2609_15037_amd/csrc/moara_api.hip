@@ -176,16 +176,17 @@ size_t mat_state_bytes(const moara_config& c, int64_t m, int64_t n, int side, in
 
 // bf: the matrix runs its early subspace iterations on the bf16 V (other orientation
 // of V and bf16 copies of the iterates)
-size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w, bool bf) {
+size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w, int32_t r, bool bf) {
   const int64_t wpad = (w + 63) / 64 * 64;
   size_t b = 0;
+  b += align_up(4 * (size_t)s * r) + align_up(4 * (size_t)r * w);   // Pw, Bt
   if (bf) b += align_up(2 * (size_t)s * L) + align_up(2 * (size_t)w * s) + align_up(2 * (size_t)w * L);
   b += align_up(4 * s * w) * 2;            // Z, Z2
   b += align_up(4 * L * w) * 2;            // Y, Y2
   b += align_up(8 * (size_t)w * w) * 2;    // C, X
   b += align_up(8);                        // cmax
   b += align_up(4 * (size_t)w * w);        // Rinv
-  b += align_up(8 * (size_t)wpad * s);     // Zc
+  b += align_up(8 * (size_t)wpad * w);     // Zc (R, column-major)
   b += align_up(4 * 64);                   // off
   b += align_up(4 * wpad) + align_up(8 * wpad);
   return b;
@@ -496,6 +497,7 @@ struct RefMat {
   int idx;
   bool bf;               // early iterations on the bf16 V (large-tile GEMMs)
   void *XL, *Zt, *Yt;    // bf16: V as s x L; iterates Z^T (w x s) and Y^T (w x L)
+  float *Pw, *Bt;        // Ritz vectors before signs (s x r), (R J)_top^T (r x w)
   int64_t s, L;
   int32_t w, wpad;
   float *Z, *Z2, *Y, *Y2, *Rinv;
@@ -544,13 +546,14 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.bf = usev && (*usev)[i] && c.refresh_iters > REFRESH_F32_ITERS && x.w % 8 == 0 &&
            gemm_nt_eligible(EP_STORE_BF16, x.w, h.L, h.s, h.s, h.s, h.L, h.V, h.V, h.V, 0) &&
            gemm_nt_eligible(EP_STORE, h.s, x.w, h.L, h.L, h.L, x.w, h.V, h.V, h.V, 0);
-    need += mat_refresh_bytes(h.s, h.L, x.w, x.bf);
+    need += mat_refresh_bytes(h.s, h.L, x.w, h.r, x.bf);
     rm.push_back(x);
   }
   int rc = ensure_ref_ws(st, need);
   if (rc) return rc;
   char* p = st->ref_ws;
   auto take = [&](size_t b) { char* q = p; p += align_up(b); return q; };
+  auto h_r_of = [&](const RefMat& x) { return (size_t)st->mats[x.idx].r; };
   for (auto& x : rm) {
     if (x.bf) {
       x.XL = take(2 * (size_t)x.s * x.L);
@@ -565,7 +568,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.X = (double*)take(8 * (size_t)x.w * x.w);
     x.cmax = (double*)take(8);
     x.Rinv = (float*)take(4 * (size_t)x.w * x.w);
-    x.Zc = (double*)take(8 * (size_t)x.wpad * x.s);
+    x.Zc = (double*)take(8 * (size_t)x.wpad * x.w);
+    x.Pw = (float*)take(4 * (size_t)x.s * h_r_of(x));
+    x.Bt = (float*)take(4 * (size_t)h_r_of(x) * x.w);
     x.off = (uint32_t*)take(4 * 64);
     x.order = (int32_t*)take(4 * x.wpad);
     x.norms = (double*)take(8 * x.wpad);
@@ -585,11 +590,12 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     d.operand_bf16 = c.operand_dtype == MOARA_BF16;
     d.seed = c.refresh_seed * 0x9E3779B97F4A7C15ull + (uint64_t)(x.idx + 1) * 0xD1B54A32D192ED03ull;
     d.Z = x.Z2; d.C = x.C; d.X = x.X; d.cmax = x.cmax; d.Rinv = x.Rinv; d.Zc = x.Zc;
+    d.jl = x.w; d.Q = x.Z; d.Pw = x.Pw; d.Bt = x.Bt;
     d.P32 = h.P32; d.Pop = h.Pop; d.Ptop = h.Ptop;
     d.off = x.off; d.order = x.order; d.norms = x.norms;
     d.tile_gauss = tg; tg += gauss_tiles(x.s, x.w);
     d.tile_jac = tj; tj += jacobi_tiles(x.wpad);
-    d.tile_cm = tc; tc += colmajor_tiles(x.s, x.wpad);
+    d.tile_cm = tc; tc += r_colmajor_tiles(x.w, x.wpad);
     d.has_prev = h.hasP ? 1 : 0;
     nb_max = std::max(nb_max, x.wpad / JB);
   }
@@ -678,6 +684,22 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   auto fxtR = big_list(MOARA_SIDE_RIGHT, true, false, true), fxtL = big_list(MOARA_SIDE_LEFT, true, false, true);
   // ... and, for the others, Z^T (bf16) = transpose(Z), Y^T = Z^T X_K^T, Z2 = X_L Y  (X_K: L x s = the
   // step's V workspace, X_L: s x L = its transpose)
+  // Ritz vectors: Pw = Q Bt^T (M = s, N = r, K = w)
+  std::vector<GemmProb> pwl;
+  uint32_t tpw = 0;
+  for (int q = 0; q < nm; ++q) {
+    const RefMat& x = rm[q];
+    const int r = st->mats[x.idx].r;
+    GemmProb gp{};
+    gp.M = x.s; gp.N = r; gp.K = x.w;
+    gp.a = x.Z; gp.lda = x.w; gp.b = x.Bt; gp.ldb = x.w; gp.c = x.Pw; gp.ldc = r;
+    gp.tiles_n = gemm_tiles_n(kind, gp.N);
+    gp.vec = vec_flags_op(gp.a, x.w, 0) | (vec_flags_op(gp.b, x.w, 0) << 1);
+    set_extents(gp, 4 * (size_t)x.s * x.w, 4 * (size_t)x.w, 4 * (size_t)r * x.w, 4 * (size_t)x.w, 0, 0);
+    gp.tile_start = tpw;
+    tpw += gemm_tiles_m(kind, gp.M) * gp.tiles_n;
+    pwl.push_back(gp);
+  }
   std::vector<TransProb> tZ, tX;
   std::vector<GemmProb> nY, nZ;
   uint32_t ttz = 0, ttx = 0, tny = 0, tnz = 0;
@@ -731,6 +753,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       {tX.data(), sizeof(TransProb) * tX.size()},                     // 19
       {nY.data(), sizeof(GemmProb) * nY.size()},                      // 20
       {nZ.data(), sizeof(GemmProb) * nZ.size()},                      // 21
+      {pwl.data(), sizeof(GemmProb) * pwl.size()},                    // 22
   };
   size_t total = 0;
   std::vector<size_t> offs;
@@ -812,11 +835,16 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       HIP_TRY(gemm(A_G_ROW, 10, xt2L));
     }
   }
-  HIP_TRY(launch_to_colmajor(RD, nm, tc, stream));
+  // Rayleigh-Ritz: Z2 = Q R (CholeskyQR), SVD of the w x w factor R by one-sided Jacobi
+  // (R J has orthogonal columns, norms = Ritz values), Ritz vectors Q (R J) / norm
+  HIP_TRY(orth_Z());
+  HIP_TRY(launch_r_colmajor(RD, nm, tc, stream));
   for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.off, 0, 4 * 64, stream));
   for (int sw = 0; sw < MAX_SWEEPS; ++sw)
     for (int rr = 0; rr < nb_max - 1; ++rr) HIP_TRY(launch_jacobi_round(RD, nm, tj, rr, sw, stream));
-  HIP_TRY(launch_finalize(RD, nm, stream));
+  HIP_TRY(launch_finalize_order(RD, nm, stream));
+  HIP_TRY(launch_gemm(kind, A_KC, B_KC, EP_STORE, (const GemmProb*)D(22), nm, tpw, u, stream));
+  HIP_TRY(launch_finalize_out(RD, nm, stream));
   for (auto& x : rm) st->mats[x.idx].hasP = true;
   return MOARA_OK;
 }
@@ -833,7 +861,7 @@ int run_refresh(moara_state* st, const std::vector<int>& idx, const void* const*
   size_t bytes = 0;
   for (int i : idx) {
     const MatHost& h = st->mats[i];
-    const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), usev[i]);
+    const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), h.r, usev[i]);
     if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
       if ((rc = refresh_chunk(st, chunk, grads, stream, &usev))) return rc;
       chunk.clear();
@@ -940,7 +968,7 @@ int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, i
   for (int i = 0; i < n; ++i) {
     const Layout l = layout_of(descs[i], sides[i], cfg->block_size);
     tot += mat_state_bytes(*cfg, descs[i].rows, descs[i].cols, sides[i], l.s, l.L, l.k, ranks[i]);
-    ref += mat_refresh_bytes(l.s, l.L, subspace_width(*cfg, l.s, ranks[i]),
+    ref += mat_refresh_bytes(l.s, l.L, subspace_width(*cfg, l.s, ranks[i]), ranks[i],
                              vpath_shape_ok(*cfg, descs[i].rows, descs[i].cols, sides[i], ranks[i]));
   }
   *out_state_bytes = (int64_t)tot;
@@ -1069,7 +1097,7 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
     size_t bytes = 0;
     for (int i : need) {
       const MatHost& h = st->mats[i];
-      const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), usev[i]);
+      const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), h.r, usev[i]);
       if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
         if ((rc = refresh_chunk(st, chunk, grads, hs, &usev))) return rc;
         chunk.clear();

@@ -16,7 +16,12 @@ struct RefDev {
   double* X;          // w x w fp64 R^{-1} (upper)
   double* cmax;       // max diagonal of the Gram (pivot floor), one value
   float* Rinv;        // w x w fp32 inverse Cholesky factor
-  double* Zc;         // wpad x s fp64, column-major copy of X^T Y for the Jacobi sweeps
+  double* Zc;         // wpad x w fp64, column-major copy of the Cholesky factor R of the final
+                      // iterate (Z2 = Q R), rotated in place by the Jacobi sweeps
+  int64_t jl;         // column length of Zc (= w)
+  const float* Q;     // s x w fp32 orthonormal factor Q of the final iterate
+  float* Pw;          // s x r fp32: Q (R J)_top before signs
+  float* Bt;          // r x w fp32: (R J)_top^T, columns normalised
   float* P32;         // s x r fp32 master projector
   void* Pop;          // s x r operand dtype
   void* Ptop;         // r x s operand dtype
@@ -56,12 +61,13 @@ hipError_t launch_chol_diag(const RefDev* d, int n, int k, hipStream_t st);
 hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
 hipError_t launch_chol_update(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
 hipError_t launch_inv_col(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int J, hipStream_t st);
-hipError_t launch_to_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st);
 hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st);
-hipError_t launch_finalize(const RefDev* d, int n, hipStream_t st);
+hipError_t launch_r_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st);
+uint32_t r_colmajor_tiles(int32_t w, int32_t wpad);
+hipError_t launch_finalize_order(const RefDev* d, int n, hipStream_t st);
+hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st);
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
                                     int operand_bf16, hipStream_t st);
 uint32_t gauss_tiles(int64_t s, int32_t w);
 uint32_t gram_tiles(int32_t w);
 uint32_t jacobi_tiles(int32_t wpad);
-uint32_t colmajor_tiles(int64_t s, int32_t wpad);

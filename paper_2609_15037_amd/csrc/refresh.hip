@@ -125,27 +125,6 @@ __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, i
 }
 
 // ------------------------------------------------------------------ Zn (s x w fp32) -> Zc (wpad x s fp64)
-__global__ __launch_bounds__(256) void k_to_colmajor(const RefDev* __restrict__ ds, int n) {
-  __shared__ float tile[32][33];
-  const uint32_t t = blockIdx.x;
-  int lo = 0, hi = n - 1;
-  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_cm <= t) lo = mid; else hi = mid - 1; }
-  const RefDev& d = ds[lo];
-  const int64_t tiles_s = (d.s + 31) / 32;
-  const int64_t lt = t - d.tile_cm;
-  const int64_t ts = lt % tiles_s, tc = lt / tiles_s;
-  const int x = threadIdx.x & 31, y = threadIdx.x >> 5;
-  for (int yy = y; yy < 32; yy += 8) {
-    const int64_t row = ts * 32 + yy, col = tc * 32 + x;
-    tile[yy][x] = (row < d.s && col < d.w) ? d.Z[row * d.w + col] : 0.f;
-  }
-  __syncthreads();
-  for (int yy = y; yy < 32; yy += 8) {
-    const int64_t col = tc * 32 + yy, row = ts * 32 + x;
-    if (col < d.wpad && row < d.s) d.Zc[col * d.s + row] = (double)tile[x][yy];
-  }
-}
-
 // ------------------------------------------------------------------ one Jacobi round
 // Workgroup = (matrix, block pair). Blocks of JB columns are paired by the
 // circle method: over nb-1 rounds every pair of the nb blocks meets once.
@@ -177,7 +156,7 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   if (sweep > 0 && __uint_as_float(d.off[sweep - 1]) < 1e-13f) return;   // converged
   const int ba = circle(pair, round, nb), bb = circle(nb - 1 - pair, round, nb);
   const int tid = threadIdx.x;
-  const int64_t s = d.s;
+  const int64_t s = d.jl;   // column length
   auto colp = [&](int x) -> double* { return d.Zc + (int64_t)((x < JB) ? ba * JB + x : bb * JB + (x - JB)) * s; };
 
   // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
@@ -362,26 +341,57 @@ __global__ __launch_bounds__(256) void k_transpose(const TransProb* __restrict__
   }
 }
 
+// ------------------------------------------------------------------ R -> column-major
+// Zc[j][i] = R[i][j] for i <= j < w (R: upper Cholesky factor left in C, row-major);
+// zero below the diagonal (C still holds Gram entries there) and in padded columns.
+__global__ __launch_bounds__(256) void k_r_colmajor(const RefDev* __restrict__ ds, int n) {
+  __shared__ double tile[32][33];
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_cm <= t) lo = mid; else hi = mid - 1; }
+  const RefDev& d = ds[lo];
+  const int w = d.w;
+  const int64_t tiles_i = (w + 31) / 32;
+  const int64_t lt = t - d.tile_cm;
+  const int64_t ti = lt % tiles_i, tj = lt / tiles_i;
+  const int x = threadIdx.x & 31, y = threadIdx.x >> 5;
+  for (int yy = y; yy < 32; yy += 8) {
+    const int64_t i = ti * 32 + yy, j = tj * 32 + x;
+    tile[yy][x] = (i < w && j < w && i <= j) ? d.C[i * w + j] : 0.0;
+  }
+  __syncthreads();
+  for (int yy = y; yy < 32; yy += 8) {
+    const int64_t j = tj * 32 + yy, i = ti * 32 + x;
+    if (j < d.wpad && i < w) d.Zc[j * d.jl + i] = tile[x][yy];
+  }
+}
+
 // ------------------------------------------------------------------ finalize
-// One workgroup per matrix: column norms, order by decreasing norm, normalise
-// the first r, make each column's largest-magnitude entry positive (lowest index
-// on ties), write P (fp32 master and both operand copies). An all-zero iterate
-// (V == 0) keeps the previous projector, or yields the first r canonical basis
-// vectors when there is none; numerically null directions also fall back to e_j.
-__global__ __launch_bounds__(256) void k_finalize(const RefDev* __restrict__ ds) {
+// After the Jacobi sweeps Zc = R J has orthogonal columns whose norms are the Ritz
+// values; the Ritz vectors are Q (R J) / norm. k_finalize_order (one workgroup per
+// matrix): column norms, order by decreasing norm, Bt = the first r columns,
+// normalised (zero for numerically null directions). A GEMM then forms Pw = Q Bt^T.
+// k_finalize_out (one workgroup per matrix): make each column's largest-magnitude
+// entry positive (lowest index on ties) and write P (fp32 master and both operand
+// copies). An all-zero iterate (V == 0) keeps the previous projector, or yields the
+// first r canonical basis vectors when there is none; numerically null directions
+// also fall back to e_j.
+__global__ __launch_bounds__(256) void k_finalize_order(const RefDev* __restrict__ ds) {
   const RefDev& d = ds[blockIdx.x];
   const int tid = threadIdx.x;
-  const int64_t s = d.s;
+  const int64_t L = d.jl;
+  // an all-zero final iterate has R = I (zero-Gram fallback of the factorisation):
+  // its Ritz values are all zero
+  const bool zero = !(d.cmax[0] > 0.0);
   __shared__ double red[256];
-  __shared__ int redi[256];
   for (int c = 0; c < d.wpad; ++c) {
-    const double* col = d.Zc + (int64_t)c * s;
+    const double* col = d.Zc + (int64_t)c * L;
     double a = 0.0;
-    for (int64_t i = tid; i < s; i += 256) a = fma(col[i], col[i], a);
+    for (int64_t i = tid; i < L; i += 256) a = fma(col[i], col[i], a);
     red[tid] = a;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] += red[tid + o]; __syncthreads(); }
-    if (tid == 0) d.norms[c] = sqrt(red[0]);
+    if (tid == 0) d.norms[c] = zero ? 0.0 : sqrt(red[0]);
     __syncthreads();
   }
   for (int c = tid; c < d.wpad; c += 256) {
@@ -395,17 +405,31 @@ __global__ __launch_bounds__(256) void k_finalize(const RefDev* __restrict__ ds)
   }
   __syncthreads();
   const double nmax = d.norms[d.order[0]];
-  if (!(nmax > 0.0) && d.has_prev) return;   // V == 0: keep the previous projector
   for (int j = 0; j < d.r; ++j) {
     const int src = d.order[j];
     const double nrm = d.norms[src];
-    const double* col = d.Zc + (int64_t)src * s;
+    const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
+    const double* col = d.Zc + (int64_t)src * L;
+    for (int64_t i = tid; i < d.w; i += 256) d.Bt[(int64_t)j * d.w + i] = deg ? 0.f : (float)(col[i] / nrm);
+  }
+}
+
+__global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__ ds) {
+  const RefDev& d = ds[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int64_t s = d.s;
+  __shared__ float red[256];
+  __shared__ int redi[256];
+  const double nmax = d.norms[d.order[0]];
+  if (!(nmax > 0.0) && d.has_prev) return;   // V == 0: keep the previous projector
+  for (int j = 0; j < d.r; ++j) {
+    const double nrm = d.norms[d.order[j]];
     const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
     // sign: entry of largest magnitude, lowest index on ties
-    double best = -1.0;
+    float best = -1.f;
     int bi = 0;
     for (int64_t i = tid; i < s; i += 256) {
-      const double v = deg ? (i == (j % s) ? 1.0 : 0.0) : fabs(col[i]);
+      const float v = deg ? (i == (j % s) ? 1.f : 0.f) : fabsf(d.Pw[i * d.r + j]);
       if (v > best) { best = v; bi = (int)i; }
     }
     red[tid] = best;
@@ -420,10 +444,9 @@ __global__ __launch_bounds__(256) void k_finalize(const RefDev* __restrict__ ds)
       }
       __syncthreads();
     }
-    const double sgn = deg ? 1.0 : ((col[redi[0]] < 0.0) ? -1.0 : 1.0);
-    const double scale = deg ? 0.0 : sgn / nrm;
+    const float sgn = deg ? 1.f : ((d.Pw[(int64_t)redi[0] * d.r + j] < 0.f) ? -1.f : 1.f);
     for (int64_t i = tid; i < s; i += 256) {
-      const float v = deg ? (i == (j % s) ? 1.f : 0.f) : (float)(col[i] * scale);
+      const float v = deg ? (i == (j % s) ? 1.f : 0.f) : sgn * d.Pw[i * d.r + j];
       d.P32[i * d.r + j] = v;
       if (d.operand_bf16) {
         ((bf16*)d.Pop)[i * d.r + j] = f2bf(v);
@@ -457,7 +480,6 @@ __global__ __launch_bounds__(256) void k_convert_projector(const float* __restri
 uint32_t gauss_tiles(int64_t s, int32_t w) { return (uint32_t)((s * w + GAUSS_PER_WG - 1) / GAUSS_PER_WG); }
 uint32_t gram_tiles(int32_t w) { const int T = (w + 63) / 64; return (uint32_t)(T * (T + 1) / 2); }
 uint32_t jacobi_tiles(int32_t wpad) { return (uint32_t)(wpad / JB / 2); }
-uint32_t colmajor_tiles(int64_t s, int32_t wpad) { return (uint32_t)(((s + 31) / 32) * (wpad / 32)); }
 
 hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st) {
   if (!total) return hipSuccess;
@@ -467,11 +489,6 @@ hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st) 
 hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st) {
   if (!total) return hipSuccess;
   hipLaunchKernelGGL(k_gram, dim3(total), dim3(256), 0, st, g, n);
-  return hipGetLastError();
-}
-hipError_t launch_to_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st) {
-  if (!total) return hipSuccess;
-  hipLaunchKernelGGL(k_to_colmajor, dim3(total), dim3(256), 0, st, d, n);
   return hipGetLastError();
 }
 hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st) {
@@ -485,9 +502,20 @@ hipError_t launch_transpose(const TransProb* t, int n, uint32_t total, hipStream
   hipLaunchKernelGGL(k_transpose, dim3(total), dim3(256), 0, st, t, n);
   return hipGetLastError();
 }
-hipError_t launch_finalize(const RefDev* d, int n, hipStream_t st) {
+uint32_t r_colmajor_tiles(int32_t w, int32_t wpad) { return (uint32_t)(((w + 31) / 32) * ((wpad + 31) / 32)); }
+hipError_t launch_r_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_r_colmajor, dim3(total), dim3(256), 0, st, d, n);
+  return hipGetLastError();
+}
+hipError_t launch_finalize_order(const RefDev* d, int n, hipStream_t st) {
   if (!n) return hipSuccess;
-  hipLaunchKernelGGL(k_finalize, dim3(n), dim3(256), 0, st, d);
+  hipLaunchKernelGGL(k_finalize_order, dim3(n), dim3(256), 0, st, d);
+  return hipGetLastError();
+}
+hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st) {
+  if (!n) return hipSuccess;
+  hipLaunchKernelGGL(k_finalize_out, dim3(n), dim3(256), 0, st, d);
   return hipGetLastError();
 }
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
