@@ -65,6 +65,28 @@ __device__ __forceinline__ void ab_acc(const double (*A)[LDB], const double (*Bm
   }
 }
 
+// fp64 MFMA form of the 64 x 64 block products (v_mfma_f64_16x16x4: lane l supplies
+// A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
+// Wave w accumulates rows [16w, 16w+16) of the product, all 64 columns (four 16 x 16
+// tiles): acc[jt] += op(A)[rows][t] * B[t][16 jt ..], op(A) = A^T when TA.
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+template <bool TA>
+__device__ __forceinline__ void mfma_blk(const double (*A)[LDB], const double (*Bm)[LDB], f64x4 (&acc)[4]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = 16 * wave + (lane & 15);
+#pragma unroll 4
+  for (int ks = 0; ks < NB / 4; ++ks) {
+    const int t = 4 * ks + (lane >> 4);
+    const double a = TA ? A[t][i] : A[i][t];
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+      acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Bm[t][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+  }
+}
+// element (row, col) of the 64 x 64 block held in acc[jt][r]
+__device__ __forceinline__ int mfma_row(int r) { return 16 * (threadIdx.x >> 6) + 4 * r + ((threadIdx.x & 63) >> 4); }
+__device__ __forceinline__ int mfma_col(int jt) { return 16 * jt + (threadIdx.x & 15); }
+
 __global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds, int k) {
   const RefDev& d = ds[blockIdx.x];
   const int w = d.w;
@@ -171,15 +193,16 @@ __global__ __launch_bounds__(256) void k_chol_update(const RefDev* __restrict__ 
   load_blk(Ra, d.C, w, k, a);
   load_blk(Rc, d.C, w, k, c);
   __syncthreads();
-  double acc[4][4] = {};
-  atb_acc(Ra, Rc, acc);
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  f64x4 acc[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
+  for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+  mfma_blk<true>(Ra, Rc, acc);   // R_ka^T R_kc
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = a * NB + ty * 4 + q, cc = c * NB + tx * 4 + u;
-      if (r < w && cc < w) d.C[(int64_t)r * w + cc] -= acc[q][u];
+  for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = a * NB + mfma_row(r), col = c * NB + mfma_col(jt);
+      if (row < w && col < w) d.C[(int64_t)row * w + col] -= acc[jt][r];
     }
 }
 
@@ -192,32 +215,35 @@ __global__ __launch_bounds__(256) void k_inv_col(const RefDev* __restrict__ ds, 
   const int I = (int)(t - pref[mi]);
   __shared__ double Ab[NB][LDB];
   __shared__ double Bb[NB][LDB];
-  double acc[4][4] = {};
+  f64x4 acc[4];
+#pragma unroll
+  for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
   for (int tb = I; tb < J; ++tb) {
     load_blk(Ab, d.X, w, I, tb);
     load_blk(Bb, d.C, w, tb, J);
     __syncthreads();
-    ab_acc(Ab, Bb, acc);
+    mfma_blk<false>(Ab, Bb, acc);   // += X_I,tb R_tb,J
     __syncthreads();
   }
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
+  for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) Ab[ty * 4 + q][tx * 4 + u] = acc[q][u];
+    for (int r = 0; r < 4; ++r) Ab[mfma_row(r)][mfma_col(jt)] = acc[jt][r];
   load_blk(Bb, d.X, w, J, J);
   __syncthreads();
-  double out[4][4] = {};
-  ab_acc(Ab, Bb, out);
+  f64x4 out[4];
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
+  for (int jt = 0; jt < 4; ++jt) out[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+  mfma_blk<false>(Ab, Bb, out);      // (sum) X_JJ
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = I * NB + ty * 4 + q, c = J * NB + tx * 4 + u;
-      if (r < w && c < w) {
-        const int64_t g = (int64_t)r * w + c;
-        d.X[g] = -out[q][u];
-        d.Rinv[g] = (float)(-out[q][u]);
+  for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int row = I * NB + mfma_row(r), col = J * NB + mfma_col(jt);
+      if (row < w && col < w) {
+        const int64_t g = (int64_t)row * w + col;
+        d.X[g] = -out[jt][r];
+        d.Rinv[g] = (float)(-out[jt][r]);
       }
     }
 }
