@@ -134,10 +134,11 @@ __device__ __forceinline__ int circle(int pos, int round, int nb) {
 
 constexpr int PW = 2 * JB;   // 64 columns per pair
 // Inner Jacobi sweeps per pair visit. The pair's Gram need not be diagonalised
-// exactly on every visit: the outer sweeps converge just as fast with two inner
-// sweeps per visit, and the visits of one round then take about the same time.
+// exactly on every visit: with one inner sweep the outer iteration needs about one
+// more sweep to reach the same off-diagonal level, but every visit is much cheaper
+// and the visits of one round take about the same time (measured fastest of 1-3).
 #ifndef JAC_INNER_SWEEPS
-#define JAC_INNER_SWEEPS 2
+#define JAC_INNER_SWEEPS 1
 #endif
 
 __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
