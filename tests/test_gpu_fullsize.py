@@ -1,0 +1,180 @@
+"""Parity at the full sizes of the Llama-2-7B, Qwen2-7B and DeepSeek-MoE workloads.
+
+* The 7B stack runs all 224 matrices in one state, so every launch has exactly
+  the configuration bench.py times; the oracle checks one layer of it (all seven
+  matrices, element by element).
+* One Qwen2-7B layer (GQA k/v 512 x 3584, MLP 18944 x 3584) is checked element by
+  element, and its attention projectors after a refresh by principal angles.
+* One DeepSeek-MoE layer with routed experts: 6 of 64 experts active per step,
+  inactive experts bit-identical, active ones against the oracle, and per-expert
+  refresh on an expert's first active step.
+
+Step parity uses a seeded random orthonormal projector on both sides (the step
+is defined for any P); refresh parity uses the oracle's SVD.
+"""
+import dataclasses
+
+import numpy as np
+import pytest
+
+import workloads as WL
+from oracle import moara_oracle as O
+from tests.harness import (TOL_BF16, Case, adam_sensitivity, case_from_workload, compare, gpu_state, have_gpu,
+                           oracle_cfg, rng, slices_of, to_dev, to_np)
+
+pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not have_gpu(), reason="needs an MI355X GPU")]
+
+
+def _M():
+    from paper_2609_15037_amd import moara as M
+    return M
+
+
+def random_projector(s: int, r: int, key) -> np.ndarray:
+    """Seeded random s x r orthonormal matrix, rounded to fp32."""
+    g = rng(7, *key).standard_normal((s, r))
+    return O.round_f32(np.linalg.qr(g)[0])
+
+
+def check_matrices(M, st, c: Case, idx, Wd, Wo, ost, masks, report):
+    for j, i in enumerate(idx):
+        Wg = to_np(Wd[i])
+        compare(f"W[{i}]", Wg, Wo[j], TOL_BF16, report, masks[j])
+        compare(f"exp_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG), ost[j].exp_avg, TOL_BF16, report)
+        compare(f"exp_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG_SQ), ost[j].exp_avg_sq, TOL_BF16,
+                report)
+        compare(f"mag_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG), ost[j].mag_avg, TOL_BF16, report)
+        compare(f"mag_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG_SQ), ost[j].mag_avg_sq, TOL_BF16,
+                report)
+
+
+def sampled_stack_parity(wl: WL.Workload, sample_layer: int, steps: int):
+    """All matrices of `wl` in one state; oracle on the matrices of `sample_layer`."""
+    import torch
+    M = _M()
+    c = case_from_workload(wl)
+    n = len(wl.matrices)
+    idx = [i for i, m in enumerate(wl.matrices) if m.layer == sample_layer]
+    st = gpu_state(c)
+    dev = torch.device("cuda")
+    wdt = torch.bfloat16
+    Wd, Gd = [], []
+    for i, m in enumerate(wl.matrices):
+        Wd.append(WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=wdt, device=dev)))
+        Gd.append(torch.empty((m.rows, m.cols), dtype=torch.float32, device=dev))
+        s = min(m.rows, m.cols)
+        M.moara_set_tensor(st, i, M.MOARA_T_P, random_projector(s, wl.rank_of(m), (i,)))
+    Wo = [to_np(Wd[i]) for i in idx]
+    ocfg = [oracle_cfg(c, i) for i in idx]
+    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[j]) for j, i in enumerate(idx)]
+    for j, i in enumerate(idx):
+        ost[j].P = random_projector(min(c.shapes[i][:2]), c.ranks[i], (i,))
+    masks = [np.zeros(c.shapes[i][:2], dtype=bool) for i in idx]
+    for t in range(steps):
+        Gs = {}
+        for i, m in enumerate(wl.matrices):
+            if i in idx:
+                Gs[i] = WL.grad_np(wl, i, t)
+                Gd[i].copy_(torch.from_numpy(Gs[i]))
+            else:
+                WL.grad_device(wl, i, t, Gd[i], active=True)
+        torch.cuda.synchronize()
+        print(f"[fullsize] {wl.name}: step {t}, {n} matrices, oracle on layer {sample_layer}", flush=True)
+        M.moara_step(st, Wd, Gd, lr=c.lr)
+        for j, i in enumerate(idx):
+            Wo[j] = O.step(Wo[j], Gs[i], ost[j], ocfg[j], c.lr)
+            V = O.decompose(Gs[i], c.block_size)[1]
+            dN = adam_sensitivity(V, ost[j].P, ost[j].side, ost[j].exp_avg_sq, ost[j].t, c.beta2, c.adam_eps)
+            masks[j] |= slices_of(dN > 0.1, ost[j].side, c.shapes[i][:2])
+        torch.cuda.synchronize()
+    report = {}
+    check_matrices(M, st, c, idx, Wd, Wo, ost, masks, report)
+    for i in idx:
+        assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == steps
+    worst = max(v for k, v in report.items() if not k.endswith("masked_frac"))
+    print(f"[fullsize] {wl.name}: worst floored rel err {worst:.3e} (tol {TOL_BF16:.0e})", flush=True)
+
+
+def test_llama2_7b_stack_one_layer_checked():
+    sampled_stack_parity(WL.WORKLOADS["llama2_7b"], sample_layer=31, steps=2)
+
+
+def test_qwen2_7b_layer():
+    sampled_stack_parity(WL.subset(WL.WORKLOADS["qwen2_7b"], [27]), sample_layer=27, steps=2)
+
+
+def test_qwen2_7b_attention_refresh():
+    import torch
+    M = _M()
+    wl = WL.subset(WL.WORKLOADS["qwen2_7b"], [0])
+    keep = [i for i, m in enumerate(wl.matrices) if m.module in (WL.Q, WL.K, WL.V, WL.O)]
+    wl = dataclasses.replace(wl, matrices=tuple(wl.matrices[i] for i in keep))
+    c = case_from_workload(wl)
+    st = gpu_state(c)
+    Gs = [WL.grad_np(wl, i, 0) for i in range(len(wl.matrices))]
+    print("[fullsize] qwen2_7b attention refresh", flush=True)
+    M.moara_refresh_projector(st, [to_dev(g, "f32") for g in Gs])
+    torch.cuda.synchronize()
+    for i, G in enumerate(Gs):
+        Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+        _, V = O.decompose(G, c.block_size)
+        ref = O.truncated_svd(V, c.ranks[i], O.projection_side(*G.shape))
+        np.testing.assert_allclose(Pg.T @ Pg, np.eye(Pg.shape[1]), atol=2e-5)
+        ang = O.max_principal_angle(Pg, ref)
+        print(f"[fullsize] {wl.matrices[i].name} {G.shape} r={c.ranks[i]}: principal angle {ang:.2e}", flush=True)
+        assert ang <= 1e-3
+
+
+def test_deepseek_moe_layer_routed_experts():
+    """8 routed experts (of the layer's 64; routing keeps its 6-of-64 draw, so some
+    of them are idle on a step) + 2 shared + attention, per-expert refresh (T=200:
+    a matrix refreshes on its first active step), three steps. The refresh is checked
+    by principal angles against the oracle's SVD; the oracle's step then uses the
+    GPU's projector so that the updates compare element by element."""
+    import torch
+    M = _M()
+    full = WL.subset(WL.WORKLOADS["deepseek_moe"], [0])
+    act_all = [WL.active_set(full, t) for t in range(3)]
+    keep = [i for i, m in enumerate(full.matrices) if not m.routed or m.expert < 8]
+    wl = dataclasses.replace(full, matrices=tuple(full.matrices[i] for i in keep))
+    c = case_from_workload(wl)
+    n = len(wl.matrices)
+    st = gpu_state(c, refresh_interval=200)
+    Wd = [WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
+          for i, m in enumerate(wl.matrices)]
+    W0 = [to_np(w) for w in Wd]
+    Wo = [w.copy() for w in W0]
+    ocfg = [oracle_cfg(c, i) for i in range(n)]          # refresh handled here, with the GPU's P
+    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[i]) for i in range(n)]
+    report, refreshed, worst_angle = {}, 0, 0.0
+    for t in range(3):
+        act = np.array([act_all[t][k] for k in keep], dtype=np.uint8)
+        Gs = [WL.grad_np(full, k, t, active=bool(a)) for k, a in zip(keep, act)]
+        print(f"[fullsize] deepseek_moe step {t}: {int(act.sum())} of {n} matrices active", flush=True)
+        M.moara_step(st, Wd, [to_dev(g, "f32") if a else None for g, a in zip(Gs, act)], lr=c.lr, active=act)
+        torch.cuda.synchronize()
+        for i in range(n):
+            if not act[i]:
+                continue
+            if ost[i].t == 0:   # first active step: the GPU refreshed this matrix's projector
+                Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+                _, V = O.decompose(Gs[i], c.block_size)
+                ref = O.truncated_svd(V, c.ranks[i], O.projection_side(*Gs[i].shape))
+                ang = O.max_principal_angle(Pg, ref)
+                worst_angle = max(worst_angle, ang)
+                assert ang <= 1e-3, f"{wl.matrices[i].name}: refresh principal angle {ang:.2e}"
+                ost[i].P = O.round_f32(Pg)
+                refreshed += 1
+            Wo[i] = O.step(Wo[i], Gs[i], ost[i], ocfg[i], c.lr)
+    for i in range(n):
+        t_gpu = M.moara_get_tensor(st, i, M.MOARA_T_STEP)
+        assert t_gpu == ost[i].t, f"{wl.matrices[i].name}: counter {t_gpu} vs {ost[i].t}"
+        Wg = to_np(Wd[i])
+        if ost[i].t == 0:
+            assert np.array_equal(Wg, W0[i]), f"{wl.matrices[i].name}: idle expert changed"
+            continue
+        compare(f"W[{i}]", Wg, Wo[i], TOL_BF16, report)
+        compare(f"exp_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG), ost[i].exp_avg, TOL_BF16, report)
+        compare(f"mag_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG), ost[i].mag_avg, TOL_BF16, report)
+    print(f"[fullsize] deepseek_moe: {sum(o.t > 0 for o in ost)} of {n} matrices stepped, {refreshed} refreshes "
+          f"(worst angle {worst_angle:.2e}), worst floored rel err {max(report.values()):.3e}", flush=True)
