@@ -68,11 +68,14 @@ __device__ __forceinline__ int find_prob(const GemmProb* probs, int n, uint32_t 
   return lo;
 }
 
-// 2 x NWN waves, each owning a 128 x WTN sub-tile (4 x WTN/32 MFMA blocks); the tile
-// is 256 x (NWN WTN); NS LDS stages.
-template <int EP, int NWN, int WTN, int NS>
-__global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_nt(const GemmProb* __restrict__ probs, GemmUniform U) {
-  constexpr int NW = 2 * NWN, TBN = NWN * WTN, NB = WTN / 32;
+// NWM x NWN waves, each owning a WTM x WTN sub-tile (WTM/32 x WTN/32 MFMA blocks);
+// the tile is 256 x (NWN WTN) (NWM WTM = 256); NS LDS stages; OCC workgroups per CU
+// (the second launch bound is the minimum number of waves per SIMD).
+template <int EP, int NWM, int NWN, int WTN, int NS, int OCC>
+__global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_gemm_nt(const GemmProb* __restrict__ probs, GemmUniform U) {
+  constexpr int NW = NWM * NWN, TBN = NWN * WTN, NB = WTN / 32;
+  constexpr int WTM = TBM / NWM, MB = WTM / 32;
+  static_assert(NWM * WTM == TBM && MB >= 2 && MB <= 4 && NB <= 4, "wave layout");
   constexpr int EPLD = WTN + 4;                      // fp32 row stride of the epilogue staging slab
   constexpr int EPWAVE = 32 * EPLD;                  // floats per wave slab
   constexpr int TILEB = TBN * ROWB, STAGEB = TILEA + TILEB;
@@ -85,7 +88,7 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
   tile_coords(t - P.tile_start, (uint32_t)((P.M + TBM - 1) / TBM), P.tiles_n, tm, tn);
   const int64_t row0 = (int64_t)tm * TBM, col0 = (int64_t)tn * TBN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % NWM, wn = wave / NWM;
 
   // ---- DMA address map: wave w fills 1 KB slots [SA w, SA w + SA) of the A tile and
   // [SB w, SB w + SB) of the B tile (16 rows per slot)
@@ -152,9 +155,9 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
     else __builtin_amdgcn_raw_ptr_buffer_load_lds(rp0, sink, 16, off, 0, 0, 0);
   };
 
-  f32x16 acc[4][NB];
+  f32x16 acc[MB][NB];
 #pragma unroll
-  for (int mb = 0; mb < 4; ++mb)
+  for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
@@ -166,8 +169,8 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
   for (int ks = 0; ks < 2; ++ks) {
     const int c = 2 * ks + (lane >> 5);
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      const int R = 128 * wm + 32 * mb + (lane & 31);
+    for (int mb = 0; mb < MB; ++mb) {
+      const int R = WTM * wm + 32 * mb + (lane & 31);
       offa[mb][ks] = R * ROWB + ((c ^ swz(R)) << 4);
     }
 #pragma unroll
@@ -192,13 +195,13 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
   auto read_frags = [&](int stage, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
     const char* st = smem + stage * STAGEB;
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) fa[mb] = *reinterpret_cast<const bf16x8*>(st + offa[mb][ks]);
+    for (int mb = 0; mb < MB; ++mb) fa[mb] = *reinterpret_cast<const bf16x8*>(st + offa[mb][ks]);
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) fb[nb] = *reinterpret_cast<const bf16x8*>(st + offb[nb][ks]);
   };
   auto mfma_all = [&](const bf16x8 (&fa)[4], const bf16x8 (&fb)[4]) {
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb)
+    for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
       for (int nb = 0; nb < NB; ++nb)
         acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fb[nb], fa[mb], acc[mb][nb], 0, 0, 0);
@@ -248,7 +251,7 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
   // latency is paid once per slab (moments) or once per tile (W) rather than once
   // per row group.
   float* slab = reinterpret_cast<float*>(smem) + wave * EPWAVE;
-  const int64_t wrow0 = row0 + 128 * wm, wcol0 = col0 + WTN * wn;
+  const int64_t wrow0 = row0 + WTM * wm, wcol0 = col0 + WTN * wn;
   auto stage_slab = [&](int mb) {
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
@@ -265,7 +268,7 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
     const int cc = 4 * (lane % LPR);
     const int64_t col = wcol0 + cc;
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
+    for (int mb = 0; mb < MB; ++mb) {
       stage_slab(mb);
       __syncthreads();
 #pragma unroll
@@ -293,15 +296,16 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
     constexpr int LPR = WTN / 4, RPP = 64 / LPR, HP = 16 / RPP;   // HP passes per half-slab
     const int cc = 4 * (lane % LPR);
     const int64_t col = wcol0 + cc;
-    float4 ev[2][HP], qv[2][HP];
+    constexpr int DB = OCC * NW <= 8 ? 2 : 1;   // register double buffer only at two waves per SIMD
+    float4 ev[DB][HP], qv[DB][HP];
     auto load_half = [&](int h) {   // h = 2 mb + half
 #pragma unroll
       for (int p = 0; p < HP; ++p) {
         const int64_t row = wrow0 + 16 * h + RPP * p + lane / LPR;
         if (row < P.M && col < P.N) {
           const int64_t idx = row * P.ldc + col;
-          ev[h & 1][p] = *reinterpret_cast<const float4*>(P.e1 + idx);
-          qv[h & 1][p] = *reinterpret_cast<const float4*>(P.e2 + idx);
+          ev[h % DB][p] = *reinterpret_cast<const float4*>(P.e1 + idx);
+          qv[h % DB][p] = *reinterpret_cast<const float4*>(P.e2 + idx);
         }
       }
     };
@@ -313,7 +317,7 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
         if (row < P.M && col < P.N) {
           const float4 v = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
           const int64_t idx = row * P.ldc + col;
-          float4 e = ev[h & 1][p], q = qv[h & 1][p];
+          float4 e = ev[h % DB][p], q = qv[h % DB][p];
           bf16x4 o;
           o[0] = f2bf(adam_out(v.x, e.x, q.x, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
           o[1] = f2bf(adam_out(v.y, e.y, q.y, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
@@ -325,16 +329,29 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
         }
       }
     };
-    load_half(0);
+    if constexpr (DB == 2) {
+      load_half(0);
 #pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-      load_half(2 * mb + 1);
-      stage_slab(mb);
-      __syncthreads();
-      compute_half(2 * mb);
-      if (mb < 3) load_half(2 * mb + 2);
-      compute_half(2 * mb + 1);
-      __syncthreads();
+      for (int mb = 0; mb < MB; ++mb) {
+        load_half(2 * mb + 1);
+        stage_slab(mb);
+        __syncthreads();
+        compute_half(2 * mb);
+        if (mb < MB - 1) load_half(2 * mb + 2);
+        compute_half(2 * mb + 1);
+        __syncthreads();
+      }
+    } else {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        load_half(2 * mb);
+        stage_slab(mb);
+        __syncthreads();
+        compute_half(2 * mb);
+        load_half(2 * mb + 1);
+        compute_half(2 * mb + 1);
+        __syncthreads();
+      }
     }
   } else {
     // LPR lanes x 8 columns per row, RPP rows per pass, PPS passes per slab
@@ -343,24 +360,25 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
     const int64_t col = wcol0 + cc;
     const bool one_mag = (U.B & 7) == 0;   // 8 aligned columns never straddle a block
     if (U.weight_bf16 && one_mag) {
-      // W and magnitudes two slabs ahead (register double buffer)
-      bf16x8 wv[2][PPS];
-      float mg[2][PPS];
+      // W and magnitudes DB slabs ahead (register double buffer with one workgroup per CU)
+      constexpr int DB = OCC * NW <= 8 ? 2 : 1;
+      bf16x8 wv[DB][PPS];
+      float mg[DB][PPS];
       auto load_w = [&](int mb) {
 #pragma unroll
         for (int p = 0; p < PPS; ++p) {
           const int64_t row = wrow0 + 32 * mb + RPP * p + lane / LPR;
-          mg[mb & 1][p] = 1.f;
+          mg[mb % DB][p] = 1.f;
           if (row < P.M && col < P.N) {
-            wv[mb & 1][p] = *reinterpret_cast<const bf16x8*>((const bf16*)P.c + row * P.ldc + col);
-            if (P.dM) mg[mb & 1][p] = P.dM[row * P.dM_ld + col / U.B];
+            wv[mb % DB][p] = *reinterpret_cast<const bf16x8*>((const bf16*)P.c + row * P.ldc + col);
+            if (P.dM) mg[mb % DB][p] = P.dM[row * P.dM_ld + col / U.B];
           }
         }
       };
       load_w(0);
-      load_w(1);
+      if (DB == 2) load_w(1);
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
+      for (int mb = 0; mb < MB; ++mb) {
         stage_slab(mb);
         __syncthreads();
 #pragma unroll
@@ -371,20 +389,20 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
             const float4 v0 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
             const float4 v1 = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc + 4);
             const float v[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
-            const float m = mg[mb & 1][p];
+            const float m = mg[mb % DB][p];
             bf16x8 o;
 #pragma unroll
-            for (int q = 0; q < 8; ++q) o[q] = f2bf(bf2f(wv[mb & 1][p][q]) - U.lr * bf2f(f2bf(U.scale * (m * v[q]))));
+            for (int q = 0; q < 8; ++q) o[q] = f2bf(bf2f(wv[mb % DB][p][q]) - U.lr * bf2f(f2bf(U.scale * (m * v[q]))));
             *reinterpret_cast<bf16x8*>((bf16*)P.c + row * P.ldc + col) = o;
           }
         }
         __syncthreads();
-        if (mb + 2 < 4) load_w(mb + 2);
+        if (mb + DB < MB) load_w(mb + DB);
       }
     } else {
       // general form: fp32 W, or block sizes that split an 8-column group
 #pragma unroll
-      for (int mb = 0; mb < 4; ++mb) {
+      for (int mb = 0; mb < MB; ++mb) {
         stage_slab(mb);
         __syncthreads();
 #pragma unroll 2
@@ -433,20 +451,31 @@ __global__ __launch_bounds__(128 * NWN, (NWN * WTN == 256 ? 1 : 2)) void k_gemm_
 
 }  // namespace
 
-// Variants (measured on the 7B-shaped step, the first is the fastest):
-//   1: 256 x 256 tiles, eight waves of 128 x 64, four LDS stages, one workgroup per CU;
+// Variants (8 layers of the 7B-shaped step, projection / back-projection ms):
+//   1: 256 x 256 tiles, eight waves of 128 x 64, four LDS stages, one workgroup per CU
+//      (3.54 / 4.11);
 //   2: 256 x 256 tiles, four waves of 128 x 128 (accumulators in AGPRs), four stages
-//      (faster main loop, but half the waves to hide the epilogue's memory latency);
-//   3: 256 x 128 tiles, four waves of 128 x 64, three stages, two workgroups per CU.
+//      (faster main loop, but half the waves to hide the epilogue's memory latency;
+//      4.36 / 4.59);
+//   3: 256 x 128 tiles, four waves of 128 x 64, three stages, two workgroups per CU
+//      (3.86 / 4.36);
+//   4: 256 x 128 tiles, eight waves of 64 x 64, three stages, two workgroups per CU
+//      (3.61 / 3.89);
+//   5: 256 x 256 tiles, sixteen waves of 64 x 64, four stages, one workgroup per CU
+//      (3.28 / 3.88) -- the default.
 #ifndef GEMM_NT_VARIANT
-#define GEMM_NT_VARIANT 1
+#define GEMM_NT_VARIANT 5
 #endif
 #if GEMM_NT_VARIANT == 1
-constexpr int V_NWN = 4, V_WTN = 64, V_NS = 4;
+constexpr int V_NWM = 2, V_NWN = 4, V_WTN = 64, V_NS = 4, V_OCC = 1;
 #elif GEMM_NT_VARIANT == 2
-constexpr int V_NWN = 2, V_WTN = 128, V_NS = 4;
+constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 128, V_NS = 4, V_OCC = 1;
+#elif GEMM_NT_VARIANT == 3
+constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 64, V_NS = 3, V_OCC = 2;
+#elif GEMM_NT_VARIANT == 4
+constexpr int V_NWM = 4, V_NWN = 2, V_WTN = 64, V_NS = 3, V_OCC = 2;
 #else
-constexpr int V_NWN = 2, V_WTN = 64, V_NS = 3;
+constexpr int V_NWM = 4, V_NWN = 4, V_WTN = 64, V_NS = 4, V_OCC = 1;
 #endif
 constexpr int GEMM_NT_BN = V_NWN * V_WTN;
 uint32_t gemm_nt_tiles_m(int64_t M) { return (uint32_t)((M + TBM - 1) / TBM); }
@@ -474,13 +503,13 @@ bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int6
 }
 
 namespace {
-template <int NWN, int WTN, int NS>
+template <int NWM, int NWN, int WTN, int NS, int OCC>
 hipError_t launch_nt(int ep, const GemmProb* probs_dev, uint32_t total_tiles, const GemmUniform& u, hipStream_t st) {
-  const dim3 grid(total_tiles), block(128 * NWN);
-  if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
-  else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
-  else if (ep == EP_STORE) hipLaunchKernelGGL((k_gemm_nt<EP_STORE, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
-  else if (ep == EP_STORE_BF16) hipLaunchKernelGGL((k_gemm_nt<EP_STORE_BF16, NWN, WTN, NS>), grid, block, 0, st, probs_dev, u);
+  const dim3 grid(total_tiles), block(64 * NWM * NWN);
+  if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_STORE) hipLaunchKernelGGL((k_gemm_nt<EP_STORE, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_STORE_BF16) hipLaunchKernelGGL((k_gemm_nt<EP_STORE_BF16, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -491,5 +520,5 @@ hipError_t launch_gemm_nt(int ep, const GemmProb* probs_dev, int nprob, uint32_t
   if (total_tiles == 0 || nprob == 0) return hipSuccess;
   GemmUniform u = u0;
   u.nprob = nprob;
-  return launch_nt<V_NWN, V_WTN, V_NS>(ep, probs_dev, total_tiles, u, st);
+  return launch_nt<V_NWM, V_NWN, V_WTN, V_NS, V_OCC>(ep, probs_dev, total_tiles, u, st);
 }
