@@ -114,6 +114,9 @@ __global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds
     for (int e = tid; e < NB * NB; e += 256) { const int i = e >> 6, j = e & 63; D[i][j] = (i == j) ? 1.0 : 0.0; }
     __syncthreads();
   } else {
+    // right-looking, one column per step; the trailing update maps lane -> column and
+    // the four waves stride over the rows (no integer division in the inner loop)
+    const int cx = tid & 63, ry = tid >> 6;
     for (int j = 0; j < kb; ++j) {
       if (tid == 0) {
         double v = D[j][j];
@@ -123,9 +126,9 @@ __global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds
       __syncthreads();
       if (tid > j && tid < kb) D[j][tid] /= D[j][j];
       __syncthreads();
-      for (int e = tid; e < kb * kb; e += 256) {
-        const int a = e / kb, c = e % kb;
-        if (a > j && c >= a) D[a][c] -= D[j][a] * D[j][c];
+      if (cx > j && cx < kb) {
+        const double djc = D[j][cx];
+        for (int a = j + 1 + ry; a <= cx; a += 4) D[a][cx] -= D[j][a] * djc;
       }
       __syncthreads();
     }
