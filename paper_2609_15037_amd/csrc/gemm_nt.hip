@@ -25,6 +25,16 @@
 //   EP_STORE / EP_STORE_BF16: C stored as fp32 / bf16 (the refresh's subspace products).
 #include "gemm.h"
 
+#ifndef EPDB_ADAM
+#define EPDB_ADAM 4
+#endif
+#ifndef EPA_ROWS
+#define EPA_ROWS 4
+#endif
+#ifndef EPDB_UPD
+#define EPDB_UPD 1
+#endif
+
 namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -81,7 +91,8 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
   constexpr int TILEB = TBN * ROWB, STAGEB = TILEA + TILEB;
   constexpr int SA = 16 / NW, SB = (TBN / 16) / NW;   // 1 KB DMA slots per wave per stage
   constexpr int OPS = SA + SB;                        // DMA instructions per wave per stage
-  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGEB + NW * 1024];
+  constexpr int SMEM = NS * STAGEB > NW * EPWAVE * 4 ? NS * STAGEB : NW * EPWAVE * 4;
+  __shared__ __attribute__((aligned(1024))) char smem[SMEM];
   const uint32_t t = xcd_remap(blockIdx.x, gridDim.x);
   const GemmProb& P = probs[find_prob(probs, U.nprob, t)];
   uint32_t tm, tn;
@@ -119,40 +130,6 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 #pragma unroll
     for (int j = 0; j < SB; ++j)
       __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(base + TILEA + (SB * wave + j) * 1024), 16, vb[j], so, 0, 0);
-  };
-
-  // ---- cache warm-up for the epilogue: during the last PFN steps of the main loop each
-  // wave DMAs one 1 KB piece of the tile's epilogue operand (bf16 W; the code also
-  // covers the two fp32 moment arrays) into a private LDS sink that is never read, so
-  // that the epilogue's loads find it in L2 / the memory-side cache instead of HBM.
-  constexpr int RW = 256 / NW;                      // tile rows per wave
-  const bool pf_w = EP == EP_UPDATE && U.weight_bf16;
-  const int rbytes = EP == EP_ADAM ? TBN * 4 : TBN * 2;   // bytes of one tile row of the operand
-  const int rpi = 1024 / rbytes, lpr = rbytes / 16;       // rows per DMA, lanes per row
-  // (measured: the warm-up pays off for the back-projection, whose K is short and whose
-  // epilogue moves W; for the projection the extra DMA traffic costs more than it saves)
-  const int PFN = (EP == EP_ADAM) ? 0 : (pf_w ? RW / rpi : 0);
-  const __amdgpu_buffer_rsrc_t rp0 = __builtin_amdgcn_make_buffer_rsrc(
-      EP == EP_ADAM ? (void*)P.e1 : P.c, (short)0, (int)(P.M * P.ldc * (EP == EP_ADAM ? 4 : 2)), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rp1 = __builtin_amdgcn_make_buffer_rsrc(
-      EP == EP_ADAM ? (void*)P.e2 : P.c, (short)0, (int)(P.M * P.ldc * (EP == EP_ADAM ? 4 : 2)), 0x00020000);
-  const int nk0 = (int)(P.K / TBK);
-  const int kt0 = (nk0 - 1 - PFN > 0) ? nk0 - 1 - PFN : 0;    // first step that prefetches
-  auto pf_count = [&](int i) { return (i >= kt0 && i < kt0 + PFN && i < nk0 - 1) ? 1 : 0; };
-  auto prefetch = [&](int i) {
-    if (!pf_count(i)) return;
-    const int j = i - kt0;
-    const int half = (EP == EP_ADAM) ? (j >= RW / rpi) : 0;
-    const int jj = j - half * (RW / rpi);
-    const int64_t row = row0 + RW * wave + rpi * jj + lane / lpr;
-    const int64_t r2 = row < P.M ? row : P.M - 1;
-    const int ew = EP == EP_ADAM ? 4 : 8;             // elements per 16 bytes
-    const int64_t col = col0 + ew * (lane % lpr);
-    const int64_t c2 = col < P.N ? col : P.N - ew;
-    const uint32_t off = (uint32_t)((r2 * P.ldc + c2) * (EP == EP_ADAM ? 4 : 2));
-    lds_void* sink = (lds_void*)(smem + NS * STAGEB + wave * 1024);
-    if (half) __builtin_amdgcn_raw_ptr_buffer_load_lds(rp1, sink, 16, off, 0, 0, 0);
-    else __builtin_amdgcn_raw_ptr_buffer_load_lds(rp0, sink, 16, off, 0, 0, 0);
   };
 
   f32x16 acc[MB][NB];
@@ -222,19 +199,16 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
     __builtin_amdgcn_sched_barrier(0);
     mfma_all(fa0, fb0);
     __builtin_amdgcn_sched_barrier(0);
-    // stage kt+1 was issued in step kt+2-NS; what may stay in flight is everything
-    // issued after it: that step's prefetch and the later steps' stages and prefetches
+    // stage kt+1 was issued in step kt+2-NS; the stages issued in the later steps
+    // (kt+3-NS .. kt-1) may stay in flight
     {
       int newer = 0;
-      for (int i = kt + 2 - NS; i < kt; ++i) {
-        newer += pf_count(i);
-        if (i > kt + 2 - NS && i + NS - 1 < nk) newer += OPS;
-      }
+      for (int i = kt + 3 - NS; i < kt; ++i)
+        if (i + NS - 1 < nk) newer += OPS;
       wait_vm(newer);
     }
     stage_barrier();
     if (kt + NS - 1 < nk) issue(kt + NS - 1, (kt + NS - 1) % NS);
-    prefetch(kt);
     read_frags((kt + 1) % NS, 0, fa0, fb0);
     __builtin_amdgcn_sched_barrier(0);
     mfma_all(fa1, fb1);
@@ -243,7 +217,12 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
   read_frags(kt % NS, 1, fa1, fb1);
   mfma_all(fa0, fb0);
   mfma_all(fa1, fb1);
-  __syncthreads();   // every wave is done with the stages: LDS becomes the epilogue slab
+  // Every wave is done with the stages and its DMA writes have landed:
+  // LDS becomes the epilogue slabs. Each wave then uses only its own slab, and a wave's
+  // LDS accesses complete in program order, so the epilogue needs no further barrier
+  // (its global loads stay in flight across slabs).
+  wait_vm(0);
+  __syncthreads();
 
   // ---- epilogue, one 32-row slab (block row mb) of the wave's sub-tile at a time.
   // The global operands of the epilogue (moments, or W and the block magnitudes)
@@ -270,7 +249,6 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb) {
       stage_slab(mb);
-      __syncthreads();
 #pragma unroll
       for (int p = 0; p < PPS; ++p) {
         const int rr = RPP * p + lane / LPR;
@@ -287,21 +265,21 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
           }
         }
       }
-      __syncthreads();
     }
   } else if constexpr (EP == EP_ADAM) {
-    // LPR lanes x 4 columns per row, RPP rows per pass, 32 / RPP passes per slab. The
-    // moments move in half-slabs through a register double buffer: the loads of the
-    // next half are in flight while the current one is computed.
-    constexpr int LPR = WTN / 4, RPP = 64 / LPR, HP = 16 / RPP;   // HP passes per half-slab
+    // LPR lanes x 4 columns per row, RPP rows per pass. The moments move in pieces of PR
+    // rows through a ring of DB register buffers: while one piece is computed, the loads
+    // of the next DB - 1 pieces are in flight.
+    constexpr int LPR = WTN / 4, RPP = 64 / LPR;
+    constexpr int PR = EPA_ROWS, NPC = 32 / PR, HPP = PR / RPP, NPT = MB * NPC, DB = EPDB_ADAM;
+    static_assert(PR % RPP == 0 && 32 % PR == 0 && DB >= 1, "epilogue pieces");
     const int cc = 4 * (lane % LPR);
     const int64_t col = wcol0 + cc;
-    constexpr int DB = OCC * NW <= 8 ? 2 : 1;   // register double buffer only at two waves per SIMD
-    float4 ev[DB][HP], qv[DB][HP];
-    auto load_half = [&](int h) {   // h = 2 mb + half
+    float4 ev[DB][HPP], qv[DB][HPP];
+    auto load_piece = [&](int h) {   // rows [PR h, PR h + PR) of the wave's sub-tile
 #pragma unroll
-      for (int p = 0; p < HP; ++p) {
-        const int64_t row = wrow0 + 16 * h + RPP * p + lane / LPR;
+      for (int p = 0; p < HPP; ++p) {
+        const int64_t row = wrow0 + PR * h + RPP * p + lane / LPR;
         if (row < P.M && col < P.N) {
           const int64_t idx = row * P.ldc + col;
           ev[h % DB][p] = *reinterpret_cast<const float4*>(P.e1 + idx);
@@ -309,11 +287,11 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
         }
       }
     };
-    auto compute_half = [&](int h) {
+    auto compute_piece = [&](int h) {
 #pragma unroll
-      for (int p = 0; p < HP; ++p) {
-        const int rr = 16 * (h & 1) + RPP * p + lane / LPR;
-        const int64_t row = wrow0 + 16 * h + RPP * p + lane / LPR;
+      for (int p = 0; p < HPP; ++p) {
+        const int rr = PR * (h % NPC) + RPP * p + lane / LPR;
+        const int64_t row = wrow0 + PR * h + RPP * p + lane / LPR;
         if (row < P.M && col < P.N) {
           const float4 v = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
           const int64_t idx = row * P.ldc + col;
@@ -329,29 +307,14 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
         }
       }
     };
-    if constexpr (DB == 2) {
-      load_half(0);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        load_half(2 * mb + 1);
-        stage_slab(mb);
-        __syncthreads();
-        compute_half(2 * mb);
-        if (mb < MB - 1) load_half(2 * mb + 2);
-        compute_half(2 * mb + 1);
-        __syncthreads();
-      }
-    } else {
+    for (int h = 0; h < DB - 1; ++h)
+      if (h < NPT) load_piece(h);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        load_half(2 * mb);
-        stage_slab(mb);
-        __syncthreads();
-        compute_half(2 * mb);
-        load_half(2 * mb + 1);
-        compute_half(2 * mb + 1);
-        __syncthreads();
-      }
+    for (int h = 0; h < NPT; ++h) {
+      if (h + DB - 1 < NPT) load_piece(h + DB - 1);
+      if (h % NPC == 0) stage_slab(h / NPC);
+      compute_piece(h);
     }
   } else {
     // LPR lanes x 8 columns per row, RPP rows per pass, PPS passes per slab
@@ -361,7 +324,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
     const bool one_mag = (U.B & 7) == 0;   // 8 aligned columns never straddle a block
     if (U.weight_bf16 && one_mag) {
       // W and magnitudes DB slabs ahead (register double buffer with one workgroup per CU)
-      constexpr int DB = OCC * NW <= 8 ? 2 : 1;
+      constexpr int DB = EPDB_UPD;
       bf16x8 wv[DB][PPS];
       float mg[DB][PPS];
       auto load_w = [&](int mb) {
@@ -380,7 +343,6 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         stage_slab(mb);
-        __syncthreads();
 #pragma unroll
         for (int p = 0; p < PPS; ++p) {
           const int rr = RPP * p + lane / LPR;
@@ -396,7 +358,6 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
             *reinterpret_cast<bf16x8*>((bf16*)P.c + row * P.ldc + col) = o;
           }
         }
-        __syncthreads();
         if (mb + DB < MB) load_w(mb + DB);
       }
     } else {
@@ -404,7 +365,6 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb) {
         stage_slab(mb);
-        __syncthreads();
 #pragma unroll 2
         for (int p = 0; p < PPS; ++p) {
           const int rr = RPP * p + lane / LPR;
@@ -443,7 +403,6 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
             }
           }
         }
-        __syncthreads();
       }
     }
   }
@@ -451,7 +410,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 
 }  // namespace
 
-// Variants (8 layers of the 7B-shaped step, projection / back-projection ms):
+// Variants (8 layers of the 7B-shaped step, projection / back-projection ms, measured
+// with an earlier epilogue that kept the back-projection at four stages and warmed W
+// into the cache during the last K steps):
 //   1: 256 x 256 tiles, eight waves of 128 x 64, four LDS stages, one workgroup per CU
 //      (3.54 / 4.11);
 //   2: 256 x 256 tiles, four waves of 128 x 128 (accumulators in AGPRs), four stages
@@ -462,20 +423,25 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 //   4: 256 x 128 tiles, eight waves of 64 x 64, three stages, two workgroups per CU
 //      (3.61 / 3.89);
 //   5: 256 x 256 tiles, sixteen waves of 64 x 64, four stages, one workgroup per CU
-//      (3.28 / 3.88) -- the default.
+//      (3.28 / 3.88) -- the default; its back-projection (K = r, 16 to 32 steps) now
+//      runs five stages, which hides the pipeline fill of the short K loop better
+//      than the cache warm-up did (-4 % on that kernel).
+// Starting the first round of workgroups at staggered times, so that the epilogues of
+// different CUs (or of the two workgroups of a CU) do not coincide, changed nothing
+// measurable in any variant.
 #ifndef GEMM_NT_VARIANT
 #define GEMM_NT_VARIANT 5
 #endif
 #if GEMM_NT_VARIANT == 1
-constexpr int V_NWM = 2, V_NWN = 4, V_WTN = 64, V_NS = 4, V_OCC = 1;
+constexpr int V_NWM = 2, V_NWN = 4, V_WTN = 64, V_NS = 4, V_NSU = 4, V_OCC = 1;
 #elif GEMM_NT_VARIANT == 2
-constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 128, V_NS = 4, V_OCC = 1;
+constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 128, V_NS = 4, V_NSU = 4, V_OCC = 1;
 #elif GEMM_NT_VARIANT == 3
-constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 64, V_NS = 3, V_OCC = 2;
+constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 64, V_NS = 3, V_NSU = 3, V_OCC = 2;
 #elif GEMM_NT_VARIANT == 4
-constexpr int V_NWM = 4, V_NWN = 2, V_WTN = 64, V_NS = 3, V_OCC = 2;
+constexpr int V_NWM = 4, V_NWN = 2, V_WTN = 64, V_NS = 3, V_NSU = 3, V_OCC = 2;
 #else
-constexpr int V_NWM = 4, V_NWN = 4, V_WTN = 64, V_NS = 4, V_OCC = 1;
+constexpr int V_NWM = 4, V_NWN = 4, V_WTN = 64, V_NS = 4, V_NSU = 5, V_OCC = 1;
 #endif
 constexpr int GEMM_NT_BN = V_NWN * V_WTN;
 uint32_t gemm_nt_tiles_m(int64_t M) { return (uint32_t)((M + TBM - 1) / TBM); }
@@ -503,11 +469,11 @@ bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int6
 }
 
 namespace {
-template <int NWM, int NWN, int WTN, int NS, int OCC>
+template <int NWM, int NWN, int WTN, int NS, int NSU, int OCC>
 hipError_t launch_nt(int ep, const GemmProb* probs_dev, uint32_t total_tiles, const GemmUniform& u, hipStream_t st) {
   const dim3 grid(total_tiles), block(64 * NWM * NWN);
   if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
-  else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWM, NWN, WTN, NSU, OCC>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_STORE) hipLaunchKernelGGL((k_gemm_nt<EP_STORE, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_STORE_BF16) hipLaunchKernelGGL((k_gemm_nt<EP_STORE_BF16, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
   else return hipErrorInvalidValue;
@@ -520,5 +486,5 @@ hipError_t launch_gemm_nt(int ep, const GemmProb* probs_dev, int nprob, uint32_t
   if (total_tiles == 0 || nprob == 0) return hipSuccess;
   GemmUniform u = u0;
   u.nprob = nprob;
-  return launch_nt<V_NWM, V_NWN, V_WTN, V_NS, V_OCC>(ep, probs_dev, total_tiles, u, st);
+  return launch_nt<V_NWM, V_NWN, V_WTN, V_NS, V_NSU, V_OCC>(ep, probs_dev, total_tiles, u, st);
 }
