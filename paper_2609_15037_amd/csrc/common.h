@@ -50,6 +50,14 @@ struct StepParams {
 };
 
 // ---------------------------------------------------------------- helpers
+// Blocked ("K-panel") layout of a bf16 GEMM operand with `rows` rows and reduction
+// length K (a multiple of 32): element (i, k) sits at ((k / 32) * rows + i) * 32 + k % 32.
+// The 64-byte row segments of one 32-wide K step of consecutive rows are then one
+// contiguous run, which the large-tile GEMM streams with whole-line DMA loads.
+__host__ __device__ __forceinline__ int64_t kp_index(int64_t i, int64_t k, int64_t rows) {
+  return ((k >> 5) * rows + i) * 32 + (k & 31);
+}
+
 __device__ __forceinline__ float bf2f(bf16 x) { return (float)x; }
 __device__ __forceinline__ bf16 f2bf(float x) { return (bf16)x; }   // round to nearest even
 

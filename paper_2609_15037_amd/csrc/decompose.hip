@@ -122,7 +122,7 @@ __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ ma
             const float inv = 1.0f / (sqrtf(ss) + p.decomp_eps);
             bf16x4 o;
             o[0] = f2bf(v[u].x * inv); o[1] = f2bf(v[u].y * inv); o[2] = f2bf(v[u].z * inv); o[3] = f2bf(v[u].w * inv);
-            *reinterpret_cast<bf16x4*>(d.Vb + row * n + c) = o;
+            *reinterpret_cast<bf16x4*>(d.Vb + kp_index(row, c, d.m)) = o;   // blocked, K = n
           }
         }
       }
@@ -204,7 +204,7 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
         bf16x8 o;
 #pragma unroll
         for (int e = 0; e < 8; ++e) o[e] = T[(8 * g + e) * VT_PITCH + cl];
-        *reinterpret_cast<bf16x8*>(d.Vb + col * m + row0 + 8 * g) = o;
+        *reinterpret_cast<bf16x8*>(d.Vb + kp_index(col, row0 + 8 * g, n)) = o;   // blocked V' (n x m), K = m
       }
     }
     __syncthreads();

@@ -43,7 +43,8 @@ struct GemmProb {
   uint32_t tile_start;
   uint32_t tiles_n;
   int32_t vec;        // bit0: A may use 16-byte loads, bit1: B may
-  int32_t pad_;
+  int32_t kp;         // blocked layout (kp_index, bf16 only): bit0 A (rows M), bit1 B (rows N),
+                      // bit2 the EP_ADAM output c (rows M); K a multiple of 32
   uint32_t a_bytes;   // extent of the A array (buffer loads past it return 0); 0 = unknown
   uint32_t b_bytes;   // extent of the B array
   uint32_t inv_bytes; // extent of the inv array

@@ -134,12 +134,14 @@ struct BfA {
       for (int u = 0; u < TASKS; ++u) {
         const int idx = tid + NT * u;
         const int64_t gr = row0 + (idx >> 3), gk = k0 + (idx & 7) * 8;
+        const bool kpa = P.kp & 1;   // blocked layout: 8-element chunks never straddle a 32-block
         if constexpr (FAST) {
-          this->u[u] = bld16(R.a, (uint32_t)((gr * P.lda + gk) * 2));
+          this->u[u] = bld16(R.a, (uint32_t)((kpa ? kp_index(gr, gk, P.M) : gr * P.lda + gk) * 2));
         } else {
           bf16x8 t;
 #pragma unroll
-          for (int e = 0; e < 8; ++e) t[e] = (gr < P.M && gk + e < P.K) ? A[gr * P.lda + gk + e] : f2bf(0.f);
+          for (int e = 0; e < 8; ++e)
+            t[e] = (gr < P.M && gk + e < P.K) ? A[kpa ? kp_index(gr, gk + e, P.M) : gr * P.lda + gk + e] : f2bf(0.f);
           this->u[u] = *reinterpret_cast<uint4*>(&t);
         }
       }
@@ -206,12 +208,14 @@ struct BfB {
     for (int q = 0; q < TASKS; ++q) {
       const int idx = tid + NT * q;
       const int64_t gj = col0 + (idx >> 3), gk = k0 + (idx & 7) * 8;
+      const bool kpb = P.kp & 2;
       if constexpr (FAST) {
-        u[q] = bld16(R.b, (uint32_t)((gj * P.ldb + gk) * 2));
+        u[q] = bld16(R.b, (uint32_t)((kpb ? kp_index(gj, gk, P.N) : gj * P.ldb + gk) * 2));
       } else {
         bf16x8 t;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) t[e] = (gj < P.N && gk + e < P.K) ? Bp[gj * P.ldb + gk + e] : f2bf(0.f);
+        for (int e = 0; e < 8; ++e)
+          t[e] = (gj < P.N && gk + e < P.K) ? Bp[kpb ? kp_index(gj, gk + e, P.N) : gj * P.ldb + gk + e] : f2bf(0.f);
         u[q] = *reinterpret_cast<uint4*>(&t);
       }
     }
@@ -416,7 +420,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, const GemmUniform& U
             if constexpr (KIND == KIND_BF16) {
               bf16x4 t;
               t[0] = f2bf(o[0]); t[1] = f2bf(o[1]); t[2] = f2bf(o[2]); t[3] = f2bf(o[3]);
-              *reinterpret_cast<bf16x4*>((bf16*)P.c + idx) = t;
+              *reinterpret_cast<bf16x4*>((bf16*)P.c + ((P.kp & 4) ? kp_index(row, col, P.M) : idx)) = t;
             } else {
               *reinterpret_cast<float4*>((float*)P.c + idx) = make_float4(o[0], o[1], o[2], o[3]);
             }
@@ -425,7 +429,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, const GemmUniform& U
               if (col + q >= P.N) continue;
               P.e1[idx + q] = e[q];
               P.e2[idx + q] = s2[q];
-              if constexpr (KIND == KIND_BF16) ((bf16*)P.c)[idx + q] = f2bf(o[q]);
+              if constexpr (KIND == KIND_BF16) ((bf16*)P.c)[(P.kp & 4) ? kp_index(row, col + q, P.M) : idx + q] = f2bf(o[q]);
               else ((float*)P.c)[idx + q] = o[q];
             }
           }

@@ -106,30 +106,35 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
   const __amdgpu_buffer_rsrc_t ra = __builtin_amdgcn_make_buffer_rsrc((void*)P.a, (short)0, (int)P.a_bytes, 0x00020000);
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)P.b, (short)0, (int)P.b_bytes, 0x00020000);
   static_assert(SA <= 4 && SB <= 4, "DMA slot arrays");
+  // blocked operands: one K step of the tile's rows is a contiguous 64-byte-per-row run,
+  // the next K step starts rows * 64 bytes further; row-major: the next 64 bytes of each row
+  const bool kpa = P.kp & 1, kpb = P.kp & 2;
+  const uint32_t sta = kpa ? (uint32_t)P.M * 64u : (uint32_t)(TBK * 2);
+  const uint32_t stb = kpb ? (uint32_t)P.N * 64u : (uint32_t)(TBK * 2);
   uint32_t va[4], vb[4];   // (fixed extent: a template-dependent array bound here drops the host launch stub)
 #pragma unroll
   for (int j = 0; j < SA; ++j) {
     const int R = 16 * (SA * wave + j) + (lane >> 2);
     const int c = (lane & 3) ^ swz(R);
     const int64_t ga = (row0 + R < P.M) ? row0 + R : P.M - 1;
-    va[j] = (uint32_t)(ga * P.lda * 2 + c * 16);
+    va[j] = (uint32_t)((kpa ? ga * 64 : ga * P.lda * 2) + c * 16);
   }
 #pragma unroll
   for (int j = 0; j < SB; ++j) {
     const int R = 16 * (SB * wave + j) + (lane >> 2);
     const int c = (lane & 3) ^ swz(R);
     const int64_t gb = (col0 + R < P.N) ? col0 + R : P.N - 1;
-    vb[j] = (uint32_t)(gb * P.ldb * 2 + c * 16);
+    vb[j] = (uint32_t)((kpb ? gb * 64 : gb * P.ldb * 2) + c * 16);
   }
   auto issue = [&](int kt, int slot) {
     char* base = smem + slot * STAGEB;
-    const int so = kt * TBK * 2;
+    const int soa = (int)(kt * sta), sob = (int)(kt * stb);
 #pragma unroll
     for (int j = 0; j < SA; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(base + (SA * wave + j) * 1024), 16, va[j], so, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(base + (SA * wave + j) * 1024), 16, va[j], soa, 0, 0);
 #pragma unroll
     for (int j = 0; j < SB; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(base + TILEA + (SB * wave + j) * 1024), 16, vb[j], so, 0, 0);
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(base + TILEA + (SB * wave + j) * 1024), 16, vb[j], sob, 0, 0);
   };
 
   f32x16 acc[MB][NB];
@@ -303,7 +308,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
           o[3] = f2bf(adam_out(v.w, e.w, q.w, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
           *reinterpret_cast<float4*>(P.e1 + idx) = e;
           *reinterpret_cast<float4*>(P.e2 + idx) = q;
-          *reinterpret_cast<bf16x4*>((bf16*)P.c + idx) = o;
+          *reinterpret_cast<bf16x4*>((bf16*)P.c + ((P.kp & 4) ? kp_index(row, col, P.M) : idx)) = o;
         }
       }
     };

@@ -48,7 +48,8 @@ struct MatHost {
   float *exp1 = nullptr, *exp2 = nullptr, *P32 = nullptr;
   void *N = nullptr, *Pop = nullptr, *Ptop = nullptr;
   bool vpath = false;    // the decomposition writes V in bf16 for the large-tile projection
-  void* V = nullptr;     // m x n (RIGHT) or n x m (LEFT) bf16 direction workspace
+  void* V = nullptr;     // L x s bf16 direction workspace, blocked layout (kp_index, K = s)
+  bool kp = false;       // Ptop (K = s), Pop and N (K = r) in the blocked layout too
 };
 
 struct TimedLaunch {
@@ -399,6 +400,7 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
       g.a = h.V; g.lda = h.s;
       g.b = h.Ptop; g.ldb = h.s;
       g.c = h.N; g.ldc = h.r;
+      g.kp = 1 | (h.kp ? 2 | 4 : 0);
       g.e1 = h.exp1; g.e2 = h.exp2;
       g.bc1 = bc1; g.bc2 = bc2;
       g.a_bytes = (uint32_t)(2 * (size_t)h.L * h.s);
@@ -418,6 +420,7 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
         b.M = h.m; b.N = h.n; b.K = h.r;
         b.a = ba; b.b = bb;
         b.lda = h.r; b.ldb = h.r;
+        b.kp = h.kp ? 3 : 0;
         b.c = weights[i]; b.ldc = h.n;
         b.dM = st->cfg.decompose ? h.dM : nullptr; b.dM_ld = h.k;
         b.a_bytes = (uint32_t)(2 * rows_a * h.r);
@@ -431,6 +434,7 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
         b.M = h.m; b.N = h.n; b.K = h.r;
         b.a = ba; b.b = bb;
         b.lda = h.r; b.ldb = h.r;
+        b.kp = h.kp ? 3 : 0;
         b.c = weights[i]; b.ldc = h.n;
         b.dM = st->cfg.decompose ? h.dM : nullptr; b.dM_ld = h.k;
         b.tiles_n = gemm_tiles_n(kind, b.N);
@@ -449,6 +453,7 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
     g.inv = st->cfg.decompose ? h.inv : nullptr; g.inv_ld = h.k;
     g.b = h.Ptop; g.ldb = h.s;
     g.c = h.N; g.ldc = h.r;
+    g.kp = h.kp ? 2 | 4 : 0;
     g.e1 = h.exp1; g.e2 = h.exp2;
     g.bc1 = bc1;
     g.bc2 = bc2;
@@ -591,7 +596,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     d.seed = c.refresh_seed * 0x9E3779B97F4A7C15ull + (uint64_t)(x.idx + 1) * 0xD1B54A32D192ED03ull;
     d.Z = x.Z2; d.C = x.C; d.X = x.X; d.cmax = x.cmax; d.Rinv = x.Rinv; d.Zc = x.Zc;
     d.jl = x.w; d.Q = x.Z; d.Pw = x.Pw; d.Bt = x.Bt;
-    d.P32 = h.P32; d.Pop = h.Pop; d.Ptop = h.Ptop;
+    d.P32 = h.P32; d.Pop = h.Pop; d.Ptop = h.Ptop; d.kp = h.kp ? 1 : 0;
     d.off = x.off; d.order = x.order; d.norms = x.norms;
     d.tile_gauss = tg; tg += gauss_tiles(x.s, x.w);
     d.tile_jac = tj; tj += jacobi_tiles(x.wpad);
@@ -712,12 +717,13 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     a.tiles_c = (int32_t)((x.w + 63) / 64); a.tile_start = ttz; ttz += transpose_tiles(x.s, x.w);
     tZ.push_back(a);
     TransProb b{};
-    b.in = h.V; b.out = x.XL; b.rows = x.L; b.cols = x.s; b.ldi = x.s; b.ldo = x.L; b.in_f32 = 0;
+    b.in = h.V; b.out = x.XL; b.rows = x.L; b.cols = x.s; b.ldi = x.s; b.ldo = x.L; b.in_f32 = 0; b.in_kp = 1;
     b.tiles_c = (int32_t)((x.s + 63) / 64); b.tile_start = ttx; ttx += transpose_tiles(x.L, x.s);
     tX.push_back(b);
     GemmProb y{};
     y.M = x.w; y.N = x.L; y.K = x.s;
     y.a = x.Zt; y.lda = x.s; y.b = h.V; y.ldb = x.s; y.c = x.Yt; y.ldc = x.L;
+    y.kp = 2;   // V is blocked
     y.a_bytes = (uint32_t)(2 * (size_t)x.w * x.s); y.b_bytes = (uint32_t)(2 * (size_t)x.L * x.s);
     y.tiles_n = gemm_nt_tiles_n(y.N); y.tile_start = tny; tny += gemm_nt_tiles_m(y.M) * y.tiles_n;
     nY.push_back(y);
@@ -1011,6 +1017,7 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
     h.m = descs[i].rows; h.n = descs[i].cols; h.r = ranks[i]; h.side = sides[i];
     h.s = l.s; h.L = l.L; h.k = (int32_t)l.k;
     h.vpath = vpath_shape_ok(*cfg, h.m, h.n, h.side, h.r);
+    h.kp = h.vpath && cfg->operand_dtype == MOARA_BF16 && h.r % 32 == 0;
     tot += mat_state_bytes(*cfg, h.m, h.n, h.side, h.s, h.L, h.k, h.r);
   }
   if (hipMalloc(&st->block, tot) != hipSuccess) { free_state(st); return fail(MOARA_E_OOM, "state of %zu bytes", tot); }
@@ -1192,7 +1199,8 @@ int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* ho
   HIP_TRY(hipStreamSynchronize(hs));
   HIP_TRY(hipMemcpyAsync(dst, src, need, hipMemcpyHostToDevice, hs));
   if (which == MOARA_T_P) {
-    HIP_TRY(launch_convert_projector(h.P32, h.Pop, h.Ptop, h.s, h.r, st->cfg.operand_dtype == MOARA_BF16, hs));
+    HIP_TRY(launch_convert_projector(h.P32, h.Pop, h.Ptop, h.s, h.r, st->cfg.operand_dtype == MOARA_BF16, h.kp ? 1 : 0,
+                                     hs));
     h.hasP = true;
   }
   HIP_TRY(hipStreamSynchronize(hs));

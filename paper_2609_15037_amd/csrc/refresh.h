@@ -25,6 +25,8 @@ struct RefDev {
   float* P32;         // s x r fp32 master projector
   void* Pop;          // s x r operand dtype
   void* Ptop;         // r x s operand dtype
+  int32_t kp;         // 1: Pop and Ptop in the blocked operand layout (kp_index; bf16)
+  int32_t pad_kp;
   uint32_t* off;      // per-sweep max off-diagonal (float bits), >= n_sweeps entries
   int32_t* order;     // wpad scratch: column order by norm
   double* norms;      // wpad scratch
@@ -49,7 +51,8 @@ struct TransProb {
   void* out;            // cols x rows bf16, row stride ldo
   int64_t rows, cols, ldi, ldo;
   int32_t in_f32, tiles_c;   // tiles_c: 64-wide tiles along cols
-  uint32_t tile_start, pad_;
+  uint32_t tile_start;
+  int32_t in_kp;             // 1: bf16 input in the blocked layout (kp_index(r, c, rows))
 };
 uint32_t transpose_tiles(int64_t rows, int64_t cols);
 hipError_t launch_transpose(const TransProb* t, int n, uint32_t total, hipStream_t st);
@@ -67,7 +70,7 @@ uint32_t r_colmajor_tiles(int32_t w, int32_t wpad);
 hipError_t launch_finalize_order(const RefDev* d, int n, hipStream_t st);
 hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st);
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
-                                    int operand_bf16, hipStream_t st);
+                                    int operand_bf16, int kp, hipStream_t st);
 uint32_t gauss_tiles(int64_t s, int32_t w);
 uint32_t gram_tiles(int32_t w);
 uint32_t jacobi_tiles(int32_t wpad);

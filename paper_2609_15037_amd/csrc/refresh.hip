@@ -331,7 +331,8 @@ __global__ __launch_bounds__(256) void k_transpose(const TransProb* __restrict__
     float v = 0.f;
     if (r0 + r < P.rows && c0 + c < P.cols) {
       const int64_t i = (r0 + r) * P.ldi + c0 + c;
-      v = P.in_f32 ? ((const float*)P.in)[i] : (float)((const bf16*)P.in)[i];
+      v = P.in_f32 ? ((const float*)P.in)[i]
+                   : (float)((const bf16*)P.in)[P.in_kp ? kp_index(r0 + r, c0 + c, P.rows) : i];
     }
     T[r][c] = v;
   }
@@ -450,8 +451,8 @@ __global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__
       const float v = deg ? (i == (j % s) ? 1.f : 0.f) : sgn * d.Pw[i * d.r + j];
       d.P32[i * d.r + j] = v;
       if (d.operand_bf16) {
-        ((bf16*)d.Pop)[i * d.r + j] = f2bf(v);
-        ((bf16*)d.Ptop)[(int64_t)j * s + i] = f2bf(v);
+        ((bf16*)d.Pop)[d.kp ? kp_index(i, j, s) : i * d.r + j] = f2bf(v);
+        ((bf16*)d.Ptop)[d.kp ? kp_index(j, i, d.r) : (int64_t)j * s + i] = f2bf(v);
       } else {
         ((float*)d.Pop)[i * d.r + j] = v;
         ((float*)d.Ptop)[(int64_t)j * s + i] = v;
@@ -462,14 +463,14 @@ __global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__
 }
 
 __global__ __launch_bounds__(256) void k_convert_projector(const float* __restrict__ P32, void* Pop, void* Ptop,
-                                                           int64_t s, int64_t r, int bf) {
+                                                           int64_t s, int64_t r, int bf, int kp) {
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (e >= s * r) return;
   const int64_t i = e / r, j = e % r;
   const float v = P32[e];
   if (bf) {
-    ((bf16*)Pop)[e] = f2bf(v);
-    ((bf16*)Ptop)[j * s + i] = f2bf(v);
+    ((bf16*)Pop)[kp ? kp_index(i, j, s) : e] = f2bf(v);
+    ((bf16*)Ptop)[kp ? kp_index(j, i, r) : j * s + i] = f2bf(v);
   } else {
     ((float*)Pop)[e] = v;
     ((float*)Ptop)[j * s + i] = v;
@@ -520,10 +521,10 @@ hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st) {
   return hipGetLastError();
 }
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
-                                    int operand_bf16, hipStream_t st) {
+                                    int operand_bf16, int kp, hipStream_t st) {
   const int64_t total = s * r;
   if (!total) return hipSuccess;
   hipLaunchKernelGGL(k_convert_projector, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st, P32, Pop, Ptop,
-                     s, r, operand_bf16);
+                     s, r, operand_bf16, kp);
   return hipGetLastError();
 }
