@@ -15,11 +15,11 @@
 // path.
 //
 // When the step's GEMMs take bf16 operands, the same pass also writes the
-// direction tensor V = G * inv in bf16 (2 B/element), in the layout in which
-// the projection reads it contiguously along its reduction index: row-major
-// m x n for a RIGHT projection (V Q), transposed n x m for a LEFT one (P^T V,
-// k_decompose_vt, which stages a 64-row x 256-column slab in LDS so that each
-// transposed row segment is written as 128 contiguous bytes).
+// direction tensor V = G * inv in bf16 (2 B/element), oriented so that the
+// projection's reduction index runs along its rows (m x n for a RIGHT projection
+// V Q, transposed n x m for a LEFT one P^T V) and stored in the blocked K-panel
+// layout of the large-tile GEMM (kp_index). The transposed form comes from
+// k_decompose_vt, which stages a 64-row x 256-column slab in LDS.
 #include "common.h"
 
 namespace {
@@ -98,6 +98,44 @@ __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ ma
     }
     return;
   }
+  if (fast && B <= 128) {
+    // Row pairs: the two half-waves take rows 2p and 2p + 1 (blocks of B <= 128 columns
+    // stay inside a half-wave), so that each bf16 store of V covers both rows of a
+    // 32-column block, i.e. whole 128-byte lines of the blocked layout.
+    constexpr int UNR = 8;
+    const int gl = B >> 2;   // lanes per block
+    const int lgB = __builtin_ctz(B);
+    const int hl = lane & 31;
+    for (int rp = wave; 2 * rp < rows; rp += 4) {
+      const int rr = 2 * rp + (lane >> 5);
+      const bool rok = rr < rows;
+      const int64_t row = row0 + rr;
+      const float* g = d.G + row * n;
+      for (int64_t c00 = 0; c00 < n; c00 += 128 * UNR) {
+        float4 v[UNR];
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int64_t c = c00 + 128 * u + 4 * hl;
+          v[u] = (rok && c < n) ? *reinterpret_cast<const float4*>(g + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int u = 0; u < UNR; ++u) {
+          const int64_t c = c00 + 128 * u + 4 * hl;
+          float ss = v[u].x * v[u].x + v[u].y * v[u].y + v[u].z * v[u].z + v[u].w * v[u].w;
+          ss = group_sum(ss, gl);
+          if (rok && c < n) {
+            if ((hl & (gl - 1)) == 0) sums[rr * k + (int)(c >> lgB)] = ss;
+            if (d.Vb) {
+              const float inv = 1.0f / (sqrtf(ss) + p.decomp_eps);
+              bf16x4 o;
+              o[0] = f2bf(v[u].x * inv); o[1] = f2bf(v[u].y * inv); o[2] = f2bf(v[u].z * inv); o[3] = f2bf(v[u].w * inv);
+              *reinterpret_cast<bf16x4*>(d.Vb + kp_index(row, c, d.m)) = o;   // blocked, K = n
+            }
+          }
+        }
+      }
+    }
+  } else
   for (int rr = wave; rr < rows; rr += 4) {
     const int64_t row = row0 + rr;
     const float* g = d.G + row * n;
