@@ -4,16 +4,19 @@
 //
 //   C[M x N] = sum_k A[i][k] * B[j][k]     (A: M x K, B: N x K, both row-major)
 //
-// Workgroup tile 256 x 256, eight waves (2 along M x 4 along N), each wave a
-// 128 x 64 sub-tile of 4 x 2 v_mfma_f32_32x32x16_bf16 blocks (128 fp32
-// accumulators per lane). K advances in steps of 32 through a ring of four LDS
-// stages (32 KB each) filled by direct global->LDS buffer loads (no register
-// staging), three stages in flight ahead of the one being multiplied, one
-// barrier per step. Each 64-byte tile row holds four 16-byte chunks stored at
-// chunk ^ f(row), f(row) = ((row >> 1) & 3) ^ ((row >> 3) & 1), so that the
-// 16-byte fragment reads of 8- and 16-lane groups hit distinct banks; the
-// lane -> global address map of the DMA loads applies the same permutation.
-// Rows past M (N) re-read the last valid row and are never stored.
+// Default configuration: workgroup tile 256 x 256, sixteen waves (4 along M x 4 along
+// N), each wave a 64 x 64 sub-tile of 2 x 2 v_mfma_f32_32x32x16_bf16 blocks (64 fp32
+// accumulators per lane), one workgroup per CU. K advances in steps of 32 through a
+// ring of LDS stages (32 KB each: four for the projection, five for the back-projection
+// whose K loop is short) filled by direct global->LDS buffer loads (no register
+// staging), the stages ahead of the one being multiplied in flight, one barrier per
+// step. Operands may be row-major or in the blocked K-panel layout (kp_index), where
+// one K step of the tile's rows is a contiguous run and the DMA loads move whole lines.
+// Each 64-byte tile row holds four 16-byte chunks stored at chunk ^ f(row),
+// f(row) = ((row >> 1) & 3) ^ ((row >> 3) & 1), so that the 16-byte fragment reads of
+// 8- and 16-lane groups hit distinct banks; the lane -> global address map of the DMA
+// loads applies the same permutation. Rows past M (N) re-read the last valid row and
+// are never stored.
 //
 // The MFMA is issued as C^T = B A^T: lane l of block (mb, nb), register j holds
 //   row = 32 mb + (l & 31), col = 32 nb + 8 (j / 4) + 4 (l / 32) + (j % 4)
