@@ -221,12 +221,37 @@ __global__ __launch_bounds__(256) void k_inv_col(const RefDev* __restrict__ ds, 
   f64x4 acc[4];
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+  // the next step's two blocks are loaded into registers while the current pair is
+  // multiplied from LDS
+  double pa[16], pb[16];
+  auto fetch = [&](int tb) {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int e = threadIdx.x + 256 * q, i = e >> 6, j = e & 63;
+      const int ra = I * NB + i, ca = tb * NB + j, rb = tb * NB + i, cb = J * NB + j;
+      pa[q] = (ra < w && ca < w) ? d.X[(int64_t)ra * w + ca] : 0.0;
+      pb[q] = (rb < w && cb < w) ? d.C[(int64_t)rb * w + cb] : 0.0;
+    }
+  };
+  auto publish = [&]() {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int e = threadIdx.x + 256 * q, i = e >> 6, j = e & 63;
+      Ab[i][j] = pa[q];
+      Bb[i][j] = pb[q];
+    }
+  };
+  fetch(I);
+  publish();
+  __syncthreads();
   for (int tb = I; tb < J; ++tb) {
-    load_blk(Ab, d.X, w, I, tb);
-    load_blk(Bb, d.C, w, tb, J);
-    __syncthreads();
+    if (tb + 1 < J) fetch(tb + 1);
     mfma_blk<false>(Ab, Bb, acc);   // += X_I,tb R_tb,J
     __syncthreads();
+    if (tb + 1 < J) {
+      publish();
+      __syncthreads();
+    }
   }
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt)

@@ -48,7 +48,8 @@ struct GemmProb {
   uint32_t a_bytes;   // extent of the A array (buffer loads past it return 0); 0 = unknown
   uint32_t b_bytes;   // extent of the B array
   uint32_t inv_bytes; // extent of the inv array
-  uint32_t pad2_;
+  uint32_t tri_b;     // fp32 kind: 1 = B[j][k] is zero for k > j (upper triangular right factor),
+                      // so a tile's K loop stops after its last column
 };
 
 struct GemmUniform {

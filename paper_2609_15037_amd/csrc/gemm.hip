@@ -598,7 +598,9 @@ __device__ __forceinline__ void mainloop_f32(const GemmProb& P, const GemmUnifor
   const Rs R = make_rs(P);
   FA<AM, FAST> ra;
   FB<BMODE, FAST> rb;
-  const int nk = (int)((P.K + BK - 1) / BK);
+  // an upper triangular right factor contributes nothing past the tile's last column
+  const int64_t kend = (P.tri_b && col0 + 128 < P.K) ? col0 + 128 : P.K;
+  const int nk = (int)((kend + BK - 1) / BK);
   auto compute = [&](const float* Ac, const float* Bc) {
 #pragma unroll
     for (int kk = 0; kk < BK / 2; ++kk) {

@@ -629,6 +629,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       gp.a = onY ? (const void*)x.Y : (const void*)x.Z2;
       gp.lda = x.w;
       gp.b = x.Rinv; gp.ldb = x.w;
+      gp.tri_b = 1;   // Rinv is upper triangular (its lower part is zero)
       gp.c = onY ? (void*)x.Y2 : (void*)x.Z;
       gp.ldc = x.w;
       gp.tiles_n = gemm_tiles_n(kind, gp.N);

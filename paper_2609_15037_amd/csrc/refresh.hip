@@ -56,7 +56,7 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
 
 // ------------------------------------------------------------------ fp64 Gram C = A^T A
 // One workgroup per 64 x 64 tile of the upper triangle. fp32 rows are staged in
-// LDS as fp64 (32 rows per chunk, two buffers, next chunk prefetched into
+// LDS as fp64 (32 rows per chunk, two buffers, the next two chunks in flight in
 // registers) and multiplied on v_mfma_f64_16x16x4; wave w owns tile rows
 // [16w, 16w+16).
 typedef double f64x4 __attribute__((ext_vector_type(4)));
@@ -72,35 +72,32 @@ __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, i
   const int tj = ti + rem;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = (int)((g.rows + 31) / 32);
-  float pi[8], pj[8];
-  auto load_chunk = [&](int c) {
+  // Two chunks of global loads stay in flight in a register ring while the current
+  // chunk is multiplied from LDS: chunk c + 1 in slot (c + 1) & 1, chunk c + 2 in slot c & 1.
+  float pi[2][8], pj[2][8];
+  auto load_chunk = [&](int c, float (&xi)[8], float (&xj)[8]) {
     const int64_t l0 = (int64_t)c * 32;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const int e = tid + 256 * q, l = e >> 6, cc = e & 63;
       const int64_t row = l0 + l;
       const int ci = ti * 64 + cc, cj = tj * 64 + cc;
-      pi[q] = (row < g.rows && ci < g.w) ? g.A[row * g.lda + ci] : 0.f;
-      pj[q] = (row < g.rows && cj < g.w) ? g.A[row * g.lda + cj] : 0.f;
+      xi[q] = (row < g.rows && ci < g.w) ? g.A[row * g.lda + ci] : 0.f;
+      xj[q] = (row < g.rows && cj < g.w) ? g.A[row * g.lda + cj] : 0.f;
     }
   };
-  auto store_chunk = [&](int b) {
+  auto store_chunk = [&](int b, const float (&xi)[8], const float (&xj)[8]) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const int e = tid + 256 * q;
-      Ai[b][e >> 6][e & 63] = (double)pi[q];
-      Aj[b][e >> 6][e & 63] = (double)pj[q];
+      Ai[b][e >> 6][e & 63] = (double)xi[q];
+      Aj[b][e >> 6][e & 63] = (double)xj[q];
     }
   };
   f64x4 acc[4];
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
-  load_chunk(0);
-  store_chunk(0);
-  __syncthreads();
-  for (int c = 0; c < nch; ++c) {
-    if (c + 1 < nch) load_chunk(c + 1);
-    const int b = c & 1;
+  auto mult = [&](int b) {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       const int kr = 4 * ks + (lane >> 4);
@@ -109,7 +106,21 @@ __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, i
       for (int jt = 0; jt < 4; ++jt)
         acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Aj[b][kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
     }
-    if (c + 1 < nch) store_chunk(b ^ 1);
+  };
+  load_chunk(0, pi[0], pj[0]);
+  store_chunk(0, pi[0], pj[0]);
+  if (1 < nch) load_chunk(1, pi[1], pj[1]);
+  if (2 < nch) load_chunk(2, pi[0], pj[0]);
+  __syncthreads();
+  for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
+    mult(0);                                               // chunk c (LDS buffer 0)
+    if (c + 1 < nch) store_chunk(1, pi[1], pj[1]);
+    if (c + 3 < nch) load_chunk(c + 3, pi[1], pj[1]);
+    __syncthreads();
+    if (c + 1 >= nch) break;
+    mult(1);                                               // chunk c + 1 (LDS buffer 1)
+    if (c + 2 < nch) store_chunk(0, pi[0], pj[0]);
+    if (c + 4 < nch) load_chunk(c + 4, pi[0], pj[0]);
     __syncthreads();
   }
 #pragma unroll
@@ -163,36 +174,45 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
   // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
   // Wave w owns Gram rows [16w, 16w+16) and all 64 columns (four 16 x 16 tiles).
-  // 32-row chunks alternate between two LDS buffers; the next chunk's global
+  // 32-row chunks alternate between two LDS buffers; the next two chunks' global
   // loads are in flight while the current one is multiplied.
   const int lane = tid & 63, wave = tid >> 6;
   const int nch = (int)((s + 31) / 32);
-  double pre[8];
-  auto load_chunk = [&](int c) {
+  // Two chunks of global loads stay in flight in a register ring (chunk c + 1 in slot
+  // (c + 1) & 1, chunk c + 2 in slot c & 1) while chunk c is used from LDS.
+  double pre[2][8];
+  auto load_chunk = [&](int c, double (&x8)[8]) {
     const int64_t r0 = (int64_t)c * 32;
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const int e = tid + 256 * q, x = e >> 5, l = e & 31;
-      pre[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
+      x8[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
     }
   };
-  auto store_chunk = [&](double (*Tb)[PW + 1]) {
+  auto store_chunk = [&](double (*Tb)[PW + 1], const double (&x8)[8]) {
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       const int e = tid + 256 * q;
-      Tb[e & 31][e >> 5] = pre[q];
+      Tb[e & 31][e >> 5] = x8[q];
     }
+  };
+  auto prime = [&]() {   // chunk 0 -> T[0]; chunks 1, 2 in flight
+    load_chunk(0, pre[0]);
+    store_chunk(T[0], pre[0]);
+    if (1 < nch) load_chunk(1, pre[1]);
+    if (2 < nch) load_chunk(2, pre[0]);
+    __syncthreads();
+  };
+  // after using chunk c from T[c & 1]: publish chunk c + 1, refill its slot with c + 3
+  auto advance = [&](int c, double (&slot)[8]) {
+    if (c + 1 < nch) store_chunk(T[(c + 1) & 1], slot);
+    if (c + 3 < nch) load_chunk(c + 3, slot);
   };
   {
     f64x4 acc[4];
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
-    load_chunk(0);
-    store_chunk(T[0]);
-    __syncthreads();
-    for (int c = 0; c < nch; ++c) {
-      if (c + 1 < nch) load_chunk(c + 1);
-      double (*Tc)[PW + 1] = T[c & 1];
+    auto mult = [&](double (*Tc)[PW + 1]) {
 #pragma unroll
       for (int ks = 0; ks < 8; ++ks) {
         const int kr = 4 * ks + (lane >> 4);
@@ -201,7 +221,15 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
         for (int jt = 0; jt < 4; ++jt)
           acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Tc[kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
       }
-      if (c + 1 < nch) store_chunk(T[(c + 1) & 1]);
+    };
+    prime();
+    for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
+      mult(T[0]);
+      advance(c, pre[1]);
+      __syncthreads();
+      if (c + 1 >= nch) break;
+      mult(T[1]);
+      advance(c + 1, pre[0]);
       __syncthreads();
     }
 #pragma unroll
@@ -284,14 +312,8 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, 32 rows at a time on
   // fp64 MFMA; wave w computes rows [16 (w&1), +16) x columns [32 (w>>1), +32).
   // Results go through LDS so the write-back is column-contiguous.
-  load_chunk(0);
-  store_chunk(T[0]);
-  __syncthreads();
   const int rt = wave & 1, cb = 2 * (wave >> 1);
-  for (int c = 0; c < nch; ++c) {
-    const int64_t r0 = (int64_t)c * 32;
-    if (c + 1 < nch) load_chunk(c + 1);
-    double (*Tc)[PW + 1] = T[c & 1];
+  auto rotate = [&](int c, double (*Tc)[PW + 1]) {
     f64x4 o0 = {0.0, 0.0, 0.0, 0.0}, o1 = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int ks = 0; ks < PW / 4; ++ks) {
@@ -305,12 +327,26 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
       O[16 * rt + 4 * r + (lane >> 4)][16 * cb + (lane & 15)] = o0[r];
       O[16 * rt + 4 * r + (lane >> 4)][16 * (cb + 1) + (lane & 15)] = o1[r];
     }
-    if (c + 1 < nch) store_chunk(T[(c + 1) & 1]);
-    __syncthreads();
+  };
+  auto write_out = [&](int c) {
+    const int64_t r0 = (int64_t)c * 32;
     for (int e = tid; e < 32 * PW; e += 256) {
       const int x = e >> 5, l = e & 31;
       if (r0 + l < s) colp(x)[r0 + l] = O[l][x];
     }
+  };
+  prime();
+  for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
+    rotate(c, T[0]);
+    advance(c, pre[1]);
+    __syncthreads();
+    write_out(c);
+    __syncthreads();
+    if (c + 1 >= nch) break;
+    rotate(c + 1, T[1]);
+    advance(c + 1, pre[0]);
+    __syncthreads();
+    write_out(c + 1);
     __syncthreads();
   }
 }
