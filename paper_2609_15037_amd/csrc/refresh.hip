@@ -61,8 +61,9 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
 // [16w, 16w+16).
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, int n) {
-  __shared__ double Ai[2][32][64 + 1];
-  __shared__ double Aj[2][32][64 + 1];
+  // row stride 66 doubles keeps every 4-column group 16-byte aligned for b128 stores
+  __shared__ __attribute__((aligned(16))) double Ai[2][32][64 + 2];
+  __shared__ __attribute__((aligned(16))) double Aj[2][32][64 + 2];
   const uint32_t t = blockIdx.x;
   int lo = 0, hi = n - 1;
   while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (gs[mid].tile_start <= t) lo = mid; else hi = mid - 1; }
@@ -72,26 +73,35 @@ __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, i
   const int tj = ti + rem;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int nch = (int)((g.rows + 31) / 32);
+  // 16-byte loads of four columns when rows and the width allow them
+  const bool vec = (g.lda & 3) == 0 && (g.w & 3) == 0 && (((uintptr_t)g.A) & 15) == 0;
   // Two chunks of global loads stay in flight in a register ring while the current
   // chunk is multiplied from LDS: chunk c + 1 in slot (c + 1) & 1, chunk c + 2 in slot c & 1.
-  float pi[2][8], pj[2][8];
-  auto load_chunk = [&](int c, float (&xi)[8], float (&xj)[8]) {
+  // Thread e of a chunk (two per thread) covers row e / 16, columns 4 (e % 16) .. + 3.
+  float4 pi[2][2], pj[2][2];
+  auto load4 = [&](int64_t row, int col) -> float4 {
+    if (row >= g.rows || col >= g.w) return make_float4(0.f, 0.f, 0.f, 0.f);
+    const float* src = g.A + row * g.lda + col;
+    if (vec) return *reinterpret_cast<const float4*>(src);
+    return make_float4(src[0], col + 1 < g.w ? src[1] : 0.f, col + 2 < g.w ? src[2] : 0.f, col + 3 < g.w ? src[3] : 0.f);
+  };
+  auto load_chunk = [&](int c, float4 (&xi)[2], float4 (&xj)[2]) {
     const int64_t l0 = (int64_t)c * 32;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + 256 * q, l = e >> 6, cc = e & 63;
-      const int64_t row = l0 + l;
-      const int ci = ti * 64 + cc, cj = tj * 64 + cc;
-      xi[q] = (row < g.rows && ci < g.w) ? g.A[row * g.lda + ci] : 0.f;
-      xj[q] = (row < g.rows && cj < g.w) ? g.A[row * g.lda + cj] : 0.f;
+    for (int q = 0; q < 2; ++q) {
+      const int e = tid + 256 * q, l = e >> 4, c4 = (e & 15) * 4;
+      xi[q] = load4(l0 + l, ti * 64 + c4);
+      xj[q] = load4(l0 + l, tj * 64 + c4);
     }
   };
-  auto store_chunk = [&](int b, const float (&xi)[8], const float (&xj)[8]) {
+  auto store_chunk = [&](int b, const float4 (&xi)[2], const float4 (&xj)[2]) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + 256 * q;
-      Ai[b][e >> 6][e & 63] = (double)xi[q];
-      Aj[b][e >> 6][e & 63] = (double)xj[q];
+    for (int q = 0; q < 2; ++q) {
+      const int e = tid + 256 * q, l = e >> 4, c4 = (e & 15) * 4;
+      double2* di = reinterpret_cast<double2*>(&Ai[b][l][c4]);
+      double2* dj = reinterpret_cast<double2*>(&Aj[b][l][c4]);
+      di[0] = make_double2(xi[q].x, xi[q].y); di[1] = make_double2(xi[q].z, xi[q].w);
+      dj[0] = make_double2(xj[q].x, xj[q].y); dj[1] = make_double2(xj[q].z, xj[q].w);
     }
   };
   f64x4 acc[4];
@@ -144,6 +154,12 @@ __device__ __forceinline__ int circle(int pos, int round, int nb) {
 }
 
 constexpr int PW = 2 * JB;   // 64 columns per pair
+// Convergence: a pair whose largest column cosine is below JAC_TOL is not rotated, and a
+// matrix stops once a whole sweep measured below it. Cosines c between columns with
+// relative singular-value gap g perturb the singular subspaces by about c / (2 g); at
+// 1e-10 that stays below 1e-6 rad for gaps down to 1e-4, and the next sweep (quadratic
+// convergence) would only polish digits the fp32 projector does not keep.
+constexpr double JAC_TOL = 1e-10;
 // Inner Jacobi sweeps per pair visit. The pair's Gram need not be diagonalised
 // exactly on every visit: with one inner sweep the outer iteration needs about one
 // more sweep to reach the same off-diagonal level, but every visit is much cheaper
@@ -165,7 +181,7 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   const int nb = d.wpad / JB;
   const int pair = (int)(t - d.tile_jac);
   if (round >= nb - 1) return;   // this matrix has fewer blocks than the widest one
-  if (sweep > 0 && __uint_as_float(d.off[sweep - 1]) < 1e-13f) return;   // converged
+  if (sweep > 0 && __uint_as_float(d.off[sweep - 1]) < (float)JAC_TOL) return;   // converged
   const int ba = circle(pair, round, nb), bb = circle(nb - 1 - pair, round, nb);
   const int tid = threadIdx.x;
   const int64_t s = d.jl;   // column length
@@ -253,7 +269,7 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
     if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)red[0]));
-    if (red[0] < 1e-13) return;   // already orthogonal: nothing to rotate (uniform branch)
+    if (red[0] < JAC_TOL) return;   // already orthogonal: nothing to rotate (uniform branch)
   }
 
   // (2) JAC_INNER_SWEEPS sweeps of parallel cyclic Jacobi on the 64 x 64 Gram. One round
