@@ -168,12 +168,15 @@ constexpr double JAC_TOL = 1e-10;
 #define JAC_INNER_SWEEPS 1
 #endif
 
-__global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
-  __shared__ double T[2][32][PW + 1];   // (also the second 64 x 64 G buffer of the inner solve)
-  __shared__ double O[32][PW + 1];
+// LDS: the pair's Gram G and rotation J (64 x 65 fp64 each) and one 16-row chunk of the
+// columns (16 x 65); the rotation output is staged in G's space and the reduction scratch
+// in the chunk's, so two workgroups fit on a CU and one's LDS-bound inner solve overlaps
+// the other's MFMA / memory phases.
+constexpr int JR = 16;   // rows per column chunk
+__global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
   __shared__ double Gm[PW][PW + 1];
   __shared__ double Jm[PW][PW + 1];
-  __shared__ double red[256];
+  __shared__ double T[JR][PW + 1];
   const uint32_t t = blockIdx.x;
   int lo = 0, hi = n - 1;
   while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_jac <= t) lo = mid; else hi = mid - 1; }
@@ -186,65 +189,67 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   const int tid = threadIdx.x;
   const int64_t s = d.jl;   // column length
   auto colp = [&](int x) -> double* { return d.Zc + (int64_t)((x < JB) ? ba * JB + x : bb * JB + (x - JB)) * s; };
-
-  // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
-  // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
-  // Wave w owns Gram rows [16w, 16w+16) and all 64 columns (four 16 x 16 tiles).
-  // 32-row chunks alternate between two LDS buffers; the next two chunks' global
-  // loads are in flight while the current one is multiplied.
   const int lane = tid & 63, wave = tid >> 6;
-  const int nch = (int)((s + 31) / 32);
-  // Two chunks of global loads stay in flight in a register ring (chunk c + 1 in slot
+  const int nch = (int)((s + JR - 1) / JR);
+
+  // Column chunks: 16 rows x 64 columns, thread e = tid + 256 q covers column e / 16,
+  // row e % 16. Two chunks stay in flight in a register ring (chunk c + 1 in slot
   // (c + 1) & 1, chunk c + 2 in slot c & 1) while chunk c is used from LDS.
-  double pre[2][8];
-  auto load_chunk = [&](int c, double (&x8)[8]) {
-    const int64_t r0 = (int64_t)c * 32;
+  double pre[2][4];
+  auto load_chunk = [&](int c, double (&x4)[4]) {
+    const int64_t r0 = (int64_t)c * JR;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + 256 * q, x = e >> 5, l = e & 31;
-      x8[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + 256 * q, x = e >> 4, l = e & 15;
+      x4[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
     }
   };
-  auto store_chunk = [&](double (*Tb)[PW + 1], const double (&x8)[8]) {
+  auto store_chunk = [&](const double (&x4)[4]) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
+    for (int q = 0; q < 4; ++q) {
       const int e = tid + 256 * q;
-      Tb[e & 31][e >> 5] = x8[q];
+      T[e & 15][e >> 4] = x4[q];
     }
   };
-  auto prime = [&]() {   // chunk 0 -> T[0]; chunks 1, 2 in flight
+  auto prime = [&]() {   // chunk 0 -> T; chunks 1, 2 in flight
     load_chunk(0, pre[0]);
-    store_chunk(T[0], pre[0]);
+    store_chunk(pre[0]);
     if (1 < nch) load_chunk(1, pre[1]);
     if (2 < nch) load_chunk(2, pre[0]);
     __syncthreads();
   };
-  // after using chunk c from T[c & 1]: publish chunk c + 1, refill its slot with c + 3
-  auto advance = [&](int c, double (&slot)[8]) {
-    if (c + 1 < nch) store_chunk(T[(c + 1) & 1], slot);
+  // after every wave is done with chunk c in T: publish chunk c + 1, refill its slot
+  auto advance = [&](int c, double (&slot)[4]) {
+    if (c + 1 < nch) store_chunk(slot);
     if (c + 3 < nch) load_chunk(c + 3, slot);
   };
+
+  // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
+  // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
+  // Wave w owns Gram rows [16w, 16w+16) and all 64 columns (four 16 x 16 tiles).
   {
     f64x4 acc[4];
 #pragma unroll
     for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
-    auto mult = [&](double (*Tc)[PW + 1]) {
+    auto mult = [&]() {
 #pragma unroll
-      for (int ks = 0; ks < 8; ++ks) {
+      for (int ks = 0; ks < JR / 4; ++ks) {
         const int kr = 4 * ks + (lane >> 4);
-        const double a = Tc[kr][16 * wave + (lane & 15)];
+        const double a = T[kr][16 * wave + (lane & 15)];
 #pragma unroll
         for (int jt = 0; jt < 4; ++jt)
-          acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Tc[kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+          acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, T[kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
       }
     };
     prime();
     for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
-      mult(T[0]);
+      mult();
+      __syncthreads();
       advance(c, pre[1]);
       __syncthreads();
       if (c + 1 >= nch) break;
-      mult(T[1]);
+      mult();
+      __syncthreads();
       advance(c + 1, pre[0]);
       __syncthreads();
     }
@@ -257,6 +262,7 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
   __syncthreads();
   // convergence measure of this pair (before rotating): max |g_xy| / sqrt(g_xx g_yy)
   {
+    double* red = &T[0][0];   // the chunk buffer is idle here (256 <= 16 * 65)
     double m = 0.0;
     for (int e = tid; e < PW * PW; e += 256) {
       const int x = e / PW, y = e % PW;
@@ -268,20 +274,20 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
     red[tid] = m;
     __syncthreads();
     for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
-    if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)red[0]));
-    if (red[0] < JAC_TOL) return;   // already orthogonal: nothing to rotate (uniform branch)
+    const double mx = red[0];
+    if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)mx));
+    if (mx < JAC_TOL) return;   // already orthogonal: nothing to rotate (uniform branch)
+    __syncthreads();            // red[0] is read by every thread before the chunk buffer is reused
   }
 
-  // (2) JAC_INNER_SWEEPS sweeps of parallel cyclic Jacobi on the 64 x 64 Gram. One round
-  // rotates 32 disjoint pairs (circle method) on both sides at once, G' = R^T G R,
-  // double-buffered so that a round needs a single barrier: lane l computes the
-  // rotation of pair beta = l % 32 from the current G, fetches the rotations of its
-  // row pairs alpha from lanes alpha by shuffles, writes four 2 x 2 blocks of G', and
-  // applies rotation beta to eight rows of the accumulated J. The second G buffer
-  // aliases the row-chunk buffers, which are idle during this phase.
+  // (2) JAC_INNER_SWEEPS sweeps of parallel cyclic Jacobi on the 64 x 64 Gram, in place.
+  // One round rotates 32 disjoint pairs (circle method) on both sides at once,
+  // G' = R^T G R: lane l computes the rotation of pair beta = l % 32 from the current
+  // G; after a barrier (every rotation read before any entry changes) it fetches the
+  // rotations of its row pairs alpha from lanes alpha by shuffles and rewrites four
+  // 2 x 2 blocks of G, which no other lane touches, and applies rotation beta to eight
+  // rows of the accumulated J.
   {
-    double (*Ga)[PW + 1] = Gm;
-    double (*Gb)[PW + 1] = reinterpret_cast<double (*)[PW + 1]>(&T[0][0][0]);
     const int beta = lane & 31, half = lane >> 5;
     for (int isw = 0; isw < JAC_INNER_SWEEPS; ++isw) {
       for (int rr = 0; rr < PW - 1; ++rr) {
@@ -289,7 +295,7 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
         if (pb > qb) { const int tmp = pb; pb = qb; qb = tmp; }
         double cb = 1.0, sb = 0.0;
         {
-          const double app = Ga[pb][pb], aqq = Ga[qb][qb], apq = Ga[pb][qb];
+          const double app = Gm[pb][pb], aqq = Gm[qb][qb], apq = Gm[pb][qb];
           const double den = sqrt(app * aqq);
           if (den > 0.0 && fabs(apq) > 1e-16 * den) {
             const double zeta = (aqq - app) / (2.0 * apq);
@@ -298,19 +304,20 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
             sb = cb * tt;
           }
         }
+        __syncthreads();
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int alpha = 2 * (4 * wave + i) + half;
           int pa = circle(alpha, rr, PW), qa = circle(PW - 1 - alpha, rr, PW);
           if (pa > qa) { const int tmp = pa; pa = qa; qa = tmp; }
           const double ca = __shfl(cb, alpha, 64), sa = __shfl(sb, alpha, 64);
-          const double g_pp = Ga[pa][pb], g_pq = Ga[pa][qb], g_qp = Ga[qa][pb], g_qq = Ga[qa][qb];
+          const double g_pp = Gm[pa][pb], g_pq = Gm[pa][qb], g_qp = Gm[qa][pb], g_qq = Gm[qa][qb];
           const double r_pp = ca * g_pp - sa * g_qp, r_pq = ca * g_pq - sa * g_qq;   // rows
           const double r_qp = sa * g_pp + ca * g_qp, r_qq = sa * g_pq + ca * g_qq;
-          Gb[pa][pb] = cb * r_pp - sb * r_pq;                                          // columns
-          Gb[pa][qb] = sb * r_pp + cb * r_pq;
-          Gb[qa][pb] = cb * r_qp - sb * r_qq;
-          Gb[qa][qb] = sb * r_qp + cb * r_qq;
+          Gm[pa][pb] = cb * r_pp - sb * r_pq;                                          // columns
+          Gm[pa][qb] = sb * r_pp + cb * r_pq;
+          Gm[qa][pb] = cb * r_qp - sb * r_qq;
+          Gm[qa][qb] = sb * r_qp + cb * r_qq;
         }
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
@@ -320,49 +327,44 @@ __global__ __launch_bounds__(256) void k_jacobi_round(const RefDev* __restrict__
           Jm[a][qb] = sb * jp + cb * jq;
         }
         __syncthreads();
-        double (*tmp)[PW + 1] = Ga; Ga = Gb; Gb = tmp;
       }
     }
   }
 
-  // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, 32 rows at a time on
-  // fp64 MFMA; wave w computes rows [16 (w&1), +16) x columns [32 (w>>1), +32).
-  // Results go through LDS so the write-back is column-contiguous.
-  const int rt = wave & 1, cb = 2 * (wave >> 1);
-  auto rotate = [&](int c, double (*Tc)[PW + 1]) {
-    f64x4 o0 = {0.0, 0.0, 0.0, 0.0}, o1 = {0.0, 0.0, 0.0, 0.0};
+  // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, 16 rows at a time on
+  // fp64 MFMA; wave w computes the chunk's 16 rows x columns [16w, 16w+16). The
+  // result goes through LDS (G's space, idle now) so the write-back is column-contiguous.
+  double (*O)[PW + 1] = Gm;
+  auto rotate = [&]() {
+    f64x4 o = {0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int ks = 0; ks < PW / 4; ++ks) {
       const int y = 4 * ks + (lane >> 4);
-      const double a = Tc[16 * rt + (lane & 15)][y];
-      o0 = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Jm[y][16 * cb + (lane & 15)], o0, 0, 0, 0);
-      o1 = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Jm[y][16 * (cb + 1) + (lane & 15)], o1, 0, 0, 0);
+      o = __builtin_amdgcn_mfma_f64_16x16x4f64(T[lane & 15][y], Jm[y][16 * wave + (lane & 15)], o, 0, 0, 0);
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      O[16 * rt + 4 * r + (lane >> 4)][16 * cb + (lane & 15)] = o0[r];
-      O[16 * rt + 4 * r + (lane >> 4)][16 * (cb + 1) + (lane & 15)] = o1[r];
-    }
+    for (int r = 0; r < 4; ++r) O[4 * r + (lane >> 4)][16 * wave + (lane & 15)] = o[r];
   };
   auto write_out = [&](int c) {
-    const int64_t r0 = (int64_t)c * 32;
-    for (int e = tid; e < 32 * PW; e += 256) {
-      const int x = e >> 5, l = e & 31;
+    const int64_t r0 = (int64_t)c * JR;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + 256 * q, x = e >> 4, l = e & 15;
       if (r0 + l < s) colp(x)[r0 + l] = O[l][x];
     }
   };
   prime();
   for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
-    rotate(c, T[0]);
-    advance(c, pre[1]);
+    rotate();
     __syncthreads();
     write_out(c);
+    advance(c, pre[1]);
     __syncthreads();
     if (c + 1 >= nch) break;
-    rotate(c + 1, T[1]);
-    advance(c + 1, pre[0]);
+    rotate();
     __syncthreads();
     write_out(c + 1);
+    advance(c + 1, pre[0]);
     __syncthreads();
   }
 }
