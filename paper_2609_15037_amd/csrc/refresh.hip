@@ -56,14 +56,14 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
 
 // ------------------------------------------------------------------ fp64 Gram C = A^T A
 // One workgroup per 64 x 64 tile of the upper triangle. fp32 rows are staged in
-// LDS as fp64 (32 rows per chunk, two buffers, the next two chunks in flight in
-// registers) and multiplied on v_mfma_f64_16x16x4; wave w owns tile rows
-// [16w, 16w+16).
+// LDS as fp64 (32 rows per chunk, the next two chunks in flight in registers) and
+// multiplied on v_mfma_f64_16x16x4; wave w owns tile rows [16w, 16w+16).
 typedef double f64x4 __attribute__((ext_vector_type(4)));
-__global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, int n) {
-  // row stride 66 doubles keeps every 4-column group 16-byte aligned for b128 stores
-  __shared__ __attribute__((aligned(16))) double Ai[2][32][64 + 2];
-  __shared__ __attribute__((aligned(16))) double Aj[2][32][64 + 2];
+__global__ __launch_bounds__(256, 4) void k_gram(const GramProb* __restrict__ gs, int n) {
+  // One LDS buffer per operand (34 KB in all, four workgroups per CU); row stride 66
+  // doubles keeps every 4-column group 16-byte aligned for b128 stores.
+  __shared__ __attribute__((aligned(16))) double Ai[32][64 + 2];
+  __shared__ __attribute__((aligned(16))) double Aj[32][64 + 2];
   const uint32_t t = blockIdx.x;
   int lo = 0, hi = n - 1;
   while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (gs[mid].tile_start <= t) lo = mid; else hi = mid - 1; }
@@ -94,12 +94,12 @@ __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, i
       xj[q] = load4(l0 + l, tj * 64 + c4);
     }
   };
-  auto store_chunk = [&](int b, const float4 (&xi)[2], const float4 (&xj)[2]) {
+  auto store_chunk = [&](const float4 (&xi)[2], const float4 (&xj)[2]) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
       const int e = tid + 256 * q, l = e >> 4, c4 = (e & 15) * 4;
-      double2* di = reinterpret_cast<double2*>(&Ai[b][l][c4]);
-      double2* dj = reinterpret_cast<double2*>(&Aj[b][l][c4]);
+      double2* di = reinterpret_cast<double2*>(&Ai[l][c4]);
+      double2* dj = reinterpret_cast<double2*>(&Aj[l][c4]);
       di[0] = make_double2(xi[q].x, xi[q].y); di[1] = make_double2(xi[q].z, xi[q].w);
       dj[0] = make_double2(xj[q].x, xj[q].y); dj[1] = make_double2(xj[q].z, xj[q].w);
     }
@@ -107,29 +107,31 @@ __global__ __launch_bounds__(256) void k_gram(const GramProb* __restrict__ gs, i
   f64x4 acc[4];
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
-  auto mult = [&](int b) {
+  auto mult = [&]() {
 #pragma unroll
     for (int ks = 0; ks < 8; ++ks) {
       const int kr = 4 * ks + (lane >> 4);
-      const double a = Ai[b][kr][16 * wave + (lane & 15)];
+      const double a = Ai[kr][16 * wave + (lane & 15)];
 #pragma unroll
       for (int jt = 0; jt < 4; ++jt)
-        acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Aj[b][kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+        acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, Aj[kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
     }
   };
   load_chunk(0, pi[0], pj[0]);
-  store_chunk(0, pi[0], pj[0]);
+  store_chunk(pi[0], pj[0]);
   if (1 < nch) load_chunk(1, pi[1], pj[1]);
   if (2 < nch) load_chunk(2, pi[0], pj[0]);
   __syncthreads();
   for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
-    mult(0);                                               // chunk c (LDS buffer 0)
-    if (c + 1 < nch) store_chunk(1, pi[1], pj[1]);
+    mult();                                                // chunk c
+    __syncthreads();
+    if (c + 1 < nch) store_chunk(pi[1], pj[1]);
     if (c + 3 < nch) load_chunk(c + 3, pi[1], pj[1]);
     __syncthreads();
     if (c + 1 >= nch) break;
-    mult(1);                                               // chunk c + 1 (LDS buffer 1)
-    if (c + 2 < nch) store_chunk(0, pi[0], pj[0]);
+    mult();                                                // chunk c + 1
+    __syncthreads();
+    if (c + 2 < nch) store_chunk(pi[0], pj[0]);
     if (c + 4 < nch) load_chunk(c + 4, pi[0], pj[0]);
     __syncthreads();
   }
