@@ -35,36 +35,6 @@ __device__ __forceinline__ void load_blk(double (*dst)[LDB], const double* M, in
   }
 }
 
-// out[x][y] += sum_t A[t][x] * B[t][y]   (A, B in LDS, 64 x 64); thread owns a 4 x 4 block
-__device__ __forceinline__ void atb_acc(const double (*A)[LDB], const double (*Bm)[LDB], double (&acc)[4][4]) {
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-#pragma unroll 4
-  for (int t = 0; t < NB; ++t) {
-    double a[4], b[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) { a[q] = A[t][ty * 4 + q]; b[q] = Bm[t][tx * 4 + q]; }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
-  }
-}
-
-// out[x][y] += sum_t A[x][t] * B[t][y]
-__device__ __forceinline__ void ab_acc(const double (*A)[LDB], const double (*Bm)[LDB], double (&acc)[4][4]) {
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
-#pragma unroll 4
-  for (int t = 0; t < NB; ++t) {
-    double a[4], b[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) { a[q] = A[ty * 4 + q][t]; b[q] = Bm[t][tx * 4 + q]; }
-#pragma unroll
-    for (int q = 0; q < 4; ++q)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) acc[q][u] = fma(a[q], b[u], acc[q][u]);
-  }
-}
-
 // fp64 MFMA form of the 64 x 64 block products (v_mfma_f64_16x16x4: lane l supplies
 // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
 // Wave w accumulates rows [16w, 16w+16) of the product, all 64 columns (four 16 x 16
@@ -156,33 +126,50 @@ __global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds
   }
 }
 
-__global__ __launch_bounds__(256) void k_chol_panel(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
-                                                    int n, int k) {
+__global__ __launch_bounds__(256, 4) void k_chol_panel(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
+                                                       int n, int k) {
   const uint32_t t = blockIdx.x;
   const int mi = find_pref(pref, n, t);
   const RefDev& d = ds[mi];
   const int w = d.w;
   const int j = k + 1 + (int)(t - pref[mi]);
-  __shared__ double Xk[NB][LDB];
+  // R_kj = X_kk^T C_kj: C_kj in LDS, each wave's 16 columns of X_kk straight into its MFMA
+  // operand registers (A[i][t] = X_kk[t][16 w + i])
   __shared__ double Cb[NB][LDB];
-  load_blk(Xk, d.X, w, k, k);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double av[NB / 4];
+  {
+    const int col = k * NB + 16 * wave + (lane & 15);
+#pragma unroll
+    for (int ks = 0; ks < NB / 4; ++ks) {
+      const int row = k * NB + 4 * ks + (lane >> 4);
+      av[ks] = (row < w && col < w) ? d.X[(int64_t)row * w + col] : 0.0;
+    }
+  }
   load_blk(Cb, d.C, w, k, j);
   __syncthreads();
-  double acc[4][4] = {};
-  atb_acc(Xk, Cb, acc);   // (X_kk)^T C_kj
-  const int tx = threadIdx.x & 15, ty = threadIdx.x >> 4;
+  f64x4 acc[4];
+#pragma unroll
+  for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+#pragma unroll
+  for (int ks = 0; ks < NB / 4; ++ks) {
+    const int tr = 4 * ks + (lane >> 4);
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+      acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[ks], Cb[tr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+  }
   const bool zero = !(d.cmax[0] > 0.0);
 #pragma unroll
-  for (int q = 0; q < 4; ++q)
+  for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int r = k * NB + ty * 4 + q, c = j * NB + tx * 4 + u;
-      if (r < w && c < w) d.C[(int64_t)r * w + c] = zero ? 0.0 : acc[q][u];
+    for (int r = 0; r < 4; ++r) {
+      const int row = k * NB + mfma_row(r), col = j * NB + mfma_col(jt);
+      if (row < w && col < w) d.C[(int64_t)row * w + col] = zero ? 0.0 : acc[jt][r];
     }
 }
 
-__global__ __launch_bounds__(256) void k_chol_update(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
-                                                     int n, int k) {
+__global__ __launch_bounds__(256, 4) void k_chol_update(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
+                                                        int n, int k) {
   const uint32_t t = blockIdx.x;
   const int mi = find_pref(pref, n, t);
   const RefDev& d = ds[mi];
@@ -191,15 +178,32 @@ __global__ __launch_bounds__(256) void k_chol_update(const RefDev* __restrict__ 
   int rem = (int)(t - pref[mi]), ta = 0;
   while (rem >= T - ta) { rem -= T - ta; ++ta; }
   const int a = k + 1 + ta, c = a + rem;
-  __shared__ double Ra[NB][LDB];
+  // R_kc is shared by the four waves through LDS; each wave's 16 columns of R_ka go
+  // straight from memory into its MFMA operand registers (A[i][t] = R_ka[t][16 w + i]),
+  // so a workgroup needs 33 KB of LDS and four fit on a CU.
   __shared__ double Rc[NB][LDB];
-  load_blk(Ra, d.C, w, k, a);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double av[NB / 4];
+  {
+    const int col = a * NB + 16 * wave + (lane & 15);
+#pragma unroll
+    for (int ks = 0; ks < NB / 4; ++ks) {
+      const int row = k * NB + 4 * ks + (lane >> 4);
+      av[ks] = (row < w && col < w) ? d.C[(int64_t)row * w + col] : 0.0;
+    }
+  }
   load_blk(Rc, d.C, w, k, c);
   __syncthreads();
   f64x4 acc[4];
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
-  mfma_blk<true>(Ra, Rc, acc);   // R_ka^T R_kc
+#pragma unroll
+  for (int ks = 0; ks < NB / 4; ++ks) {
+    const int tr = 4 * ks + (lane >> 4);
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+      acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[ks], Rc[tr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);   // R_ka^T R_kc
+  }
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
