@@ -269,7 +269,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
           } else {
             bf16x4 o;
             o[0] = f2bf(v.x); o[1] = f2bf(v.y); o[2] = f2bf(v.z); o[3] = f2bf(v.w);
-            *reinterpret_cast<bf16x4*>((bf16*)P.c + idx) = o;
+            *reinterpret_cast<bf16x4*>((bf16*)P.c + ((P.kp & 4) ? kp_index(row, col, P.M) : idx)) = o;
           }
         }
       }

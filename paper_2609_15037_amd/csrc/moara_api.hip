@@ -585,7 +585,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   const GemmUniform u = make_uniform(st, 0.f);
 
   std::vector<RefDev> rd(nm);
-  uint32_t tg = 0, tj = 0, tc = 0;
+  uint32_t tg = 0, tj = 0, tc = 0, tnorm = 0;
   int nb_max = 2;
   for (int q = 0; q < nm; ++q) {
     const RefMat& x = rm[q];
@@ -601,6 +601,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     d.tile_gauss = tg; tg += gauss_tiles(x.s, x.w);
     d.tile_jac = tj; tj += jacobi_tiles(x.wpad);
     d.tile_cm = tc; tc += r_colmajor_tiles(x.w, x.wpad);
+    d.tile_norm = tnorm; tnorm += norm_tiles(x.wpad);
     d.has_prev = h.hasP ? 1 : 0;
     nb_max = std::max(nb_max, x.wpad / JB);
   }
@@ -714,23 +715,25 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     if (!x.bf) continue;
     const MatHost& h = st->mats[x.idx];
     TransProb a{};
-    a.in = x.Z; a.out = x.Zt; a.rows = x.s; a.cols = x.w; a.ldi = x.w; a.ldo = x.s; a.in_f32 = 1;
+    a.in = x.Z; a.out = x.Zt; a.rows = x.s; a.cols = x.w; a.ldi = x.w; a.ldo = x.s; a.in_f32 = 1; a.out_kp = 1;
     a.tiles_c = (int32_t)((x.w + 63) / 64); a.tile_start = ttz; ttz += transpose_tiles(x.s, x.w);
     tZ.push_back(a);
     TransProb b{};
     b.in = h.V; b.out = x.XL; b.rows = x.L; b.cols = x.s; b.ldi = x.s; b.ldo = x.L; b.in_f32 = 0; b.in_kp = 1;
+    b.out_kp = 1;
     b.tiles_c = (int32_t)((x.s + 63) / 64); b.tile_start = ttx; ttx += transpose_tiles(x.L, x.s);
     tX.push_back(b);
     GemmProb y{};
     y.M = x.w; y.N = x.L; y.K = x.s;
     y.a = x.Zt; y.lda = x.s; y.b = h.V; y.ldb = x.s; y.c = x.Yt; y.ldc = x.L;
-    y.kp = 2;   // V is blocked
+    y.kp = 1 | 2 | 4;   // Zt, V and the output Yt in the blocked layout (K = s for Zt and V, L for Yt)
     y.a_bytes = (uint32_t)(2 * (size_t)x.w * x.s); y.b_bytes = (uint32_t)(2 * (size_t)x.L * x.s);
     y.tiles_n = gemm_nt_tiles_n(y.N); y.tile_start = tny; tny += gemm_nt_tiles_m(y.M) * y.tiles_n;
     nY.push_back(y);
     GemmProb z{};
     z.M = x.s; z.N = x.w; z.K = x.L;
     z.a = x.XL; z.lda = x.L; z.b = x.Yt; z.ldb = x.L; z.c = x.Z2; z.ldc = x.w;
+    z.kp = 1 | 2;       // XL and Yt blocked (K = L)
     z.a_bytes = (uint32_t)(2 * (size_t)x.s * x.L); z.b_bytes = (uint32_t)(2 * (size_t)x.w * x.L);
     z.tiles_n = gemm_nt_tiles_n(z.N); z.tile_start = tnz; tnz += gemm_nt_tiles_m(z.M) * z.tiles_n;
     nZ.push_back(z);
@@ -849,7 +852,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.off, 0, 4 * 64, stream));
   for (int sw = 0; sw < MAX_SWEEPS; ++sw)
     for (int rr = 0; rr < nb_max - 1; ++rr) HIP_TRY(launch_jacobi_round(RD, nm, tj, rr, sw, stream));
-  HIP_TRY(launch_finalize_order(RD, nm, stream));
+  HIP_TRY(launch_finalize_order(RD, nm, tnorm, stream));
   HIP_TRY(launch_gemm(kind, A_KC, B_KC, EP_STORE, (const GemmProb*)D(22), nm, tpw, u, stream));
   HIP_TRY(launch_finalize_out(RD, nm, stream));
   for (auto& x : rm) st->mats[x.idx].hasP = true;

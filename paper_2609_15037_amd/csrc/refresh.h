@@ -30,7 +30,7 @@ struct RefDev {
   uint32_t* off;      // per-sweep max off-diagonal (float bits), >= n_sweeps entries
   int32_t* order;     // wpad scratch: column order by norm
   double* norms;      // wpad scratch
-  uint32_t tile_gauss, tile_jac, tile_cm;   // per-launch workgroup prefixes
+  uint32_t tile_gauss, tile_jac, tile_cm, tile_norm;   // per-launch workgroup prefixes
   int32_t has_prev;   // 1: a projector exists (an all-zero V keeps it)
 };
 
@@ -53,6 +53,8 @@ struct TransProb {
   int32_t in_f32, tiles_c;   // tiles_c: 64-wide tiles along cols
   uint32_t tile_start;
   int32_t in_kp;             // 1: bf16 input in the blocked layout (kp_index(r, c, rows))
+  int32_t out_kp;            // 1: output in the blocked layout (kp_index(c, r, cols))
+  int32_t pad_;
 };
 uint32_t transpose_tiles(int64_t rows, int64_t cols);
 hipError_t launch_transpose(const TransProb* t, int n, uint32_t total, hipStream_t st);
@@ -67,7 +69,8 @@ hipError_t launch_inv_col(const RefDev* d, const uint32_t* pref, int n, uint32_t
 hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st);
 hipError_t launch_r_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st);
 uint32_t r_colmajor_tiles(int32_t w, int32_t wpad);
-hipError_t launch_finalize_order(const RefDev* d, int n, hipStream_t st);
+uint32_t norm_tiles(int32_t wpad);
+hipError_t launch_finalize_order(const RefDev* d, int n, uint32_t norm_total, hipStream_t st);
 hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st);
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
                                     int operand_bf16, int kp, hipStream_t st);

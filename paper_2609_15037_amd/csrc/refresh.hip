@@ -395,7 +395,8 @@ __global__ __launch_bounds__(256) void k_transpose(const TransProb* __restrict__
   __syncthreads();
   for (int e = threadIdx.x; e < 64 * 64; e += 256) {
     const int c = e >> 6, r = e & 63;
-    if (r0 + r < P.rows && c0 + c < P.cols) ((bf16*)P.out)[(c0 + c) * P.ldo + r0 + r] = (bf16)T[r][c];
+    if (r0 + r < P.rows && c0 + c < P.cols)
+      ((bf16*)P.out)[P.out_kp ? kp_index(c0 + c, r0 + r, P.cols) : (c0 + c) * P.ldo + r0 + r] = (bf16)T[r][c];
   }
 }
 
@@ -429,34 +430,49 @@ __global__ __launch_bounds__(256) void k_r_colmajor(const RefDev* __restrict__ d
 // values; the Ritz vectors are Q (R J) / norm. k_finalize_order (one workgroup per
 // matrix): column norms, order by decreasing norm, Bt = the first r columns,
 // normalised (zero for numerically null directions). A GEMM then forms Pw = Q Bt^T.
-// k_finalize_out (one workgroup per matrix): make each column's largest-magnitude
+// k_finalize_out (FO_SPLIT workgroups per matrix): make each column's largest-magnitude
 // entry positive (lowest index on ties) and write P (fp32 master and both operand
 // copies). An all-zero iterate (V == 0) keeps the previous projector, or yields the
 // first r canonical basis vectors when there is none; numerically null directions
 // also fall back to e_j.
-__global__ __launch_bounds__(256) void k_finalize_order(const RefDev* __restrict__ ds) {
-  const RefDev& d = ds[blockIdx.x];
-  const int tid = threadIdx.x;
+// Column norms of R J (the Ritz values): NORM_COLS columns per workgroup, one wave per
+// column at a time (butterfly sum).
+constexpr int NORM_COLS = 16;
+__global__ __launch_bounds__(256) void k_col_norms(const RefDev* __restrict__ ds, int n) {
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = n - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_norm <= t) lo = mid; else hi = mid - 1; }
+  const RefDev& d = ds[lo];
+  const int c0 = (int)(t - d.tile_norm) * NORM_COLS;
   const int64_t L = d.jl;
   // an all-zero final iterate has R = I (zero-Gram fallback of the factorisation):
   // its Ritz values are all zero
   const bool zero = !(d.cmax[0] > 0.0);
-  __shared__ double red[256];
-  for (int c = 0; c < d.wpad; ++c) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int c = c0 + wave; c < c0 + NORM_COLS && c < d.wpad; c += 4) {
     const double* col = d.Zc + (int64_t)c * L;
     double a = 0.0;
-    for (int64_t i = tid; i < L; i += 256) a = fma(col[i], col[i], a);
-    red[tid] = a;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] += red[tid + o]; __syncthreads(); }
-    if (tid == 0) d.norms[c] = zero ? 0.0 : sqrt(red[0]);
-    __syncthreads();
+    for (int64_t i = lane; i < L; i += 64) a = fma(col[i], col[i], a);
+    a = wave_sum_d(a);
+    if (lane == 0) d.norms[c] = zero ? 0.0 : sqrt(a);
   }
+}
+
+__global__ __launch_bounds__(256) void k_finalize_order(const RefDev* __restrict__ ds) {
+  const RefDev& d = ds[blockIdx.x];
+  const int tid = threadIdx.x;
+  const int64_t L = d.jl;
+  // rank of every column by decreasing norm (ties by index), norms read from LDS
+  __shared__ double nl[2048];
+  const bool in_lds = d.wpad <= 2048;
+  if (in_lds)
+    for (int c = tid; c < d.wpad; c += 256) nl[c] = d.norms[c];
+  __syncthreads();
   for (int c = tid; c < d.wpad; c += 256) {
-    const double nc = d.norms[c];
+    const double nc = in_lds ? nl[c] : d.norms[c];
     int rank = 0;
     for (int c2 = 0; c2 < d.wpad; ++c2) {
-      const double n2 = d.norms[c2];
+      const double n2 = in_lds ? nl[c2] : d.norms[c2];
       rank += (n2 > nc) || (n2 == nc && c2 < c);
     }
     d.order[rank] = c;
@@ -472,38 +488,33 @@ __global__ __launch_bounds__(256) void k_finalize_order(const RefDev* __restrict
   }
 }
 
+// FO_SPLIT workgroups per matrix; each wave takes one column at a time (butterfly
+// argmax over its lanes, no workgroup barriers).
+constexpr int FO_SPLIT = 8;
 __global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__ ds) {
-  const RefDev& d = ds[blockIdx.x];
-  const int tid = threadIdx.x;
+  const RefDev& d = ds[blockIdx.x / FO_SPLIT];
+  const int part = blockIdx.x % FO_SPLIT;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int64_t s = d.s;
-  __shared__ float red[256];
-  __shared__ int redi[256];
   const double nmax = d.norms[d.order[0]];
   if (!(nmax > 0.0) && d.has_prev) return;   // V == 0: keep the previous projector
-  for (int j = 0; j < d.r; ++j) {
+  for (int j = 4 * part + wave; j < d.r; j += 4 * FO_SPLIT) {
     const double nrm = d.norms[d.order[j]];
     const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
     // sign: entry of largest magnitude, lowest index on ties
     float best = -1.f;
     int bi = 0;
-    for (int64_t i = tid; i < s; i += 256) {
+    for (int64_t i = lane; i < s; i += 64) {
       const float v = deg ? (i == (j % s) ? 1.f : 0.f) : fabsf(d.Pw[i * d.r + j]);
       if (v > best) { best = v; bi = (int)i; }
     }
-    red[tid] = best;
-    redi[tid] = bi;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) {
-      if (tid < o) {
-        if (red[tid + o] > red[tid] || (red[tid + o] == red[tid] && redi[tid + o] < redi[tid])) {
-          red[tid] = red[tid + o];
-          redi[tid] = redi[tid + o];
-        }
-      }
-      __syncthreads();
+    for (int o = 32; o > 0; o >>= 1) {   // every lane ends with the same (value, lowest index)
+      const float ob = __shfl_xor(best, o, 64);
+      const int oi = __shfl_xor(bi, o, 64);
+      if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
     }
-    const float sgn = deg ? 1.f : ((d.Pw[(int64_t)redi[0] * d.r + j] < 0.f) ? -1.f : 1.f);
-    for (int64_t i = tid; i < s; i += 256) {
+    const float sgn = deg ? 1.f : ((d.Pw[(int64_t)bi * d.r + j] < 0.f) ? -1.f : 1.f);
+    for (int64_t i = lane; i < s; i += 64) {
       const float v = deg ? (i == (j % s) ? 1.f : 0.f) : sgn * d.Pw[i * d.r + j];
       d.P32[i * d.r + j] = v;
       if (d.operand_bf16) {
@@ -514,7 +525,6 @@ __global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__
         ((float*)d.Ptop)[(int64_t)j * s + i] = v;
       }
     }
-    __syncthreads();
   }
 }
 
@@ -566,14 +576,16 @@ hipError_t launch_r_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t
   hipLaunchKernelGGL(k_r_colmajor, dim3(total), dim3(256), 0, st, d, n);
   return hipGetLastError();
 }
-hipError_t launch_finalize_order(const RefDev* d, int n, hipStream_t st) {
+uint32_t norm_tiles(int32_t wpad) { return (uint32_t)((wpad + NORM_COLS - 1) / NORM_COLS); }
+hipError_t launch_finalize_order(const RefDev* d, int n, uint32_t norm_total, hipStream_t st) {
   if (!n) return hipSuccess;
+  hipLaunchKernelGGL(k_col_norms, dim3(norm_total), dim3(256), 0, st, d, n);
   hipLaunchKernelGGL(k_finalize_order, dim3(n), dim3(256), 0, st, d);
   return hipGetLastError();
 }
 hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st) {
   if (!n) return hipSuccess;
-  hipLaunchKernelGGL(k_finalize_out, dim3(n), dim3(256), 0, st, d);
+  hipLaunchKernelGGL(k_finalize_out, dim3(n * FO_SPLIT), dim3(256), 0, st, d);
   return hipGetLastError();
 }
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
