@@ -37,10 +37,10 @@ def parse():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
-    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama2_7b")
     ap.add_argument("--operand", default=None, help="GEMM operand dtype override: bf16 | f32")
-    ap.add_argument("--refresh-reps", type=int, default=1)
+    ap.add_argument("--refresh-reps", type=int, default=3, help="refreshes timed; the median is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-layers", type=int, default=1)
     ap.add_argument("--layers", type=int, default=None, help="use only the first N layers (profiling runs)")
@@ -69,12 +69,14 @@ def v_path(wl, m, operand: str) -> bool:
     return k <= 512 and m.cols % 32 == 0
 
 
-def algorithmic_cost(wl, operand: str, weight_bytes: int):
+def algorithmic_cost(wl, operand: str, weight_bytes: int, mask=None):
     """Per-step algorithmic bytes and flops per kernel (what each kernel of this split must
-    move or compute, given its inputs and outputs)."""
+    move or compute, given its inputs and outputs), over the matrices in `mask` (all if None)."""
     ob = 2 if operand == "bf16" else 4
     cost = {"decompose": [0, 0], "project": [0, 0], "backproject": [0, 0]}
-    for m in wl.matrices:
+    for i, m in enumerate(wl.matrices):
+        if mask is not None and not mask[i]:
+            continue
         r = wl.rank_of(m)
         M, N = m.rows, m.cols
         s, L = (M, N) if M <= N else (N, M)
@@ -117,12 +119,14 @@ def measured_traffic(kernel: str, workload: str):
     return val if rec == h.hexdigest() else None
 
 
-def method_cost(wl, operand_bytes: int, weight_bytes: int):
+def method_cost(wl, operand_bytes: int, weight_bytes: int, mask=None):
     """What the method itself must move and compute per step, whatever the kernel split:
     read G, read+write W, read+write the two direction moments, read+write the two
-    magnitude moments, read P; two GEMMs of 2mnr flops each."""
+    magnitude moments, read P; two GEMMs of 2mnr flops each (matrices in `mask`, all if None)."""
     by, fl = 0, 0
-    for m in wl.matrices:
+    for i, m in enumerate(wl.matrices):
+        if mask is not None and not mask[i]:
+            continue
         r = wl.rank_of(m)
         M, N = m.rows, m.cols
         s, L = min(M, N), max(M, N)
@@ -251,18 +255,25 @@ def main():
         log(f"[bench] calibration copy: {nb} bytes read, {nb} bytes written")
         del src, dst
 
-    # ---- steps
+    # ---- steps (MoE batches: per layer and step, moe_active of the moe_routed experts are
+    # active, drawn by the workload's router; inactive matrices are skipped)
     lr = wl.lr
-    for _ in range(a.warmup):
-        M.moara_step(st, W, G, lr, stream=stream)
+    moe = wl.moe_routed > 0
+    masks = [WL.active_set(wl, k) if moe else None for k in range(a.warmup + a.steps)]
+    act_u8 = [M.moara_active_mask(st, m) if m is not None else None for m in masks]
+    sargs = M.StepArgs(st, W, G)   # pointer arrays checked once, outside the timed region
+    sizes = np.array([m.rows * m.cols for m in wl.matrices], dtype=np.float64)
+    params_timed = sum(float(sizes[masks[a.warmup + k]].sum()) if moe else float(wl.n_params) for k in range(a.steps))
+    for k in range(a.warmup):
+        M.moara_step(st, W, G, lr, active=act_u8[k], stream=stream, args=sargs)
     torch.cuda.synchronize()
     M.moara_reset_kernel_stats(st, stream=stream)
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_host = time.perf_counter()
     e0.record(stream)
-    for _ in range(a.steps):
-        M.moara_step(st, W, G, lr, stream=stream)
+    for k in range(a.steps):
+        M.moara_step(st, W, G, lr, active=act_u8[a.warmup + k], stream=stream, args=sargs)
     e1.record(stream)
     torch.cuda.synchronize()
     host_s = time.perf_counter() - t_host
@@ -277,7 +288,15 @@ def main():
         nl, ms = M.moara_kernel_stats(st, kid, stream=stream)
         kern[name] = {"launches": nl, "ms_total": ms, "ms_per_step": ms / max(1, a.steps),
                       "ms_per_launch": ms / max(1, nl)}
-    cost = algorithmic_cost(wl, operand, wb)
+    if moe:   # per-step average over the timed steps' active sets
+        cost = {kk: [0.0, 0.0] for kk in ("decompose", "project", "backproject")}
+        for k in range(a.steps):
+            ck = algorithmic_cost(wl, operand, wb, masks[a.warmup + k])
+            for kk in cost:
+                cost[kk][0] += ck[kk][0] / a.steps
+                cost[kk][1] += ck[kk][1] / a.steps
+    else:
+        cost = algorithmic_cost(wl, operand, wb)
     peak_mfma = PEAK_BF16 if operand == "bf16" else PEAK_F32
     for name, (bytes_, flops) in cost.items():
         t = kern[name]["ms_per_step"] / 1e3
@@ -304,14 +323,18 @@ def main():
                  "avg_launch_ms": dk["ms_total"] / max(1, dk["launches"]),
                  "traffic": measured_traffic(dom, wl.name) if not a.layers else None})
 
-    mb, mf = method_cost(wl, ob, wb)
+    if moe:
+        mb = sum(method_cost(wl, ob, wb, masks[a.warmup + k])[0] for k in range(a.steps)) / a.steps
+        mf = sum(method_cost(wl, ob, wb, masks[a.warmup + k])[1] for k in range(a.steps)) / a.steps
+    else:
+        mb, mf = method_cost(wl, ob, wb)
     step_roof_ms = max(mb / PEAK_HBM, mf / peak_mfma) * 1e3
     q_used = a.refresh_iters if a.refresh_iters else wl.refresh_iters
     rf = refresh_flops(wl, wl.refresh_oversample, q_used)
     ref_med = float(np.median(ref_ms))
     out = {
         "metric": "params updated/sec per optimizer step at Llama-2-7B shapes; ms per projector refresh",
-        "value": wl.n_params / (ms_step / 1e3),
+        "value": params_timed / (ms_total / 1e3),
         "unit": "params/s",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": ms_step,
@@ -323,6 +346,8 @@ def main():
                    "gemm_operands": operand, "refresh": {"oversample": wl.refresh_oversample,
                                                          "iters": q_used}},
         "ms_per_refresh": ref_med,
+        "refresh_ms_all": ref_ms,
+        "params_per_step": params_timed / a.steps,
         "refresh_tflops": rf / (ref_med / 1e3) / 1e12,
         "refresh_frac_fp32_peak": rf / (ref_med / 1e3) / PEAK_F32,
         "amortized_ms_per_step_T200": ms_step + ref_med / 200.0,

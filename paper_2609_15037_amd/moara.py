@@ -236,11 +236,34 @@ def moara_refresh_projector(st: State, grads, active=None, stream=None):
     _check(lib().moara_refresh_projector(st.handle, g, _active_array(st, active), _stream_ptr(stream)))
 
 
-def moara_step(st: State, weights, grads, lr: float, active=None, stream=None):
-    wd = "bf16" if st.cfg.weight_dtype == MOARA_BF16 else "f32"
-    w = _ptr_array(st, weights, "weights", wd, active)
-    g = _ptr_array(st, grads, "grads", "f32", active)
-    _check(lib().moara_step(st.handle, w, g, _active_array(st, active), ctypes.c_float(lr), _stream_ptr(stream)))
+class StepArgs:
+    """Pointer arrays of a fixed set of weight and gradient tensors, checked once, for callers
+    that step the same buffers many times (the per-call checks cost microseconds per matrix)."""
+
+    def __init__(self, st: State, weights, grads):
+        wd = "bf16" if st.cfg.weight_dtype == MOARA_BF16 else "f32"
+        self.w = _ptr_array(st, weights, "weights", wd, None)
+        self.g = _ptr_array(st, grads, "grads", "f32", None)
+        self.keep = (list(weights), list(grads))   # the tensors must outlive the arrays
+
+
+def moara_active_mask(st: State, active):
+    """An active mask in the C layout (one uint8 per matrix), reusable across calls."""
+    return _active_array(st, active)
+
+
+def moara_step(st: State, weights, grads, lr: float, active=None, stream=None, args: StepArgs = None):
+    """moara_step of the C ABI. With `args` (a StepArgs of the same tensors) the pointer
+    arrays are reused and `weights` / `grads` are ignored; `active` may be a mask from
+    moara_active_mask."""
+    if args is not None:
+        w, g = args.w, args.g
+    else:
+        wd = "bf16" if st.cfg.weight_dtype == MOARA_BF16 else "f32"
+        w = _ptr_array(st, weights, "weights", wd, active)
+        g = _ptr_array(st, grads, "grads", "f32", active)
+    act = active if isinstance(active, ctypes.Array) else _active_array(st, active)
+    _check(lib().moara_step(st.handle, w, g, act, ctypes.c_float(lr), _stream_ptr(stream)))
 
 
 def _tensor_shape(st: State, mat: int, which: int):
