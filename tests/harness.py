@@ -75,10 +75,18 @@ def gpu_state(c: Case, refresh_interval: int = 0, refresh_iters=None, oversample
     return M.moara_create_state(cfg, descs)
 
 
-def to_dev(a: np.ndarray, dtype: str):
+def to_dev(a: np.ndarray, dtype: str, offset: int = 0):
+    """Device copy of `a` in fp32 or bf16. offset > 0 places it `offset` elements into a
+    larger allocation, so that its address is not 16-byte aligned (exercises the library's
+    paths for caller buffers the large-tile kernels cannot take)."""
     import torch
     t = torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda()
-    return t.to(torch.bfloat16) if dtype == "bf16" else t
+    t = t.to(torch.bfloat16) if dtype == "bf16" else t
+    if offset:
+        flat = torch.zeros(t.numel() + offset, dtype=t.dtype, device=t.device)
+        flat[offset:] = t.reshape(-1)
+        t = flat[offset:].view(t.shape)
+    return t
 
 
 def to_np(t) -> np.ndarray:

@@ -35,14 +35,20 @@ def _weights(c: Case, seed):
             for i, (m, n, _) in enumerate(c.shapes)]
 
 
-def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=False):
+def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=False, misalign: bool = False,
+                refresh_misaligned: bool = False):
+    """Steps on the GPU and in the oracle from the same inputs. The projector comes from
+    the oracle's SVD (set into the library), or, with refresh_misaligned, from the library's
+    own refresh of the first gradients placed at unaligned addresses (all-fp32 refresh
+    path); the oracle then uses the library's P, so the steps test the projector copies
+    that the refresh wrote."""
     import torch
     M = _M()
     tol = TOL_F32 if (c.weight_dtype == "f32" and c.operand_dtype == "f32") else TOL_BF16
     n = len(c.shapes)
     grad_fn = grad_fn or (lambda t, i: _grad(c, seed, t, i))
     st = gpu_state(c)
-    Wd = [to_dev(w, c.weight_dtype) for w in _weights(c, seed)]
+    Wd = [to_dev(w, c.weight_dtype, offset=1 if misalign else 0) for w in _weights(c, seed)]
     W0 = [to_np(w) for w in Wd]
     Wo = [w.copy() for w in W0]
     ocfg = [oracle_cfg(c, i) for i in range(n)]
@@ -52,12 +58,17 @@ def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=Fa
     masks_u = [np.zeros(c.shapes[i][:2], dtype=bool) for i in range(n)]   # update check (dN > 0.01)
     for t in range(steps):
         Gs = [grad_fn(t, i) for i in range(n)]
-        if t == 0:
+        if t == 0 and refresh_misaligned:
+            M.moara_refresh_projector(st, [to_dev(g, "f32", offset=1) for g in Gs])
+            torch.cuda.synchronize()
+            for i in range(n):
+                ost[i].P = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+        elif t == 0:
             for i in range(n):
                 P = oracle_projector(Gs[i], c, i)
                 M.moara_set_tensor(st, i, M.MOARA_T_P, P)
                 ost[i].P = P
-        Gd = [to_dev(g, "f32") for g in Gs]
+        Gd = [to_dev(g, "f32", offset=1 if misalign else 0) for g in Gs]
         print(f"[parity] step {t} n={n} B={c.block_size} op={c.operand_dtype} w={c.weight_dtype}", flush=True)
         M.moara_step(st, Wd, Gd, lr=c.lr)
         for i in range(n):
@@ -104,6 +115,23 @@ def test_llama300m_layers_bf16():
     wl = WL.subset(WL.WORKLOADS["llama_300m"], [0, 23])
     c = case_from_workload(wl)
     step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t))
+
+
+def test_llama300m_layer_misaligned_caller_buffers():
+    # W and G one element past a 16-byte boundary: no bf16 V workspace this step, the
+    # projection and back-projection take the grouped fallback GEMM, which must read and
+    # write the blocked projector copies and N
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [3])
+    c = case_from_workload(wl)
+    step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t), misalign=True)
+
+
+def test_llama300m_layer_refresh_then_steps():
+    # the step reads the operand copies of P that the refresh's output kernel wrote
+    # (blocked layout); the oracle steps with the same P (the library's fp32 master)
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [7])
+    c = case_from_workload(wl)
+    step_parity(c, 2, grad_fn=lambda t, i: WL.grad_np(wl, i, t), refresh_misaligned=True)
 
 
 def test_llama300m_layer_fp32_operands():
