@@ -434,6 +434,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 //      (3.28 / 3.88) -- the default; its back-projection (K = r, 16 to 32 steps) now
 //      runs five stages, which hides the pipeline fill of the short K loop better
 //      than the cache warm-up did (-4 % on that kernel).
+// Re-measured with blocked operands and barrier-free epilogues (stand-alone copy of the
+// kernel on 8 layers' worth of problems, projection / back-projection ms): variant 5
+// 2.64 / 2.95, variant 4 3.04 / 3.11, variant 1 2.87 / 3.52.
 // Starting the first round of workgroups at staggered times, so that the epilogues of
 // different CUs (or of the two workgroups of a CU) do not coincide, changed nothing
 // measurable in any variant.
