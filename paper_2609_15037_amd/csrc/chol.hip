@@ -4,9 +4,11 @@
 //   for each panel k:  diag(k)   factor C_kk = R_kk^T R_kk and invert R_kk (one WG per matrix)
 //                      panel(k)  R_kj = R_kk^{-T} C_kj for j > k           (one WG per block)
 //                      update(k) C_ac -= R_ka^T R_kc for k < a <= c        (one WG per block)
-//   for each block column J:  X_IJ = -(sum_{I<=t<J} X_It R_tJ) X_JJ for I < J  (one WG per block)
-// with X = R^{-1}. Pivots not above 1e-13 * max(diag C) are raised to that floor
-// so rank-deficient iterates stay finite; an all-zero Gram gives R = I.
+//   then X = R^{-1} by recursive doubling over the blocks (k_trtri).
+// Pivots not above 1e-13 * max(diag C) are raised to that floor so rank-deficient
+// iterates stay finite; an all-zero Gram gives R = I.
+#include <algorithm>
+
 #include "refresh.h"
 
 namespace {
@@ -213,28 +215,51 @@ __global__ __launch_bounds__(256, 4) void k_chol_update(const RefDev* __restrict
     }
 }
 
-__global__ __launch_bounds__(256) void k_inv_col(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
-                                                 int n, int J) {
+// Triangular inverse X = R^{-1} by recursive doubling over the 64 x 64 blocks. Level l
+// (l = 1, 2, ...) pairs the already inverted halves A = blocks [p 2^l, p 2^l + 2^(l-1))
+// and B = [p 2^l + 2^(l-1), min((p + 1) 2^l, nb)) of every super-block p and forms
+//   X_AB = -X_AA R_AB X_BB
+// in two launches: phase 0 T = R_AB X_BB, phase 1 X_AB = -X_AA T. T waits in the
+// (otherwise unused) strictly lower part of X, its block (i, j) transposed at block
+// (j, i), which holds exactly the rows and columns of T's block even at a partial edge block. The
+// diagonal blocks X_kk come from k_chol_diag. A dependency chain is at most 2^(l-1)
+// block products long, against up to nb - 1 for a column-by-column inverse. One
+// workgroup per 64 x 64 output block; its K loop loads the next block pair into
+// registers while the current one is multiplied from LDS.
+__global__ __launch_bounds__(256, 2) void k_trtri(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
+                                               int n, int l, int phase) {
   const uint32_t t = blockIdx.x;
   const int mi = find_pref(pref, n, t);
   const RefDev& d = ds[mi];
-  const int w = d.w;
-  const int I = (int)(t - pref[mi]);
+  const int w = d.w, nb = nblk(w);
+  const int h = 1 << (l - 1);
+  int rem = (int)(t - pref[mi]), A0 = 0, nB = 1;
+  for (int p = 0; p * 2 * h + h < nb; ++p) {   // pairs with a non-empty B half
+    const int a0 = p * 2 * h, cnt = h * (min(a0 + 2 * h, nb) - a0 - h);
+    if (rem < cnt) { A0 = a0; nB = min(a0 + 2 * h, nb) - a0 - h; break; }
+    rem -= cnt;
+  }
+  const int B0 = A0 + h;
+  const int I = A0 + rem / nB, J = B0 + rem % nB;
+  // phase 0: sum over tb = B0 .. J of R_{I,tb} X_{tb,J}   (R in the upper part of C)
+  // phase 1: sum over tb = I .. B0-1 of X_{I,tb} T_{tb,J} (T_{tb,J}^T parked at X block (J, tb))
+  const int tlo = phase == 0 ? B0 : I, thi = phase == 0 ? J : B0 - 1;
   __shared__ double Ab[NB][LDB];
   __shared__ double Bb[NB][LDB];
   f64x4 acc[4];
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
-  // the next step's two blocks are loaded into registers while the current pair is
-  // multiplied from LDS
   double pa[16], pb[16];
   auto fetch = [&](int tb) {
+    const double* Am = phase == 0 ? d.C : d.X;
+    const int ar = I, ac = tb;                       // A block (I, tb)
+    const int br = phase == 0 ? tb : J, bc = phase == 0 ? J : tb;   // B block (phase 1: transposed)
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       const int e = threadIdx.x + 256 * q, i = e >> 6, j = e & 63;
-      const int ra = I * NB + i, ca = tb * NB + j, rb = tb * NB + i, cb = J * NB + j;
-      pa[q] = (ra < w && ca < w) ? d.X[(int64_t)ra * w + ca] : 0.0;
-      pb[q] = (rb < w && cb < w) ? d.C[(int64_t)rb * w + cb] : 0.0;
+      const int ra = ar * NB + i, ca = ac * NB + j, rb = br * NB + i, cb = bc * NB + j;
+      pa[q] = (ra < w && ca < w) ? Am[(int64_t)ra * w + ca] : 0.0;
+      pb[q] = (rb < w && cb < w) ? d.X[(int64_t)rb * w + cb] : 0.0;
     }
   };
   auto publish = [&]() {
@@ -242,42 +267,45 @@ __global__ __launch_bounds__(256) void k_inv_col(const RefDev* __restrict__ ds, 
     for (int q = 0; q < 16; ++q) {
       const int e = threadIdx.x + 256 * q, i = e >> 6, j = e & 63;
       Ab[i][j] = pa[q];
-      Bb[i][j] = pb[q];
+      if (phase == 0) Bb[i][j] = pb[q];
+      else Bb[j][i] = pb[q];   // X block (J, tb) holds T_{tb,J}^T
     }
   };
-  fetch(I);
+  fetch(tlo);
   publish();
   __syncthreads();
-  for (int tb = I; tb < J; ++tb) {
-    if (tb + 1 < J) fetch(tb + 1);
-    mfma_blk<false>(Ab, Bb, acc);   // += X_I,tb R_tb,J
+  for (int tb = tlo; tb <= thi; ++tb) {
+    if (tb < thi) fetch(tb + 1);
+    mfma_blk<false>(Ab, Bb, acc);
     __syncthreads();
-    if (tb + 1 < J) {
+    if (tb < thi) {
       publish();
       __syncthreads();
     }
   }
+  if (phase == 0) {   // park T_{I,J}^T at block (J, I), transposed through LDS
 #pragma unroll
-  for (int jt = 0; jt < 4; ++jt)
+    for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) Ab[mfma_row(r)][mfma_col(jt)] = acc[jt][r];
-  load_blk(Bb, d.X, w, J, J);
-  __syncthreads();
-  f64x4 out[4];
-#pragma unroll
-  for (int jt = 0; jt < 4; ++jt) out[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
-  mfma_blk<false>(Ab, Bb, out);      // (sum) X_JJ
-#pragma unroll
-  for (int jt = 0; jt < 4; ++jt)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int row = I * NB + mfma_row(r), col = J * NB + mfma_col(jt);
-      if (row < w && col < w) {
-        const int64_t g = (int64_t)row * w + col;
-        d.X[g] = -out[jt][r];
-        d.Rinv[g] = (float)(-out[jt][r]);
-      }
+      for (int r = 0; r < 4; ++r) Ab[mfma_col(jt)][mfma_row(r)] = acc[jt][r];
+    __syncthreads();
+    for (int e = threadIdx.x; e < NB * NB; e += 256) {
+      const int i = e >> 6, j = e & 63, row = J * NB + i, col = I * NB + j;
+      if (row < w && col < w) d.X[(int64_t)row * w + col] = Ab[i][j];
     }
+  } else {
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = I * NB + mfma_row(r), col = J * NB + mfma_col(jt);
+        if (row < w && col < w) {
+          const int64_t g = (int64_t)row * w + col;
+          d.X[g] = -acc[jt][r];
+          d.Rinv[g] = (float)(-acc[jt][r]);
+        }
+      }
+  }
 }
 
 }  // namespace
@@ -299,8 +327,15 @@ hipError_t launch_chol_update(const RefDev* d, const uint32_t* pref, int n, uint
   hipLaunchKernelGGL(k_chol_update, dim3(total), dim3(256), 0, st, d, pref, n, k);
   return hipGetLastError();
 }
-hipError_t launch_inv_col(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int J, hipStream_t st) {
+int trtri_levels(int32_t nbmax) { int l = 0; while ((1 << l) < nbmax) ++l; return l; }
+uint32_t trtri_tiles(int32_t w, int l) {
+  const int nb = (w + NB - 1) / NB, h = 1 << (l - 1);
+  uint32_t c = 0;
+  for (int a0 = 0; a0 + h < nb; a0 += 2 * h) c += (uint32_t)(h * (std::min(a0 + 2 * h, nb) - a0 - h));
+  return c;
+}
+hipError_t launch_trtri(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int l, int phase, hipStream_t st) {
   if (!total) return hipSuccess;
-  hipLaunchKernelGGL(k_inv_col, dim3(total), dim3(256), 0, st, d, pref, n, J);
+  hipLaunchKernelGGL(k_trtri, dim3(total), dim3(256), 0, st, d, pref, n, l, phase);
   return hipGetLastError();
 }

@@ -668,18 +668,26 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   // workgroup prefixes of the blocked Cholesky / inverse launches (same for every orth of the chunk)
   int nbmax = 1;
   for (auto& x : rm) nbmax = std::max(nbmax, chol_blocks(x.w));
-  std::vector<uint32_t> pan_pref((size_t)nbmax * nm), upd_pref((size_t)nbmax * nm), inv_pref((size_t)nbmax * nm);
-  std::vector<uint32_t> pan_tot(nbmax), upd_tot(nbmax), inv_tot(nbmax);
+  const int nlev = trtri_levels(nbmax);
+  std::vector<uint32_t> pan_pref((size_t)nbmax * nm), upd_pref((size_t)nbmax * nm), inv_pref((size_t)std::max(1, nlev) * nm);
+  std::vector<uint32_t> pan_tot(nbmax), upd_tot(nbmax), inv_tot(std::max(1, nlev));
   for (int k = 0; k < nbmax; ++k) {
-    uint32_t tp = 0, tu = 0, ti = 0;
+    uint32_t tp = 0, tu = 0;
     for (int q = 0; q < nm; ++q) {
       const int nb = chol_blocks(rm[q].w);
       const int T = std::max(0, nb - k - 1);
       pan_pref[(size_t)k * nm + q] = tp; tp += (uint32_t)T;
       upd_pref[(size_t)k * nm + q] = tu; tu += (uint32_t)(T * (T + 1) / 2);
-      inv_pref[(size_t)k * nm + q] = ti; ti += (uint32_t)(k < nb ? k : 0);
     }
-    pan_tot[k] = tp; upd_tot[k] = tu; inv_tot[k] = ti;
+    pan_tot[k] = tp; upd_tot[k] = tu;
+  }
+  for (int l = 1; l <= nlev; ++l) {   // recursive-doubling levels of the triangular inverse
+    uint32_t ti = 0;
+    for (int q = 0; q < nm; ++q) {
+      inv_pref[(size_t)(l - 1) * nm + q] = ti;
+      ti += trtri_tiles(rm[q].w, l);
+    }
+    inv_tot[l - 1] = ti;
   }
   auto gZ2 = gram_list(false), gY = gram_list(true);
   auto aZ = apply_list(false), aY = apply_list(true);
@@ -799,8 +807,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       if (e == hipSuccess) e = launch_chol_panel(RD, PAN + (size_t)k * nm, nm, pan_tot[k], k, stream);
       if (e == hipSuccess) e = launch_chol_update(RD, UPD + (size_t)k * nm, nm, upd_tot[k], k, stream);
     }
-    for (int J = 1; J < nbmax && e == hipSuccess; ++J)
-      e = launch_inv_col(RD, INV + (size_t)J * nm, nm, inv_tot[J], J, stream);
+    for (int l = 1; l <= nlev && e == hipSuccess; ++l)
+      for (int ph = 0; ph < 2 && e == hipSuccess; ++ph)
+        e = launch_trtri(RD, INV + (size_t)(l - 1) * nm, nm, inv_tot[l - 1], l, ph, stream);
     return e;
   };
   auto orth_Z = [&]() -> hipError_t {        // Z <- orth(Z2)

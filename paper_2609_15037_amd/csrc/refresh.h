@@ -65,7 +65,9 @@ int chol_blocks(int32_t w);
 hipError_t launch_chol_diag(const RefDev* d, int n, int k, hipStream_t st);
 hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
 hipError_t launch_chol_update(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
-hipError_t launch_inv_col(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int J, hipStream_t st);
+int trtri_levels(int32_t nbmax);
+uint32_t trtri_tiles(int32_t w, int l);
+hipError_t launch_trtri(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int l, int phase, hipStream_t st);
 hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st);
 hipError_t launch_r_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t st);
 uint32_t r_colmajor_tiles(int32_t w, int32_t wpad);
