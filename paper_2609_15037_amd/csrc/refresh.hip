@@ -170,15 +170,23 @@ constexpr double JAC_TOL = 1e-10;
 #define JAC_INNER_SWEEPS 1
 #endif
 
-// LDS: the pair's Gram G and rotation J (64 x 65 fp64 each) and one 16-row chunk of the
-// columns (16 x 65); the rotation output is staged in G's space and the reduction scratch
-// in the chunk's, so two workgroups fit on a CU and one's LDS-bound inner solve overlaps
-// the other's MFMA / memory phases.
-constexpr int JR = 16;   // rows per column chunk
+// LDS: two 64 x 65 fp64 regions. Region A holds the pair's Gram G during the inner
+// solve; during the column passes it holds the current 32-row chunk of the 64 columns
+// (rows 0-31) and, in the rotation pass, the rotated chunk (rows 32-63). Region B holds
+// the rotation J (and the convergence reduction's scratch before J is built). 66.5 KB,
+// so two workgroups share a CU and one's LDS-bound inner solve overlaps the other's
+// MFMA / memory phases.
+constexpr int JR = 32;   // rows per column chunk
+#ifndef JAC_RING
+#define JAC_RING 2
+#endif
+static_assert(JR * PW == 8 * 256 && 2 * JR == PW, "chunk mapping: 8 elements per thread");
 __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
-  __shared__ double Gm[PW][PW + 1];
+  __shared__ double Am[PW][PW + 1];
   __shared__ double Jm[PW][PW + 1];
-  __shared__ double T[JR][PW + 1];
+  double (*Gm)[PW + 1] = Am;         // inner solve
+  double (*T)[PW + 1] = Am;          // column chunk (rows 0 .. JR-1)
+  double (*O)[PW + 1] = Am + JR;     // rotated chunk (rows JR .. 2 JR-1)
   const uint32_t t = blockIdx.x;
   int lo = 0, hi = n - 1;
   while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ds[mid].tile_jac <= t) lo = mid; else hi = mid - 1; }
@@ -194,77 +202,95 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
   const int lane = tid & 63, wave = tid >> 6;
   const int nch = (int)((s + JR - 1) / JR);
 
-  // Column chunks: 16 rows x 64 columns, thread e = tid + 256 q covers column e / 16,
-  // row e % 16. Two chunks stay in flight in a register ring (chunk c + 1 in slot
-  // (c + 1) & 1, chunk c + 2 in slot c & 1) while chunk c is used from LDS.
-  double pre[2][4];
-  auto load_chunk = [&](int c, double (&x4)[4]) {
+  // Column chunks: JR rows x 64 columns; thread e = tid + 256 q covers column e / JR,
+  // row e % JR (a wave reads two whole 256-byte column segments per instruction).
+  // While chunk c is used from LDS, chunks c + 1 .. c + JAC_RING are in flight in a
+  // register ring (chunk x in slot x % JAC_RING).
+  double pre[JAC_RING][8];
+  auto load_chunk = [&](int c, double (&x8)[8]) {
     const int64_t r0 = (int64_t)c * JR;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = tid + 256 * q, x = e >> 4, l = e & 15;
-      x4[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q, x = e / JR, l = e % JR;
+      x8[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
     }
   };
-  auto store_chunk = [&](const double (&x4)[4]) {
+  auto store_chunk = [&](const double (&x8)[8]) {
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < 8; ++q) {
       const int e = tid + 256 * q;
-      T[e & 15][e >> 4] = x4[q];
+      T[e % JR][e / JR] = x8[q];
     }
   };
-  auto prime = [&]() {   // chunk 0 -> T; chunks 1, 2 in flight
-    load_chunk(0, pre[0]);
+  auto prime = [&]() {   // chunk 0 -> T; chunks 1 .. JAC_RING in flight
+#pragma unroll
+    for (int k = 0; k < JAC_RING; ++k)
+      if (k < nch) load_chunk(k, pre[k]);
     store_chunk(pre[0]);
-    if (1 < nch) load_chunk(1, pre[1]);
-    if (2 < nch) load_chunk(2, pre[0]);
+    if (JAC_RING < nch) load_chunk(JAC_RING, pre[0]);
     __syncthreads();
   };
-  // after every wave is done with chunk c in T: publish chunk c + 1, refill its slot
-  auto advance = [&](int c, double (&slot)[4]) {
+  // after every wave is done with chunk c in T: publish chunk c + 1 from its slot and
+  // refill that slot with chunk c + 1 + JAC_RING
+  auto advance = [&](int c, double (&slot)[8]) {
     if (c + 1 < nch) store_chunk(slot);
-    if (c + 3 < nch) load_chunk(c + 3, slot);
+    if (c + 1 + JAC_RING < nch) load_chunk(c + 1 + JAC_RING, slot);
   };
 
   // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
   // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
-  // Wave w owns Gram rows [16w, 16w+16) and all 64 columns (four 16 x 16 tiles).
+  // G is symmetric: only its ten 16 x 16 tiles (it, jt) with it <= jt are computed,
+  // three or two per wave, and mirrored when G is written.
   {
-    f64x4 acc[4];
+    // wave w's tiles, packed as it * 4 + jt; 0xFF = none
+    const uint32_t tiles = wave == 0 ? 0xFF020100u : wave == 1 ? 0xFF060503u : wave == 2 ? 0xFFFF0A07u : 0xFFFF0F0Bu;
+    const int nt = wave < 2 ? 3 : 2;
+    f64x4 acc[3];
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+    for (int k = 0; k < 3; ++k) acc[k] = f64x4{0.0, 0.0, 0.0, 0.0};
     auto mult = [&]() {
 #pragma unroll
       for (int ks = 0; ks < JR / 4; ++ks) {
         const int kr = 4 * ks + (lane >> 4);
-        const double a = T[kr][16 * wave + (lane & 15)];
 #pragma unroll
-        for (int jt = 0; jt < 4; ++jt)
-          acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(a, T[kr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+        for (int k = 0; k < 3; ++k) {
+          if (k < nt) {
+            const int tl = (tiles >> (8 * k)) & 0xFF, it = tl >> 2, jt = tl & 3;
+            acc[k] = __builtin_amdgcn_mfma_f64_16x16x4f64(T[kr][16 * it + (lane & 15)], T[kr][16 * jt + (lane & 15)],
+                                                         acc[k], 0, 0, 0);
+          }
+        }
       }
     };
     prime();
-    for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
-      mult();
-      __syncthreads();
-      advance(c, pre[1]);
-      __syncthreads();
-      if (c + 1 >= nch) break;
-      mult();
-      __syncthreads();
-      advance(c + 1, pre[0]);
-      __syncthreads();
+    for (int c0 = 0; c0 < nch; c0 += JAC_RING) {   // unrolled by the ring size: static slots
+#pragma unroll
+      for (int k = 0; k < JAC_RING; ++k) {
+        if (c0 + k >= nch) break;
+        mult();
+        __syncthreads();
+        advance(c0 + k, pre[(k + 1) % JAC_RING]);
+        __syncthreads();
+      }
     }
+    // T is idle now (the last pass ended with a barrier): write G over it
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
+    for (int k = 0; k < 3; ++k) {
+      if (k < nt) {
+        const int tl = (tiles >> (8 * k)) & 0xFF, it = tl >> 2, jt = tl & 3;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) Gm[16 * wave + 4 * r + (lane >> 4)][16 * jt + (lane & 15)] = acc[jt][r];
+        for (int r = 0; r < 4; ++r) {
+          const int i = 16 * it + 4 * r + (lane >> 4), j = 16 * jt + (lane & 15);
+          Gm[i][j] = acc[k][r];
+          if (it != jt) Gm[j][i] = acc[k][r];
+        }
+      }
+    }
   }
-  for (int e = tid; e < PW * PW; e += 256) Jm[e / PW][e % PW] = (e / PW == e % PW) ? 1.0 : 0.0;
   __syncthreads();
   // convergence measure of this pair (before rotating): max |g_xy| / sqrt(g_xx g_yy)
   {
-    double* red = &T[0][0];   // the chunk buffer is idle here (256 <= 16 * 65)
+    double* red = &Jm[0][0];   // J is built after this reduction
     double m = 0.0;
     for (int e = tid; e < PW * PW; e += 256) {
       const int x = e / PW, y = e % PW;
@@ -279,8 +305,10 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
     const double mx = red[0];
     if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)mx));
     if (mx < JAC_TOL) return;   // already orthogonal: nothing to rotate (uniform branch)
-    __syncthreads();            // red[0] is read by every thread before the chunk buffer is reused
+    __syncthreads();            // red[0] is read by every thread before J overwrites it
   }
+  for (int e = tid; e < PW * PW; e += 256) Jm[e / PW][e % PW] = (e / PW == e % PW) ? 1.0 : 0.0;
+  __syncthreads();
 
   // (2) JAC_INNER_SWEEPS sweeps of parallel cyclic Jacobi on the 64 x 64 Gram, in place.
   // One round rotates 32 disjoint pairs (circle method) on both sides at once,
@@ -333,41 +361,43 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
     }
   }
 
-  // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, 16 rows at a time on
-  // fp64 MFMA; wave w computes the chunk's 16 rows x columns [16w, 16w+16). The
-  // result goes through LDS (G's space, idle now) so the write-back is column-contiguous.
-  double (*O)[PW + 1] = Gm;
+  // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, JR rows at a time on
+  // fp64 MFMA; wave w computes the chunk's JR rows x columns [16w, 16w+16) (J's
+  // fragment is shared by the two 16-row halves). The result goes through LDS (region
+  // A's upper half) so the write-back is column-contiguous.
   auto rotate = [&]() {
-    f64x4 o = {0.0, 0.0, 0.0, 0.0};
+    f64x4 o[2] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
 #pragma unroll
     for (int ks = 0; ks < PW / 4; ++ks) {
       const int y = 4 * ks + (lane >> 4);
-      o = __builtin_amdgcn_mfma_f64_16x16x4f64(T[lane & 15][y], Jm[y][16 * wave + (lane & 15)], o, 0, 0, 0);
+      const double jv = Jm[y][16 * wave + (lane & 15)];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) o[h] = __builtin_amdgcn_mfma_f64_16x16x4f64(T[16 * h + (lane & 15)][y], jv, o[h], 0, 0, 0);
     }
 #pragma unroll
-    for (int r = 0; r < 4; ++r) O[4 * r + (lane >> 4)][16 * wave + (lane & 15)] = o[r];
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) O[16 * h + 4 * r + (lane >> 4)][16 * wave + (lane & 15)] = o[h][r];
   };
   auto write_out = [&](int c) {
     const int64_t r0 = (int64_t)c * JR;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = tid + 256 * q, x = e >> 4, l = e & 15;
+    for (int q = 0; q < 8; ++q) {
+      const int e = tid + 256 * q, x = e / JR, l = e % JR;
       if (r0 + l < s) colp(x)[r0 + l] = O[l][x];
     }
   };
   prime();
-  for (int c = 0; c < nch; c += 2) {   // unrolled by two so that the ring slots stay static
-    rotate();
-    __syncthreads();
-    write_out(c);
-    advance(c, pre[1]);
-    __syncthreads();
-    if (c + 1 >= nch) break;
-    rotate();
-    __syncthreads();
-    write_out(c + 1);
-    advance(c + 1, pre[0]);
-    __syncthreads();
+  for (int c0 = 0; c0 < nch; c0 += JAC_RING) {   // unrolled by the ring size: static slots
+#pragma unroll
+    for (int k = 0; k < JAC_RING; ++k) {
+      if (c0 + k >= nch) break;
+      rotate();
+      __syncthreads();
+      write_out(c0 + k);
+      advance(c0 + k, pre[(k + 1) % JAC_RING]);
+      __syncthreads();
+    }
   }
 }
 
