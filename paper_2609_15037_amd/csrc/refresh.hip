@@ -180,8 +180,22 @@ constexpr int JR = 32;   // rows per column chunk
 #ifndef JAC_RING
 #define JAC_RING 2
 #endif
-static_assert(JR * PW == 8 * 256 && 2 * JR == PW, "chunk mapping: 8 elements per thread");
-__global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
+#ifndef JAC_WAVES
+#define JAC_WAVES 8
+#endif
+constexpr int JNT = 64 * JAC_WAVES;    // threads per workgroup
+constexpr int JEPT = JR * PW / JNT;    // chunk elements per thread
+static_assert(2 * JR == PW && JEPT * JNT == JR * PW && (JAC_WAVES == 4 || JAC_WAVES == 8), "chunk mapping");
+// Gram tiles (it, jt), it <= jt, of each wave, packed as it * 4 + jt per byte (0xFF = none).
+// Waves w and w + 4 share a SIMD; the per-SIMD counts are 3, 3, 2, 2 in both layouts.
+__device__ __forceinline__ uint32_t gram_tiles(int wave) {
+  if (JAC_WAVES == 4)
+    return wave == 0 ? 0xFF020100u : wave == 1 ? 0xFF060503u : wave == 2 ? 0xFFFF0A07u : 0xFFFF0F0Bu;
+  constexpr uint32_t tab[8] = {0xFFFF0100u, 0xFFFF0605u, 0xFFFFFF02u, 0xFFFFFF03u,
+                               0xFFFFFF07u, 0xFFFFFF0Au, 0xFFFFFF0Bu, 0xFFFFFF0Fu};
+  return tab[wave];
+}
+__global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
   __shared__ double Am[PW][PW + 1];
   __shared__ double Jm[PW][PW + 1];
   double (*Gm)[PW + 1] = Am;         // inner solve
@@ -202,23 +216,23 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
   const int lane = tid & 63, wave = tid >> 6;
   const int nch = (int)((s + JR - 1) / JR);
 
-  // Column chunks: JR rows x 64 columns; thread e = tid + 256 q covers column e / JR,
+  // Column chunks: JR rows x 64 columns; thread e = tid + JNT q covers column e / JR,
   // row e % JR (a wave reads two whole 256-byte column segments per instruction).
   // While chunk c is used from LDS, chunks c + 1 .. c + JAC_RING are in flight in a
   // register ring (chunk x in slot x % JAC_RING).
-  double pre[JAC_RING][8];
-  auto load_chunk = [&](int c, double (&x8)[8]) {
+  double pre[JAC_RING][JEPT];
+  auto load_chunk = [&](int c, double (&x8)[JEPT]) {
     const int64_t r0 = (int64_t)c * JR;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + 256 * q, x = e / JR, l = e % JR;
+    for (int q = 0; q < JEPT; ++q) {
+      const int e = tid + JNT * q, x = e / JR, l = e % JR;
       x8[q] = (r0 + l < s) ? colp(x)[r0 + l] : 0.0;
     }
   };
-  auto store_chunk = [&](const double (&x8)[8]) {
+  auto store_chunk = [&](const double (&x8)[JEPT]) {
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + 256 * q;
+    for (int q = 0; q < JEPT; ++q) {
+      const int e = tid + JNT * q;
       T[e % JR][e / JR] = x8[q];
     }
   };
@@ -232,19 +246,18 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
   };
   // after every wave is done with chunk c in T: publish chunk c + 1 from its slot and
   // refill that slot with chunk c + 1 + JAC_RING
-  auto advance = [&](int c, double (&slot)[8]) {
+  auto advance = [&](int c, double (&slot)[JEPT]) {
     if (c + 1 < nch) store_chunk(slot);
     if (c + 1 + JAC_RING < nch) load_chunk(c + 1 + JAC_RING, slot);
   };
 
   // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
   // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
-  // G is symmetric: only its ten 16 x 16 tiles (it, jt) with it <= jt are computed,
-  // three or two per wave, and mirrored when G is written.
+  // G is symmetric: only its ten 16 x 16 tiles (it, jt) with it <= jt are computed
+  // (gram_tiles) and mirrored when G is written.
   {
-    // wave w's tiles, packed as it * 4 + jt; 0xFF = none
-    const uint32_t tiles = wave == 0 ? 0xFF020100u : wave == 1 ? 0xFF060503u : wave == 2 ? 0xFFFF0A07u : 0xFFFF0F0Bu;
-    const int nt = wave < 2 ? 3 : 2;
+    const uint32_t tiles = gram_tiles(wave);
+    const int nt = ((tiles & 0xFF) != 0xFF) + ((tiles >> 8 & 0xFF) != 0xFF) + ((tiles >> 16 & 0xFF) != 0xFF);
     f64x4 acc[3];
 #pragma unroll
     for (int k = 0; k < 3; ++k) acc[k] = f64x4{0.0, 0.0, 0.0, 0.0};
@@ -292,7 +305,7 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
   {
     double* red = &Jm[0][0];   // J is built after this reduction
     double m = 0.0;
-    for (int e = tid; e < PW * PW; e += 256) {
+    for (int e = tid; e < PW * PW; e += JNT) {
       const int x = e / PW, y = e % PW;
       if (x < y) {
         const double den = sqrt(Gm[x][x] * Gm[y][y]);
@@ -301,22 +314,22 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
     }
     red[tid] = m;
     __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
+    for (int o = JNT / 2; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
     const double mx = red[0];
     if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)mx));
     if (mx < JAC_TOL) return;   // already orthogonal: nothing to rotate (uniform branch)
     __syncthreads();            // red[0] is read by every thread before J overwrites it
   }
-  for (int e = tid; e < PW * PW; e += 256) Jm[e / PW][e % PW] = (e / PW == e % PW) ? 1.0 : 0.0;
+  for (int e = tid; e < PW * PW; e += JNT) Jm[e / PW][e % PW] = (e / PW == e % PW) ? 1.0 : 0.0;
   __syncthreads();
 
   // (2) JAC_INNER_SWEEPS sweeps of parallel cyclic Jacobi on the 64 x 64 Gram, in place.
   // One round rotates 32 disjoint pairs (circle method) on both sides at once,
   // G' = R^T G R: lane l computes the rotation of pair beta = l % 32 from the current
   // G; after a barrier (every rotation read before any entry changes) it fetches the
-  // rotations of its row pairs alpha from lanes alpha by shuffles and rewrites four
-  // 2 x 2 blocks of G, which no other lane touches, and applies rotation beta to eight
-  // rows of the accumulated J.
+  // rotations of its row pairs alpha from lanes alpha by shuffles and rewrites
+  // 16 / JAC_WAVES 2 x 2 blocks of G, which no other lane touches, and applies rotation
+  // beta to 32 / JAC_WAVES rows of the accumulated J.
   {
     const int beta = lane & 31, half = lane >> 5;
     for (int isw = 0; isw < JAC_INNER_SWEEPS; ++isw) {
@@ -336,8 +349,8 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
         }
         __syncthreads();
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int alpha = 2 * (4 * wave + i) + half;
+        for (int i = 0; i < 16 / JAC_WAVES; ++i) {
+          const int alpha = 2 * (16 / JAC_WAVES * wave + i) + half;
           int pa = circle(alpha, rr, PW), qa = circle(PW - 1 - alpha, rr, PW);
           if (pa > qa) { const int tmp = pa; pa = qa; qa = tmp; }
           const double ca = __shfl(cb, alpha, 64), sa = __shfl(sb, alpha, 64);
@@ -350,8 +363,8 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
           Gm[qa][qb] = sb * r_qp + cb * r_qq;
         }
 #pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int a = half + 2 * (wave + 4 * i);
+        for (int i = 0; i < 32 / JAC_WAVES; ++i) {
+          const int a = half + 2 * (wave + JAC_WAVES * i);
           const double jp = Jm[a][pb], jq = Jm[a][qb];
           Jm[a][pb] = cb * jp - sb * jq;
           Jm[a][qb] = sb * jp + cb * jq;
@@ -362,28 +375,34 @@ __global__ __launch_bounds__(256, 2) void k_jacobi_round(const RefDev* __restric
   }
 
   // (3) rotate the 64 columns: Zc[:, pair] <- Zc[:, pair] J, JR rows at a time on
-  // fp64 MFMA; wave w computes the chunk's JR rows x columns [16w, 16w+16) (J's
-  // fragment is shared by the two 16-row halves). The result goes through LDS (region
-  // A's upper half) so the write-back is column-contiguous.
+  // fp64 MFMA; wave w computes columns [16 (w % 4), +16) of the chunk's 16-row halves
+  // h = w / 4, w / 4 + 4, ... (with four waves both halves share J's fragment). The
+  // result goes through LDS (region A's upper half) so the write-back is
+  // column-contiguous.
+  constexpr int NH = 8 / JAC_WAVES;   // 16-row halves per wave
+  const int cbk = wave & 3, h0 = wave >> 2;
   auto rotate = [&]() {
-    f64x4 o[2] = {{0.0, 0.0, 0.0, 0.0}, {0.0, 0.0, 0.0, 0.0}};
+    f64x4 o[NH];
+#pragma unroll
+    for (int h = 0; h < NH; ++h) o[h] = f64x4{0.0, 0.0, 0.0, 0.0};
 #pragma unroll
     for (int ks = 0; ks < PW / 4; ++ks) {
       const int y = 4 * ks + (lane >> 4);
-      const double jv = Jm[y][16 * wave + (lane & 15)];
+      const double jv = Jm[y][16 * cbk + (lane & 15)];
 #pragma unroll
-      for (int h = 0; h < 2; ++h) o[h] = __builtin_amdgcn_mfma_f64_16x16x4f64(T[16 * h + (lane & 15)][y], jv, o[h], 0, 0, 0);
+      for (int h = 0; h < NH; ++h)
+        o[h] = __builtin_amdgcn_mfma_f64_16x16x4f64(T[16 * (h0 + h) + (lane & 15)][y], jv, o[h], 0, 0, 0);
     }
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < NH; ++h)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) O[16 * h + 4 * r + (lane >> 4)][16 * wave + (lane & 15)] = o[h][r];
+      for (int r = 0; r < 4; ++r) O[16 * (h0 + h) + 4 * r + (lane >> 4)][16 * cbk + (lane & 15)] = o[h][r];
   };
   auto write_out = [&](int c) {
     const int64_t r0 = (int64_t)c * JR;
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const int e = tid + 256 * q, x = e / JR, l = e % JR;
+    for (int q = 0; q < JEPT; ++q) {
+      const int e = tid + JNT * q, x = e / JR, l = e % JR;
       if (r0 + l < s) colp(x)[r0 + l] = O[l][x];
     }
   };
@@ -591,7 +610,7 @@ hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st)
 }
 hipError_t launch_jacobi_round(const RefDev* d, int n, uint32_t total, int round, int sweep, hipStream_t st) {
   if (!total) return hipSuccess;
-  hipLaunchKernelGGL(k_jacobi_round, dim3(total), dim3(256), 0, st, d, n, round, sweep);
+  hipLaunchKernelGGL(k_jacobi_round, dim3(total), dim3(JNT), 0, st, d, n, round, sweep);
   return hipGetLastError();
 }
 uint32_t transpose_tiles(int64_t rows, int64_t cols) { return (uint32_t)(((rows + 63) / 64) * ((cols + 63) / 64)); }
