@@ -153,7 +153,12 @@ int moara_resolve_matrix(const moara_config* cfg, const moara_matrix_desc* desc,
 
 /* Device bytes a state for these n matrices would hold (persistent state plus
  * the per-step workspace; the refresh workspace is reported separately because
- * it is sized per refresh batch). Errors as moara_create_state's validation. */
+ * it is sized per refresh batch: a refresh works through its matrices in chunks
+ * of at most 96 GiB of workspace, so the figure is the smaller of the whole
+ * batch's need and that bound plus one matrix's share). The environment
+ * variable MOARA_REFRESH_CHUNK_MIB, when set to a positive integer, replaces the
+ * bound (in MiB) for this call and for later refreshes. Errors as
+ * moara_create_state's validation. */
 int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, int32_t n,
                       int64_t* out_state_bytes, int64_t* out_refresh_workspace_bytes);
 

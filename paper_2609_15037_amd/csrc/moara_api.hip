@@ -4,6 +4,7 @@
 #include <math.h>
 #include <stdarg.h>
 #include <stdio.h>
+#include <stdlib.h>
 #include <string.h>
 
 #include <algorithm>
@@ -868,20 +869,39 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   return MOARA_OK;
 }
 
-constexpr size_t REFRESH_BUDGET = (size_t)48 << 30;   // device bytes per refresh chunk
+// Device bytes per refresh chunk. One chunk per refresh is fastest (the latency-bound
+// Cholesky chains and Jacobi rounds then cover every matrix in one launch sequence):
+// a Llama-2-7B-shaped stack needs about 70 GB, a third of one MI355X's 288 GB.
+#ifndef MOARA_REFRESH_BUDGET_GIB
+#define MOARA_REFRESH_BUDGET_GIB 96
+#endif
+constexpr size_t REFRESH_BUDGET = (size_t)MOARA_REFRESH_BUDGET_GIB << 30;
 
-int run_refresh(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream) {
-  if (idx.empty()) return MOARA_OK;
-  std::vector<char> usev(st->n, 0);
-  for (int i : idx) usev[i] = st->mats[i].vpath && (((uintptr_t)grads[i] & 15) == 0);
-  int rc = run_decompose(st, idx, grads, false, stream, &usev);
-  if (rc) return rc;
+// Chunk budget: REFRESH_BUDGET, or MOARA_REFRESH_CHUNK_MIB (MiB) from the environment
+// when that is set to a positive integer (callers short of device memory; tests use it
+// to run one refresh in several chunks).
+size_t refresh_budget() {
+  const char* e = getenv("MOARA_REFRESH_CHUNK_MIB");
+  if (e && *e) {
+    char* end = nullptr;
+    const long long v = strtoll(e, &end, 10);
+    if (end && *end == 0 && v > 0) return (size_t)v << 20;
+  }
+  return REFRESH_BUDGET;
+}
+
+// Refresh the matrices idx in order, in chunks whose workspace stays within the budget
+// (a matrix larger than the budget forms a chunk of its own).
+int refresh_in_chunks(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream,
+                      const std::vector<char>& usev) {
+  const size_t budget = refresh_budget();
   std::vector<int> chunk;
   size_t bytes = 0;
+  int rc;
   for (int i : idx) {
     const MatHost& h = st->mats[i];
     const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), h.r, usev[i]);
-    if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
+    if (!chunk.empty() && bytes + b > budget) {
       if ((rc = refresh_chunk(st, chunk, grads, stream, &usev))) return rc;
       chunk.clear();
       bytes = 0;
@@ -890,6 +910,15 @@ int run_refresh(moara_state* st, const std::vector<int>& idx, const void* const*
     bytes += b;
   }
   return refresh_chunk(st, chunk, grads, stream, &usev);
+}
+
+int run_refresh(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream) {
+  if (idx.empty()) return MOARA_OK;
+  std::vector<char> usev(st->n, 0);
+  for (int i : idx) usev[i] = st->mats[i].vpath && (((uintptr_t)grads[i] & 15) == 0);
+  int rc = run_decompose(st, idx, grads, false, stream, &usev);
+  if (rc) return rc;
+  return refresh_in_chunks(st, idx, grads, stream, usev);
 }
 
 }  // namespace
@@ -991,7 +1020,7 @@ int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, i
                              vpath_shape_ok(*cfg, descs[i].rows, descs[i].cols, sides[i], ranks[i]));
   }
   *out_state_bytes = (int64_t)tot;
-  if (out_refresh_workspace_bytes) *out_refresh_workspace_bytes = (int64_t)std::min(ref, REFRESH_BUDGET + ref / (size_t)n);
+  if (out_refresh_workspace_bytes) *out_refresh_workspace_bytes = (int64_t)std::min(ref, refresh_budget() + ref / (size_t)n);
   return MOARA_OK;
 }
 
@@ -1112,22 +1141,7 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
     rc = run_decompose(st, idx, grads, true, hs, &usev);
     if (rc) return rc;
   }
-  if (!need.empty()) {
-    std::vector<int> chunk;
-    size_t bytes = 0;
-    for (int i : need) {
-      const MatHost& h = st->mats[i];
-      const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), h.r, usev[i]);
-      if (!chunk.empty() && bytes + b > REFRESH_BUDGET) {
-        if ((rc = refresh_chunk(st, chunk, grads, hs, &usev))) return rc;
-        chunk.clear();
-        bytes = 0;
-      }
-      chunk.push_back(i);
-      bytes += b;
-    }
-    if ((rc = refresh_chunk(st, chunk, grads, hs, &usev))) return rc;
-  }
+  if (!need.empty() && (rc = refresh_in_chunks(st, need, grads, hs, usev))) return rc;
   rc = run_project_back(st, idx, weights, grads, lr, hs, &usev);
   if (rc) return rc;
   for (int i : idx) st->mats[i].t += 1;

@@ -113,6 +113,22 @@ def test_create_state_validates_before_touching_the_gpu(field, value, code):
     assert e.value.status == code
 
 
+def test_refresh_workspace_follows_the_chunk_budget(monkeypatch):
+    """The refresh workspace is the whole batch's need unless the chunk budget
+    (MOARA_REFRESH_CHUNK_MIB) is smaller; then it is that budget plus one matrix's share."""
+    _lib()
+    cfg = M.moara_default_config(rank_table=[64] * 10, block_size=64, operand_dtype=M.MOARA_BF16)
+    descs = M.make_descs([(1024, 1024, 0)] * 4)
+    monkeypatch.delenv("MOARA_REFRESH_CHUNK_MIB", raising=False)
+    _, whole = M.moara_state_bytes(cfg, descs)
+    monkeypatch.setenv("MOARA_REFRESH_CHUNK_MIB", "1")
+    _, small = M.moara_state_bytes(cfg, descs)
+    assert small == (1 << 20) + whole // 4 < whole
+    for bad in ("0", "-3", "12x", ""):   # ignored: the default budget applies
+        monkeypatch.setenv("MOARA_REFRESH_CHUNK_MIB", bad)
+        assert M.moara_state_bytes(cfg, descs)[1] == whole
+
+
 def test_state_bytes_counts_fp32_moments_projector_copies_and_v_workspace():
     _lib()
     cfg = M.moara_default_config(rank_table=[64] * 10, block_size=64, operand_dtype=M.MOARA_BF16)

@@ -213,6 +213,29 @@ def test_refresh_lowrank_llama300m_layer():
     print(f"[refresh] worst principal angle {worst:.2e}", flush=True)
 
 
+def test_refresh_in_several_chunks_is_bit_identical(monkeypatch):
+    """A refresh split into chunks (workspace budget below one layer's need) gives the
+    same projectors, bit for bit, as one chunk: every matrix is computed on its own."""
+    import torch
+    M = _M()
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [0])
+    c = case_from_workload(wl)
+    Gs = [to_dev(WL.grad_np(wl, i, 0), "f32") for i in range(len(wl.matrices))]
+    out = []
+    for budget in (None, "8"):
+        if budget:
+            monkeypatch.setenv("MOARA_REFRESH_CHUNK_MIB", budget)
+        else:
+            monkeypatch.delenv("MOARA_REFRESH_CHUNK_MIB", raising=False)
+        st = gpu_state(c)
+        print(f"[refresh] llama_300m layer 0, chunk budget {budget or 'default'}", flush=True)
+        M.moara_refresh_projector(st, Gs)
+        torch.cuda.synchronize()
+        out.append([M.moara_get_tensor(st, i, M.MOARA_T_P) for i in range(len(Gs))])
+    for a, b in zip(*out):
+        assert np.array_equal(a, b)
+
+
 def test_refresh_inside_step_schedule():
     import torch
     M = _M()
