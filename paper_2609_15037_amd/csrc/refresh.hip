@@ -188,7 +188,7 @@ constexpr int JEPT = JR * PW / JNT;    // chunk elements per thread
 static_assert(2 * JR == PW && JEPT * JNT == JR * PW && (JAC_WAVES == 4 || JAC_WAVES == 8), "chunk mapping");
 // Gram tiles (it, jt), it <= jt, of each wave, packed as it * 4 + jt per byte (0xFF = none).
 // Waves w and w + 4 share a SIMD; the per-SIMD counts are 3, 3, 2, 2 in both layouts.
-__device__ __forceinline__ uint32_t gram_tiles(int wave) {
+__device__ __forceinline__ uint32_t jac_gram_tiles(int wave) {
   if (JAC_WAVES == 4)
     return wave == 0 ? 0xFF020100u : wave == 1 ? 0xFF060503u : wave == 2 ? 0xFFFF0A07u : 0xFFFF0F0Bu;
   constexpr uint32_t tab[8] = {0xFFFF0100u, 0xFFFF0605u, 0xFFFFFF02u, 0xFFFFFF03u,
@@ -254,9 +254,9 @@ __global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restric
   // (1) Gram of the 64 columns on fp64 MFMA (v_mfma_f64_16x16x4: lane l supplies
   // A[l%16][l/16] and B[l/16][l%16] and receives D[4r + l/16][l%16] in register r).
   // G is symmetric: only its ten 16 x 16 tiles (it, jt) with it <= jt are computed
-  // (gram_tiles) and mirrored when G is written.
+  // (jac_gram_tiles) and mirrored when G is written.
   {
-    const uint32_t tiles = gram_tiles(wave);
+    const uint32_t tiles = jac_gram_tiles(wave);
     const int nt = ((tiles & 0xFF) != 0xFF) + ((tiles >> 8 & 0xFF) != 0xFF) + ((tiles >> 16 & 0xFF) != 0xFF);
     f64x4 acc[3];
 #pragma unroll
