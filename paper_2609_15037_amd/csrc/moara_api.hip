@@ -864,7 +864,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     for (int rr = 0; rr < nb_max - 1; ++rr) HIP_TRY(launch_jacobi_round(RD, nm, tj, rr, sw, stream));
   HIP_TRY(launch_finalize_order(RD, nm, tnorm, stream));
   HIP_TRY(launch_gemm(kind, A_KC, B_KC, EP_STORE, (const GemmProb*)D(22), nm, tpw, u, stream));
-  HIP_TRY(launch_finalize_out(RD, nm, stream));
+  int32_t rmax = 0;
+  for (auto& x : rm) rmax = std::max(rmax, st->mats[x.idx].r);
+  HIP_TRY(launch_finalize_out(RD, nm, rmax, stream));
   for (auto& x : rm) st->mats[x.idx].hasP = true;
   return MOARA_OK;
 }

@@ -73,7 +73,7 @@ hipError_t launch_r_colmajor(const RefDev* d, int n, uint32_t total, hipStream_t
 uint32_t r_colmajor_tiles(int32_t w, int32_t wpad);
 uint32_t norm_tiles(int32_t wpad);
 hipError_t launch_finalize_order(const RefDev* d, int n, uint32_t norm_total, hipStream_t st);
-hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st);
+hipError_t launch_finalize_out(const RefDev* d, int n, int32_t rmax, hipStream_t st);
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
                                     int operand_bf16, int kp, hipStream_t st);
 uint32_t gauss_tiles(int64_t s, int32_t w);

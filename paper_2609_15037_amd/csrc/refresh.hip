@@ -479,9 +479,8 @@ __global__ __launch_bounds__(256) void k_r_colmajor(const RefDev* __restrict__ d
 // values; the Ritz vectors are Q (R J) / norm. k_finalize_order (one workgroup per
 // matrix): column norms, order by decreasing norm, Bt = the first r columns,
 // normalised (zero for numerically null directions). A GEMM then forms Pw = Q Bt^T.
-// k_finalize_out (FO_SPLIT workgroups per matrix): make each column's largest-magnitude
-// entry positive (lowest index on ties) and write P (fp32 master and both operand
-// copies). An all-zero iterate (V == 0) keeps the previous projector, or yields the
+// k_finalize_out: make each column's largest-magnitude entry positive (lowest index on
+// ties) and write P (fp32 master and both operand copies). An all-zero iterate (V == 0) keeps the previous projector, or yields the
 // first r canonical basis vectors when there is none; numerically null directions
 // also fall back to e_j.
 // Column norms of R J (the Ritz values): NORM_COLS columns per workgroup, one wave per
@@ -537,43 +536,81 @@ __global__ __launch_bounds__(256) void k_finalize_order(const RefDev* __restrict
   }
 }
 
-// FO_SPLIT workgroups per matrix; each wave takes one column at a time (butterfly
-// argmax over its lanes, no workgroup barriers).
-constexpr int FO_SPLIT = 8;
-__global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__ ds) {
-  const RefDev& d = ds[blockIdx.x / FO_SPLIT];
-  const int part = blockIdx.x % FO_SPLIT;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t s = d.s;
+// k_finalize_out: one workgroup per (matrix, block of FO_COLS projector columns). Pass 1
+// finds each column's entry of largest magnitude (lowest index on ties) with row-wise,
+// coalesced reads; pass 2 writes the column block with that entry made positive: P
+// (fp32 master) and the operand copy row by row, the transposed operand copy through a
+// 32-row LDS tile so that its writes also run along its rows.
+constexpr int FO_COLS = 64;
+__global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__ ds, int cblocks) {
+  const RefDev& d = ds[blockIdx.x / cblocks];
+  const int j0 = (int)(blockIdx.x % cblocks) * FO_COLS;
+  const int r = d.r;
+  if (j0 >= r) return;
   const double nmax = d.norms[d.order[0]];
   if (!(nmax > 0.0) && d.has_prev) return;   // V == 0: keep the previous projector
-  for (int j = 4 * part + wave; j < d.r; j += 4 * FO_SPLIT) {
-    const double nrm = d.norms[d.order[j]];
-    const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
-    // sign: entry of largest magnitude, lowest index on ties
+  __shared__ float bv[4][FO_COLS];
+  __shared__ int bix[4][FO_COLS];
+  __shared__ float sg[FO_COLS];              // column sign; 0 = null direction (e_j)
+  __shared__ float tile[32][FO_COLS + 1];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int64_t s = d.s;
+  const int j = j0 + lane;
+  const bool jin = j < r;
+  {
     float best = -1.f;
     int bi = 0;
-    for (int64_t i = lane; i < s; i += 64) {
-      const float v = deg ? (i == (j % s) ? 1.f : 0.f) : fabsf(d.Pw[i * d.r + j]);
-      if (v > best) { best = v; bi = (int)i; }
+    if (jin)
+      for (int64_t i = wave; i < s; i += 4) {   // increasing rows: ties keep the lowest index
+        const float v = fabsf(d.Pw[i * r + j]);
+        if (v > best) { best = v; bi = (int)i; }
+      }
+    bv[wave][lane] = best;
+    bix[wave][lane] = bi;
+    __syncthreads();
+    if (wave == 0) {
+      for (int w2 = 1; w2 < 4; ++w2) {
+        const float ob = bv[w2][lane];
+        const int oi = bix[w2][lane];
+        if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
+      }
+      float g = 1.f;
+      if (jin) {
+        const double nrm = d.norms[d.order[j]];
+        const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
+        g = deg ? 0.f : ((d.Pw[(int64_t)bi * r + j] < 0.f) ? -1.f : 1.f);
+      }
+      sg[lane] = g;
     }
-    for (int o = 32; o > 0; o >>= 1) {   // every lane ends with the same (value, lowest index)
-      const float ob = __shfl_xor(best, o, 64);
-      const int oi = __shfl_xor(bi, o, 64);
-      if (ob > best || (ob == best && oi < bi)) { best = ob; bi = oi; }
-    }
-    const float sgn = deg ? 1.f : ((d.Pw[(int64_t)bi * d.r + j] < 0.f) ? -1.f : 1.f);
-    for (int64_t i = lane; i < s; i += 64) {
-      const float v = deg ? (i == (j % s) ? 1.f : 0.f) : sgn * d.Pw[i * d.r + j];
-      d.P32[i * d.r + j] = v;
-      if (d.operand_bf16) {
-        ((bf16*)d.Pop)[d.kp ? kp_index(i, j, s) : i * d.r + j] = f2bf(v);
-        ((bf16*)d.Ptop)[d.kp ? kp_index(j, i, d.r) : (int64_t)j * s + i] = f2bf(v);
-      } else {
-        ((float*)d.Pop)[i * d.r + j] = v;
-        ((float*)d.Ptop)[(int64_t)j * s + i] = v;
+    __syncthreads();
+  }
+  const float g = sg[lane];
+  for (int64_t i0 = 0; i0 < s; i0 += 32) {
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {   // row-major outputs: rows i0 + wave + 4 k, column j
+      const int li = wave + 4 * k;
+      const int64_t i = i0 + li;
+      if (i < s && jin) {
+        const float v = g == 0.f ? (i == (j % s) ? 1.f : 0.f) : g * d.Pw[i * r + j];
+        d.P32[i * r + j] = v;
+        if (d.operand_bf16) ((bf16*)d.Pop)[d.kp ? kp_index(i, j, s) : i * r + j] = f2bf(v);
+        else ((float*)d.Pop)[i * r + j] = v;
+        tile[li][lane] = v;
       }
     }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {   // transposed copy: row j0 + (tid >> 5) + 8 k, columns i0 ..
+      const int lj = (tid >> 5) + 8 * k, li = tid & 31;
+      const int jj = j0 + lj;
+      const int64_t i = i0 + li;
+      if (i < s && jj < r) {
+        const float v = tile[li][lj];
+        if (d.operand_bf16) ((bf16*)d.Ptop)[d.kp ? kp_index(jj, i, r) : (int64_t)jj * s + i] = f2bf(v);
+        else ((float*)d.Ptop)[(int64_t)jj * s + i] = v;
+      }
+    }
+    __syncthreads();
   }
 }
 
@@ -632,9 +669,10 @@ hipError_t launch_finalize_order(const RefDev* d, int n, uint32_t norm_total, hi
   hipLaunchKernelGGL(k_finalize_order, dim3(n), dim3(256), 0, st, d);
   return hipGetLastError();
 }
-hipError_t launch_finalize_out(const RefDev* d, int n, hipStream_t st) {
-  if (!n) return hipSuccess;
-  hipLaunchKernelGGL(k_finalize_out, dim3(n * FO_SPLIT), dim3(256), 0, st, d);
+hipError_t launch_finalize_out(const RefDev* d, int n, int32_t rmax, hipStream_t st) {
+  const int cblocks = (rmax + FO_COLS - 1) / FO_COLS;
+  if (!n || !cblocks) return hipSuccess;
+  hipLaunchKernelGGL(k_finalize_out, dim3(n * cblocks), dim3(256), 0, st, d, cblocks);
   return hipGetLastError();
 }
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
