@@ -17,6 +17,8 @@ It is a plain, slow, float64 NumPy transcription of what the paper defines:
 * Appendix D: Adam with beta=(0.9, 0.999), bias correction, zero weight decay,
   GaLore scale 0.25, magnitude branch in fp32, recomposed update cast to bf16.
 * Appendix G: optimizer-state memory formulas.
+* Section 3.2 (Eq. module_alignment): the subspace alignment diagnostic S(W, t) and
+  its module average S_tau (Algorithm 1, Phases 1-2).
 
 Readings taken where the paper is silent or ambiguous are listed in the
 repository's design notes; each is also stated at the function that uses it.
@@ -340,6 +342,53 @@ def step(W: np.ndarray, G: np.ndarray, st: OracleState, cfg: OracleConfig, lr: f
 
 def update_direction(W_old: np.ndarray, W_new: np.ndarray) -> np.ndarray:
     return np.asarray(W_new, dtype=np.float64) - np.asarray(W_old, dtype=np.float64)
+
+
+# ----------------------------------------------------------------------------
+# Subspace alignment diagnostic (Section 3.2, Eq. module_alignment; Algorithm 1,
+# Phases 1-2)
+# ----------------------------------------------------------------------------
+
+def reconstruct(G: np.ndarray, P: np.ndarray, B: int, eps: float = 1e-12, decompose_on: bool = True,
+                side: Optional[str] = None) -> np.ndarray:
+    """G_recon = Rep_B(M) (elementwise) (P P^T V): the gradient rebuilt from its block
+    magnitudes and the projection of its direction tensor onto the rank-r subspace.
+
+    The paper writes the LEFT form (P in R^{m x r}). Reading: a RIGHT matrix (m > n,
+    projector Q in R^{n x r}) uses the same construction on its projected side,
+    Rep_B(M) (elementwise) (V Q Q^T). With the decomposition off the reconstruction is
+    GaLore's, P P^T G (resp. G Q Q^T).
+    """
+    G = np.asarray(G, dtype=np.float64)
+    P = np.asarray(P, dtype=np.float64)
+    m, n = G.shape
+    side = side or projection_side(m, n)
+    if decompose_on:
+        M, V = decompose(G, B, eps)
+    else:
+        M, V = None, G
+    PV = P @ (P.T @ V) if side == LEFT else (V @ P) @ P.T
+    return recompose(M, PV, B) if decompose_on else PV
+
+
+def alignment(G: np.ndarray, P: np.ndarray, B: int, eps: float = 1e-12, decompose_on: bool = True,
+              side: Optional[str] = None) -> float:
+    """S(W, t) = cos(G, G_recon), the cosine of the two matrices as vectors (Frobenius
+    inner product over the product of Frobenius norms). Reading: 0 when G or G_recon
+    is the zero matrix (the cosine is undefined there)."""
+    G = np.asarray(G, dtype=np.float64)
+    R = reconstruct(G, P, B, eps, decompose_on, side)
+    den = float(np.linalg.norm(G)) * float(np.linalg.norm(R))
+    return float(np.sum(G * R)) / den if den > 0.0 else 0.0
+
+
+def module_alignment(samples: Iterable[Tuple[int, float]]) -> Dict[int, float]:
+    """S_tau = mean of S(W, t) over the logged steps and the matrix instances of module
+    type tau: samples are (module type, S) pairs."""
+    acc: Dict[int, list] = {}
+    for tau, s in samples:
+        acc.setdefault(int(tau), []).append(float(s))
+    return {tau: float(np.mean(v)) for tau, v in acc.items()}
 
 
 # ----------------------------------------------------------------------------

@@ -388,3 +388,71 @@ def test_floored_metric():
     assert O.floored_rel_err(b, b) == 0.0
     a = b + np.array([0.0, 1e-3, 0.0])
     assert abs(O.floored_rel_err(a, b) - 1e-3 / math.sqrt(5 / 3)) < 1e-15
+
+
+# ---------------------------------------------------------------- alignment diagnostic (Section 3.2)
+
+def _orth(rng, n, r):
+    return np.linalg.qr(rng.standard_normal((n, n)))[0][:, :r]
+
+
+@pytest.mark.parametrize("shape", [(6, 10), (10, 6)])
+def test_alignment_full_rank_projector_is_one(shape):
+    # P P^T = I on the projected side: G_recon = Rep_B(M) V = G (up to eps), S = 1
+    rng = np.random.default_rng(1)
+    G = rng.standard_normal(shape)
+    s = min(shape)
+    for B in (1, 3, 4, 64):
+        assert abs(O.alignment(G, _orth(rng, s, s), B) - 1.0) < 1e-12
+
+
+@pytest.mark.parametrize("shape", [(6, 10), (10, 6)])
+def test_alignment_without_decomposition_is_projected_norm_ratio(shape):
+    # cos(G, P P^T G) = ||P^T G|| / ||G|| (LEFT), cos(G, G Q Q^T) = ||G Q|| / ||G|| (RIGHT)
+    rng = np.random.default_rng(2)
+    G = rng.standard_normal(shape)
+    P = _orth(rng, min(shape), 2)
+    ref = np.linalg.norm(P.T @ G if shape[0] <= shape[1] else G @ P) / np.linalg.norm(G)
+    assert abs(O.alignment(G, P, 4, decompose_on=False) - ref) < 1e-12
+
+
+def test_alignment_support_inside_and_outside_the_subspace():
+    # LEFT 4 x 9: G lives in rows 0-1. V then lives there too (zero blocks stay zero), so
+    # P = span(e0, e1) reconstructs G exactly and its complement reconstructs nothing.
+    rng = np.random.default_rng(3)
+    G = np.zeros((4, 9))
+    G[:2] = rng.standard_normal((2, 9))
+    I = np.eye(4)
+    assert abs(O.alignment(G, I[:, :2], 4) - 1.0) < 1e-12
+    assert O.alignment(G, I[:, 2:], 4) == 0.0
+    # RIGHT 9 x 4: the same along columns 0-1 (the projector acts on the column side)
+    H = np.zeros((9, 4))
+    H[:, :2] = rng.standard_normal((9, 2))
+    assert abs(O.alignment(H, I[:, :2], 2) - 1.0) < 1e-12
+    assert O.alignment(H, I[:, 2:], 2) == 0.0
+
+
+def test_alignment_block_size_one_keeps_the_projected_columns():
+    # B = 1: M = |G|, V = sign(G); RIGHT 3 x 2 with Q = e0 keeps column 0 of V, so
+    # G_recon = [G[:, 0], 0] and S = ||G[:, 0]|| / ||G||.
+    G = np.array([[3.0, -1.0], [-2.0, 4.0], [0.5, 2.0]])
+    S = O.alignment(G, np.array([[1.0], [0.0]]), 1)
+    assert abs(S - np.linalg.norm(G[:, 0]) / np.linalg.norm(G)) < 1e-12
+
+
+def test_alignment_depends_on_the_subspace_only():
+    # P -> P O (O orthogonal, including column sign flips) leaves P P^T and S unchanged;
+    # a positive scale of G changes neither M's ratios nor V
+    rng = np.random.default_rng(4)
+    G = rng.standard_normal((8, 13))
+    P = _orth(rng, 8, 3)
+    S = O.alignment(G, P, 4)
+    Orot = np.linalg.qr(rng.standard_normal((3, 3)))[0] @ np.diag([1.0, -1.0, 1.0])
+    assert abs(O.alignment(G, P @ Orot, 4) - S) < 1e-12
+    assert abs(O.alignment(7.5 * G, P, 4) - S) < 1e-12
+    assert 0.0 < S < 1.0
+
+
+def test_module_alignment_is_the_mean_per_type():
+    got = O.module_alignment([(0, 0.2), (3, 1.0), (0, 0.4), (6, -0.5)])
+    assert got == pytest.approx({0: 0.3, 3: 1.0, 6: -0.5})
