@@ -323,6 +323,21 @@ def main():
                  "avg_launch_ms": dk["ms_total"] / max(1, dk["launches"]),
                  "traffic": measured_traffic(dom, wl.name) if not a.layers else None})
 
+    # alignment diagnostic (Section 3.2) over every matrix: one untimed call, then one timed
+    M.moara_alignment(st, G, stream=stream)
+    torch.cuda.synchronize()
+    ea0, ea1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    ea0.record(stream)
+    S = M.moara_alignment(st, G, stream=stream)
+    ea1.record(stream)
+    torch.cuda.synchronize()
+    align_ms = ea0.elapsed_time(ea1)
+    align_flops = float(sum(4.0 * m.rows * m.cols * wl.rank_of(m) for m in wl.matrices))
+    s_tau = {}
+    for m, sv in zip(wl.matrices, S):
+        s_tau.setdefault(WL.MODULE_NAMES[m.module], []).append(float(sv))
+    log(f"[bench] alignment diagnostic: {align_ms:.1f} ms")
+
     if moe:
         mb = sum(method_cost(wl, ob, wb, masks[a.warmup + k])[0] for k in range(a.steps)) / a.steps
         mf = sum(method_cost(wl, ob, wb, masks[a.warmup + k])[1] for k in range(a.steps)) / a.steps
@@ -355,6 +370,10 @@ def main():
         "step_roofline_frac": step_roof_ms / ms_step,
         "kernels": kern,
         "roofline": roof,
+        "alignment": {"ms": align_ms, "matrices": n, "alg_flops": align_flops,
+                      "tflops": align_flops / (align_ms / 1e3) / 1e12,
+                      "frac_fp32_peak": align_flops / (align_ms / 1e3) / PEAK_F32,
+                      "S_tau": {k: float(np.mean(v)) for k, v in s_tau.items()}},
         "host_clock_ms_per_step": host_s / a.steps * 1e3,
     }
     if not a.no_cpu_baseline:

@@ -202,6 +202,29 @@ int moara_refresh_projector(moara_state* st, const void* const* grads, const uin
 int moara_step(moara_state* st, void* const* weights, const void* const* grads,
                const uint8_t* active, float lr, void* stream);
 
+/* Subspace alignment diagnostic of Section 3.2 (Eq. module_alignment; the
+ * quantity logged in Algorithm 1, Phases 1-2): for every active matrix,
+ *   out_S[i] = cos(G_i, G_recon,i) = <G, G_recon>_F / (||G||_F ||G_recon||_F),
+ *   G_recon = Rep_B(M) (elementwise) (P P^T V)  for a LEFT matrix,
+ *             Rep_B(M) (elementwise) (V Q Q^T)  for a RIGHT matrix,
+ * with M, V the block decomposition of G_i (the state's B and eps_d; with
+ * decompose = 0, M = 1 and V = G) and P (Q) the matrix's current fp32 projector.
+ * 0 when G or G_recon is zero. The module average S_tau is the caller's mean
+ * of these values over logged steps and matrices of one module type.
+ * Reads only: weights, moments, projectors and step counters are unchanged.
+ * fp32 GEMM operands with fp64 sums (accumulated with atomics, so the last bits
+ * may differ between runs).
+ * grads:  host array of n device pointers to m x n row-major fp32 G (read only).
+ * active: host array of n flags (NULL = all); out_S[i] of an inactive matrix is
+ *         left as it was.
+ * out_S:  host array of n doubles, written before the call returns (the call
+ *         synchronises `stream`).
+ * Uses the refresh workspace (4 L r bytes per active matrix). Errors:
+ * MOARA_E_ARG (nulls), MOARA_E_STATE (an active matrix has no projector),
+ * MOARA_E_OOM (workspace), MOARA_E_HIP. */
+int moara_alignment(moara_state* st, const void* const* grads, const uint8_t* active,
+                    double* out_S, void* stream);
+
 /* Copy one state tensor of matrix `mat` to host memory (synchronises with the
  * state's work queued so far on `stream`). Layouts and dtypes: see MOARA_T_*
  * (fp32, except MOARA_T_STEP: one int64). bytes must equal the exact size.
@@ -225,7 +248,8 @@ enum {
   MOARA_KERN_PROJECT = 1,   /* projection GEMM + Optimizer_V epilogue  */
   MOARA_KERN_BACKPROJ = 2,  /* back-projection GEMM + update epilogue  */
   MOARA_KERN_REFRESH = 3,   /* whole refresh (all its kernels)         */
-  MOARA_NUM_KERNELS = 4
+  MOARA_KERN_ALIGN = 4,     /* alignment diagnostic GEMMs              */
+  MOARA_NUM_KERNELS = 5
 };
 int moara_set_timing(moara_state* st, int32_t enable);
 int moara_kernel_stats(moara_state* st, int32_t kernel, int64_t* out_launches, double* out_total_ms,

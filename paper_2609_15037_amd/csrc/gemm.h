@@ -23,7 +23,10 @@ enum { B_KC = 0, B_NC = 1 };
 //   EP_UPDATE : W[i][j] -= lr * scale * dM[i][j/B] * C[i][j] (bf16 or fp32 W in c)
 //   EP_STORE  : c[i*ldc + j] = C[i][j] (fp32)
 //   EP_STORE_BF16: c[i*ldc + j] = bf16(C[i][j])   (large-tile path only)
-enum { EP_ADAM = 0, EP_UPDATE = 1, EP_STORE = 2, EP_STORE_BF16 = 3 };
+//   EP_ALIGN  : alignment sums (fp32 kind): with R[i][j] = M[i][j/B] * C[i][j], M = 1 / inv - eps
+//               (inv = nullptr: M = 1) and G[i][j] = c[i*ldc + j] (read only), adds
+//               sum G R, sum R^2 and sum G^2 of the tile to red[0..2] (fp64 atomics)
+enum { EP_ADAM = 0, EP_UPDATE = 1, EP_STORE = 2, EP_STORE_BF16 = 3, EP_ALIGN = 4 };
 
 struct GemmProb {
   int64_t M, N, K;
@@ -50,13 +53,14 @@ struct GemmProb {
   uint32_t inv_bytes; // extent of the inv array
   uint32_t tri_b;     // fp32 kind: 1 = B[j][k] is zero for k > j (upper triangular right factor),
                       // so a tile's K loop stops after its last column
+  double* red;        // EP_ALIGN accumulators (three per problem)
 };
 
 struct GemmUniform {
   int32_t B;            // decomposition block size (A_G_* scaling, EP_UPDATE)
   int32_t nprob;
   int32_t weight_bf16;  // EP_UPDATE
-  int32_t pad_;
+  float decomp_eps;     // EP_ALIGN
   float beta1, beta2, adam_eps;
   float lr, scale;
 };

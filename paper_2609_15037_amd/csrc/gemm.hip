@@ -377,6 +377,7 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, const GemmUniform& U
                                          const f32x16 (&acc)[2][2]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
+  double s_gr = 0.0, s_rr = 0.0, s_gg = 0.0;   // EP_ALIGN partial sums
 #pragma unroll
   for (int mi = 0; mi < 2; ++mi) {
     const int64_t row = row0 + wm * 64 + mi * 32 + (lane & 31);
@@ -398,6 +399,26 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, const GemmUniform& U
           if (full) *reinterpret_cast<float4*>(C + idx) = make_float4(v[0], v[1], v[2], v[3]);
           else
             for (int q = 0; q < 4; ++q) if (col + q < P.N) C[idx + q] = v[q];
+        } else if constexpr (EP == EP_ALIGN) {
+          // G_recon = Rep_B(M) * (projected direction); the gradient is read, never written
+          const float* Gr = (const float*)P.c;
+          const float* ivr = P.inv ? P.inv + row * P.inv_ld : nullptr;
+          float gv[4] = {0.f, 0.f, 0.f, 0.f};
+          if (full) {
+            const float4 x = *reinterpret_cast<const float4*>(Gr + idx);
+            gv[0] = x.x; gv[1] = x.y; gv[2] = x.z; gv[3] = x.w;
+          } else {
+            for (int q = 0; q < 4; ++q) if (col + q < P.N) gv[q] = Gr[idx + q];
+          }
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            if (col + q >= P.N) continue;
+            const float mag = ivr ? 1.f / ivr[(col + q) / U.B] - U.decomp_eps : 1.f;
+            const double rec = (double)mag * (double)v[q], g = (double)gv[q];
+            s_gr += g * rec;
+            s_rr += rec * rec;
+            s_gg += g * g;
+          }
         } else if constexpr (EP == EP_ADAM) {
           float e[4], s2[4], o[4];
           const bool fm = (col + 4 <= P.N) && ((idx & 3) == 0);   // moments are library memory (aligned)
@@ -484,6 +505,19 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, const GemmUniform& U
           }
         }
       }
+  }
+  if constexpr (EP == EP_ALIGN) {   // wave sums (fixed butterfly), one atomic per sum and wave
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      s_gr += __shfl_xor(s_gr, o, 64);
+      s_rr += __shfl_xor(s_rr, o, 64);
+      s_gg += __shfl_xor(s_gg, o, 64);
+    }
+    if (lane == 0) {
+      atomicAdd(P.red + 0, s_gr);
+      atomicAdd(P.red + 1, s_rr);
+      atomicAdd(P.red + 2, s_gg);
+    }
   }
 }
 
@@ -693,6 +727,7 @@ hipError_t launch_gemm(int kind, int amode, int bmode, int ep, const GemmProb* p
     GEMM_F(A_G_TRANS, B_KC, EP_ADAM)
     GEMM_F(A_KC, B_KC, EP_UPDATE)
     GEMM_F(A_KC, B_KC, EP_STORE)
+    GEMM_F(A_KC, B_KC, EP_ALIGN)
     GEMM_F(A_G_ROW, B_NC, EP_STORE)
     GEMM_F(A_G_TRANS, B_NC, EP_STORE)
     GEMM_F(A_KC, B_NC, EP_STORE)

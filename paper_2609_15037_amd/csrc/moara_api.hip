@@ -1118,6 +1118,92 @@ int moara_refresh_projector(moara_state* st, const void* const* grads, const uin
   return run_refresh(st, idx, grads, (hipStream_t)stream);
 }
 
+// Subspace alignment diagnostic (Section 3.2): decompose G (inv only), R^(T) = V' P with
+// the fp32 master projector (projection GEMMs with a plain store), then the
+// reconstruction GEMM P R (LEFT) / R Q^T (RIGHT) whose epilogue scales by Rep_B(M) and
+// reduces <G, G_recon>, ||G_recon||^2 and ||G||^2 per matrix. fp32 operands throughout.
+int moara_alignment(moara_state* st, const void* const* grads, const uint8_t* active, double* out_S, void* stream) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  if (!grads || !out_S) return fail(MOARA_E_ARG, "grads/out_S is NULL");
+  std::vector<int> idx;
+  int rc = collect_active(st, grads, active, &idx, "grads");
+  if (rc) return rc;
+  for (int i : idx)
+    if (!st->mats[i].hasP) return fail(MOARA_E_STATE, "matrix %d has no projector (set one or refresh first)", i);
+  if (idx.empty()) return MOARA_OK;
+  hipStream_t hs = (hipStream_t)stream;
+  const bool dec = st->cfg.decompose != 0;
+  if (dec && (rc = run_decompose(st, idx, grads, false, hs))) return rc;
+  size_t need = 0;
+  for (int i : idx) need += align_up(4 * (size_t)st->mats[i].L * st->mats[i].r);   // R^(T), L x r fp32
+  const size_t red_off = need;
+  need += align_up(8 * 3 * idx.size());
+  if ((rc = ensure_ref_ws(st, need))) return rc;
+  double* red = (double*)(st->ref_ws + red_off);
+  std::vector<GemmProb> projR, projL, rec;
+  uint32_t tR = 0, tL = 0, tr = 0;
+  char* p = st->ref_ws;
+  for (size_t q = 0; q < idx.size(); ++q) {
+    const int i = idx[q];
+    const MatHost& h = st->mats[i];
+    const bool left = h.side == MOARA_SIDE_LEFT;
+    float* R = (float*)p;
+    p += align_up(4 * (size_t)h.L * h.r);
+    GemmProb g{};   // R^(T) (L x r) = V' P, V' = V (RIGHT) or V^T (LEFT) formed from G and inv
+    g.M = h.L; g.N = h.r; g.K = h.s;
+    g.a = grads[i]; g.lda = h.n;
+    g.inv = dec ? h.inv : nullptr; g.inv_ld = h.k;
+    g.b = h.P32; g.ldb = h.r;
+    g.c = R; g.ldc = h.r;
+    g.tiles_n = gemm_tiles_n(KIND_F32, g.N);
+    g.vec = vec_flags_g((const float*)grads[i], h.n) | (vec_flags_op(h.P32, h.r, 0) << 1);
+    set_extents(g, 4 * (size_t)h.m * h.n, 4 * (size_t)h.n, 4 * (size_t)h.s * h.r, 4 * (size_t)h.r,
+                g.inv ? 4 * (size_t)h.m * h.k : 0, 4 * (size_t)h.k);
+    const uint32_t nt = gemm_tiles_m(KIND_F32, g.M) * g.tiles_n;
+    if (left) { g.tile_start = tL; tL += nt; projL.push_back(g); }
+    else { g.tile_start = tR; tR += nt; projR.push_back(g); }
+    GemmProb b{};   // reconstructed direction (m x n) = P R (LEFT) or R Q^T (RIGHT), reduced against G
+    b.M = h.m; b.N = h.n; b.K = h.r;
+    b.a = left ? (const void*)h.P32 : (const void*)R; b.lda = h.r;
+    b.b = left ? (const void*)R : (const void*)h.P32; b.ldb = h.r;
+    b.c = (void*)grads[i]; b.ldc = h.n;
+    b.inv = dec ? h.inv : nullptr; b.inv_ld = h.k;
+    b.red = red + 3 * q;
+    b.tiles_n = gemm_tiles_n(KIND_F32, b.N);
+    b.vec = vec_flags_op(b.a, h.r, 0) | (vec_flags_op(b.b, h.r, 0) << 1);
+    set_extents(b, 4 * (size_t)h.m * h.r, 4 * (size_t)h.r, 4 * (size_t)h.n * h.r, 4 * (size_t)h.r, 0, 0);
+    b.tile_start = tr;
+    tr += gemm_tiles_m(KIND_F32, b.M) * b.tiles_n;
+    rec.push_back(b);
+  }
+  Stager sg;
+  if ((rc = begin_stage(st, sg))) return rc;
+  const size_t oR = projR.empty() ? 0 : sg.push(projR.data(), projR.size());
+  const size_t oL = projL.empty() ? 0 : sg.push(projL.data(), projL.size());
+  const size_t oB = sg.push(rec.data(), rec.size());
+  if (oR == (size_t)-1 || oL == (size_t)-1 || oB == (size_t)-1) return fail(MOARA_E_OOM, "descriptor arena too small");
+  if ((rc = end_stage(st, sg, hs))) return rc;
+  GemmUniform u = make_uniform(st, 0.f);
+  u.decomp_eps = st->cfg.decomp_eps;
+  {
+    TimerScope ts(st, MOARA_KERN_ALIGN, hs);
+    if (!projR.empty())
+      HIP_TRY(launch_gemm(KIND_F32, A_G_ROW, B_NC, EP_STORE, (const GemmProb*)(st->dev_arena + oR), (int)projR.size(), tR, u, hs));
+    if (!projL.empty())
+      HIP_TRY(launch_gemm(KIND_F32, A_G_TRANS, B_NC, EP_STORE, (const GemmProb*)(st->dev_arena + oL), (int)projL.size(), tL, u, hs));
+    HIP_TRY(hipMemsetAsync(red, 0, 8 * 3 * idx.size(), hs));
+    HIP_TRY(launch_gemm(KIND_F32, A_KC, B_KC, EP_ALIGN, (const GemmProb*)(st->dev_arena + oB), (int)rec.size(), tr, u, hs));
+  }
+  std::vector<double> sums(3 * idx.size());
+  HIP_TRY(hipMemcpyAsync(sums.data(), red, 8 * sums.size(), hipMemcpyDeviceToHost, hs));
+  HIP_TRY(hipStreamSynchronize(hs));
+  for (size_t q = 0; q < idx.size(); ++q) {
+    const double den = sqrt(sums[3 * q + 1]) * sqrt(sums[3 * q + 2]);
+    out_S[idx[q]] = den > 0.0 ? sums[3 * q] / den : 0.0;
+  }
+  return MOARA_OK;
+}
+
 int moara_step(moara_state* st, void* const* weights, const void* const* grads, const uint8_t* active, float lr,
                void* stream) {
   if (!st) return fail(MOARA_E_ARG, "state is NULL");

@@ -26,12 +26,13 @@ MOARA_NUM_MODULES = 10
 MOARA_SIDE_AUTO, MOARA_SIDE_LEFT, MOARA_SIDE_RIGHT = 0, 1, 2
 MOARA_F32, MOARA_BF16 = 0, 1
 MOARA_T_P, MOARA_T_EXP_AVG, MOARA_T_EXP_AVG_SQ, MOARA_T_MAG_AVG, MOARA_T_MAG_AVG_SQ, MOARA_T_STEP = range(6)
-MOARA_KERN_DECOMPOSE, MOARA_KERN_PROJECT, MOARA_KERN_BACKPROJ, MOARA_KERN_REFRESH = range(4)
+MOARA_KERN_DECOMPOSE, MOARA_KERN_PROJECT, MOARA_KERN_BACKPROJ, MOARA_KERN_REFRESH, MOARA_KERN_ALIGN = range(5)
 MOARA_NUM_KERNELS = 4
 
 EXPORTED = (
     "moara_default_config", "moara_allocate_ranks", "moara_resolve_matrix", "moara_state_bytes",
-    "moara_create_state", "moara_refresh_projector", "moara_step", "moara_get_tensor", "moara_set_tensor",
+    "moara_create_state", "moara_refresh_projector", "moara_step", "moara_alignment", "moara_get_tensor",
+    "moara_set_tensor",
     "moara_set_timing", "moara_kernel_stats", "moara_reset_kernel_stats", "moara_matrix_info",
     "moara_destroy_state", "moara_last_error", "moara_version",
 )
@@ -89,6 +90,7 @@ def lib():
         "moara_create_state": (ctypes.c_int, [P(moara_config), P(moara_matrix_desc), i32, vp, P(vp)]),
         "moara_refresh_projector": (ctypes.c_int, [vp, P(vp), P(ctypes.c_uint8), vp]),
         "moara_step": (ctypes.c_int, [vp, P(vp), P(vp), P(ctypes.c_uint8), ctypes.c_float, vp]),
+        "moara_alignment": (ctypes.c_int, [vp, P(vp), P(ctypes.c_uint8), P(ctypes.c_double), vp]),
         "moara_get_tensor": (ctypes.c_int, [vp, i32, i32, vp, ctypes.c_size_t, vp]),
         "moara_set_tensor": (ctypes.c_int, [vp, i32, i32, vp, ctypes.c_size_t, vp]),
         "moara_set_timing": (ctypes.c_int, [vp, i32]),
@@ -234,6 +236,16 @@ def _active_array(st: State, active):
 def moara_refresh_projector(st: State, grads, active=None, stream=None):
     g = _ptr_array(st, grads, "grads", "f32", active)
     _check(lib().moara_refresh_projector(st.handle, g, _active_array(st, active), _stream_ptr(stream)))
+
+
+def moara_alignment(st: State, grads, active=None, stream=None) -> np.ndarray:
+    """moara_alignment of the C ABI: S(W, t) = cos(G, G_recon) per matrix as a float64
+    array of n entries (NaN for inactive matrices)."""
+    g = _ptr_array(st, grads, "grads", "f32", active)
+    out = np.full(st.n, np.nan, dtype=np.float64)
+    _check(lib().moara_alignment(st.handle, g, _active_array(st, active),
+                                 out.ctypes.data_as(ctypes.POINTER(ctypes.c_double)), _stream_ptr(stream)))
+    return out
 
 
 class StepArgs:

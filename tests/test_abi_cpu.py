@@ -155,3 +155,11 @@ def test_state_bytes_counts_fp32_moments_projector_copies_and_v_workspace():
         s, L, k, r = min(m, n), max(m, n), -(-n // 64), 64
         exp32 += 4 * al(4 * m * k) + 2 * al(4 * L * r) + al(4 * L * r) + al(4 * s * r) + 2 * al(4 * s * r)
     assert sb32 == exp32
+
+
+def test_alignment_rejects_bad_arguments_before_any_gpu_work():
+    L = _lib()
+    import ctypes
+    out = (ctypes.c_double * 2)()
+    assert L.moara_alignment(None, None, None, out, None) == M.MOARA_E_ARG
+    assert b"state is NULL" in L.moara_last_error()

@@ -93,6 +93,16 @@ def sampled_stack_parity(wl: WL.Workload, sample_layer: int, steps: int):
         assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == steps
     worst = max(v for k, v in report.items() if not k.endswith("masked_frac"))
     print(f"[fullsize] {wl.name}: worst floored rel err {worst:.3e} (tol {TOL_BF16:.0e})", flush=True)
+    # alignment diagnostic over the whole stack (one launch sequence), the sampled layer
+    # against the oracle with the same projectors and the last step's gradients
+    print(f"[fullsize] {wl.name}: alignment diagnostic, {n} matrices", flush=True)
+    S = M.moara_alignment(st, Gd)
+    samples = []
+    for j, i in enumerate(idx):
+        ref = O.alignment(Gs[i], ost[j].P, c.block_size)
+        assert abs(S[i] - ref) <= 1e-5, (wl.matrices[i].name, S[i], ref)
+        samples.append((wl.matrices[i].module, S[i]))
+    print(f"[fullsize] {wl.name}: S per module type {O.module_alignment(samples)}", flush=True)
 
 
 def test_llama2_7b_stack_one_layer_checked():

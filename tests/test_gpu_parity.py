@@ -350,3 +350,47 @@ def test_step_without_projector_is_rejected_before_launch():
     assert e.value.status == M.MOARA_E_STATE
     with pytest.raises(ValueError):
         M.moara_step(st, [W.t()], [to_dev(_grad(c, 0, 0, 0), "f32")], lr=1e-3)
+
+
+# ------------------------------------------------------------------ alignment diagnostic (Section 3.2)
+# S is a cosine of fp32-GEMM results summed in fp64: it matches the oracle's fp64 value to
+# about 1e-6 (K <= 1000 here); the bar is 1e-5, under the fp32 bar of 1e-4.
+
+@pytest.mark.parametrize("decompose,op", [(True, "f32"), (True, "bf16"), (False, "f32")])
+def test_alignment_matches_oracle(decompose, op):
+    import torch
+    M = _M()
+    c = Case(shapes=[(300, 452, WL.Q), (452, 300, WL.GATE), (129, 1000, WL.DOWN), (77, 130, WL.K), (5, 3, WL.V)],
+             ranks=[37, 50, 64, 9, 2], block_size=48, decompose=decompose, operand_dtype=op)
+    st = gpu_state(c)
+    Gs = [_grad(c, 6, 0, i) for i in range(len(c.shapes))]
+    Gs[4][:] = 0.0   # an all-zero gradient: S = 0 by definition
+    Gd = [to_dev(g, "f32") for g in Gs]
+    print(f"[alignment] decompose={decompose} operands={op}", flush=True)
+    M.moara_refresh_projector(st, Gd)
+    steps0 = [M.moara_get_tensor(st, i, M.MOARA_T_STEP) for i in range(len(Gs))]
+    S = M.moara_alignment(st, Gd)
+    for i, G in enumerate(Gs):
+        P = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+        ref = O.alignment(G, P, c.block_size, decompose_on=decompose)
+        assert abs(S[i] - ref) <= 1e-5, (i, S[i], ref)
+        assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == steps0[i]
+    assert S[4] == 0.0 and all(0.0 < S[i] < 1.0 for i in range(4))
+    # an active mask leaves the other entries alone
+    S2 = M.moara_alignment(st, Gd, active=[False, True, False, True, False])
+    assert np.isnan(S2[0]) and np.isnan(S2[2]) and np.isnan(S2[4])
+    assert abs(S2[1] - S[1]) <= 1e-12 and abs(S2[3] - S[3]) <= 1e-12
+
+
+def test_alignment_full_rank_projector_is_one_and_needs_a_projector():
+    import torch
+    M = _M()
+    c = Case(shapes=[(64, 96, WL.Q), (96, 40, WL.UP)], ranks=[64, 40], block_size=32)
+    st = gpu_state(c)
+    Gd = [to_dev(_grad(c, 7, 0, i), "f32") for i in range(2)]
+    with pytest.raises(M.MoaraError) as e:
+        M.moara_alignment(st, Gd)
+    assert e.value.status == M.MOARA_E_STATE
+    M.moara_refresh_projector(st, Gd)
+    S = M.moara_alignment(st, Gd)
+    assert np.all(np.abs(S - 1.0) <= 1e-5), S
