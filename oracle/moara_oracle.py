@@ -130,6 +130,13 @@ def paper_state_bytes(shapes: Sequence[Tuple[int, int]], ranks: Sequence[int], b
 # Section 3.1 / Appendix B.1: block-wise magnitude-direction decomposition
 # ----------------------------------------------------------------------------
 
+def flatten(G: np.ndarray) -> np.ndarray:
+    """Appendix B.1 (flattened tensors): keep the first axis, flatten all the others into
+    the column axis, G_flat = reshape(G, s0, s1 * ... * s_{r-1}) in row-major order."""
+    G = np.asarray(G)
+    return G.reshape(G.shape[0], -1)
+
+
 def n_blocks(n: int, B: int) -> int:
     """k = n_pad / B with n_pad the smallest multiple of B that is >= n."""
     return -(-n // B)

@@ -142,10 +142,27 @@ def moara_allocate_ranks(r_base: int, types: Sequence[int], donors: Sequence[int
     return list(out)
 
 
+def flatten_shape(shape) -> tuple:
+    """The matrix a weight tensor is treated as (Appendix B.1, flattened tensors): the
+    first axis stays, all remaining axes are flattened into the column axis, so a
+    contiguous s0 x s1 x ... tensor is the row-major s0 x (s1 * ...) matrix."""
+    shape = tuple(int(x) for x in shape)
+    if len(shape) < 2:
+        raise ValueError(f"a weight needs at least two axes, got shape {shape}")
+    n = 1
+    for x in shape[1:]:
+        n *= x
+    return shape[0], n
+
+
 def make_descs(shapes_modules) -> ctypes.Array:
-    """[(rows, cols, module[, rank_override[, side]]), ...] -> moara_matrix_desc array."""
+    """[(rows, cols, module[, rank_override[, side]]), ...] -> moara_matrix_desc array.
+    An entry may also start with a full tensor shape, ((s0, s1, ...), module[, ...]),
+    which is flattened by flatten_shape."""
     arr = (moara_matrix_desc * len(shapes_modules))()
     for i, t in enumerate(shapes_modules):
+        if isinstance(t[0], (tuple, list)):
+            t = (*flatten_shape(t[0]), *t[1:])
         arr[i].rows, arr[i].cols, arr[i].module = int(t[0]), int(t[1]), int(t[2])
         arr[i].rank_override = int(t[3]) if len(t) > 3 else 0
         arr[i].side = int(t[4]) if len(t) > 4 else MOARA_SIDE_AUTO
@@ -217,9 +234,11 @@ def _ptr_array(st: State, tensors, what: str, dtype_name: str, active):
                 continue
         if t is None:
             raise ValueError(f"{what}[{i}] is None for an active matrix")
-        if not t.is_cuda or t.dtype != tdt or not t.is_contiguous() or tuple(t.shape) != st.shapes[i]:
-            raise ValueError(f"{what}[{i}]: need a contiguous {dtype_name} CUDA tensor of shape {st.shapes[i]}, "
-                             f"got {tuple(t.shape)} {t.dtype} cuda={t.is_cuda} contiguous={t.is_contiguous()}")
+        if (not t.is_cuda or t.dtype != tdt or not t.is_contiguous() or t.dim() < 2
+                or flatten_shape(t.shape) != st.shapes[i]):
+            raise ValueError(f"{what}[{i}]: need a contiguous {dtype_name} CUDA tensor of shape {st.shapes[i]} "
+                             f"(or with that flattened shape), got {tuple(t.shape)} {t.dtype} cuda={t.is_cuda} "
+                             f"contiguous={t.is_contiguous()}")
         arr[i] = t.data_ptr()
     return arr
 

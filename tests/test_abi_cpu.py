@@ -163,3 +163,13 @@ def test_alignment_rejects_bad_arguments_before_any_gpu_work():
     out = (ctypes.c_double * 2)()
     assert L.moara_alignment(None, None, None, out, None) == M.MOARA_E_ARG
     assert b"state is NULL" in L.moara_last_error()
+
+
+def test_nd_shapes_flatten_into_descriptors():
+    assert M.flatten_shape((64, 8, 3, 3)) == (64, 72)
+    d = M.make_descs([((64, 8, 3, 3), 0), (32, 48, 1), ((10, 7), 2, 5)])
+    assert (d[0].rows, d[0].cols, d[0].module) == (64, 72, 0)
+    assert (d[1].rows, d[1].cols) == (32, 48)
+    assert (d[2].rows, d[2].cols, d[2].rank_override) == (10, 7, 5)
+    with pytest.raises(ValueError):
+        M.flatten_shape((5,))

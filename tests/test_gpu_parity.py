@@ -142,7 +142,7 @@ def test_llama300m_layer_fp32_operands():
     step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t))
 
 
-@pytest.mark.parametrize("B", [48, 20, 1, 256, 1000])
+@pytest.mark.parametrize("B", [1, 16, 32, 64, 128, 512, 1024, 48, 20, 256, 1000])   # the block sizes of Fig. 3, then odd ones
 def test_ragged_shapes_and_block_sizes(B):
     # several tiles in every dimension plus ragged tails; n % 4 != 0 forces scalar loads
     c = Case(shapes=[(300, 452, WL.Q), (452, 300, WL.GATE), (129, 1000, WL.DOWN), (77, 130, WL.K), (5, 3, WL.V)],
@@ -394,3 +394,26 @@ def test_alignment_full_rank_projector_is_one_and_needs_a_projector():
     M.moara_refresh_projector(st, Gd)
     S = M.moara_alignment(st, Gd)
     assert np.all(np.abs(S - 1.0) <= 1e-5), S
+
+
+def test_nd_weights_step_as_their_flattened_matrices():
+    """A weight with more than two axes is the matrix of its first axis by all others
+    (Appendix B.1): stepping N-d tensors gives bit for bit the result of the 2-D matrices."""
+    import torch
+    M = _M()
+    shapes_nd = [(64, 8, 3, 3), (96, 4, 10)]
+    c = Case(shapes=[(*M.flatten_shape(s), WL.Q) for s in shapes_nd], ranks=[16, 12], block_size=16)
+    Ws = _weights(c, 3)
+    outs = []
+    for nd in (False, True):
+        st = gpu_state(c, refresh_interval=2)
+        Wd = [to_dev(w, "f32") for w in Ws]
+        Wv = [w.view(s) for w, s in zip(Wd, shapes_nd)] if nd else Wd
+        for t in range(3):
+            Gd = [to_dev(_grad(c, 8, t, i), "f32") for i in range(2)]
+            Gv = [g.view(s) for g, s in zip(Gd, shapes_nd)] if nd else Gd
+            M.moara_step(st, Wv, Gv, lr=1e-3)
+        torch.cuda.synchronize()
+        outs.append([w.clone() for w in Wd])
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)

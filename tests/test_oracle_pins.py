@@ -456,3 +456,14 @@ def test_alignment_depends_on_the_subspace_only():
 def test_module_alignment_is_the_mean_per_type():
     got = O.module_alignment([(0, 0.2), (3, 1.0), (0, 0.4), (6, -0.5)])
     assert got == pytest.approx({0: 0.3, 3: 1.0, 6: -0.5})
+
+
+def test_flatten_keeps_axis_zero_and_blocks_run_over_the_flattened_columns():
+    # a 2 x 3 x 4 tensor is the 2 x 12 matrix of its rows; with B = 4 the blocks of
+    # row 0 are its three axis-1 slices (12 contiguous values split in runs of 4)
+    G = np.arange(24, dtype=np.float64).reshape(2, 3, 4) - 11.5
+    F = O.flatten(G)
+    assert F.shape == (2, 12)
+    np.testing.assert_array_equal(F[1], G[1].ravel())
+    M, _ = O.decompose(F, 4)
+    np.testing.assert_allclose(M[0], [np.linalg.norm(G[0, j]) for j in range(3)], rtol=1e-15)
