@@ -27,7 +27,7 @@ MOARA_SIDE_AUTO, MOARA_SIDE_LEFT, MOARA_SIDE_RIGHT = 0, 1, 2
 MOARA_F32, MOARA_BF16 = 0, 1
 MOARA_T_P, MOARA_T_EXP_AVG, MOARA_T_EXP_AVG_SQ, MOARA_T_MAG_AVG, MOARA_T_MAG_AVG_SQ, MOARA_T_STEP = range(6)
 MOARA_KERN_DECOMPOSE, MOARA_KERN_PROJECT, MOARA_KERN_BACKPROJ, MOARA_KERN_REFRESH, MOARA_KERN_ALIGN = range(5)
-MOARA_NUM_KERNELS = 4
+MOARA_NUM_KERNELS = 5
 
 EXPORTED = (
     "moara_default_config", "moara_allocate_ranks", "moara_resolve_matrix", "moara_state_bytes",
