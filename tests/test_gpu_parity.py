@@ -117,6 +117,15 @@ def test_llama300m_layers_bf16():
     step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t))
 
 
+@pytest.mark.parametrize("name", ["llama32_300m", "qwen25_350m", "deepseek_v2_350m"])
+def test_350m_model_family_layers(name):
+    # GQA key/value projections (256 x 1024, r = 128 and the full rank 256) and the
+    # DeepSeek-V2 MLA projections (q_a, q_b, kv_a, kv_b) at B = 32
+    wl = WL.subset(WL.WORKLOADS[name], [0, 23])
+    c = case_from_workload(wl)
+    step_parity(c, 2, grad_fn=lambda t, i: WL.grad_np(wl, i, t))
+
+
 def test_llama300m_layer_misaligned_caller_buffers():
     # W and G one element past a 16-byte boundary: no bf16 V workspace this step, the
     # projection and back-projection take the grouped fallback GEMM, which must read and

@@ -104,6 +104,25 @@ def _dense_layer(layer: int, d: int, ffn: int, kv: Optional[int] = None) -> List
     ]
 
 
+def _mla_layer(layer: int, d: int, ffn: int, heads: int, q_lora: int, kv_lora: int, nope: int, rope: int,
+               vdim: int) -> List[MatrixSpec]:
+    """DeepSeek-V2 Multi-head Latent Attention layer plus a dense MLP. Module types (a
+    reading: the paper assigns ranks per q/k/v/o type only): the query down/up projections
+    are q, the joint key-value down projection (latent plus the shared rope key) is k, the
+    key-value up projection is v, the output projection is o."""
+    p = f"layer{layer}."
+    return [
+        MatrixSpec(p + "q_a", Q, q_lora, d, layer),
+        MatrixSpec(p + "q_b", Q, heads * (nope + rope), q_lora, layer),
+        MatrixSpec(p + "kv_a", K, kv_lora + rope, d, layer),
+        MatrixSpec(p + "kv_b", V, heads * (nope + vdim), kv_lora, layer),
+        MatrixSpec(p + "o", O, d, heads * vdim, layer),
+        MatrixSpec(p + "gate", GATE, ffn, d, layer),
+        MatrixSpec(p + "up", UP, ffn, d, layer),
+        MatrixSpec(p + "down", DOWN, d, ffn, layer),
+    ]
+
+
 def _moe_layer(layer: int, d: int, eff: int, routed: int, shared: int) -> List[MatrixSpec]:
     p = f"layer{layer}."
     out = [MatrixSpec(p + n, t, d, d, layer) for n, t in (("q", Q), ("k", K), ("v", V), ("o", O))]
@@ -164,6 +183,24 @@ def build_workloads() -> dict:
         block_size=128, weight_dtype="bf16", operand_dtype="bf16",
         lowrank_rank=256, lowrank_power=0.8, noise_std=1e-4, steps=200, n_layers=28,
         moe_routed=64, moe_active=6)
+    # model-family comparison at 350M scale (Appendix D model table): d = 1024, 24 layers,
+    # 16 query heads of 64; GQA with 4 key-value heads; ranks of the Phase 3 rule at
+    # r_base = 256 (D = {q, k}, R = {down}, delta_r = 128); B = 32 as for Llama 2 350M
+    r350 = _ranks(q=128, k=128, v=256, o=256, gate=256, up=256, down=512)
+    for name, ffn, desc in (("llama32_300m", 2736, "Llama-3.2-300M-shaped GQA stack"),
+                            ("qwen25_350m", 2816, "Qwen2.5/Qwen3-350M-shaped GQA stack")):
+        w[name] = Workload(
+            name=name, description=f"{desc}: 24 layers d=1024, k/v 256x1024 (4 kv heads), ffn={ffn}, bf16 weights",
+            matrices=_stack(24, _dense_layer, 1024, ffn, 256), rank_table=r350,
+            block_size=32, weight_dtype="bf16", operand_dtype="bf16",
+            lowrank_rank=64, lowrank_power=1.0, noise_std=1e-4, steps=200, n_layers=24)
+    w["deepseek_v2_350m"] = Workload(
+        name="deepseek_v2_350m",
+        description="DeepSeek-V2-350M-shaped MLA stack: 24 layers d=1024, q_lora 768, kv_lora 256, "
+                    "head dims 64/32/64, 16 heads, dense ffn=2736, bf16 weights",
+        matrices=_stack(24, _mla_layer, 1024, 2736, 16, 768, 256, 64, 32, 64), rank_table=r350,
+        block_size=32, weight_dtype="bf16", operand_dtype="bf16",
+        lowrank_rank=64, lowrank_power=1.0, noise_std=1e-4, steps=200, n_layers=24)
     return w
 
 
