@@ -19,7 +19,7 @@
 // projection's reduction index runs along its rows (m x n for a RIGHT projection
 // V Q, transposed n x m for a LEFT one P^T V) and stored in the blocked K-panel
 // layout of the large-tile GEMM (kp_index). The transposed form comes from
-// k_decompose_vt, which stages a 64-row x 256-column slab in LDS.
+// k_decompose_vt, which stages a 32-row x 256-column slab in LDS.
 #include "common.h"
 
 namespace {
@@ -183,16 +183,24 @@ __global__ __launch_bounds__(256) void k_decompose(const MatDev* __restrict__ ma
   }
 }
 
-// Transposed-V variant (LEFT projections): one workgroup per 64 rows. For each
-// 256-column slab every wave loads 16 of the rows (float4 per lane, 16 loads in
+// Transposed-V variant (LEFT projections): one workgroup per VT_ROWS (32) rows. For each
+// 256-column slab every wave loads VT_RPW of the rows (float4 per lane, all in
 // flight), reduces the block sums, writes V in bf16 into an LDS slab
-// T[64][256] (row-major, conflict-free 4-byte stores) and records the sums; the
-// slab is then written out transposed, 8 lanes per output row (16 bytes each),
-// i.e. 128-byte segments of Vt. The odd 4-byte pitch of T keeps the 8 row groups
-// read by one instruction on distinct banks. Optimizer_M then runs over the
-// 64 x k sums as in k_decompose. Preconditions (checked by the host): B a power
-// of two in [4, 256], n % 4 == 0, m % 8 == 0, k <= DEC_VT_MAX_K, G 16-byte aligned.
-constexpr int VT_ROWS = 64, VT_COLS = 256, VT_PITCH = VT_COLS + 2;   // bf16 elements
+// T[VT_ROWS][256] (row-major, conflict-free 4-byte stores) and records the sums; the
+// slab is then written out transposed, VT_ROWS / 8 lanes per output column (16 bytes
+// each), i.e. 64-byte (one K panel) segments of Vt. The odd 4-byte pitch of T keeps the
+// row groups read by one instruction on distinct banks. Optimizer_M then runs over the
+// VT_ROWS x k sums as in k_decompose. 32-row slabs (143 VGPRs, three waves per SIMD)
+// measured 1.7 % faster than 64-row ones (231 VGPRs, two). Preconditions (checked by
+// the host): B a power of two in [4, 256], n % 4 == 0, m % 32 == 0, k <= DEC_VT_MAX_K,
+// G 16-byte aligned.
+#ifndef DEC_VT_ROWS
+#define DEC_VT_ROWS 32
+#endif
+constexpr int VT_ROWS = DEC_VT_ROWS, VT_COLS = 256, VT_PITCH = VT_COLS + 2;   // bf16 elements
+constexpr int VT_RPW = VT_ROWS / 4;    // rows per wave
+constexpr int VT_GRP = VT_ROWS / 8;    // 8-row groups of a column (16-byte output runs)
+static_assert(VT_ROWS % 32 == 0, "whole 32-row K panels of the blocked output");
 
 __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__ mats, StepParams p, int adam_m) {
   __shared__ float sums[VT_ROWS * DEC_VT_MAX_K];
@@ -205,22 +213,22 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int B = p.B, gl = B >> 2, k = d.k, lgB = __builtin_ctz(B);
   const int64_t n = d.n, m = d.m;
-  // the slab loop is software-pipelined: the 16 loads of the next slab are issued
+  // the slab loop is software-pipelined: the VT_RPW loads of the next slab are issued
   // before the current slab is reduced, transposed and written out
-  float4 va[16], vb[16];
-  auto load = [&](int64_t c0, float4 (&v)[16]) {
+  float4 va[VT_RPW], vb[VT_RPW];
+  auto load = [&](int64_t c0, float4 (&v)[VT_RPW]) {
     const int64_t c = c0 + 4 * lane;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < VT_RPW; ++i) {
       const int rr = wave + 4 * i;
       v[i] = (rr < rows && c < n) ? *reinterpret_cast<const float4*>(d.G + (row0 + rr) * n + c)
                                   : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   };
-  auto process = [&](int64_t c0, const float4 (&v)[16]) {
+  auto process = [&](int64_t c0, const float4 (&v)[VT_RPW]) {
     const int64_t c = c0 + 4 * lane;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) {
+    for (int i = 0; i < VT_RPW; ++i) {
       const int rr = wave + 4 * i;
       float ss = v[i].x * v[i].x + v[i].y * v[i].y + v[i].z * v[i].z + v[i].w * v[i].w;
       ss = group_sum(ss, gl);
@@ -234,9 +242,9 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
     }
     __syncthreads();
 #pragma unroll 2
-    for (int it = 0; it < 8; ++it) {
+    for (int it = 0; it < VT_GRP; ++it) {
       const int q = it * 256 + (int)threadIdx.x;
-      const int cl = q >> 3, g = q & 7;
+      const int cl = q / VT_GRP, g = q % VT_GRP;
       const int64_t col = c0 + cl;
       if (col < n && 8 * g < rows) {
         bf16x8 o;
