@@ -35,22 +35,28 @@ import torch
 
 from . import moara as M
 
-# module ids of the usual Llama / Qwen / DeepSeek parameter names (last two name parts)
+# module ids of the usual Llama / Qwen / DeepSeek parameter names (last two name parts);
+# MLP projections inside an MoE expert ("...experts.3.gate_proj.weight",
+# "...shared_experts.up_proj.weight") take the expert types
 _MODULE_OF = {
     "q_proj": M.MOARA_Q, "k_proj": M.MOARA_K, "v_proj": M.MOARA_V, "o_proj": M.MOARA_O,
     "gate_proj": M.MOARA_GATE, "up_proj": M.MOARA_UP, "down_proj": M.MOARA_DOWN,
 }
+_EXPERT_OF = {M.MOARA_GATE: M.MOARA_EXP_GATE, M.MOARA_UP: M.MOARA_EXP_UP, M.MOARA_DOWN: M.MOARA_EXP_DOWN}
 
 
 def moara_targets(model: torch.nn.Module) -> Tuple[List[Tuple[torch.nn.Parameter, int]], List[torch.nn.Parameter]]:
     """Split a model's trainable parameters into MoARa targets, (weight, module id) for the
-    q/k/v/o/gate/up/down projection weights (`*.q_proj.weight` and so on), and the rest."""
+    q/k/v/o/gate/up/down projection weights (`*.q_proj.weight` and so on; expert types for
+    MLP projections under a module path containing "expert"), and the rest."""
     targets, others = [], []
     for name, p in model.named_parameters():
         if not p.requires_grad:
             continue
         parts = name.split(".")
         mod = _MODULE_OF.get(parts[-2]) if len(parts) >= 2 and parts[-1] == "weight" and p.dim() >= 2 else None
+        if mod is not None and any("expert" in q for q in parts[:-2]):
+            mod = _EXPERT_OF.get(mod, mod)
         if mod is None:
             others.append(p)
         else:
@@ -114,11 +120,14 @@ class MoARa(torch.optim.Optimizer):
         """The library state (created at the first step), e.g. for moara_alignment."""
         return self._st
 
-    def _grads(self) -> List[torch.Tensor]:
+    def _grads(self) -> List[Optional[torch.Tensor]]:
+        """fp32 contiguous gradients of the targets; None where a target has no gradient
+        (e.g. a routed expert no token reached this step: it is skipped, its state kept)."""
         out = []
         for i, p in enumerate(self.param_groups[0]["params"]):
             if p.grad is None:
-                raise RuntimeError(f"target weight {i} has no gradient")
+                out.append(None)
+                continue
             g = p.grad
             if g.dtype != torch.float32 or not g.is_contiguous():
                 if self._g32[i] is None:
@@ -137,7 +146,11 @@ class MoARa(torch.optim.Optimizer):
         tg = self.param_groups[0]
         if self._st is None:
             self._st = M.moara_create_state(self._cfg, self._descs)
-        M.moara_step(self._st, list(tg["params"]), self._grads(), lr=float(tg["lr"]))
+        grads = self._grads()
+        active = [g is not None for g in grads]
+        if any(active):
+            M.moara_step(self._st, list(tg["params"]), grads, lr=float(tg["lr"]),
+                         active=None if all(active) else active)
         if self._adamw is not None:
             og = self.param_groups[1]
             for g in self._adamw.param_groups:   # the schedule drives both groups

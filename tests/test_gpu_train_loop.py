@@ -81,3 +81,44 @@ def test_other_parameters_follow_adamw_and_state_dict_round_trips():
         o.zero_grad()
     for (n1, p1), (n2, p2) in zip(model.named_parameters(), model2.named_parameters()):
         assert torch.equal(p1.detach(), p2.detach()), n1
+
+
+def test_experts_without_gradient_are_skipped():
+    """Routed experts that no token reached have no gradient: their weights, moments and
+    step counters stay as they were (the library's skip rule), the others step."""
+    from paper_2609_15037_amd import moara as M
+    from paper_2609_15037_amd.optim import MoARa, moara_targets
+
+    class Expert(torch.nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.up_proj = torch.nn.Linear(64, 96, bias=False)
+            self.down_proj = torch.nn.Linear(96, 64, bias=False)
+
+        def forward(self, x):
+            return self.down_proj(torch.relu(self.up_proj(x)))
+
+    class Moe(torch.nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.experts = torch.nn.ModuleList([Expert() for _ in range(4)])
+
+    torch.manual_seed(4)
+    moe = Moe().cuda()
+    experts = moe.experts
+    targets, others = moara_targets(moe)
+    assert [m for _, m in targets[:2]] == [M.MOARA_EXP_UP, M.MOARA_EXP_DOWN]
+    ranks = [0] * 10
+    ranks[M.MOARA_EXP_UP] = ranks[M.MOARA_EXP_DOWN] = 16
+    opt = MoARa(targets, others, lr=1e-2, rank_table=ranks, block_size=32, refresh_interval=10)
+    x = torch.randn(32, 64, device="cuda")
+    before = [p.detach().clone() for p, _ in targets]
+    for _ in range(2):
+        loss = experts[0](x).square().mean() + experts[2](x).square().mean()   # experts 1 and 3 unused
+        loss.backward()
+        opt.step()
+        opt.zero_grad()
+    for i, (p, _) in enumerate(targets):
+        used = i // 2 in (0, 2)
+        assert torch.equal(p.detach(), before[i]) != used, i
+        assert M.moara_get_tensor(opt.moara_state, i, M.MOARA_T_STEP) == (2 if used else 0)

@@ -42,3 +42,21 @@ def test_targets_are_the_projection_weights():
                                              (net.attn.o_proj.weight.shape, M.MOARA_O),
                                              (net.down_proj.weight.shape, M.MOARA_DOWN)]
     assert len(o) == 4   # embedding, o_proj bias, norm weight and bias
+
+
+def test_expert_projections_take_the_expert_types():
+    class Expert(torch.nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.gate_proj = torch.nn.Linear(8, 12, bias=False)
+            self.down_proj = torch.nn.Linear(12, 8, bias=False)
+
+    class Moe(torch.nn.Module):
+        def __init__(self):
+            super().__init__()
+            self.experts = torch.nn.ModuleList([Expert(), Expert()])
+            self.up_proj = torch.nn.Linear(8, 12, bias=False)   # a dense MLP projection
+
+    t, _ = moara_targets(Moe())
+    assert [m for _, m in t] == [M.MOARA_EXP_GATE, M.MOARA_EXP_DOWN, M.MOARA_EXP_GATE, M.MOARA_EXP_DOWN,
+                                 M.MOARA_UP]
