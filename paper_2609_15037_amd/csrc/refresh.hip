@@ -173,7 +173,7 @@ constexpr double JAC_TOL = 1e-10;
 // LDS: two 64 x 65 fp64 regions. Region A holds the pair's Gram G during the inner
 // solve; during the column passes it holds the current 32-row chunk of the 64 columns
 // (rows 0-31) and, in the rotation pass, the rotated chunk (rows 32-63). Region B holds
-// the rotation J (and the convergence reduction's scratch before J is built). 66.5 KB,
+// the rotation J (and the convergence reduction's scratch before J is built). 67 KB,
 // so two workgroups share a CU and one's LDS-bound inner solve overlaps the other's
 // MFMA / memory phases.
 constexpr int JR = 32;   // rows per column chunk
@@ -198,6 +198,7 @@ __device__ __forceinline__ uint32_t jac_gram_tiles(int wave) {
 __global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restrict__ ds, int n, int round, int sweep) {
   __shared__ double Am[PW][PW + 1];
   __shared__ double Jm[PW][PW + 1];
+  __shared__ double CS[PW / 2][2];   // the round's rotations (cosine, sine) of the inner solve
   double (*Gm)[PW + 1] = Am;         // inner solve
   double (*T)[PW + 1] = Am;          // column chunk (rows 0 .. JR-1)
   double (*O)[PW + 1] = Am + JR;     // rotated chunk (rows JR .. 2 JR-1)
@@ -325,35 +326,41 @@ __global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restric
 
   // (2) JAC_INNER_SWEEPS sweeps of parallel cyclic Jacobi on the 64 x 64 Gram, in place.
   // One round rotates 32 disjoint pairs (circle method) on both sides at once,
-  // G' = R^T G R: lane l computes the rotation of pair beta = l % 32 from the current
-  // G; after a barrier (every rotation read before any entry changes) it fetches the
-  // rotations of its row pairs alpha from lanes alpha by shuffles and rewrites
-  // 16 / JAC_WAVES 2 x 2 blocks of G, which no other lane touches, and applies rotation
-  // beta to 32 / JAC_WAVES rows of the accumulated J.
+  // G' = R^T G R: lanes 0-31 of wave 0 compute the 32 rotations from the current G into
+  // CS (once per round, not redundantly in every wave: the fp64 square roots and
+  // divisions were 40 % of a round); after a barrier (every rotation computed from G
+  // before any entry changes) each lane reads rotation beta = l % 32 and the rotations
+  // of its row pairs alpha from CS, rewrites 16 / JAC_WAVES 2 x 2 blocks of G, which no
+  // other lane touches, and applies rotation beta to 32 / JAC_WAVES rows of the
+  // accumulated J. The barrier closing the round orders these writes before the next
+  // round's reads of G and CS.
   {
     const int beta = lane & 31, half = lane >> 5;
     for (int isw = 0; isw < JAC_INNER_SWEEPS; ++isw) {
       for (int rr = 0; rr < PW - 1; ++rr) {
         int pb = circle(beta, rr, PW), qb = circle(PW - 1 - beta, rr, PW);
         if (pb > qb) { const int tmp = pb; pb = qb; qb = tmp; }
-        double cb = 1.0, sb = 0.0;
-        {
+        if (tid < 32) {
+          double c = 1.0, sn = 0.0;
           const double app = Gm[pb][pb], aqq = Gm[qb][qb], apq = Gm[pb][qb];
           const double den = sqrt(app * aqq);
           if (den > 0.0 && fabs(apq) > 1e-16 * den) {
             const double zeta = (aqq - app) / (2.0 * apq);
             const double tt = (zeta >= 0.0 ? 1.0 : -1.0) / (fabs(zeta) + sqrt(1.0 + zeta * zeta));
-            cb = 1.0 / sqrt(1.0 + tt * tt);
-            sb = cb * tt;
+            c = 1.0 / sqrt(1.0 + tt * tt);
+            sn = c * tt;
           }
+          CS[tid][0] = c;
+          CS[tid][1] = sn;
         }
         __syncthreads();
+        const double cb = CS[beta][0], sb = CS[beta][1];
 #pragma unroll
         for (int i = 0; i < 16 / JAC_WAVES; ++i) {
           const int alpha = 2 * (16 / JAC_WAVES * wave + i) + half;
           int pa = circle(alpha, rr, PW), qa = circle(PW - 1 - alpha, rr, PW);
           if (pa > qa) { const int tmp = pa; pa = qa; qa = tmp; }
-          const double ca = __shfl(cb, alpha, 64), sa = __shfl(sb, alpha, 64);
+          const double ca = CS[alpha][0], sa = CS[alpha][1];
           const double g_pp = Gm[pa][pb], g_pq = Gm[pa][qb], g_qp = Gm[qa][pb], g_qq = Gm[qa][qb];
           const double r_pp = ca * g_pp - sa * g_qp, r_pq = ca * g_pq - sa * g_qq;   // rows
           const double r_qp = sa * g_pp + ca * g_qp, r_qq = sa * g_pq + ca * g_qq;
