@@ -388,6 +388,11 @@ __global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restric
   // column-contiguous.
   constexpr int NH = 8 / JAC_WAVES;   // 16-row halves per wave
   const int cbk = wave & 3, h0 = wave >> 2;
+  // J is fixed for the whole pass: each wave keeps its 64 x 16 column slice of it as
+  // MFMA B fragments in registers, so only the chunk operand is read from LDS
+  double jf[PW / 4];
+#pragma unroll
+  for (int ks = 0; ks < PW / 4; ++ks) jf[ks] = Jm[4 * ks + (lane >> 4)][16 * cbk + (lane & 15)];
   auto rotate = [&]() {
     f64x4 o[NH];
 #pragma unroll
@@ -395,10 +400,9 @@ __global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restric
 #pragma unroll
     for (int ks = 0; ks < PW / 4; ++ks) {
       const int y = 4 * ks + (lane >> 4);
-      const double jv = Jm[y][16 * cbk + (lane & 15)];
 #pragma unroll
       for (int h = 0; h < NH; ++h)
-        o[h] = __builtin_amdgcn_mfma_f64_16x16x4f64(T[16 * (h0 + h) + (lane & 15)][y], jv, o[h], 0, 0, 0);
+        o[h] = __builtin_amdgcn_mfma_f64_16x16x4f64(T[16 * (h0 + h) + (lane & 15)][y], jf[ks], o[h], 0, 0, 0);
     }
 #pragma unroll
     for (int h = 0; h < NH; ++h)
