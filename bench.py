@@ -142,7 +142,7 @@ def refresh_cost(wl, p_over: int, q: int, bf16_early: bool):
 
     Per matrix (s = min(m, n), L = max(m, n), w = r + p columns): q iterations of Y = X Z,
     Z2 = X^T Y (4 L s w flops each; the first q - 3 on bf16 MFMA when the operands are bf16,
-    taken here for every matrix), q + 2 CholeskyQRs (q + 1 of an s x w iterate, one of the
+    taken here for every matrix), q + 1 CholeskyQRs (q of an s x w iterate, one of the
     L x w one): the symmetric fp64 Gram (rows w^2), the fp64 Cholesky and triangular inverse
     (w^3 / 3 each) and the triangular fp32 product Z R^-1 (rows w^2), and the Ritz vectors
     Q B (2 s w r, fp32). The Jacobi sweeps of the Rayleigh-Ritz step are iterative and left
@@ -156,8 +156,8 @@ def refresh_cost(wl, p_over: int, q: int, bf16_early: bool):
         it = 4.0 * L * s * w
         f16 += n16 * it
         f32 += (q - n16) * it
-        rows = (q + 1) * s + L                     # rows of the q + 2 orthonormalised iterates
-        f64 += rows * w * w + (q + 2) * 2.0 * w ** 3 / 3.0
+        rows = q * s + L                           # rows of the q + 1 orthonormalised iterates
+        f64 += rows * w * w + (q + 1) * 2.0 * w ** 3 / 3.0
         f32 += rows * w * w + 2.0 * s * w * r
     t = f16 / PEAK_BF16 + f32 / PEAK_F32 + f64 / PEAK_F64
     return {"bf16_flops": f16, "f32_flops": f32, "f64_flops": f64, "roofline_ms": t * 1e3}
@@ -203,8 +203,8 @@ def cpu_baseline(wl, layers: int):
 def main():
     a = parse()
     if a.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU; --gpus must be 1 "
-                                   "(the multi-GPU sharding is a design, not part of this build)"}))
+        print(json.dumps({"error": "the MoARa library runs on exactly one GPU; --gpus must be 1 "
+                                   "(sharding over several GPUs is designed but not implemented)"}))
         return 2
     import torch
     import workloads as WL

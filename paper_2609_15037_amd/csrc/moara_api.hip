@@ -531,7 +531,10 @@ int ensure_ref_ws(moara_state* st, size_t bytes) {
 constexpr int MAX_SWEEPS = 14;
 
 // One refresh pass over a chunk of matrices. Buffer roles are fixed:
-//   Z2 <- Gaussian ; Z <- orth(Z2)
+//   Z <- Gaussian (used as it is when w <= s / 2 for every matrix of the state: such a
+//        block has condition number below 6, and orthonormalising it would not change
+//        the subspace the iteration sees; wider blocks go through Z2 <- Gaussian,
+//        Z <- orth(Z2) first)
 //   repeat: Y <- X Z ; Z2 <- X^T Y ; Z <- orth(Z2)        (q - 1 times)
 //   last  : Y <- X Z ; Y2 <- orth(Y) ; Z2 <- X^T Y2 ; Jacobi on Z2 ; P <- top r
 // usev (indexed by matrix, may be null): the bf16 V of that matrix was written by this
@@ -585,6 +588,14 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   const int kind = KIND_F32;
   const GemmUniform u = make_uniform(st, 0.f);
 
+  // the Gaussian start is orthonormalised only if some block of the state is wider than
+  // s / 2 (decided over the whole state, so a matrix's refresh does not depend on how the
+  // matrices are split into chunks or which of them are active)
+  bool orth0 = false;
+  for (int i = 0; i < st->n; ++i) {
+    const MatHost& h = st->mats[i];
+    orth0 = orth0 || 2 * (int64_t)subspace_width(c, h.s, h.r) > h.s;
+  }
   std::vector<RefDev> rd(nm);
   uint32_t tg = 0, tj = 0, tc = 0, tnorm = 0;
   int nb_max = 2;
@@ -595,7 +606,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     d.s = x.s; d.L = x.L; d.w = x.w; d.wpad = x.wpad; d.r = h.r;
     d.operand_bf16 = c.operand_dtype == MOARA_BF16;
     d.seed = c.refresh_seed * 0x9E3779B97F4A7C15ull + (uint64_t)(x.idx + 1) * 0xD1B54A32D192ED03ull;
-    d.Z = x.Z2; d.C = x.C; d.X = x.X; d.cmax = x.cmax; d.Rinv = x.Rinv; d.Zc = x.Zc;
+    d.Z = x.Z2; d.Z0 = orth0 ? x.Z2 : x.Z; d.C = x.C; d.X = x.X; d.cmax = x.cmax; d.Rinv = x.Rinv; d.Zc = x.Zc;
     d.jl = x.w; d.Q = x.Z; d.Pw = x.Pw; d.Bt = x.Bt;
     d.P32 = h.P32; d.Pop = h.Pop; d.Ptop = h.Ptop; d.kp = h.kp ? 1 : 0;
     d.off = x.off; d.order = x.order; d.norms = x.norms;
@@ -823,7 +834,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   // blocks below the diagonal of Rinv are never written by the factorisation kernels
   for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.Rinv, 0, 4 * (size_t)x.w * x.w, stream));
   HIP_TRY(launch_gauss(RD, nm, tg, stream));
-  HIP_TRY(orth_Z());
+  if (orth0) HIP_TRY(orth_Z());
   const int q_iters = c.refresh_iters;
   const int q_bf = q_iters > REFRESH_F32_ITERS ? q_iters - REFRESH_F32_ITERS : 0;
   if (!nY.empty() && q_bf > 0) HIP_TRY(launch_transpose((const TransProb*)D(19), (int)tX.size(), ttx, stream));

@@ -12,6 +12,7 @@ struct RefDev {
   int32_t operand_bf16;
   uint64_t seed;      // Philox key for the Gaussian start block
   float* Z;           // s x w fp32 (iterate, row-major)
+  float* Z0;          // s x w fp32: where the Gaussian start block goes (Z, or Z2 when it is orthonormalised first)
   double* C;          // w x w fp64 Gram, factorised in place into R (upper)
   double* X;          // w x w fp64 R^{-1} (upper)
   double* cmax;       // max diagonal of the Gram (pivot floor), one value

@@ -1,7 +1,8 @@
 // Projector refresh kernels: P <- TruncatedSVD(V, r) (Algorithm 1).
 //
 // Method (randomised subspace iteration with Rayleigh-Ritz, all on the device):
-//   Z0 = seeded Gaussian s x w block (w = r + p), Z = orth(Z0)
+//   Z = seeded Gaussian s x w block (w = r + p; for w <= s / 2 its condition number
+//       stays below 6 and it is used as it is, else Z = orth(Gaussian))
 //   repeat q times:  Y = X Z;  Zn = X^T Y;  Z = orth(Zn)      (last time: Y = orth(Y) first)
 //   Rayleigh-Ritz:   one-sided Jacobi on Zn = X^T Y (fp64) orthogonalises its columns
 //                    into (right singular vectors of X) x (singular values); the r
@@ -51,7 +52,7 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
   const float r0 = sqrtf(-2.0f * logf(u01(c[0]))), r1 = sqrtf(-2.0f * logf(u01(c[2])));
   const float a0 = 6.283185307179586f * u01(c[1]), a1 = 6.283185307179586f * u01(c[3]);
   float v[4] = {r0 * cosf(a0), r0 * sinf(a0), r1 * cosf(a1), r1 * sinf(a1)};
-  for (int q = 0; q < 4 && e0 + q < total; ++q) d.Z[e0 + q] = v[q];
+  for (int q = 0; q < 4 && e0 + q < total; ++q) d.Z0[e0 + q] = v[q];
 }
 
 // ------------------------------------------------------------------ fp64 Gram C = A^T A
