@@ -1,9 +1,9 @@
 // Blocked Cholesky factorisation and triangular inverse of the fp64 Gram
 // matrices of a refresh batch (CholeskyQR: Z = Q R with R^T R = Z^T Z, then
 // Q = Z R^{-1}). 64 x 64 blocks; every launch covers all matrices of the batch:
-//   for each panel k:  diag(k)   factor C_kk = R_kk^T R_kk and invert R_kk (one WG per matrix)
-//                      panel(k)  R_kj = R_kk^{-T} C_kj for j > k           (one WG per block)
-//                      update(k) C_ac -= R_ka^T R_kc for k < a <= c        (one WG per block)
+//   for each block row k:  row(k)    C_kc -= sum_{j<k} R_jk^T R_jc for c >= k  (one WG per block, k >= 1)
+//                          diag(k)   factor C_kk = R_kk^T R_kk and invert R_kk (one WG per matrix)
+//                          panel(k)  R_kc = R_kk^{-T} C_kc for c > k           (one WG per block)
 //   then X = R^{-1} by recursive doubling over the blocks (k_trtri).
 // Pivots not above 1e-13 * max(diag C) are raised to that floor so rank-deficient
 // iterates stay finite; an all-zero Gram gives R = I.
@@ -170,47 +170,73 @@ __global__ __launch_bounds__(256, 4) void k_chol_panel(const RefDev* __restrict_
     }
 }
 
-__global__ __launch_bounds__(256, 4) void k_chol_update(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
-                                                        int n, int k) {
+// Left-looking update of block row k before its factorisation (k >= 1):
+//   C_kc -= sum_{j < k} R_jk^T R_jc     for every block column c >= k
+// One workgroup per (matrix, c); its K loop runs over the factored block rows j < k,
+// with the next pair of blocks loaded into registers while the current one is
+// multiplied (R_jc from LDS, R_jk's 16 columns of each wave straight into its MFMA
+// operand registers: A[i][t] = R_jk[t][16 w + i]). Every block of C is read and written
+// once here, where a right-looking update would rewrite the trailing matrix after every
+// panel; the factored rows R_j. are shared by all workgroups of a matrix (L2 hits).
+__global__ __launch_bounds__(256, 2) void k_chol_row(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
+                                                     int n, int k) {
   const uint32_t t = blockIdx.x;
   const int mi = find_pref(pref, n, t);
   const RefDev& d = ds[mi];
   const int w = d.w;
-  const int T = nblk(w) - k - 1;
-  int rem = (int)(t - pref[mi]), ta = 0;
-  while (rem >= T - ta) { rem -= T - ta; ++ta; }
-  const int a = k + 1 + ta, c = a + rem;
-  // R_kc is shared by the four waves through LDS; each wave's 16 columns of R_ka go
-  // straight from memory into its MFMA operand registers (A[i][t] = R_ka[t][16 w + i]),
-  // so a workgroup needs 33 KB of LDS and four fit on a CU.
-  __shared__ double Rc[NB][LDB];
+  const int c = k + (int)(t - pref[mi]);
+  __shared__ double Rb[NB][LDB];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  double av[NB / 4];
-  {
-    const int col = a * NB + 16 * wave + (lane & 15);
+  double av[NB / 4], an[NB / 4], pb[16];
+  auto fetch = [&](int j, double (&a)[NB / 4]) {
+    const int col = k * NB + 16 * wave + (lane & 15);
 #pragma unroll
     for (int ks = 0; ks < NB / 4; ++ks) {
-      const int row = k * NB + 4 * ks + (lane >> 4);
-      av[ks] = (row < w && col < w) ? d.C[(int64_t)row * w + col] : 0.0;
+      const int row = j * NB + 4 * ks + (lane >> 4);
+      a[ks] = (row < w && col < w) ? d.C[(int64_t)row * w + col] : 0.0;
     }
-  }
-  load_blk(Rc, d.C, w, k, c);
-  __syncthreads();
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int e = threadIdx.x + 256 * q, i = e >> 6, jj = e & 63;
+      const int row = j * NB + i, col2 = c * NB + jj;
+      pb[q] = (row < w && col2 < w) ? d.C[(int64_t)row * w + col2] : 0.0;
+    }
+  };
+  auto publish = [&]() {
+#pragma unroll
+    for (int q = 0; q < 16; ++q) {
+      const int e = threadIdx.x + 256 * q;
+      Rb[e >> 6][e & 63] = pb[q];
+    }
+  };
   f64x4 acc[4];
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt) acc[jt] = f64x4{0.0, 0.0, 0.0, 0.0};
+  fetch(0, av);
+  publish();
+  __syncthreads();
+  for (int j = 0; j < k; ++j) {
+    if (j + 1 < k) fetch(j + 1, an);
 #pragma unroll
-  for (int ks = 0; ks < NB / 4; ++ks) {
-    const int tr = 4 * ks + (lane >> 4);
+    for (int ks = 0; ks < NB / 4; ++ks) {
+      const int tr = 4 * ks + (lane >> 4);
 #pragma unroll
-    for (int jt = 0; jt < 4; ++jt)
-      acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[ks], Rc[tr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);   // R_ka^T R_kc
+      for (int jt = 0; jt < 4; ++jt)
+        acc[jt] = __builtin_amdgcn_mfma_f64_16x16x4f64(av[ks], Rb[tr][16 * jt + (lane & 15)], acc[jt], 0, 0, 0);
+    }
+    __syncthreads();
+    if (j + 1 < k) {
+      publish();
+#pragma unroll
+      for (int ks = 0; ks < NB / 4; ++ks) av[ks] = an[ks];
+      __syncthreads();
+    }
   }
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = a * NB + mfma_row(r), col = c * NB + mfma_col(jt);
+      const int row = k * NB + mfma_row(r), col = c * NB + mfma_col(jt);
       if (row < w && col < w) d.C[(int64_t)row * w + col] -= acc[jt][r];
     }
 }
@@ -322,9 +348,9 @@ hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint3
   hipLaunchKernelGGL(k_chol_panel, dim3(total), dim3(256), 0, st, d, pref, n, k);
   return hipGetLastError();
 }
-hipError_t launch_chol_update(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st) {
-  if (!total) return hipSuccess;
-  hipLaunchKernelGGL(k_chol_update, dim3(total), dim3(256), 0, st, d, pref, n, k);
+hipError_t launch_chol_row(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st) {
+  if (!total || k < 1) return hipSuccess;
+  hipLaunchKernelGGL(k_chol_row, dim3(total), dim3(256), 0, st, d, pref, n, k);
   return hipGetLastError();
 }
 int trtri_levels(int32_t nbmax) { int l = 0; while ((1 << l) < nbmax) ++l; return l; }

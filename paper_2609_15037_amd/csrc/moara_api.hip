@@ -689,7 +689,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       const int nb = chol_blocks(rm[q].w);
       const int T = std::max(0, nb - k - 1);
       pan_pref[(size_t)k * nm + q] = tp; tp += (uint32_t)T;
-      upd_pref[(size_t)k * nm + q] = tu; tu += (uint32_t)(T * (T + 1) / 2);
+      upd_pref[(size_t)k * nm + q] = tu; tu += (uint32_t)(k >= 1 && k < nb ? nb - k : 0);   // row(k): c = k .. nb-1
     }
     pan_tot[k] = tp; upd_tot[k] = tu;
   }
@@ -815,9 +815,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   auto chol_inv = [&]() -> hipError_t {      // C -> R (in place), X = R^{-1}, Rinv = fp32(X)
     hipError_t e = hipSuccess;
     for (int k = 0; k < nbmax && e == hipSuccess; ++k) {
-      e = launch_chol_diag(RD, nm, k, stream);
+      e = launch_chol_row(RD, UPD + (size_t)k * nm, nm, upd_tot[k], k, stream);
+      if (e == hipSuccess) e = launch_chol_diag(RD, nm, k, stream);
       if (e == hipSuccess) e = launch_chol_panel(RD, PAN + (size_t)k * nm, nm, pan_tot[k], k, stream);
-      if (e == hipSuccess) e = launch_chol_update(RD, UPD + (size_t)k * nm, nm, upd_tot[k], k, stream);
     }
     for (int l = 1; l <= nlev && e == hipSuccess; ++l)
       for (int ph = 0; ph < 2 && e == hipSuccess; ++ph)
