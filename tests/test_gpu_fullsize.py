@@ -3,6 +3,7 @@
 * The 7B stack runs all 224 matrices in one state, so every launch has exactly
   the configuration bench.py times; the oracle checks one layer of it (all seven
   matrices, element by element).
+* One Llama-2-7B layer's seven projectors after a refresh, by principal angles.
 * One Qwen2-7B layer (GQA k/v 512 x 3584, MLP 18944 x 3584) is checked element by
   element, and its attention projectors after a refresh by principal angles.
 * One DeepSeek-MoE layer with routed experts: 6 of 64 experts active per step,
@@ -107,6 +108,33 @@ def sampled_stack_parity(wl: WL.Workload, sample_layer: int, steps: int):
 
 def test_llama2_7b_stack_one_layer_checked():
     sampled_stack_parity(WL.WORKLOADS["llama2_7b"], sample_layer=31, steps=2)
+
+
+def test_llama2_7b_layer_refresh():
+    """All seven matrices of a Llama-2-7B layer (4096 x 4096 at r = 512 / 1024, the MLP
+    11008 x 4096 and 4096 x 11008 at r = 768; subspace width w = 2r) refreshed in one
+    call, at the full q = 20 and p = r: projectors orthonormal and within 1e-3 rad of the
+    oracle's truncated SVD of V. The oracle checks q, v, gate and down (k, o and up have
+    the shapes and ranks of q, v and gate)."""
+    import torch
+    M = _M()
+    wl = WL.subset(WL.WORKLOADS["llama2_7b"], [0])
+    c = case_from_workload(wl)
+    st = gpu_state(c)
+    Gs = [WL.grad_np(wl, i, 0) for i in range(len(wl.matrices))]
+    print("[fullsize] llama2_7b layer 0 refresh", flush=True)
+    M.moara_refresh_projector(st, [to_dev(g, "f32") for g in Gs])
+    torch.cuda.synchronize()
+    for i, G in enumerate(Gs):
+        if wl.matrices[i].module not in (WL.Q, WL.V, WL.GATE, WL.DOWN):
+            continue
+        Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+        _, V = O.decompose(G, c.block_size)
+        ref = O.truncated_svd(V, c.ranks[i], O.projection_side(*G.shape))
+        np.testing.assert_allclose(Pg.T @ Pg, np.eye(Pg.shape[1]), atol=2e-5)
+        ang = O.max_principal_angle(Pg, ref)
+        print(f"[fullsize] {wl.matrices[i].name} {G.shape} r={c.ranks[i]}: principal angle {ang:.2e}", flush=True)
+        assert ang <= 1e-3
 
 
 def test_qwen2_7b_layer():
