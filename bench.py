@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--operand", default=None, help="GEMM operand dtype override: bf16 | f32")
     ap.add_argument("--refresh-reps", type=int, default=3, help="refreshes timed; the median is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-layers", type=int, default=1)
+    ap.add_argument("--cpu-sample-layers", type=int, default=2)
     ap.add_argument("--layers", type=int, default=None, help="use only the first N layers (profiling runs)")
     ap.add_argument("--refresh-iters", type=int, default=None,
                     help="override the subspace-iteration count (the default is the workload's)")
