@@ -1,0 +1,51 @@
+"""Host-side accounting of bench.py (no GPU): the refresh roofline counts the flops of the
+iteration as described (per precision), and the --gpus guard refuses more than one GPU."""
+import dataclasses
+import subprocess
+import sys
+import os
+
+import pytest
+
+import bench
+import workloads as WL
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _one_matrix(rows, cols, rank):
+    wl = WL.WORKLOADS["layer_d256"]
+    spec = dataclasses.replace(wl.matrices[0], rows=rows, cols=cols, module=WL.Q)
+    table = tuple(rank if k == WL.Q else 0 for k in range(len(wl.rank_table)))
+    return dataclasses.replace(wl, matrices=(spec,), rank_table=table)
+
+
+@pytest.mark.parametrize("bf16", [True, False])
+def test_refresh_cost_counts_each_part(bf16):
+    # s = 32, L = 64, r = 8, p = r -> w = 16, q = 5
+    wl = _one_matrix(64, 32, 8)
+    s, L, r, w, q = 32, 64, 8, 16, 5
+    c = bench.refresh_cost(wl, -1, q, bf16)
+    it = 4 * L * s * w                      # Y = X Z and Z2 = X^T Y
+    n16 = q - 3 if bf16 else 0
+    rows = q * s + L                        # q iterates of s rows and the L-row one
+    assert c["bf16_flops"] == n16 * it
+    assert c["f64_flops"] == pytest.approx(rows * w * w + (q + 1) * 2 * w ** 3 / 3)
+    assert c["f32_flops"] == pytest.approx((q - n16) * it + rows * w * w + 2 * s * w * r)
+    t = c["bf16_flops"] / bench.PEAK_BF16 + c["f32_flops"] / bench.PEAK_F32 + c["f64_flops"] / bench.PEAK_F64
+    assert c["roofline_ms"] == pytest.approx(t * 1e3)
+
+
+def test_refresh_cost_width_is_capped_by_the_short_side():
+    # r + p > s: the subspace is the whole short side (w = s)
+    wl = _one_matrix(40, 24, 16)
+    c = bench.refresh_cost(wl, -1, 4, False)
+    s, L, w = 24, 40, 24
+    assert c["f32_flops"] == pytest.approx(4 * 4 * L * s * w + (4 * s + L) * w * w + 2 * s * w * 16)
+
+
+def test_more_than_one_gpu_is_refused():
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gpus", "2"], capture_output=True,
+                       text=True, timeout=120)
+    assert r.returncode == 2
+    assert "exactly one GPU" in r.stdout
