@@ -43,7 +43,10 @@ def parse():
     ap.add_argument("--operand", default=None, help="GEMM operand dtype override: bf16 | f32")
     ap.add_argument("--refresh-reps", type=int, default=3, help="refreshes timed; the median is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-sample-layers", type=int, default=2)
+    ap.add_argument("--cpu-sample-layers", type=int, default=None,
+                    help="layers the oracle baseline runs (default: the whole stack up to 0.5 G parameters, else 2)")
+    ap.add_argument("--cpu-one-thread", action="store_true",
+                    help="also time the oracle baseline with its BLAS limited to one thread")
     ap.add_argument("--layers", type=int, default=None, help="use only the first N layers (profiling runs)")
     ap.add_argument("--refresh-iters", type=int, default=None,
                     help="override the subspace-iteration count (the default is the workload's)")
@@ -163,9 +166,12 @@ def refresh_cost(wl, p_over: int, q: int, bf16_early: bool):
     return {"bf16_flops": f16, "f32_flops": f32, "f64_flops": f64, "roofline_ms": t * 1e3}
 
 
-def cpu_baseline(wl, layers: int):
-    """The oracle (as it stands) on a bounded sample: the first `layers` layers' matrices,
-    with their projectors already set (steps only), timed on the host cores."""
+def cpu_baseline(wl, layers, one_thread: bool = False):
+    """The oracle (as it stands) on a bounded sample: the first `layers` layers' matrices
+    (None: the whole stack if it has at most 0.5 G parameters, else two layers), with their
+    projectors already set (steps only), timed on the host cores; optionally again with
+    the BLAS limited to one thread. A partial sample also reports the time it extrapolates
+    to for the whole stack (per-layer cost times the layer count)."""
     import workloads as WL
     from oracle import moara_oracle as O
     try:
@@ -174,7 +180,11 @@ def cpu_baseline(wl, layers: int):
         blas = ",".join(sorted({i.get("internal_api", "?") for i in threadpool_info()}))
     except Exception:
         threads, blas = os.cpu_count(), "?"
-    sub = WL.subset(wl, list(range(layers)))
+    layer_ids = sorted({m.layer for m in wl.matrices})
+    if layers is None:
+        layers = len(layer_ids) if wl.n_params <= 0.5e9 else 2
+    layers = max(1, min(layers, len(layer_ids)))
+    sub = WL.subset(wl, layer_ids[:layers])
     mats = sub.matrices
     Ws, Gs, sts, cfgs = [], [], [], []
     for i, m in enumerate(mats):
@@ -186,10 +196,21 @@ def cpu_baseline(wl, layers: int):
         s = min(m.rows, m.cols)
         st.P = np.linalg.qr(np.random.default_rng(i).standard_normal((s, cfg.rank)))[0]
         Ws.append(W); Gs.append(G); sts.append(st); cfgs.append(cfg)
+    import copy
+    sts1 = copy.deepcopy(sts) if one_thread else None
+    W1 = [w.copy() for w in Ws] if one_thread else None
     t0 = time.perf_counter()
     for i in range(len(mats)):
         Ws[i] = O.step(Ws[i], Gs[i], sts[i], cfgs[i], sub.lr)
     dt = time.perf_counter() - t0
+    dt1 = None
+    if one_thread:
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            for i in range(len(mats)):
+                W1[i] = O.step(W1[i], Gs[i], sts1[i], cfgs[i], sub.lr)
+            dt1 = time.perf_counter() - t0
     params = sum(m.rows * m.cols for m in mats)
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     return {"value": params / dt, "unit": "params/s", "cores": int(min(cores, threads or cores)),
@@ -197,7 +218,9 @@ def cpu_baseline(wl, layers: int):
             "sample": f"{len(mats)} matrices ({layers} layer(s)) of {wl.name}, one optimizer step each with the "
                       f"projector set, float64 NumPy ({blas}, {threads} BLAS threads, {cores} host cores); "
                       f"{params / 1e6:.1f}M params in {dt:.2f}s",
-            "seconds": dt}
+            "seconds": dt,
+            "one_thread": None if dt1 is None else {"value": params / dt1, "seconds": dt1},
+            "extrapolated_full_stack_s": None if layers == len(layer_ids) else dt * len(layer_ids) / layers}
 
 
 def main():
@@ -397,8 +420,9 @@ def main():
     }
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
-        cb = cpu_baseline(wl, a.cpu_sample_layers)
-        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample")}
+        cb = cpu_baseline(wl, a.cpu_sample_layers, a.cpu_one_thread)
+        out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample", "one_thread",
+                                                  "extrapolated_full_stack_s")}
     else:
         out["cpu_baseline"] = None
     print(json.dumps(out), flush=True)
