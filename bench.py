@@ -13,6 +13,7 @@ d=4096, ffn=11008, bf16 weights, fp32 gradients, ranks q/k 512, v/o 1024, mlp
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import json
 import os
 import platform
@@ -185,6 +186,9 @@ def cpu_baseline(wl, layers, one_thread: bool = False):
         layers = len(layer_ids) if wl.n_params <= 0.5e9 else 2
     layers = max(1, min(layers, len(layer_ids)))
     sub = WL.subset(wl, layer_ids[:layers])
+    if sub.moe_routed > 0:   # MoE: the matrices the router activates on step 0 (attention, shared, 6 routed)
+        act = WL.active_set(sub, 0)
+        sub = dataclasses.replace(sub, matrices=tuple(m for m, a in zip(sub.matrices, act) if a))
     mats = sub.matrices
     Ws, Gs, sts, cfgs = [], [], [], []
     for i, m in enumerate(mats):
@@ -215,7 +219,8 @@ def cpu_baseline(wl, layers, one_thread: bool = False):
     cores = len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count()
     return {"value": params / dt, "unit": "params/s", "cores": int(min(cores, threads or cores)),
             "kind": "oracle",
-            "sample": f"{len(mats)} matrices ({layers} layer(s)) of {wl.name}, one optimizer step each with the "
+            "sample": f"{len(mats)} {'router-active ' if wl.moe_routed else ''}matrices ({layers} layer(s)) of "
+                      f"{wl.name}, one optimizer step each with the "
                       f"projector set, float64 NumPy ({blas}, {threads} BLAS threads, {cores} host cores); "
                       f"{params / 1e6:.1f}M params in {dt:.2f}s",
             "seconds": dt,
