@@ -405,6 +405,39 @@ def test_alignment_full_rank_projector_is_one_and_needs_a_projector():
     assert np.all(np.abs(S - 1.0) <= 1e-5), S
 
 
+def test_profiling_run_gives_the_oracles_module_scores():
+    """Phases 1-2 over a short uniform-rank run: at each profiling step the device S of
+    every matrix against the oracle's with the same projector and gradient, and the
+    aggregated S_tau against the oracle's module average of those values."""
+    import torch
+    from paper_2609_15037_amd import profiling as PR
+    M = _M()
+    c = Case(shapes=[(96, 160, WL.Q), (96, 160, WL.K), (160, 96, WL.GATE), (96, 200, WL.DOWN), (96, 160, WL.Q)],
+             ranks=[16, 16, 16, 16, 16], block_size=32)
+    st = gpu_state(c, refresh_interval=4)
+    W = [to_dev(w, c.weight_dtype) for w in _weights(c, 8)]
+    prof = PR.AlignmentProfile([sh[2] for sh in c.shapes], stride=2, n_p=6)
+    samples = []
+    for t in range(1, 8):
+        Gs = [_grad(c, 9, t, i) for i in range(len(c.shapes))]
+        Gd = [to_dev(g, "f32") for g in Gs]
+        M.moara_step(st, W, Gd, lr=1e-3)   # refreshes on steps 1 and 5 (counter 0 and 4)
+        torch.cuda.synchronize()
+        if prof.due(t):
+            S = prof.record(st, Gd, t=t)
+            for i, G in enumerate(Gs):
+                P = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+                ref = O.alignment(G, P, c.block_size)
+                assert abs(S[i] - ref) <= 1e-5, (t, i, S[i], ref)
+                samples.append((c.shapes[i][2], ref))
+    assert prof.steps == [2, 4, 6]
+    ref_tau = O.module_alignment(samples)
+    got = prof.s_tau()
+    assert set(got) == set(ref_tau)
+    for tau in ref_tau:
+        assert abs(got[tau] - ref_tau[tau]) <= 1e-5, (tau, got[tau], ref_tau[tau])
+
+
 def test_nd_weights_step_as_their_flattened_matrices():
     """A weight with more than two axes is the matrix of its first axis by all others
     (Appendix B.1): stepping N-d tensors gives bit for bit the result of the 2-D matrices."""
