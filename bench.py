@@ -314,11 +314,14 @@ def main():
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     t_host = time.perf_counter()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(a.steps - 1)]   # between steps
     e0.record(stream)
     for k in range(a.steps):
         M.moara_step(st, W, G, lr, active=act_u8[a.warmup + k], stream=stream, args=sargs)
-    e1.record(stream)
+        (ev[k] if k < a.steps - 1 else e1).record(stream)
     torch.cuda.synchronize()
+    marks = [e0] + ev + [e1]
+    step_ms = [marks[k].elapsed_time(marks[k + 1]) for k in range(a.steps)]
     host_s = time.perf_counter() - t_host
     ms_total = e0.elapsed_time(e1)
     ms_step = ms_total / a.steps
@@ -396,6 +399,7 @@ def main():
         "unit": "params/s",
         "n_gpus": 1, "steps": a.steps, "warmup": a.warmup,
         "ms_per_step": ms_step,
+        "ms_per_step_median": float(np.median(step_ms)),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
         "dtype": operand, "data": "synthetic",
         "config": {"workload": wl.name, "layers": wl.n_layers, "matrices": n, "params": wl.n_params,
