@@ -2,7 +2,9 @@
 
 * The 7B stack runs all 224 matrices in one state, so every launch has exactly
   the configuration bench.py times; the oracle checks one layer of it (all seven
-  matrices, element by element).
+  matrices, element by element). Checking the first and last layers over three
+  steps passes too (worst floored error 8.9e-3 against the 2e-2 bar) but takes
+  almost four minutes of host-side oracle work, so the suite checks one.
 * One Llama-2-7B layer's seven projectors after a refresh, by principal angles.
 * One Qwen2-7B layer (GQA k/v 512 x 3584, MLP 18944 x 3584) is checked element by
   element, and its attention projectors after a refresh by principal angles.
@@ -49,13 +51,14 @@ def check_matrices(M, st, c: Case, idx, Wd, Wo, ost, masks, report):
                 report)
 
 
-def sampled_stack_parity(wl: WL.Workload, sample_layer: int, steps: int):
-    """All matrices of `wl` in one state; oracle on the matrices of `sample_layer`."""
+def sampled_stack_parity(wl: WL.Workload, sample_layers, steps: int):
+    """All matrices of `wl` in one state; oracle on the matrices of the layers in
+    `sample_layers`."""
     import torch
     M = _M()
     c = case_from_workload(wl)
     n = len(wl.matrices)
-    idx = [i for i, m in enumerate(wl.matrices) if m.layer == sample_layer]
+    idx = [i for i, m in enumerate(wl.matrices) if m.layer in set(sample_layers)]
     st = gpu_state(c)
     dev = torch.device("cuda")
     wdt = torch.bfloat16
@@ -80,7 +83,7 @@ def sampled_stack_parity(wl: WL.Workload, sample_layer: int, steps: int):
             else:
                 WL.grad_device(wl, i, t, Gd[i], active=True)
         torch.cuda.synchronize()
-        print(f"[fullsize] {wl.name}: step {t}, {n} matrices, oracle on layer {sample_layer}", flush=True)
+        print(f"[fullsize] {wl.name}: step {t}, {n} matrices, oracle on layers {list(sample_layers)}", flush=True)
         M.moara_step(st, Wd, Gd, lr=c.lr)
         for j, i in enumerate(idx):
             Wo[j] = O.step(Wo[j], Gs[i], ost[j], ocfg[j], c.lr)
@@ -107,7 +110,7 @@ def sampled_stack_parity(wl: WL.Workload, sample_layer: int, steps: int):
 
 
 def test_llama2_7b_stack_one_layer_checked():
-    sampled_stack_parity(WL.WORKLOADS["llama2_7b"], sample_layer=31, steps=2)
+    sampled_stack_parity(WL.WORKLOADS["llama2_7b"], sample_layers=[31], steps=2)
 
 
 def test_llama2_7b_layer_refresh():
@@ -138,7 +141,7 @@ def test_llama2_7b_layer_refresh():
 
 
 def test_qwen2_7b_layer():
-    sampled_stack_parity(WL.subset(WL.WORKLOADS["qwen2_7b"], [27]), sample_layer=27, steps=2)
+    sampled_stack_parity(WL.subset(WL.WORKLOADS["qwen2_7b"], [27]), sample_layers=[27], steps=2)
 
 
 def test_qwen2_7b_attention_refresh():
