@@ -383,6 +383,46 @@ def test_bf16_weight_path_rounds_update_then_result():
     assert np.all(O.round_bf16(W2) == W2) and np.all(W2 != W)
 
 
+def _fx(a):
+    from fractions import Fraction
+    return np.vectorize(lambda s: float(Fraction(s)), otypes=[np.float64])(np.array(a, dtype=object))
+
+
+@pytest.mark.parametrize("side", ["left", "right"])
+@pytest.mark.parametrize("weights", ["f32", "bf16"])
+def test_bf16_operand_step_hand_derived(side, weights):
+    """Hand-derived one-step fixture with bf16 GEMM operands (reading 19) and, for bf16
+    weights, the cast of the recomposed update before it is applied (Appendix D).
+    Where each rounding sits is visible in the result: the moments pin the rounding
+    of V and P in the projection; the fp32-weight update pins the rounding of N (and of
+    P in the back-projection) to 1e-12; the bf16-weight result differs from the one
+    without the inner cast of U in every element chosen for it."""
+    gd = golden("bf16_operand_step.json")
+    cf, c = gd["config"], gd["cases"][side]
+    G = np.array(c["G"], dtype=np.float64)
+    m, n = G.shape
+    cfg = O.OracleConfig(block_size=cf["block_size"], rank=cf["rank"], beta1=cf["beta1"], beta2=cf["beta2"],
+                         adam_eps=cf["adam_eps"], decomp_eps=cf["decomp_eps"], scale=cf["scale"],
+                         refresh_interval=1, weight_dtype=weights, operand_dtype="bf16")
+    st = O.init_state(m, n, cfg)
+    assert st.side == side
+    W0 = _fx(c["W0"])
+    W1 = O.step(W0, G, st, cfg, lr=cf["lr"])
+    # the projector is the exact top singular vector; the step uses its bf16 copy
+    np.testing.assert_allclose(O.round_bf16(st.P).ravel(), _fx(c["bf16_P"]), rtol=0, atol=0)
+    R = _fx(c["R"]).reshape(st.exp_avg.shape)
+    np.testing.assert_allclose(st.exp_avg, (1 - cf["beta1"]) * R, rtol=1e-12, atol=0)
+    np.testing.assert_allclose(st.exp_avg_sq, (1 - cf["beta2"]) * R * R, rtol=1e-12, atol=0)
+    M = np.array([[float(np.hypot(*G[i, j:j + 2])) for j in range(0, n, 2)] for i in range(m)])
+    np.testing.assert_allclose(st.mag_avg, (1 - cf["beta1"]) * M, rtol=1e-12)
+    if weights == "f32":
+        np.testing.assert_allclose(W1, _fx(c["W1_f32_weights"]), rtol=1e-12, atol=1e-15)
+    else:
+        ref, other = _fx(c["W1_bf16_weights"]), _fx(c["W1_bf16_weights_without_inner_cast"])
+        assert np.count_nonzero(ref != other) >= 6
+        np.testing.assert_array_equal(W1, ref)
+
+
 def test_floored_metric():
     b = np.array([1.0, 0.0, -2.0])
     assert O.floored_rel_err(b, b) == 0.0
