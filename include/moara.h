@@ -42,6 +42,11 @@
  *     without synchronising; the caller must keep W and G alive and unmodified
  *     until that work has run.
  *   - A state is not thread-safe: do not use one state from two threads at once.
+ *     It may be used from several streams: every call that enqueues work on a
+ *     state first makes its stream wait for the work the previous call on that
+ *     state enqueued (an event recorded on the previous call's stream), so the
+ *     state's calls run in call order whatever streams they are given. The
+ *     caller orders its own buffers (W, G) against the streams it uses.
  */
 #ifndef MOARA_H
 #define MOARA_H
@@ -119,8 +124,10 @@ typedef struct {
   int32_t refresh_oversample;            /* p >= 0 extra columns of the subspace iteration; -1 = p = r */
   int32_t refresh_iters;                 /* q >= 1 subspace-iteration sweeps (each applies V and V^T) */
   uint64_t refresh_seed;                 /* seed of the Gaussian start block       */
-  int32_t zero_grad_mode;                /* 0: inactive matrices are skipped (no state change);
-                                            1: reserved (rejected with MOARA_E_UNSUPPORTED) */
+  int32_t zero_grad_mode;                /* what moara_step does with inactive matrices (active[i] == 0):
+                                            0: skip them (no state change, t not advanced);
+                                            1: step them with G = 0 (grads[i] is not read; W moves by
+                                               the decayed moments, t advances) */
   int32_t reserved;                      /* must be 0 */
 } moara_config;
 
@@ -192,12 +199,17 @@ int moara_refresh_projector(moara_state* st, const void* const* grads, const uin
 /* One optimizer step (Algorithm 1 training phase) for every active matrix:
  * decompose, refresh if t mod T_SVD == 0 (t = the matrix's count before the
  * step), project, Adam on R and on M, back-project, update W in place; then
- * t <- t + 1. Inactive matrices (active[i] == 0) are skipped entirely: W, the
- * moments, P and t are unchanged.
+ * t <- t + 1. Inactive matrices (active[i] == 0), e.g. MoE experts that
+ * received no tokens, are skipped entirely with zero_grad_mode 0: W, the
+ * moments, P and t are unchanged. With zero_grad_mode 1 they take the same step
+ * with G = 0 instead (M = 0 and V = 0: a refresh that falls due keeps P, or sets
+ * the first r canonical basis vectors if there is none; both Adam branches decay
+ * their moments; W moves by Rep_B(dM) (.) P N; t advances); grads[i] of such a
+ * matrix is not read and may be NULL, weights[i] must be valid.
  * weights: host array of n device pointers to m x n row-major W (weight_dtype).
  * grads:   host array of n device pointers to m x n row-major fp32 G (read only).
  * lr:      learning rate eta for this step (the caller owns the schedule).
- * Errors: MOARA_E_ARG (nulls, non-finite lr), MOARA_E_STATE (an active matrix
+ * Errors: MOARA_E_ARG (nulls, non-finite lr), MOARA_E_STATE (a matrix to step
  * has no projector and T_SVD == 0), MOARA_E_HIP. */
 int moara_step(moara_state* st, void* const* weights, const void* const* grads,
                const uint8_t* active, float lr, void* stream);
@@ -238,6 +250,26 @@ int moara_get_tensor(moara_state* st, int32_t mat, int32_t which, void* host_dst
  * projector and marks it present. Synchronous. Errors as moara_get_tensor. */
 int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* host_src, size_t bytes,
                      void* stream);
+
+/* Record of the matrix's last refresh by the library (moara_refresh_projector or a
+ * refresh inside moara_step), for callers that check how TruncatedSVD (Algorithm 1)
+ * went. The refresh finishes with a Rayleigh-Ritz step whose w x w SVD is computed by
+ * one-sided Jacobi sweeps; they stop when every column pair's cosine is below 1e-8 or
+ * after a fixed number of sweeps (14).
+ *   out_sweeps:    Jacobi sweeps run;
+ *   out_converged: 1 if the sweeps met the tolerance, 0 if they stopped at the limit
+ *                  (the projector is then still orthonormal, but its directions are
+ *                  less accurate);
+ *   out_rank:      Ritz directions kept (at most r): those whose Ritz value exceeds 1e-5
+ *                  of the largest. When it is below r (V of rank below r), the other
+ *                  columns of P are an orthonormal completion (any completion is a top-r
+ *                  singular basis of such a V); 0 when V was zero;
+ *   out_offdiag:   the largest pair cosine measured in the last sweep.
+ * Any output pointer may be NULL. Synchronises `stream`. Errors: MOARA_E_ARG (null
+ * state, bad index), MOARA_E_STATE (the library has not refreshed this matrix; a
+ * projector set with moara_set_tensor has no record), MOARA_E_HIP. */
+int moara_refresh_info(moara_state* st, int32_t mat, int32_t* out_sweeps, int32_t* out_converged,
+                       int32_t* out_rank, float* out_offdiag, void* stream);
 
 /* Per-kernel timing for measurement: when enabled, moara_step and
  * moara_refresh_projector bracket each kernel launch with HIP events on the

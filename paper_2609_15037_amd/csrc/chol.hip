@@ -5,8 +5,12 @@
 //                          diag(k)   factor C_kk = R_kk^T R_kk and invert R_kk (one WG per matrix)
 //                          panel(k)  R_kc = R_kk^{-T} C_kc for c > k           (one WG per block)
 //   then X = R^{-1} by recursive doubling over the blocks (k_trtri).
-// Pivots not above 1e-13 * max(diag C) are raised to that floor so rank-deficient
-// iterates stay finite; an all-zero Gram gives R = I.
+// A pivot not above 1e-13 * max(diag C) marks a numerically dependent column (a
+// rank-deficient iterate): its row of R and its row and column of X = R^{-1} are set to
+// zero, which is the Cholesky factor and inverse of the independent columns alone, so
+// Q = Z X has orthonormal independent columns and zero dependent ones (raising such a
+// pivot to a floor instead leaves chains of 1 / sqrt(floor) factors in R^{-1} that
+// overflow its fp32 copy). An all-zero Gram gives R = I.
 #include <algorithm>
 
 #include "refresh.h"
@@ -91,12 +95,11 @@ __global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds
     const int cx = tid & 63, ry = tid >> 6;
     for (int j = 0; j < kb; ++j) {
       if (tid == 0) {
-        double v = D[j][j];
-        if (!(v > floor_piv)) v = floor_piv;
-        D[j][j] = sqrt(v);
+        const double v = D[j][j];
+        D[j][j] = (v > floor_piv) ? sqrt(v) : 0.0;   // 0: dependent column
       }
       __syncthreads();
-      if (tid > j && tid < kb) D[j][tid] /= D[j][j];
+      if (tid > j && tid < kb) D[j][tid] = D[j][j] > 0.0 ? D[j][tid] / D[j][j] : 0.0;
       __syncthreads();
       if (cx > j && cx < kb) {
         const double djc = D[j][cx];
@@ -109,11 +112,11 @@ __global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds
   if (tid < kb) {
     const int j = tid;
     for (int i = NB - 1; i >= 0; --i) Xi[i][j] = 0.0;
-    Xi[j][j] = 1.0 / D[j][j];
+    Xi[j][j] = D[j][j] > 0.0 ? 1.0 / D[j][j] : 0.0;
     for (int i = j - 1; i >= 0; --i) {
       double v = 0.0;
       for (int t = i + 1; t <= j; ++t) v += D[i][t] * Xi[t][j];
-      Xi[i][j] = -v / D[i][i];
+      Xi[i][j] = D[i][i] > 0.0 ? -v / D[i][i] : 0.0;
     }
   }
   __syncthreads();

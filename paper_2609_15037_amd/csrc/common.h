@@ -37,6 +37,8 @@ struct MatDev {
   uint32_t tile_back;  // ... in the back-projection launch
   int32_t vt;          // V output layout: 0 row-major m x n, 1 transposed n x m
   bf16* Vb;            // bf16 direction tensor V written by the decomposition (nullptr: none)
+  int32_t n_bf16;      // zero-gradient step: N is bf16 (else fp32) ...
+  int32_t n_kp;        // ... in the blocked layout kp_index(l, j, L)
 };
 
 struct StepParams {
@@ -106,6 +108,11 @@ hipError_t launch_decompose_inv_only(const MatDev* mats_dev, const StepParams& p
 hipError_t launch_decompose_vt(const MatDev* mats_dev, const StepParams& p, int adam_m, hipStream_t st);
 int decompose_tiles(int64_t m);
 int decompose_vt_tiles(int64_t m);
+// Optimizer_M and Optimizer_V of a matrix whose gradient is exactly zero (no G is read):
+// magnitude moments -> dM (when p.decompose), direction moments -> N; tile_dec holds the
+// matrix's first workgroup, zero_grad_tiles(...) workgroups per matrix.
+uint32_t zero_grad_tiles(int64_t mk, int64_t Lr);
+hipError_t launch_zero_grad(const MatDev* mats_dev, const StepParams& p, hipStream_t st);
 // limits of the V-writing decomposition paths (blocks per row)
 constexpr int DEC_VT_MAX_K = 160;    // transposed path, 64 rows per workgroup
 constexpr int DEC_ROW_MAX_K = 512;   // row-major path, 16 rows per workgroup

@@ -269,7 +269,50 @@ __global__ __launch_bounds__(256) void k_decompose_vt(const MatDev* __restrict__
     block_out(d, p, row0 + rr, j, sums[e], adam_m);
   }
 }
+// A zero gradient gives M = 0, V = 0 and R = P^T V = 0 (Algorithm 1 with G = 0), so the
+// step reduces to decaying the moments: Optimizer_M on M = 0 and Optimizer_V on R = 0,
+// through the same adam_out as the decomposition and the projection epilogue (bit for
+// bit what those kernels produce from an all-zero G). Elements [0, m k) of a matrix are
+// its magnitude blocks (only when the decomposition is on), the next L r its direction
+// moments; ZG_PER_WG elements per workgroup, consecutive threads on consecutive elements.
+constexpr int ZG_PER_WG = 2048;
+__global__ __launch_bounds__(256) void k_zero_grad(const MatDev* __restrict__ mats, StepParams p) {
+  const uint32_t t = blockIdx.x;
+  const MatDev& d = mats[find_mat(mats, p.nmat, t, [](const MatDev& x) { return x.tile_dec; })];
+  const int64_t mk = p.decompose ? d.m * d.k : 0;
+  const int64_t Lr = (int64_t)d.L * d.r;
+  const int64_t e0 = (int64_t)(t - d.tile_dec) * ZG_PER_WG;
+  for (int64_t e = e0 + threadIdx.x; e < e0 + ZG_PER_WG && e < mk + Lr; e += 256) {
+    if (e < mk) {
+      float a = d.mag1[e], q = d.mag2[e];
+      const float out = adam_out(0.f, a, q, p.beta1, p.beta2, p.adam_eps, d.bc1, d.bc2);
+      d.mag1[e] = a;
+      d.mag2[e] = q;
+      d.dM[e] = out;
+    } else {
+      const int64_t x = e - mk;   // (l, j) of the L x r moments, row-major
+      float a = d.exp1[x], q = d.exp2[x];
+      const float out = adam_out(0.f, a, q, p.beta1, p.beta2, p.adam_eps, d.bc1, d.bc2);
+      d.exp1[x] = a;
+      d.exp2[x] = q;
+      if (d.n_bf16) {
+        const int64_t l = x / d.r, j = x % d.r;
+        ((bf16*)d.N)[d.n_kp ? kp_index(l, j, d.L) : x] = f2bf(out);
+      } else {
+        ((float*)d.N)[x] = out;
+      }
+    }
+  }
+}
 }  // namespace
+
+uint32_t zero_grad_tiles(int64_t mk, int64_t Lr) { return (uint32_t)((mk + Lr + ZG_PER_WG - 1) / ZG_PER_WG); }
+
+hipError_t launch_zero_grad(const MatDev* mats_dev, const StepParams& p, hipStream_t st) {
+  if (p.total_dec == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_zero_grad, dim3(p.total_dec), dim3(256), 0, st, mats_dev, p);
+  return hipGetLastError();
+}
 
 int decompose_tiles(int64_t m) { return (int)((m + DEC_ROWS - 1) / DEC_ROWS); }
 int decompose_vt_tiles(int64_t m) { return (int)((m + VT_ROWS - 1) / VT_ROWS); }

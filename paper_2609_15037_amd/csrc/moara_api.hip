@@ -45,6 +45,7 @@ struct MatHost {
   int32_t r = 0, side = 0, k = 0;
   int64_t t = 0;
   bool hasP = false;
+  bool refreshed = false;   // the library's refresh has written this matrix's record
   float *inv = nullptr, *dM = nullptr, *mag1 = nullptr, *mag2 = nullptr;
   float *exp1 = nullptr, *exp2 = nullptr, *P32 = nullptr;
   void *N = nullptr, *Pop = nullptr, *Ptop = nullptr;
@@ -67,6 +68,7 @@ struct moara_state {
   std::vector<MatHost> mats;
   char* block = nullptr;        // all persistent device memory
   size_t block_bytes = 0;
+  int32_t* info_dev = nullptr;  // 4 ints per matrix: the last refresh's record (RefDev::info)
   // descriptor staging: pinned host ring + one device arena (stream ordered)
   static constexpr int NSLOT = 8;
   char* host_ring = nullptr;
@@ -81,6 +83,10 @@ struct moara_state {
   char* ref_arena = nullptr;      // device descriptors of the refresh (separate arena)
   size_t ref_arena_bytes = 0;
   char* ref_host = nullptr;
+  // cross-stream order: recorded on the caller's stream at the end of every call that
+  // enqueues work on the state; the next call's stream waits on it first
+  hipEvent_t order_ev = nullptr;
+  bool order_valid = false;
   // timing
   bool timing = false;
   std::vector<TimedLaunch> pending;
@@ -110,8 +116,7 @@ int validate_config(const moara_config* c) {
   if (c->operand_dtype != MOARA_F32 && c->operand_dtype != MOARA_BF16) return fail(MOARA_E_ARG, "bad operand_dtype");
   if (c->refresh_oversample < -1) return fail(MOARA_E_ARG, "refresh_oversample must be >= -1");
   if (c->refresh_iters < 1 || c->refresh_iters > 1000) return fail(MOARA_E_ARG, "refresh_iters must be in [1, 1000]");
-  if (c->zero_grad_mode == 1) return fail(MOARA_E_UNSUPPORTED, "zero_grad_mode 1 is not implemented");
-  if (c->zero_grad_mode != 0) return fail(MOARA_E_ARG, "bad zero_grad_mode");
+  if (c->zero_grad_mode != 0 && c->zero_grad_mode != 1) return fail(MOARA_E_ARG, "bad zero_grad_mode");
   if (c->reserved != 0) return fail(MOARA_E_ARG, "reserved must be 0");
   return MOARA_OK;
 }
@@ -191,6 +196,7 @@ size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w, int32_t r, bool bf) {
   b += align_up(8 * (size_t)wpad * w);     // Zc (R, column-major)
   b += align_up(4 * 64);                   // off
   b += align_up(4 * wpad) + align_up(8 * wpad);
+  b += align_up(8 * 64 * (size_t)s) + align_up(8 * 64 * (size_t)r) + align_up(8 * (size_t)s) + align_up(4 * (size_t)r);  // completion
   return b;
 }
 
@@ -230,6 +236,27 @@ int end_stage(moara_state* st, Stager& sg, hipStream_t stream) {
   return MOARA_OK;
 }
 
+// ------------------------------------------------------------------ stream order
+// Every call that enqueues work on a state makes its stream wait for the work the
+// previous call enqueued (on whatever stream), and records the event again when it
+// returns: calls on one state run in call order even across streams, so the shared
+// descriptor arenas, workspaces and state tensors are never used by two streams at once.
+struct StreamOrder {
+  moara_state* st;
+  hipStream_t stream;
+  hipError_t err = hipSuccess;
+  StreamOrder(moara_state* s, hipStream_t str) : st(s), stream(str) {
+    if (st->order_valid) err = hipStreamWaitEvent(stream, st->order_ev, 0);
+  }
+  ~StreamOrder() {
+    if (hipEventRecord(st->order_ev, stream) == hipSuccess) st->order_valid = true;
+  }
+};
+#define ORDER_ON(st_, stream_)                                                               \
+  StreamOrder order_guard_((st_), (stream_));                                               \
+  if (order_guard_.err != hipSuccess)                                                       \
+    return fail(MOARA_E_HIP, "hipStreamWaitEvent: %s", hipGetErrorString(order_guard_.err))
+
 // ------------------------------------------------------------------ timing
 hipEvent_t get_event(moara_state* st) {
   if (!st->ev_pool.empty()) {
@@ -266,9 +293,10 @@ struct TimerScope {
 
 int collect_timing(moara_state* st, hipStream_t stream) {
   if (st->pending.empty()) return MOARA_OK;
-  HIP_TRY(hipStreamSynchronize(stream));
+  (void)stream;   // the events may sit on several streams: wait for each one itself
   for (auto& tl : st->pending) {
     float ms = 0.f;
+    HIP_TRY(hipEventSynchronize(tl.b));
     HIP_TRY(hipEventElapsedTime(&ms, tl.a, tl.b));
     st->launches[tl.kind] += 1;
     st->total_ms[tl.kind] += ms;
@@ -380,8 +408,11 @@ int run_decompose(moara_state* st, const std::vector<int>& idx, const void* cons
   return MOARA_OK;
 }
 
+// back_only (indexed by matrix, may be null): N was formed without a projection (zero
+// gradient); only the back-projection and update run for that matrix.
 int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* weights, const void* const* grads,
-                     float lr, hipStream_t stream, const std::vector<char>* usev = nullptr) {
+                     float lr, hipStream_t stream, const std::vector<char>* usev = nullptr,
+                     const std::vector<char>* back_only = nullptr) {
   const int ob = st->cfg.operand_dtype == MOARA_BF16;
   const int kind = ob ? KIND_BF16 : KIND_F32;
   const int wbf = st->cfg.weight_dtype == MOARA_BF16;
@@ -447,7 +478,7 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
         back.push_back(b);
       }
     }
-    if (proj_done) continue;
+    if (proj_done || (back_only && (*back_only)[i])) continue;
     GemmProb g{};
     g.M = h.L; g.N = h.r; g.K = h.s;
     g.a = grads[i]; g.lda = h.n;
@@ -498,6 +529,51 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
   return MOARA_OK;
 }
 
+// Zero-gradient step (zero_grad_mode 1) for the listed matrices: a refresh that falls due
+// keeps the projector (V = 0), or sets the canonical one if there is none; then
+// Optimizer_M and Optimizer_V on zero inputs (k_zero_grad). The back-projection and the
+// update follow in run_project_back.
+int run_zero_grad(moara_state* st, const std::vector<int>& zidx, hipStream_t stream) {
+  if (zidx.empty()) return MOARA_OK;
+  const int T = st->cfg.refresh_interval;
+  const int obf = st->cfg.operand_dtype == MOARA_BF16;
+  for (int i : zidx) {
+    MatHost& h = st->mats[i];
+    if (T > 0 && h.t % T == 0 && !h.hasP) {
+      HIP_TRY(launch_canonical_projector(h.P32, h.Pop, h.Ptop, h.s, h.r, obf, h.kp ? 1 : 0, stream));
+      h.hasP = true;
+    }
+  }
+  std::vector<MatDev> md;
+  uint32_t tiles = 0;
+  for (int i : zidx) {
+    const MatHost& h = st->mats[i];
+    MatDev d{};
+    d.m = h.m; d.n = h.n; d.k = h.k; d.r = h.r; d.side = h.side; d.L = (int32_t)h.L; d.s = (int32_t)h.s;
+    d.dM = h.dM; d.mag1 = h.mag1; d.mag2 = h.mag2;
+    d.exp1 = h.exp1; d.exp2 = h.exp2; d.N = h.N;
+    d.n_bf16 = obf; d.n_kp = h.kp ? 1 : 0;
+    const double t1 = (double)(h.t + 1);
+    d.bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
+    d.bc2 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta2, t1)) : 1.f;
+    d.tile_dec = tiles;
+    tiles += zero_grad_tiles(st->cfg.decompose ? h.m * h.k : 0, h.L * h.r);
+    md.push_back(d);
+  }
+  Stager sg;
+  int rc = begin_stage(st, sg);
+  if (rc) return rc;
+  const size_t off = sg.push(md.data(), md.size());
+  if (off == (size_t)-1) return fail(MOARA_E_OOM, "descriptor arena too small");
+  if ((rc = end_stage(st, sg, stream))) return rc;
+  StepParams p = make_params(st, 0.f);
+  p.nmat = (int)md.size();
+  p.total_dec = tiles;
+  TimerScope ts(st, MOARA_KERN_DECOMPOSE, stream);
+  HIP_TRY(launch_zero_grad((const MatDev*)(st->dev_arena + off), p, stream));
+  return MOARA_OK;
+}
+
 // ------------------------------------------------------------------ refresh driver
 struct RefMat {
   int idx;
@@ -510,6 +586,8 @@ struct RefMat {
   double *C, *X, *cmax, *Zc, *norms;
   uint32_t* off;
   int32_t* order;
+  double* cw;            // basis completion workspace (s x 64, r x 64, s)
+  int32_t* sidx;         // basis completion indices (r)
 };
 
 int ensure_ref_ws(moara_state* st, size_t bytes) {
@@ -583,6 +661,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.off = (uint32_t*)take(4 * 64);
     x.order = (int32_t*)take(4 * x.wpad);
     x.norms = (double*)take(8 * x.wpad);
+    x.cw = (double*)take(8 * 64 * (size_t)x.s + 8 * 64 * h_r_of(x) + 8 * (size_t)x.s);
+    x.sidx = (int32_t*)take(4 * h_r_of(x));
   }
   const int nm = (int)rm.size();
   const int kind = KIND_F32;
@@ -615,6 +695,10 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     d.tile_cm = tc; tc += r_colmajor_tiles(x.w, x.wpad);
     d.tile_norm = tnorm; tnorm += norm_tiles(x.wpad);
     d.has_prev = h.hasP ? 1 : 0;
+    d.max_sweeps = MAX_SWEEPS;
+    d.info = st->info_dev + 4 * (size_t)x.idx;
+    d.cw = x.cw;
+    d.sidx = x.sidx;
     nb_max = std::max(nb_max, x.wpad / JB);
   }
   auto gram_list = [&](bool onY) {
@@ -878,7 +962,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   int32_t rmax = 0;
   for (auto& x : rm) rmax = std::max(rmax, st->mats[x.idx].r);
   HIP_TRY(launch_finalize_out(RD, nm, rmax, stream));
-  for (auto& x : rm) st->mats[x.idx].hasP = true;
+  HIP_TRY(launch_complete_basis(RD, nm, stream));
+  for (auto& x : rm) st->mats[x.idx].hasP = st->mats[x.idx].refreshed = true;
   return MOARA_OK;
 }
 
@@ -1032,6 +1117,7 @@ int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, i
     ref += mat_refresh_bytes(l.s, l.L, subspace_width(*cfg, l.s, ranks[i]), ranks[i],
                              vpath_shape_ok(*cfg, descs[i].rows, descs[i].cols, sides[i], ranks[i]));
   }
+  tot += align_up(16 * (size_t)n);   // refresh records
   *out_state_bytes = (int64_t)tot;
   if (out_refresh_workspace_bytes) *out_refresh_workspace_bytes = (int64_t)std::min(ref, refresh_budget() + ref / (size_t)n);
   return MOARA_OK;
@@ -1047,6 +1133,7 @@ static void free_state(moara_state* st) {
   if (st->ref_host) hipHostFree(st->ref_host);
   for (auto& e : st->slot_ev)
     if (e) hipEventDestroy(e);
+  if (st->order_ev) hipEventDestroy(st->order_ev);
   for (auto& tl : st->pending) { hipEventDestroy(tl.a); hipEventDestroy(tl.b); }
   for (auto e : st->ev_pool) hipEventDestroy(e);
   delete st;
@@ -1075,6 +1162,7 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
     h.kp = h.vpath && cfg->operand_dtype == MOARA_BF16 && h.r % 32 == 0;
     tot += mat_state_bytes(*cfg, h.m, h.n, h.side, h.s, h.L, h.k, h.r);
   }
+  tot += align_up(16 * (size_t)n);   // refresh records
   if (hipMalloc(&st->block, tot) != hipSuccess) { free_state(st); return fail(MOARA_E_OOM, "state of %zu bytes", tot); }
   st->block_bytes = tot;
   const int ob = elem_bytes(cfg->operand_dtype);
@@ -1093,6 +1181,7 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
     h.Ptop = take((size_t)ob * h.s * h.r);
     if (h.vpath) h.V = take(2 * (size_t)h.m * h.n);
   }
+  st->info_dev = (int32_t*)take(16 * (size_t)n);
   st->arena_bytes = 2 * align_up(sizeof(MatDev) * n) + 5 * align_up(sizeof(GemmProb) * n) + 8 * ALIGN;
   if (hipMalloc(&st->dev_arena, st->arena_bytes) != hipSuccess ||
       hipHostMalloc(&st->host_ring, st->arena_bytes * moara_state::NSLOT) != hipSuccess) {
@@ -1101,6 +1190,7 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
   }
   for (auto& e : st->slot_ev)
     if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) { free_state(st); return fail(MOARA_E_HIP, "event create"); }
+  if (hipEventCreateWithFlags(&st->order_ev, hipEventDisableTiming) != hipSuccess) { free_state(st); return fail(MOARA_E_HIP, "event create"); }
   if (hipMemsetAsync(st->block, 0, tot, hs) != hipSuccess || hipStreamSynchronize(hs) != hipSuccess) {
     free_state(st);
     return fail(MOARA_E_HIP, "zero fill of the state failed");
@@ -1126,6 +1216,8 @@ int moara_refresh_projector(moara_state* st, const void* const* grads, const uin
   std::vector<int> idx;
   int rc = collect_active(st, grads, active, &idx, "grads");
   if (rc) return rc;
+  if (idx.empty()) return MOARA_OK;
+  ORDER_ON(st, (hipStream_t)stream);
   return run_refresh(st, idx, grads, (hipStream_t)stream);
 }
 
@@ -1143,6 +1235,7 @@ int moara_alignment(moara_state* st, const void* const* grads, const uint8_t* ac
     if (!st->mats[i].hasP) return fail(MOARA_E_STATE, "matrix %d has no projector (set one or refresh first)", i);
   if (idx.empty()) return MOARA_OK;
   hipStream_t hs = (hipStream_t)stream;
+  ORDER_ON(st, hs);
   const bool dec = st->cfg.decompose != 0;
   if (dec && (rc = run_decompose(st, idx, grads, false, hs))) return rc;
   size_t need = 0;
@@ -1232,8 +1325,23 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
     if (T > 0 && h.t % T == 0) need.push_back(i);
     else if (!h.hasP) return fail(MOARA_E_STATE, "matrix %d has no projector (set one, refresh, or use refresh_interval > 0)", i);
   }
-  if (idx.empty()) return MOARA_OK;
+  // zero_grad_mode 1: the inactive matrices take a step with G = 0 (their grads entries are not read)
+  std::vector<int> zidx;
+  std::vector<char> zflag(st->n, 0);
+  if (st->cfg.zero_grad_mode == 1 && active) {
+    for (int i = 0; i < st->n; ++i) {
+      if (active[i]) continue;
+      const MatHost& h = st->mats[i];
+      if (!weights[i]) return fail(MOARA_E_ARG, "weights[%d] is NULL (zero_grad_mode 1 steps inactive matrices too)", i);
+      if (!(T > 0 && h.t % T == 0) && !h.hasP)
+        return fail(MOARA_E_STATE, "matrix %d has no projector (set one, refresh, or use refresh_interval > 0)", i);
+      zidx.push_back(i);
+      zflag[i] = 1;
+    }
+  }
+  if (idx.empty() && zidx.empty()) return MOARA_OK;
   hipStream_t hs = (hipStream_t)stream;
+  ORDER_ON(st, hs);
   std::vector<char> usev(st->n, 0);
   for (int i : idx) usev[i] = st->mats[i].vpath && (((uintptr_t)grads[i] & 15) == 0);
   if (st->cfg.decompose) {
@@ -1241,9 +1349,12 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
     if (rc) return rc;
   }
   if (!need.empty() && (rc = refresh_in_chunks(st, need, grads, hs, usev))) return rc;
-  rc = run_project_back(st, idx, weights, grads, lr, hs, &usev);
+  if ((rc = run_zero_grad(st, zidx, hs))) return rc;
+  std::vector<int> all = idx;
+  all.insert(all.end(), zidx.begin(), zidx.end());
+  rc = run_project_back(st, all, weights, grads, lr, hs, &usev, &zflag);
   if (rc) return rc;
-  for (int i : idx) st->mats[i].t += 1;
+  for (int i : all) st->mats[i].t += 1;
   return MOARA_OK;
 }
 
@@ -1278,6 +1389,7 @@ int moara_get_tensor(moara_state* st, int32_t mat, int32_t which, void* host_dst
                   : which == MOARA_T_EXP_AVG_SQ ? (const void*)h.exp2
                   : which == MOARA_T_MAG_AVG ? (const void*)h.mag1 : (const void*)h.mag2;
   const bool transpose = (which == MOARA_T_EXP_AVG || which == MOARA_T_EXP_AVG_SQ) && h.side == MOARA_SIDE_LEFT;
+  ORDER_ON(st, hs);
   HIP_TRY(hipStreamSynchronize(hs));
   if (!transpose) {
     HIP_TRY(hipMemcpyAsync(host_dst, src, need, hipMemcpyDeviceToHost, hs));
@@ -1322,6 +1434,7 @@ int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* ho
       for (int64_t j = 0; j < h.r; ++j) tmp[l * h.r + j] = in[j * h.L + l];
     src = tmp.data();
   }
+  ORDER_ON(st, hs);
   HIP_TRY(hipStreamSynchronize(hs));
   HIP_TRY(hipMemcpyAsync(dst, src, need, hipMemcpyHostToDevice, hs));
   if (which == MOARA_T_P) {
@@ -1330,6 +1443,23 @@ int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* ho
     h.hasP = true;
   }
   HIP_TRY(hipStreamSynchronize(hs));
+  return MOARA_OK;
+}
+
+int moara_refresh_info(moara_state* st, int32_t mat, int32_t* out_sweeps, int32_t* out_converged,
+                       int32_t* out_rank, float* out_offdiag, void* stream) {
+  if (!st) return fail(MOARA_E_ARG, "state is NULL");
+  if (mat < 0 || mat >= st->n) return fail(MOARA_E_ARG, "matrix index %d out of range", mat);
+  if (!st->mats[mat].refreshed) return fail(MOARA_E_STATE, "matrix %d has not been refreshed by the library", mat);
+  hipStream_t hs = (hipStream_t)stream;
+  int32_t rec[4];
+  ORDER_ON(st, hs);
+  HIP_TRY(hipStreamSynchronize(hs));
+  HIP_TRY(hipMemcpy(rec, st->info_dev + 4 * (size_t)mat, sizeof rec, hipMemcpyDeviceToHost));
+  if (out_sweeps) *out_sweeps = rec[0];
+  if (out_converged) *out_converged = rec[1];
+  if (out_rank) *out_rank = rec[2];
+  if (out_offdiag) memcpy(out_offdiag, &rec[3], 4);
   return MOARA_OK;
 }
 

@@ -33,7 +33,18 @@ struct RefDev {
   double* norms;      // wpad scratch
   uint32_t tile_gauss, tile_jac, tile_cm, tile_norm;   // per-launch workgroup prefixes
   int32_t has_prev;   // 1: a projector exists (an all-zero V keeps it)
+  int32_t max_sweeps; // Jacobi sweeps launched
+  int32_t* info;      // 4 ints of the state, written by the refresh: [0] Jacobi sweeps run,
+                      // [1] 1 = converged, [2] numerical rank (kept Ritz directions, <= r),
+                      // [3] largest pair cosine of the last sweep measured (float bits)
+  double* cw;         // basis completion workspace: s x 64 block, r x 64 coefficients, s row norms
+  int32_t* sidx;      // basis completion: the r canonical indices, by increasing row norm
 };
+
+// Ritz directions whose value is not above this fraction of the largest one are
+// numerically null: an fp32 subspace iteration cannot resolve them (its GEMMs carry
+// relative errors of order 1e-6), so their columns are completed to an orthonormal basis.
+constexpr double RITZ_NULL_REL = 1e-5;
 
 constexpr int JB = 32;   // Jacobi column block; a pair holds 2*JB columns
 
@@ -75,8 +86,12 @@ uint32_t r_colmajor_tiles(int32_t w, int32_t wpad);
 uint32_t norm_tiles(int32_t wpad);
 hipError_t launch_finalize_order(const RefDev* d, int n, uint32_t norm_total, hipStream_t st);
 hipError_t launch_finalize_out(const RefDev* d, int n, int32_t rmax, hipStream_t st);
+hipError_t launch_complete_basis(const RefDev* d, int n, hipStream_t st);
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
                                     int operand_bf16, int kp, hipStream_t st);
+// P = the first r canonical basis vectors (the projector of an all-zero V with none before)
+hipError_t launch_canonical_projector(float* P32, void* Pop, void* Ptop, int64_t s, int64_t r, int operand_bf16,
+                                      int kp, hipStream_t st);
 uint32_t gauss_tiles(int64_t s, int32_t w);
 uint32_t gram_tiles(int32_t w);
 uint32_t jacobi_tiles(int32_t wpad);

@@ -495,9 +495,13 @@ __global__ __launch_bounds__(256) void k_r_colmajor(const RefDev* __restrict__ d
 // k_finalize_out: make each column's largest-magnitude entry positive (lowest index on
 // ties) and write P (fp32 master and both operand copies). An all-zero iterate (V == 0) keeps the previous projector, or yields the
 // first r canonical basis vectors when there is none; numerically null directions
-// also fall back to e_j.
+// (Ritz value not above RITZ_NULL_REL of the largest) are written as e_j here and
+// replaced by an orthonormal completion (k_complete_basis) when some directions were kept.
 // Column norms of R J (the Ritz values): NORM_COLS columns per workgroup, one wave per
 // column at a time (butterfly sum).
+__device__ __forceinline__ bool null_dir(double nrm, double nmax) {
+  return !(nrm > 1e-300) || !(nrm > RITZ_NULL_REL * nmax);
+}
 constexpr int NORM_COLS = 16;
 __global__ __launch_bounds__(256) void k_col_norms(const RefDev* __restrict__ ds, int n) {
   const uint32_t t = blockIdx.x;
@@ -526,26 +530,42 @@ __global__ __launch_bounds__(256) void k_finalize_order(const RefDev* __restrict
   // rank of every column by decreasing norm (ties by index), norms read from LDS
   __shared__ double nl[2048];
   const bool in_lds = d.wpad <= 2048;
+  // a norm that is not a finite number >= 0 ranks as -1, so the keys are totally ordered
+  // and the ranks form a permutation of 0 .. wpad-1 (every entry of order is written)
+  auto key = [](double v) { return (v >= 0.0 && v <= 1.7976931348623157e308) ? v : -1.0; };
   if (in_lds)
-    for (int c = tid; c < d.wpad; c += 256) nl[c] = d.norms[c];
+    for (int c = tid; c < d.wpad; c += 256) nl[c] = key(d.norms[c]);
   __syncthreads();
   for (int c = tid; c < d.wpad; c += 256) {
-    const double nc = in_lds ? nl[c] : d.norms[c];
+    const double nc = in_lds ? nl[c] : key(d.norms[c]);
     int rank = 0;
     for (int c2 = 0; c2 < d.wpad; ++c2) {
-      const double n2 = in_lds ? nl[c2] : d.norms[c2];
+      const double n2 = in_lds ? nl[c2] : key(d.norms[c2]);
       rank += (n2 > nc) || (n2 == nc && c2 < c);
     }
     d.order[rank] = c;
   }
   __syncthreads();
   const double nmax = d.norms[d.order[0]];
+  int kept = 0;
   for (int j = 0; j < d.r; ++j) {
     const int src = d.order[j];
     const double nrm = d.norms[src];
-    const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
+    const bool deg = null_dir(nrm, nmax);
+    kept += deg ? 0 : 1;
     const double* col = d.Zc + (int64_t)src * L;
     for (int64_t i = tid; i < d.w; i += 256) d.Bt[(int64_t)j * d.w + i] = deg ? 0.f : (float)(col[i] / nrm);
+  }
+  if (tid == 0) {
+    // the first sweep whose measured pair cosines all fell below the tolerance ended the
+    // iteration (later sweeps returned at once and left their entries at zero)
+    int sw = 0;
+    while (sw < d.max_sweeps && !(__uint_as_float(d.off[sw]) < (float)JAC_TOL)) ++sw;
+    const bool conv = sw < d.max_sweeps;
+    d.info[0] = conv ? sw + 1 : d.max_sweeps;
+    d.info[1] = conv ? 1 : 0;
+    d.info[2] = kept;
+    d.info[3] = (int32_t)d.off[conv ? sw : d.max_sweeps - 1];
   }
 }
 
@@ -590,8 +610,7 @@ __global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__
       float g = 1.f;
       if (jin) {
         const double nrm = d.norms[d.order[j]];
-        const bool deg = !(nrm > 1e-300) || !(nrm > 1e-12 * nmax);
-        g = deg ? 0.f : ((d.Pw[(int64_t)bi * r + j] < 0.f) ? -1.f : 1.f);
+        g = null_dir(nrm, nmax) ? 0.f : ((d.Pw[(int64_t)bi * r + j] < 0.f) ? -1.f : 1.f);
       }
       sg[lane] = g;
     }
@@ -624,6 +643,217 @@ __global__ __launch_bounds__(256) void k_finalize_out(const RefDev* __restrict__
       }
     }
     __syncthreads();
+  }
+}
+
+// ------------------------------------------------------------------ basis completion
+// When only rho < r Ritz directions lie above the null level (V of rank below r), the
+// remaining r - rho columns of P are completed to an orthonormal basis of the complement
+// of the kept ones; any such completion is a top-r singular basis of a rank-deficient V.
+// Candidates are the canonical vectors e_c at which the kept columns are smallest (rows
+// of P by increasing squared norm, ties by index). Blocks of up to CB of them are
+// projected off every column written so far, twice (classical Gram-Schmidt with
+// reorthogonalisation), orthonormalised by the Cholesky factor of their CB x CB Gram
+// matrix (after each projection), signed like the Ritz vectors (largest-magnitude entry
+// positive, lowest index on ties) and appended to P and its operand copies. fp64
+// arithmetic, one workgroup per matrix; a matrix whose directions were all kept (or
+// whose V is zero) returns at once.
+constexpr int CB = 64;
+typedef double CbTile[CB + 1];
+
+// acc (4 x 4 per thread: rows 4 (tid >> 4) + x, columns 4 (tid & 15) + y of a CB x CB
+// tile) += sum_{k < K} fa(i, k) fb(k, j). ACOL: A is staged column by column (fa reads
+// consecutive i at consecutive addresses).
+template <bool ACOL, class FA, class FB>
+__device__ void cb_mm(double (&acc)[4][4], int64_t K, FA fa, FB fb, CbTile* As, CbTile* Bs) {
+  const int tid = threadIdx.x, ti = tid >> 4, tj = tid & 15;
+  for (int64_t k0 = 0; k0 < K; k0 += CB) {
+    __syncthreads();   // earlier readers of As / Bs are done
+    for (int e = tid; e < CB * CB; e += 256) {
+      const int i = ACOL ? (e & (CB - 1)) : (e / CB), k = ACOL ? (e / CB) : (e & (CB - 1));
+      As[i][k] = (k0 + k < K) ? fa(i, k0 + k) : 0.0;
+    }
+    for (int e = tid; e < CB * CB; e += 256) {
+      const int k = e / CB, j = e & (CB - 1);
+      Bs[k][j] = (k0 + k < K) ? fb(k0 + k, j) : 0.0;
+    }
+    __syncthreads();
+    const int kk = (int)((K - k0) < CB ? (K - k0) : CB);
+    for (int k = 0; k < kk; ++k) {
+      double a[4], b[4];
+#pragma unroll
+      for (int x = 0; x < 4; ++x) { a[x] = As[4 * ti + x][k]; b[x] = Bs[k][4 * tj + x]; }
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) acc[x][y] = fma(a[x], b[y], acc[x][y]);
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void k_complete_basis(const RefDev* __restrict__ ds) {
+  const RefDev& d = ds[blockIdx.x];
+  const int r = d.r, rho = d.info[2];
+  if (rho <= 0 || rho >= r) return;
+  __shared__ CbTile As[CB], Bs[CB], Hs[CB], Xs[CB];
+  __shared__ double bvl[4][CB];
+  __shared__ int bil[4][CB];
+  __shared__ double sgn[CB];
+  const int tid = threadIdx.x, ti = tid >> 4, tj = tid & 15;
+  const int64_t s = d.s;
+  float* P = d.P32;
+  double* Cb = d.cw;                     // s x CB
+  double* T = d.cw + s * CB;             // r x CB
+  double* rn = T + (int64_t)r * CB;      // s
+  const int q = r - rho;
+  for (int64_t i = tid; i < s; i += 256) {
+    double a = 0.0;
+    for (int k = 0; k < rho; ++k) { const double v = P[i * r + k]; a = fma(v, v, a); }
+    rn[i] = a;
+  }
+  __syncthreads();
+  for (int64_t i = tid; i < s; i += 256) {
+    const double v = rn[i];
+    int64_t rank = 0;
+    for (int64_t c = 0; c < s; ++c) { const double u = rn[c]; rank += (u < v) || (u == v && c < i); }
+    if (rank < q) d.sidx[rank] = (int32_t)i;
+  }
+  __syncthreads();
+  for (int b0 = 0; b0 < q; b0 += CB) {
+    const int nb = (q - b0) < CB ? (q - b0) : CB;
+    const int J = rho + b0;              // columns of P written so far
+    const int32_t* S = d.sidx + b0;
+    // Cb = E_S - P_J P_J[S, :]^T  (columns >= nb stay zero)
+    for (int64_t r0 = 0; r0 < s; r0 += CB) {
+      double acc[4][4] = {};
+      cb_mm<false>(acc, J, [&](int i, int64_t k) { return r0 + i < s ? (double)P[(r0 + i) * r + k] : 0.0; },
+                   [&](int64_t k, int j) { return j < nb ? (double)P[(int64_t)S[j] * r + k] : 0.0; }, As, Bs);
+#pragma unroll
+      for (int x = 0; x < 4; ++x)
+#pragma unroll
+        for (int y = 0; y < 4; ++y) {
+          const int64_t i = r0 + 4 * ti + x;
+          const int j = 4 * tj + y;
+          if (i < s) Cb[i * CB + j] = j < nb ? ((i == S[j]) ? 1.0 : 0.0) - acc[x][y] : 0.0;
+        }
+    }
+    for (int pass = 0; pass < 2; ++pass) {
+      // T = P_J^T Cb ; Cb -= P_J T
+      for (int t0 = 0; t0 < J; t0 += CB) {
+        double acc[4][4] = {};
+        cb_mm<true>(acc, s, [&](int i, int64_t k) { return t0 + i < J ? (double)P[k * r + t0 + i] : 0.0; },
+                    [&](int64_t k, int j) { return Cb[k * CB + j]; }, As, Bs);
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y)
+            if (t0 + 4 * ti + x < J) T[(int64_t)(t0 + 4 * ti + x) * CB + 4 * tj + y] = acc[x][y];
+      }
+      __syncthreads();
+      for (int64_t r0 = 0; r0 < s; r0 += CB) {
+        double acc[4][4] = {};
+        cb_mm<false>(acc, J, [&](int i, int64_t k) { return r0 + i < s ? (double)P[(r0 + i) * r + k] : 0.0; },
+                     [&](int64_t k, int j) { return T[k * CB + j]; }, As, Bs);
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y) {
+            const int64_t i = r0 + 4 * ti + x;
+            if (i < s) Cb[i * CB + 4 * tj + y] -= acc[x][y];
+          }
+      }
+      // Gram H = Cb^T Cb, unit diagonal past nb
+      {
+        double acc[4][4] = {};
+        cb_mm<true>(acc, s, [&](int i, int64_t k) { return Cb[k * CB + i]; },
+                    [&](int64_t k, int j) { return Cb[k * CB + j]; }, As, Bs);
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y) {
+            const int i = 4 * ti + x, j = 4 * tj + y;
+            Hs[i][j] = (i < nb && j < nb) ? acc[x][y] : (i == j ? 1.0 : 0.0);
+          }
+      }
+      __syncthreads();
+      // Cholesky H = R^T R in place (upper triangle), pivots floored at 1e-28 of the largest
+      double hmax = 0.0;
+      for (int k = 0; k < CB; ++k) hmax = fmax(hmax, Hs[k][k]);
+      const double floor_piv = 1e-28 * hmax + 1e-300;
+      for (int k = 0; k < CB; ++k) {
+        const double pk = Hs[k][k] > floor_piv ? Hs[k][k] : floor_piv;
+        const double dk = sqrt(pk);
+        __syncthreads();   // every thread has read Hs[k][k]
+        for (int j = k + tid; j < CB; j += 256) Hs[k][j] = (j == k) ? dk : Hs[k][j] / dk;
+        __syncthreads();
+        for (int e = tid; e < CB * CB; e += 256) {
+          const int i = e / CB, j = e & (CB - 1);
+          if (i > k && j >= i) Hs[i][j] -= Hs[k][i] * Hs[k][j];
+        }
+        __syncthreads();
+      }
+      // X = R^{-1} (upper triangular), one column per thread
+      for (int e = tid; e < CB * CB; e += 256) Xs[e / CB][e & (CB - 1)] = 0.0;
+      __syncthreads();
+      if (tid < CB) {
+        const int j = tid;
+        Xs[j][j] = 1.0 / Hs[j][j];
+        for (int i = j - 1; i >= 0; --i) {
+          double a = 0.0;
+          for (int k = i + 1; k <= j; ++k) a = fma(Hs[i][k], Xs[k][j], a);
+          Xs[i][j] = -a / Hs[i][i];
+        }
+      }
+      __syncthreads();
+      // Cb <- Cb X
+      for (int64_t r0 = 0; r0 < s; r0 += CB) {
+        double acc[4][4] = {};
+        cb_mm<false>(acc, CB, [&](int i, int64_t k) { return r0 + i < s ? Cb[(r0 + i) * CB + k] : 0.0; },
+                     [&](int64_t k, int j) { return Xs[k][j]; }, As, Bs);
+        __syncthreads();   // the whole row block is staged before it is overwritten
+#pragma unroll
+        for (int x = 0; x < 4; ++x)
+#pragma unroll
+          for (int y = 0; y < 4; ++y) {
+            const int64_t i = r0 + 4 * ti + x;
+            if (i < s) Cb[i * CB + 4 * tj + y] = acc[x][y];
+          }
+      }
+      __syncthreads();
+    }
+    // signs: each column's largest-magnitude entry positive (lowest index on ties)
+    {
+      const int j = tid & (CB - 1), part = tid >> 6;
+      double best = -1.0;
+      int bi = 0;
+      for (int64_t i = part; i < s; i += 4) {
+        const double v = fabs(Cb[i * CB + j]);
+        if (v > best) { best = v; bi = (int)i; }
+      }
+      bvl[part][j] = best;
+      bil[part][j] = bi;
+      __syncthreads();
+      if (tid < CB) {
+        for (int p2 = 1; p2 < 4; ++p2)
+          if (bvl[p2][j] > best || (bvl[p2][j] == best && bil[p2][j] < bi)) { best = bvl[p2][j]; bi = bil[p2][j]; }
+        sgn[j] = Cb[(int64_t)bi * CB + j] < 0.0 ? -1.0 : 1.0;
+      }
+      __syncthreads();
+    }
+    for (int64_t e = tid; e < s * nb; e += 256) {
+      const int64_t i = e / nb;
+      const int j = (int)(e % nb), col = J + j;
+      const float v = (float)(sgn[j] * Cb[i * CB + j]);
+      P[i * r + col] = v;
+      if (d.operand_bf16) {
+        ((bf16*)d.Pop)[d.kp ? kp_index(i, col, s) : i * r + col] = f2bf(v);
+        ((bf16*)d.Ptop)[d.kp ? kp_index(col, i, r) : (int64_t)col * s + i] = f2bf(v);
+      } else {
+        ((float*)d.Pop)[i * r + col] = v;
+        ((float*)d.Ptop)[(int64_t)col * s + i] = v;
+      }
+    }
+    __syncthreads();   // the next block reads these columns
   }
 }
 
@@ -687,6 +917,24 @@ hipError_t launch_finalize_out(const RefDev* d, int n, int32_t rmax, hipStream_t
   if (!n || !cblocks) return hipSuccess;
   hipLaunchKernelGGL(k_finalize_out, dim3(n * cblocks), dim3(256), 0, st, d, cblocks);
   return hipGetLastError();
+}
+hipError_t launch_complete_basis(const RefDev* d, int n, hipStream_t st) {
+  if (!n) return hipSuccess;
+  hipLaunchKernelGGL(k_complete_basis, dim3(n), dim3(256), 0, st, d);
+  return hipGetLastError();
+}
+__global__ __launch_bounds__(256) void k_canonical_projector(float* __restrict__ P32, int64_t s, int64_t r) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e < s * r) P32[e] = (e / r == e % r) ? 1.f : 0.f;
+}
+hipError_t launch_canonical_projector(float* P32, void* Pop, void* Ptop, int64_t s, int64_t r, int operand_bf16,
+                                      int kp, hipStream_t st) {
+  const int64_t total = s * r;
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_canonical_projector, dim3((uint32_t)((total + 255) / 256)), dim3(256), 0, st, P32, s, r);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return launch_convert_projector(P32, Pop, Ptop, s, r, operand_bf16, kp, st);
 }
 hipError_t launch_convert_projector(const float* P32, void* Pop, void* Ptop, int64_t s, int64_t r,
                                     int operand_bf16, int kp, hipStream_t st) {

@@ -32,7 +32,7 @@ MOARA_NUM_KERNELS = 5
 EXPORTED = (
     "moara_default_config", "moara_allocate_ranks", "moara_resolve_matrix", "moara_state_bytes",
     "moara_create_state", "moara_refresh_projector", "moara_step", "moara_alignment", "moara_get_tensor",
-    "moara_set_tensor",
+    "moara_set_tensor", "moara_refresh_info",
     "moara_set_timing", "moara_kernel_stats", "moara_reset_kernel_stats", "moara_matrix_info",
     "moara_destroy_state", "moara_last_error", "moara_version",
 )
@@ -93,6 +93,7 @@ def lib():
         "moara_alignment": (ctypes.c_int, [vp, P(vp), P(ctypes.c_uint8), P(ctypes.c_double), vp]),
         "moara_get_tensor": (ctypes.c_int, [vp, i32, i32, vp, ctypes.c_size_t, vp]),
         "moara_set_tensor": (ctypes.c_int, [vp, i32, i32, vp, ctypes.c_size_t, vp]),
+        "moara_refresh_info": (ctypes.c_int, [vp, i32, P(i32), P(i32), P(i32), P(ctypes.c_float), vp]),
         "moara_set_timing": (ctypes.c_int, [vp, i32]),
         "moara_kernel_stats": (ctypes.c_int, [vp, i32, P(i64), P(ctypes.c_double), vp]),
         "moara_reset_kernel_stats": (ctypes.c_int, [vp, vp]),
@@ -291,7 +292,8 @@ def moara_step(st: State, weights, grads, lr: float, active=None, stream=None, a
         w, g = args.w, args.g
     else:
         wd = "bf16" if st.cfg.weight_dtype == MOARA_BF16 else "f32"
-        w = _ptr_array(st, weights, "weights", wd, active)
+        # zero_grad_mode 1 updates the weights of inactive matrices too: check all of them
+        w = _ptr_array(st, weights, "weights", wd, None if st.cfg.zero_grad_mode == 1 else active)
         g = _ptr_array(st, grads, "grads", "f32", active)
     act = active if isinstance(active, ctypes.Array) else _active_array(st, active)
     _check(lib().moara_step(st.handle, w, g, act, ctypes.c_float(lr), _stream_ptr(stream)))
@@ -327,6 +329,14 @@ def moara_set_tensor(st: State, mat: int, which: int, value, stream=None):
         if a.shape != _tensor_shape(st, mat, which):
             raise ValueError(f"tensor {which} of matrix {mat} must have shape {_tensor_shape(st, mat, which)}")
     _check(lib().moara_set_tensor(st.handle, int(mat), int(which), a.ctypes.data, a.nbytes, _stream_ptr(stream)))
+
+
+def moara_refresh_info(st: State, mat: int, stream=None) -> dict:
+    """moara_refresh_info of the C ABI: the record of the matrix's last refresh."""
+    sw, cv, rk, off = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_int32(), ctypes.c_float()
+    _check(lib().moara_refresh_info(st.handle, int(mat), ctypes.byref(sw), ctypes.byref(cv), ctypes.byref(rk),
+                                    ctypes.byref(off), _stream_ptr(stream)))
+    return {"sweeps": sw.value, "converged": bool(cv.value), "rank": rk.value, "offdiag": off.value}
 
 
 def moara_set_timing(st: State, enable: bool):

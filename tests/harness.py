@@ -61,7 +61,7 @@ def oracle_cfg(c: Case, i: int, refresh_interval: int = 0) -> O.OracleConfig:
                           decompose=c.decompose, weight_dtype=c.weight_dtype, operand_dtype=c.operand_dtype)
 
 
-def gpu_state(c: Case, refresh_interval: int = 0, refresh_iters=None, oversample=None, seed: int = 0):
+def gpu_state(c: Case, refresh_interval: int = 0, refresh_iters=None, oversample=None, seed: int = 0, **extra):
     from paper_2609_15037_amd import moara as M
     refresh_iters = c.refresh_iters if refresh_iters is None else refresh_iters
     oversample = c.refresh_oversample if oversample is None else oversample
@@ -70,7 +70,7 @@ def gpu_state(c: Case, refresh_interval: int = 0, refresh_iters=None, oversample
         refresh_interval=refresh_interval, decompose=1 if c.decompose else 0,
         weight_dtype=M.MOARA_BF16 if c.weight_dtype == "bf16" else M.MOARA_F32,
         operand_dtype=M.MOARA_BF16 if c.operand_dtype == "bf16" else M.MOARA_F32,
-        refresh_iters=refresh_iters, refresh_oversample=oversample, refresh_seed=seed)
+        refresh_iters=refresh_iters, refresh_oversample=oversample, refresh_seed=seed, **extra)
     descs = M.make_descs([(m, n, mod, r) for (m, n, mod), r in zip(c.shapes, c.ranks)])
     return M.moara_create_state(cfg, descs)
 

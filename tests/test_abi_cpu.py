@@ -99,7 +99,7 @@ def test_resolve_matrix_errors():
 @pytest.mark.parametrize("field,value,code", [
     ("block_size", 0, -1), ("beta1", 1.0, -1), ("beta2", -0.1, -1), ("adam_eps", 0.0, -1),
     ("weight_decay", 0.01, -4), ("grad_dtype", 1, -4), ("operand_dtype", 7, -1), ("refresh_iters", 0, -1),
-    ("refresh_interval", -1, -1), ("zero_grad_mode", 1, -4), ("decompose", 2, -1), ("reserved", 3, -1),
+    ("refresh_interval", -1, -1), ("zero_grad_mode", 2, -1), ("decompose", 2, -1), ("reserved", 3, -1),
 ])
 def test_create_state_validates_before_touching_the_gpu(field, value, code):
     _lib()
@@ -146,6 +146,7 @@ def test_state_bytes_counts_fp32_moments_projector_copies_and_v_workspace():
         if n % 4 == 0 and r % 4 == 0 and ((left and m % 32 == 0 and k <= 160) or
                                           (not left and n % 32 == 0 and k <= 512)):
             exp += al(2 * m * n)
+    exp += al(16 * len(shapes))   # one refresh record (four int32) per matrix
     assert sb == exp and rb > 0
     # fp32 operands never materialise V
     cfg32 = M.moara_default_config(rank_table=[64] * 10, block_size=64, operand_dtype=M.MOARA_F32)
@@ -154,6 +155,7 @@ def test_state_bytes_counts_fp32_moments_projector_copies_and_v_workspace():
     for m, n in shapes:
         s, L, k, r = min(m, n), max(m, n), -(-n // 64), 64
         exp32 += 4 * al(4 * m * k) + 2 * al(4 * L * r) + al(4 * L * r) + al(4 * s * r) + 2 * al(4 * s * r)
+    exp32 += al(16 * len(shapes))
     assert sb32 == exp32
 
 

@@ -205,6 +205,9 @@ def test_refresh_layer_d256_principal_angles():
     Ps = [M.moara_get_tensor(st, i, M.MOARA_T_P) for i in range(len(Gs))]
     worst = _angles_vs_oracle(c, Gs, Ps)
     print(f"[refresh] worst principal angle {worst:.2e}", flush=True)
+    for i in range(len(Gs)):   # the Jacobi sweeps met their tolerance and kept all r directions
+        info = M.moara_refresh_info(st, i)
+        assert info["converged"] and info["rank"] == c.ranks[i] and info["offdiag"] < 1e-8, (i, info)
 
 
 def test_refresh_lowrank_llama300m_layer():
@@ -220,6 +223,9 @@ def test_refresh_lowrank_llama300m_layer():
     Ps = [M.moara_get_tensor(st, i, M.MOARA_T_P) for i in range(len(Gs))]
     worst = _angles_vs_oracle(c, Gs, Ps)
     print(f"[refresh] worst principal angle {worst:.2e}", flush=True)
+    for i in range(len(Gs)):
+        info = M.moara_refresh_info(st, i)
+        assert info["converged"] and info["rank"] == c.ranks[i], (i, info)
 
 
 def test_refresh_in_several_chunks_is_bit_identical(monkeypatch):
@@ -265,6 +271,55 @@ def test_refresh_inside_step_schedule():
         assert not np.array_equal(seen[1][i], seen[2][i])
 
 
+def _rank_deficient_grad(kind, m, n, rank, seed):
+    """Gradients whose direction tensor V has rank `rank` < r. 'rows': only rows 5.. 5+rank
+    of G are nonzero (V keeps those rows, any block size); 'lowrank': G = A B^T of that
+    rank, used with one block per row so that V = diag(1/M) G keeps the rank."""
+    g = rng(seed, 11, m, n, rank)
+    G = np.zeros((m, n))
+    if kind == "rows":
+        G[5:5 + rank] = g.standard_normal((rank, n))
+    else:
+        G = g.standard_normal((m, rank)) @ g.standard_normal((rank, n))
+    return (1e-3 * G).astype(np.float32)
+
+
+@pytest.mark.parametrize("op", ["f32", "bf16"])
+def test_refresh_rank_deficient_direction(op):
+    """V of rank below r (Alg. 1 TruncatedSVD of a rank-deficient V): the projector must stay
+    orthonormal, its span must contain range(V), and its leading directions (those with
+    nonzero singular values) must match the oracle's; the remaining columns complete the
+    basis (any orthonormal completion is a top-r singular basis of V)."""
+    import torch
+    M = _M()
+    specs = [("rows", 96, 160, 16, 3, 32, WL.Q), ("rows", 256, 384, 64, 20, 64, WL.K),
+             ("lowrank", 160, 96, 24, 10, 96, WL.GATE), ("lowrank", 384, 256, 64, 40, 256, WL.UP)]
+    for (kind, m, n, r, rank, B, mod), seed in ((sp, sd) for sp in specs for sd in (0, 1)):
+        c = Case(shapes=[(m, n, mod)], ranks=[r], block_size=B, operand_dtype=op)
+        st = gpu_state(c)
+        G = _rank_deficient_grad(kind, m, n, rank, seed)
+        print(f"[refresh] rank-deficient V: {kind} {m}x{n} r={r} rank(V)={rank} B={B} op={op} seed={seed}",
+              flush=True)
+        M.moara_refresh_projector(st, [to_dev(G, "f32")])
+        torch.cuda.synchronize()
+        P = M.moara_get_tensor(st, 0, M.MOARA_T_P).astype(np.float64)
+        _, V = O.decompose(G, B)
+        side = O.projection_side(m, n)
+        X = V if side == O.LEFT else V.T            # columns live in the projected space
+        orth = float(np.max(np.abs(P.T @ P - np.eye(r))))
+        resid = float(np.linalg.norm(X - P @ (P.T @ X)) / np.linalg.norm(X))
+        ref = O.truncated_svd(V, rank, side)
+        ang = O.max_principal_angle(P[:, :rank], ref)
+        print(f"[refresh]   |P^T P - I| {orth:.2e}, |V - P P^T V|/|V| {resid:.2e}, "
+              f"leading-{rank} angle {ang:.2e}", flush=True)
+        info = M.moara_refresh_info(st, 0)
+        print(f"[refresh]   record {info}", flush=True)
+        assert orth <= 2e-5
+        assert resid <= 1e-4
+        assert ang <= 1e-3
+        assert info["rank"] == rank
+
+
 def test_zero_gradient_refresh_keeps_previous_projector():
     import torch
     M = _M()
@@ -302,6 +357,113 @@ def test_inactive_matrices_are_untouched():
     assert M.moara_get_tensor(st, 1, M.MOARA_T_STEP) == 0
     assert M.moara_get_tensor(st, 0, M.MOARA_T_STEP) == 4
     assert not np.any(M.moara_get_tensor(st, 1, M.MOARA_T_EXP_AVG))
+
+
+@pytest.mark.parametrize("op,wdt", [("f32", "f32"), ("bf16", "bf16")])
+def test_zero_grad_mode_steps_inactive_matrices_with_zero_gradient(op, wdt):
+    """zero_grad_mode 1: an inactive matrix takes the step of G = 0 (Algorithm 1 with a zero
+    gradient: M = V = 0, both Adam branches decay their moments, W moves by
+    Rep_B(dM) (.) P N). Against the oracle's step(W, 0) with the same projector, and bit for
+    bit against mode 0 with the zero gradient passed explicitly as an active matrix."""
+    import torch
+    M = _M()
+    c = Case(shapes=[(128, 192, WL.EXP_GATE), (128, 192, WL.EXP_UP), (192, 128, WL.EXP_DOWN)], ranks=[16] * 3,
+             block_size=64, operand_dtype=op, weight_dtype=wdt, weight_std=0.02 if wdt == "bf16" else 1e-3)
+    tol = TOL_F32 if op == "f32" else TOL_BF16
+    n = 3
+    masks = [[1, 1, 1], [1, 0, 1], [0, 0, 1], [1, 1, 0], [0, 1, 0]]
+    grads = [[_grad(c, 12, t, i) for i in range(n)] for t in range(len(masks))]
+    st = gpu_state(c, zero_grad_mode=1)
+    ref = gpu_state(c)
+    Wd = [to_dev(w, wdt) for w in _weights(c, 0)]
+    Wr = [to_dev(w, wdt) for w in _weights(c, 0)]
+    Wo = [to_np(w) for w in Wd]
+    ocfg = [oracle_cfg(c, i) for i in range(n)]
+    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[i]) for i in range(n)]
+    for i in range(n):
+        P = oracle_projector(grads[0][i], c, i)
+        for s_ in (st, ref):
+            M.moara_set_tensor(s_, i, M.MOARA_T_P, P)
+        ost[i].P = P
+    zero = [torch.zeros(c.shapes[i][:2], device="cuda") for i in range(n)]
+    for t, mask in enumerate(masks):
+        print(f"[zero-grad] step {t} active {mask} op={op} w={wdt}", flush=True)
+        act = np.array(mask, dtype=np.uint8)
+        M.moara_step(st, Wd, [to_dev(grads[t][i], "f32") if mask[i] else None for i in range(n)], lr=c.lr,
+                     active=act)
+        M.moara_step(ref, Wr, [to_dev(grads[t][i], "f32") if mask[i] else zero[i] for i in range(n)], lr=c.lr)
+        for i in range(n):
+            G = grads[t][i] if mask[i] else np.zeros(c.shapes[i][:2])
+            Wo[i] = O.step(Wo[i], G, ost[i], ocfg[i], c.lr)
+    torch.cuda.synchronize()
+    report = {}
+    for i in range(n):
+        assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == len(masks)
+        assert torch.equal(Wd[i], Wr[i]), f"matrix {i}: zero_grad_mode 1 differs from an explicit zero gradient"
+        for k in (M.MOARA_T_EXP_AVG, M.MOARA_T_EXP_AVG_SQ, M.MOARA_T_MAG_AVG, M.MOARA_T_MAG_AVG_SQ):
+            assert np.array_equal(M.moara_get_tensor(st, i, k), M.moara_get_tensor(ref, i, k))
+        compare(f"W[{i}]", to_np(Wd[i]), Wo[i], tol, report)
+        if wdt == "f32":
+            compare_update(f"dW[{i}]", to_np(Wd[i]) - _weights(c, 0)[i], Wo[i] - _weights(c, 0)[i],
+                           max(tol, TOL_UPDATE_F32), report)
+        compare(f"exp_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG), ost[i].exp_avg, tol, report)
+        compare(f"exp_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG_SQ), ost[i].exp_avg_sq, tol, report)
+        compare(f"mag_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG), ost[i].mag_avg, tol, report)
+        compare(f"mag_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG_SQ), ost[i].mag_avg_sq, tol, report)
+    print(f"[zero-grad] worst floored rel err {max(report.values()):.3e} (tol {tol:.0e})", flush=True)
+
+
+def test_zero_grad_mode_first_refresh_sets_canonical_projector():
+    """A matrix that is inactive on its first step in zero_grad_mode 1 gets the projector of
+    a zero V (the first r canonical basis vectors), zero moments stay zero, W does not move
+    (N = 0 at t = 1), and t advances; its refresh on a later active step replaces P."""
+    import torch
+    M = _M()
+    c = Case(shapes=[(96, 160, WL.EXP_GATE), (160, 96, WL.EXP_DOWN)], ranks=[8, 12], block_size=32)
+    st = gpu_state(c, refresh_interval=2, zero_grad_mode=1)
+    Wd = [to_dev(w, "f32") for w in _weights(c, 0)]
+    W0 = [w.clone() for w in Wd]
+    M.moara_step(st, Wd, [to_dev(_grad(c, 3, 0, 0), "f32"), None], lr=1e-3, active=[1, 0])
+    torch.cuda.synchronize()
+    assert torch.equal(Wd[1], W0[1])
+    np.testing.assert_array_equal(M.moara_get_tensor(st, 1, M.MOARA_T_P), np.eye(96, 12, dtype=np.float32))
+    assert M.moara_get_tensor(st, 1, M.MOARA_T_STEP) == 1
+    assert not np.any(M.moara_get_tensor(st, 1, M.MOARA_T_EXP_AVG))
+    with pytest.raises(M.MoaraError) as e:   # no refresh record: the library did not refresh it
+        M.moara_refresh_info(st, 1)
+    assert e.value.status == M.MOARA_E_STATE
+    G1 = [_grad(c, 3, t, 1) for t in (1, 2)]
+    M.moara_step(st, Wd, [to_dev(_grad(c, 3, 1, 0), "f32"), to_dev(G1[0], "f32")], lr=1e-3)
+    M.moara_step(st, Wd, [to_dev(_grad(c, 3, 2, 0), "f32"), to_dev(G1[1], "f32")], lr=1e-3)   # t = 2: refresh
+    torch.cuda.synchronize()
+    _angles_vs_oracle(Case(shapes=[c.shapes[1]], ranks=[12], block_size=32), [G1[1]],
+                      [M.moara_get_tensor(st, 1, M.MOARA_T_P)])
+    info = M.moara_refresh_info(st, 1)
+    assert info["converged"] and info["rank"] == 12 and 1 <= info["sweeps"] <= 14, info
+
+
+def test_state_used_from_two_streams_keeps_call_order():
+    """Steps of one state alternating between two streams give bit for bit the result of
+    one stream: each call waits for the work the previous call enqueued."""
+    import torch
+    M = _M()
+    c = Case(shapes=[(256, 384, WL.Q), (384, 256, WL.GATE)], ranks=[32, 48], block_size=64, operand_dtype="bf16",
+             weight_dtype="bf16", weight_std=0.02)
+    grads = [[to_dev(_grad(c, 13, t, i), "f32") for i in range(2)] for t in range(6)]
+    outs = []
+    for two in (False, True):
+        st = gpu_state(c, refresh_interval=3)
+        Wd = [to_dev(w, "bf16") for w in _weights(c, 0)]
+        streams = [torch.cuda.Stream(), torch.cuda.Stream()] if two else [torch.cuda.current_stream()]
+        torch.cuda.synchronize()
+        for t in range(6):
+            M.moara_step(st, Wd, grads[t], lr=1e-3, stream=streams[t % len(streams)])
+        torch.cuda.synchronize()
+        outs.append(([w.clone() for w in Wd], [M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG) for i in range(2)]))
+    for a, b in zip(outs[0][0], outs[1][0]):
+        assert torch.equal(a, b)
+    for a, b in zip(outs[0][1], outs[1][1]):
+        assert np.array_equal(a, b)
 
 
 def test_checkpoint_roundtrip_is_bit_identical():
