@@ -214,6 +214,32 @@ int moara_refresh_projector(moara_state* st, const void* const* grads, const uin
 int moara_step(moara_state* st, void* const* weights, const void* const* grads,
                const uint8_t* active, float lr, void* stream);
 
+/* moara_step for callers that cannot allocate device memory (code under HIP graph
+ * capture, allocation-free serving or training loops, harnesses that forbid hipMalloc).
+ * Same arguments, semantics and results as moara_step, bit for bit, but it calls no
+ * hipMalloc, hipFree, hipHostMalloc or other device/pinned allocator: the step's
+ * descriptors, and when a refresh falls due its descriptors and workspace, live in one
+ * fixed array of MOARA_NOALLOC_SCRATCH_BYTES per GPU that the library holds until the
+ * process ends (its address on each GPU is looked up once, when a state is created on
+ * that GPU). A due refresh runs in chunks that fit the array.
+ * Limits, checked before anything is enqueued (nothing changes on error):
+ * MOARA_E_UNSUPPORTED when the state's step descriptors take more than the array minus
+ * 8 MiB, or when one matrix due for a refresh needs more workspace than the rest of it
+ * (e.g. 18944 x 3584 at r = 1024; every Llama-2-7B, Llama-300M and DeepSeek-MoE matrix
+ * fits). Such matrices are refreshed with moara_step or moara_refresh_projector, or with
+ * refresh_interval = 0 and explicit refreshes outside the allocation-free region.
+ * Sharing: every call on one GPU uses that GPU's array, and the array keeps the last
+ * call's contents (every region a call reads is written or cleared by it first). Calls on
+ * one GPU are ordered on the GPU through an event that each call records and the next
+ * one's stream waits on, but calls from two host threads at the same time on one GPU
+ * race: serialise them. Per-kernel timing (moara_set_timing) is not recorded. Host
+ * bookkeeping uses ordinary heap memory; a refresh chunk's descriptors are copied from
+ * it synchronously (the call then waits for that copy). Errors: as moara_step, plus
+ * MOARA_E_UNSUPPORTED for the limits above. */
+#define MOARA_NOALLOC_SCRATCH_BYTES (512ull << 20)
+int moara_step_noalloc(moara_state* st, void* const* weights, const void* const* grads,
+                       const uint8_t* active, float lr, void* stream);
+
 /* Subspace alignment diagnostic of Section 3.2 (Eq. module_alignment; the
  * quantity logged in Algorithm 1, Phases 1-2): for every active matrix,
  *   out_S[i] = cos(G_i, G_recon,i) = <G, G_recon>_F / (||G||_F ||G_recon||_F),

@@ -8,6 +8,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -39,6 +40,39 @@ int fail(int code, const char* fmt, ...) {
 
 constexpr size_t ALIGN = 256;
 size_t align_up(size_t x) { return (x + ALIGN - 1) & ~(ALIGN - 1); }
+
+// ------------------------------------------------------------------ allocation-free scratch
+// moara_step_noalloc takes every buffer beyond the caller's and the state's own memory
+// (step and refresh descriptors, the refresh workspace) from this fixed array instead of
+// allocating. Each GPU the library runs on holds one copy until the process ends. In host
+// code `scratch` names a host-side stand-in: the device address of a GPU's copy comes
+// from hipGetSymbolAddress with that GPU current (scratch_init, called when a state is
+// created) and only that address is ever handed to kernels or copies.
+constexpr size_t NOALLOC_SCRATCH_BYTES = (size_t)MOARA_NOALLOC_SCRATCH_BYTES;
+constexpr size_t NOALLOC_REF_DESC_BYTES = (size_t)8 << 20;   // refresh descriptors of one chunk
+constexpr int MAX_DEVICES = 64;
+}  // namespace
+static __device__ __align__(256) char scratch[NOALLOC_SCRATCH_BYTES];
+namespace {
+std::mutex g_scratch_mu;
+char* g_scratch_ptr[MAX_DEVICES] = {};
+hipEvent_t g_scratch_ev[MAX_DEVICES] = {};   // recorded at the end of every no-alloc call on the GPU
+bool g_scratch_ev_valid[MAX_DEVICES] = {};
+
+int scratch_init(int dev) {
+  if (dev < 0 || dev >= MAX_DEVICES) return fail(MOARA_E_ARG, "device %d out of range for the scratch table", dev);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (g_scratch_ptr[dev]) return MOARA_OK;
+  void* p = nullptr;
+  const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  if (e != hipSuccess || !p) return fail(MOARA_E_HIP, "hipGetSymbolAddress(scratch): %s", hipGetErrorString(e));
+  hipEvent_t ev = nullptr;
+  const hipError_t e2 = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+  if (e2 != hipSuccess) return fail(MOARA_E_HIP, "scratch event: %s", hipGetErrorString(e2));
+  g_scratch_ptr[dev] = (char*)p;
+  g_scratch_ev[dev] = ev;
+  return MOARA_OK;
+}
 
 struct MatHost {
   int64_t m = 0, n = 0, L = 0, s = 0;
@@ -87,6 +121,9 @@ struct moara_state {
   // enqueues work on the state; the next call's stream waits on it first
   hipEvent_t order_ev = nullptr;
   bool order_valid = false;
+  // inside moara_step_noalloc: dev_arena, ref_arena and ref_ws point into the scratch
+  // array (NoallocView) and nothing may be allocated
+  bool noalloc = false;
   // timing
   bool timing = false;
   std::vector<TimedLaunch> pending;
@@ -592,6 +629,9 @@ struct RefMat {
 
 int ensure_ref_ws(moara_state* st, size_t bytes) {
   if (bytes <= st->ref_ws_bytes) return MOARA_OK;
+  if (st->noalloc)
+    return fail(MOARA_E_UNSUPPORTED, "refresh workspace of %zu bytes exceeds the no-alloc scratch (%zu bytes)", bytes,
+                st->ref_ws_bytes);
   if (st->ref_ws) {
     HIP_TRY(hipDeviceSynchronize());
     hipFree(st->ref_ws);
@@ -872,6 +912,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   size_t total = 0;
   std::vector<size_t> offs;
   for (auto& pp : parts) { offs.push_back(total); total += align_up(pp.b ? pp.b : 1); }
+  if (total > st->ref_arena_bytes && st->noalloc)
+    return fail(MOARA_E_UNSUPPORTED, "refresh descriptors of %zu bytes exceed the no-alloc scratch (%zu bytes)", total,
+                st->ref_arena_bytes);
   if (total > st->ref_arena_bytes) {
     HIP_TRY(hipStreamSynchronize(stream));
     if (st->ref_arena) hipFree(st->ref_arena);
@@ -883,9 +926,18 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   }
   // the pinned buffer and arena are shared by all refresh chunks: wait for earlier users
   HIP_TRY(hipStreamSynchronize(stream));
-  for (size_t q = 0; q < parts.size(); ++q)
-    if (parts[q].b) memcpy(st->ref_host + offs[q], parts[q].p, parts[q].b);
-  HIP_TRY(hipMemcpyAsync(st->ref_arena, st->ref_host, total, hipMemcpyHostToDevice, stream));
+  if (st->noalloc) {
+    // no pinned buffer of our own: copy from ordinary host memory and wait for the copy
+    std::vector<char> hb(total);
+    for (size_t q = 0; q < parts.size(); ++q)
+      if (parts[q].b) memcpy(hb.data() + offs[q], parts[q].p, parts[q].b);
+    HIP_TRY(hipMemcpyAsync(st->ref_arena, hb.data(), total, hipMemcpyHostToDevice, stream));
+    HIP_TRY(hipStreamSynchronize(stream));
+  } else {
+    for (size_t q = 0; q < parts.size(); ++q)
+      if (parts[q].b) memcpy(st->ref_host + offs[q], parts[q].p, parts[q].b);
+    HIP_TRY(hipMemcpyAsync(st->ref_arena, st->ref_host, total, hipMemcpyHostToDevice, stream));
+  }
   auto D = [&](int q) { return (const void*)(st->ref_arena + offs[q]); };
   const RefDev* RD = (const RefDev*)D(0);
 
@@ -988,27 +1040,78 @@ size_t refresh_budget() {
   return REFRESH_BUDGET;
 }
 
+// Upper bound of one refresh chunk's descriptor bytes (refresh_chunk's parts: RefDev,
+// two Gram lists, at most ten GEMM lists, two transpose lists and the Cholesky and
+// inverse prefix arrays, each part aligned).
+size_t ref_desc_bound(size_t nm, int nbmax) {
+  const int nlev = std::max(1, trtri_levels(nbmax));
+  return 24 * ALIGN + nm * (sizeof(RefDev) + 2 * sizeof(GramProb) + 10 * sizeof(GemmProb) + 2 * sizeof(TransProb) +
+                            4 * (2 * (size_t)nbmax + (size_t)nlev));
+}
+
 // Refresh the matrices idx in order, in chunks whose workspace stays within the budget
-// (a matrix larger than the budget forms a chunk of its own).
+// (a matrix larger than the budget forms a chunk of its own). Without allocation the
+// budget is the scratch array's workspace part, and a chunk's descriptors must also fit
+// its descriptor part.
 int refresh_in_chunks(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream,
                       const std::vector<char>& usev) {
-  const size_t budget = refresh_budget();
+  const bool na = st->noalloc;
+  const size_t budget = na ? st->ref_ws_bytes : refresh_budget();
   std::vector<int> chunk;
   size_t bytes = 0;
+  int nbm = 1;
   int rc;
   for (int i : idx) {
     const MatHost& h = st->mats[i];
-    const size_t b = mat_refresh_bytes(h.s, h.L, subspace_width(st->cfg, h.s, h.r), h.r, usev[i]);
-    if (!chunk.empty() && bytes + b > budget) {
+    const int32_t w = subspace_width(st->cfg, h.s, h.r);
+    const size_t b = mat_refresh_bytes(h.s, h.L, w, h.r, usev[i]);
+    const int nbm2 = std::max(nbm, chol_blocks(w));
+    if (!chunk.empty() &&
+        (bytes + b > budget || (na && ref_desc_bound(chunk.size() + 1, nbm2) > st->ref_arena_bytes))) {
       if ((rc = refresh_chunk(st, chunk, grads, stream, &usev))) return rc;
       chunk.clear();
       bytes = 0;
+      nbm = 1;
     }
     chunk.push_back(i);
     bytes += b;
+    nbm = std::max(nbm, chol_blocks(w));
   }
   return refresh_chunk(st, chunk, grads, stream, &usev);
 }
+
+// For the duration of one moara_step_noalloc call, the state's descriptor arena,
+// refresh descriptor arena and refresh workspace are views into the scratch array:
+//   [0, A)               step descriptors (A = the state's arena size)
+//   [A, A + RD)          refresh descriptors of one chunk
+//   [A + RD, capacity)   refresh workspace
+// Timing events are off (creating them could allocate). Restored on exit.
+struct NoallocView {
+  moara_state* st;
+  bool on;
+  char *arena = nullptr, *ws = nullptr, *ra = nullptr;
+  size_t wsb = 0, rab = 0;
+  bool timing = false;
+  NoallocView(moara_state* s, char* base, bool enable) : st(s), on(enable) {
+    if (!on) return;
+    arena = st->dev_arena; ws = st->ref_ws; wsb = st->ref_ws_bytes; ra = st->ref_arena; rab = st->ref_arena_bytes;
+    timing = st->timing;
+    const size_t A = align_up(st->arena_bytes);
+    st->dev_arena = base;
+    st->ref_arena = base + A;
+    st->ref_arena_bytes = NOALLOC_REF_DESC_BYTES;
+    st->ref_ws = base + A + NOALLOC_REF_DESC_BYTES;
+    st->ref_ws_bytes = NOALLOC_SCRATCH_BYTES - A - NOALLOC_REF_DESC_BYTES;
+    st->timing = false;
+    st->noalloc = true;
+  }
+  ~NoallocView() {
+    if (!on) return;
+    st->dev_arena = arena; st->ref_ws = ws; st->ref_ws_bytes = wsb; st->ref_arena = ra; st->ref_arena_bytes = rab;
+    st->timing = timing;
+    st->noalloc = false;
+  }
+};
 
 int run_refresh(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream) {
   if (idx.empty()) return MOARA_OK;
@@ -1151,6 +1254,7 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
   st->cfg = *cfg;
   st->n = n;
   if (hipGetDevice(&st->device) != hipSuccess) { free_state(st); return fail(MOARA_E_HIP, "hipGetDevice failed (no GPU?)"); }
+  if ((rc = scratch_init(st->device))) { free_state(st); return rc; }   // this GPU's scratch address, once
   st->mats.resize(n);
   size_t tot = 0;
   for (int i = 0; i < n; ++i) {
@@ -1308,8 +1412,8 @@ int moara_alignment(moara_state* st, const void* const* grads, const uint8_t* ac
   return MOARA_OK;
 }
 
-int moara_step(moara_state* st, void* const* weights, const void* const* grads, const uint8_t* active, float lr,
-               void* stream) {
+static int step_impl(moara_state* st, void* const* weights, const void* const* grads, const uint8_t* active,
+                     float lr, void* stream, bool noalloc) {
   if (!st) return fail(MOARA_E_ARG, "state is NULL");
   if (!weights || !grads) return fail(MOARA_E_ARG, "weights/grads is NULL");
   if (!isfinite(lr)) return fail(MOARA_E_ARG, "lr must be finite");
@@ -1341,7 +1445,30 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
   }
   if (idx.empty() && zidx.empty()) return MOARA_OK;
   hipStream_t hs = (hipStream_t)stream;
+  char* base = nullptr;
+  if (noalloc) {
+    // every limit is checked before anything is enqueued
+    base = (st->device >= 0 && st->device < MAX_DEVICES) ? g_scratch_ptr[st->device] : nullptr;
+    if (!base) return fail(MOARA_E_STATE, "no scratch address for device %d", st->device);
+    const size_t A = align_up(st->arena_bytes);
+    if (A + NOALLOC_REF_DESC_BYTES >= NOALLOC_SCRATCH_BYTES)
+      return fail(MOARA_E_UNSUPPORTED, "the state's step descriptors (%zu bytes) do not fit the no-alloc scratch", A);
+    const size_t wcap = NOALLOC_SCRATCH_BYTES - A - NOALLOC_REF_DESC_BYTES;
+    for (int i : need) {
+      const MatHost& h = st->mats[i];
+      const int32_t w = subspace_width(st->cfg, h.s, h.r);
+      const bool bf = h.vpath && (((uintptr_t)grads[i] & 15) == 0);
+      const size_t b = mat_refresh_bytes(h.s, h.L, w, h.r, bf);
+      if (b > wcap)
+        return fail(MOARA_E_UNSUPPORTED,
+                    "matrix %d (%lld x %lld, r = %d) needs a refresh workspace of %zu bytes, more than the %zu bytes "
+                    "the no-alloc scratch holds (refresh it with moara_step or moara_refresh_projector)",
+                    i, (long long)h.m, (long long)h.n, h.r, b, wcap);
+    }
+  }
   ORDER_ON(st, hs);
+  if (noalloc && g_scratch_ev_valid[st->device]) HIP_TRY(hipStreamWaitEvent(hs, g_scratch_ev[st->device], 0));
+  NoallocView view(st, base, noalloc);
   std::vector<char> usev(st->n, 0);
   for (int i : idx) usev[i] = st->mats[i].vpath && (((uintptr_t)grads[i] & 15) == 0);
   if (st->cfg.decompose) {
@@ -1355,7 +1482,21 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads, 
   rc = run_project_back(st, all, weights, grads, lr, hs, &usev, &zflag);
   if (rc) return rc;
   for (int i : all) st->mats[i].t += 1;
+  if (noalloc) {
+    HIP_TRY(hipEventRecord(g_scratch_ev[st->device], hs));
+    g_scratch_ev_valid[st->device] = true;
+  }
   return MOARA_OK;
+}
+
+int moara_step(moara_state* st, void* const* weights, const void* const* grads, const uint8_t* active, float lr,
+               void* stream) {
+  return step_impl(st, weights, grads, active, lr, stream, false);
+}
+
+int moara_step_noalloc(moara_state* st, void* const* weights, const void* const* grads, const uint8_t* active,
+                       float lr, void* stream) {
+  return step_impl(st, weights, grads, active, lr, stream, true);
 }
 
 static int tensor_geometry(moara_state* st, int32_t mat, int32_t which, size_t* bytes) {

@@ -31,7 +31,8 @@ MOARA_NUM_KERNELS = 5
 
 EXPORTED = (
     "moara_default_config", "moara_allocate_ranks", "moara_resolve_matrix", "moara_state_bytes",
-    "moara_create_state", "moara_refresh_projector", "moara_step", "moara_alignment", "moara_get_tensor",
+    "moara_create_state", "moara_refresh_projector", "moara_step", "moara_step_noalloc", "moara_alignment",
+    "moara_get_tensor",
     "moara_set_tensor", "moara_refresh_info",
     "moara_set_timing", "moara_kernel_stats", "moara_reset_kernel_stats", "moara_matrix_info",
     "moara_destroy_state", "moara_last_error", "moara_version",
@@ -90,6 +91,7 @@ def lib():
         "moara_create_state": (ctypes.c_int, [P(moara_config), P(moara_matrix_desc), i32, vp, P(vp)]),
         "moara_refresh_projector": (ctypes.c_int, [vp, P(vp), P(ctypes.c_uint8), vp]),
         "moara_step": (ctypes.c_int, [vp, P(vp), P(vp), P(ctypes.c_uint8), ctypes.c_float, vp]),
+        "moara_step_noalloc": (ctypes.c_int, [vp, P(vp), P(vp), P(ctypes.c_uint8), ctypes.c_float, vp]),
         "moara_alignment": (ctypes.c_int, [vp, P(vp), P(ctypes.c_uint8), P(ctypes.c_double), vp]),
         "moara_get_tensor": (ctypes.c_int, [vp, i32, i32, vp, ctypes.c_size_t, vp]),
         "moara_set_tensor": (ctypes.c_int, [vp, i32, i32, vp, ctypes.c_size_t, vp]),
@@ -284,10 +286,14 @@ def moara_active_mask(st: State, active):
     return _active_array(st, active)
 
 
-def moara_step(st: State, weights, grads, lr: float, active=None, stream=None, args: StepArgs = None):
-    """moara_step of the C ABI. With `args` (a StepArgs of the same tensors) the pointer
-    arrays are reused and `weights` / `grads` are ignored; `active` may be a mask from
-    moara_active_mask."""
+MOARA_NOALLOC_SCRATCH_BYTES = 512 << 20
+
+
+def moara_step(st: State, weights, grads, lr: float, active=None, stream=None, args: StepArgs = None,
+               noalloc: bool = False):
+    """moara_step of the C ABI (moara_step_noalloc with noalloc=True). With `args` (a
+    StepArgs of the same tensors) the pointer arrays are reused and `weights` / `grads` are
+    ignored; `active` may be a mask from moara_active_mask."""
     if args is not None:
         w, g = args.w, args.g
     else:
@@ -296,7 +302,13 @@ def moara_step(st: State, weights, grads, lr: float, active=None, stream=None, a
         w = _ptr_array(st, weights, "weights", wd, None if st.cfg.zero_grad_mode == 1 else active)
         g = _ptr_array(st, grads, "grads", "f32", active)
     act = active if isinstance(active, ctypes.Array) else _active_array(st, active)
-    _check(lib().moara_step(st.handle, w, g, act, ctypes.c_float(lr), _stream_ptr(stream)))
+    fn = lib().moara_step_noalloc if noalloc else lib().moara_step
+    _check(fn(st.handle, w, g, act, ctypes.c_float(lr), _stream_ptr(stream)))
+
+
+def moara_step_noalloc(st: State, weights, grads, lr: float, active=None, stream=None, args: StepArgs = None):
+    """moara_step_noalloc of the C ABI: moara_step without any device allocation."""
+    moara_step(st, weights, grads, lr, active=active, stream=stream, args=args, noalloc=True)
 
 
 def _tensor_shape(st: State, mat: int, which: int):
