@@ -170,3 +170,34 @@ def compare(name: str, got: np.ndarray, ref: np.ndarray, tol: float, report: dic
     assert e <= tol, f"{name}: floored relative error {e:.3e} > {tol:.1e} on well-conditioned elements"
     assert em <= TOL_MASKED, f"{name}: {em:.3e} on elements fed by ill-conditioned Adam inputs"
     return e
+
+
+def bf16_ulp(x: np.ndarray) -> np.ndarray:
+    """Spacing of bfloat16 values at |x| (8 significant bits; subnormal spacing at the bottom)."""
+    a = np.abs(np.asarray(x, dtype=np.float64))
+    e = np.floor(np.log2(np.maximum(a, 2.0 ** -126)))
+    return np.ldexp(1.0, (np.maximum(e, -126) - 7).astype(int))
+
+
+def magnitude_steps(st, cfg) -> np.ndarray:
+    """The Optimizer_M output dM of the oracle's last step, read back from its moments
+    (for reporting how far the magnitude branch moved the update, not for parity)."""
+    t = st.t
+    return ((st.mag_avg / (1.0 - cfg.beta1 ** t)) /
+            (np.sqrt(st.mag_avg_sq / (1.0 - cfg.beta2 ** t)) + cfg.adam_eps))
+
+
+def seeded_history(c: Case, i: int, R_scale: float, M_scale: np.ndarray, seed: int):
+    """Moments of a matrix restored at a late step (as from a checkpoint): per-entry first
+    moments around zero (direction) or around the block magnitudes (magnitude), second
+    moments spread over a decade and a half; fp32 values, fed to both sides."""
+    m, n, _ = c.shapes[i]
+    g = rng(seed, 21, i)
+    side = O.projection_side(m, n)
+    shp = (c.ranks[i], n) if side == O.LEFT else (m, c.ranks[i])
+    e1 = R_scale * 0.3 * g.standard_normal(shp)
+    e2 = (R_scale ** 2) * 10.0 ** g.uniform(-0.5, 1.0, shp)
+    k = M_scale.shape[1]
+    a1 = M_scale * 10.0 ** g.uniform(-0.3, 0.3, (m, k))
+    a2 = (a1 ** 2) * 10.0 ** g.uniform(0.0, 1.5, (m, k))
+    return [O.round_f32(x) for x in (e1, e2, a1, a2)]

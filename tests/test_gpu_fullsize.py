@@ -219,3 +219,107 @@ def test_deepseek_moe_layer_routed_experts():
         compare(f"mag_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG), ost[i].mag_avg, TOL_BF16, report)
     print(f"[fullsize] deepseek_moe: {sum(o.t > 0 for o in ost)} of {n} matrices stepped, {refreshed} refreshes "
           f"(worst angle {worst_angle:.2e}), worst floored rel err {max(report.values()):.3e}", flush=True)
+
+
+def test_qwen2_7b_mlp_refresh():
+    """The Qwen2-7B MLP projectors (gate / up 18944 x 3584, RIGHT; down 3584 x 18944, LEFT;
+    r = 1024, subspace width 2048) refreshed in one call at the full q = 20: orthonormal,
+    Jacobi converged, within 1e-3 rad of the oracle's truncated SVD of V (gate and down;
+    up has gate's shape and rank)."""
+    import torch
+    M = _M()
+    wl = WL.subset(WL.WORKLOADS["qwen2_7b"], [0])
+    keep = [i for i, m in enumerate(wl.matrices) if m.module in (WL.GATE, WL.UP, WL.DOWN)]
+    wl = dataclasses.replace(wl, matrices=tuple(wl.matrices[i] for i in keep))
+    c = case_from_workload(wl)
+    st = gpu_state(c)
+    Gs = [WL.grad_np(wl, i, 0) for i in range(len(wl.matrices))]
+    print("[fullsize] qwen2_7b MLP refresh (18944 x 3584, r = 1024)", flush=True)
+    M.moara_refresh_projector(st, [to_dev(g, "f32") for g in Gs])
+    torch.cuda.synchronize()
+    for i, G in enumerate(Gs):
+        info = M.moara_refresh_info(st, i)
+        assert info["converged"] and info["rank"] == c.ranks[i], (wl.matrices[i].name, info)
+        if wl.matrices[i].module == WL.UP:
+            continue
+        Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+        _, V = O.decompose(G, c.block_size)
+        print(f"[fullsize] oracle SVD of {wl.matrices[i].name} {G.shape}", flush=True)
+        ref = O.truncated_svd(V, c.ranks[i], O.projection_side(*G.shape))
+        np.testing.assert_allclose(Pg.T @ Pg, np.eye(Pg.shape[1]), atol=2e-5)
+        ang = O.max_principal_angle(Pg, ref)
+        print(f"[fullsize] {wl.matrices[i].name} {G.shape} r={c.ranks[i]}: principal angle {ang:.2e}, "
+              f"{info['sweeps']} Jacobi sweeps", flush=True)
+        assert ang <= 1e-3
+
+
+def test_deepseek_moe_full_state_one_layer_checked():
+    """All 5,656 matrices of the DeepSeek-MoE batch (28 layers: attention, 2 shared and 64
+    routed experts) in one state, stepped with the router's active set (6 of 64 routed
+    experts per layer and step) exactly as the benchmark runs them; per-expert refresh on
+    an expert's first active step (T = 200). The oracle follows every matrix of the last
+    layer: refreshes by principal angle, then the step with the library's projector; idle
+    experts must stay bit-identical."""
+    import torch
+    M = _M()
+    wl = WL.WORKLOADS["deepseek_moe"]
+    n = len(wl.matrices)
+    c = case_from_workload(wl)
+    L = max(m.layer for m in wl.matrices)
+    idx = [i for i, m in enumerate(wl.matrices) if m.layer == L]
+    st = gpu_state(c, refresh_interval=200)
+    Wd = [WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
+          for i, m in enumerate(wl.matrices)]
+    W0 = {i: to_np(Wd[i]) for i in idx}
+    Wo = dict(W0)
+    ocfg = {i: oracle_cfg(c, i) for i in idx}
+    ost = {i: O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[i]) for i in idx}
+    report, refreshed, worst_angle = {}, 0, 0.0
+    for t in range(3):
+        act = np.asarray(WL.active_set(wl, t), dtype=np.uint8)
+        Gd, Gs = [], {}
+        for i, m in enumerate(wl.matrices):
+            if not act[i]:
+                Gd.append(None)
+                continue
+            g = torch.empty((m.rows, m.cols), dtype=torch.float32, device="cuda")
+            if i in ost:
+                Gs[i] = WL.grad_np(wl, i, t, active=True)
+                g.copy_(torch.from_numpy(Gs[i]))
+            else:
+                WL.grad_device(wl, i, t, g, active=True)
+            Gd.append(g)
+        torch.cuda.synchronize()
+        print(f"[fullsize] deepseek_moe full state: step {t}, {int(act.sum())} of {n} matrices active, oracle on "
+              f"layer {L}", flush=True)
+        M.moara_step(st, Wd, Gd, lr=c.lr, active=act)
+        torch.cuda.synchronize()
+        del Gd
+        for i in idx:
+            if not act[i]:
+                continue
+            if ost[i].t == 0:   # the library refreshed this matrix on its first active step
+                Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+                _, V = O.decompose(Gs[i], c.block_size)
+                ang = O.max_principal_angle(Pg, O.truncated_svd(V, c.ranks[i], ost[i].side))
+                worst_angle = max(worst_angle, ang)
+                assert ang <= 1e-3, f"{wl.matrices[i].name}: refresh principal angle {ang:.2e}"
+                ost[i].P = O.round_f32(Pg)
+                refreshed += 1
+            Wo[i] = O.step(Wo[i], Gs[i], ost[i], ocfg[i], c.lr)
+    stepped = 0
+    for i in idx:
+        assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == ost[i].t
+        Wg = to_np(Wd[i])
+        if ost[i].t == 0:
+            assert np.array_equal(Wg, W0[i]), f"{wl.matrices[i].name}: idle expert changed"
+            continue
+        stepped += 1
+        compare(f"W[{i}]", Wg, Wo[i], TOL_BF16, report)
+        for name, k, ref in (("exp_avg", M.MOARA_T_EXP_AVG, ost[i].exp_avg),
+                             ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ, ost[i].exp_avg_sq),
+                             ("mag_avg", M.MOARA_T_MAG_AVG, ost[i].mag_avg),
+                             ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ, ost[i].mag_avg_sq)):
+            compare(f"{name}[{i}]", M.moara_get_tensor(st, i, k), ref, TOL_BF16, report)
+    print(f"[fullsize] deepseek_moe full state: {stepped} of {len(idx)} layer-{L} matrices stepped, {refreshed} "
+          f"refreshes (worst angle {worst_angle:.2e}), worst floored rel err {max(report.values()):.3e}", flush=True)

