@@ -163,7 +163,10 @@ constexpr int PW = 2 * JB;   // 64 columns per pair
 // 1e-8 that stays below 5e-5 rad for gaps down to 1e-4 (well inside what the subspace
 // iteration itself resolves) and below fp32 rounding for gaps above 0.1. A tolerance
 // of 1e-10 cost about 5 % more sweep time for digits the fp32 projector does not keep.
-constexpr double JAC_TOL = 1e-8;
+#ifndef MOARA_JAC_TOL
+#define MOARA_JAC_TOL 1e-8
+#endif
+constexpr double JAC_TOL = MOARA_JAC_TOL;
 // Inner Jacobi sweeps per pair visit. The pair's Gram need not be diagonalised
 // exactly on every visit: with one inner sweep the outer iteration needs about one
 // more sweep to reach the same off-diagonal level, but every visit is much cheaper

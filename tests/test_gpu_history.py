@@ -174,3 +174,70 @@ def test_llama300m_layer_across_refreshes_keeps_moments(op):
     else:
         c.weight_std = 1e-2
     history_parity(c, 7, 9, lambda t, i: WL.grad_np(wl, i, t), refresh_interval=3, t0=9999, block_scale=False)
+
+
+def test_llama300m_layer_through_the_t200_refresh():
+    """The Llama-300M configuration's own schedule (T = 200) on one layer from a fresh state,
+    bf16 weights and operands: the library runs steps 0 .. 198 (its t = 0 refresh is checked
+    by principal angle); the oracle then starts from the library's state after step 198 (W,
+    projector, all four moments and the counter, read through moara_get_tensor) and follows
+    steps 199, 200 (the refresh, with moments accumulated over 200 steps) and 201. W and all
+    four moments are compared after each of those steps."""
+    import torch
+    M = _M()
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [11])
+    c = case_from_workload(wl)
+    n = len(wl.matrices)
+    st = gpu_state(c, refresh_interval=200)
+    Wd = [WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
+          for i, m in enumerate(wl.matrices)]
+    angles = []
+    for t in range(199):
+        if t % 50 == 0:
+            print(f"[history] llama_300m layer 11, step {t} (library only)", flush=True)
+        G = [WL.grad_np(wl, i, t) for i in range(n)] if t == 0 else None
+        Gd = [to_dev(g, "f32") for g in G] if t == 0 else [
+            WL.grad_device(wl, i, t, torch.empty((m.rows, m.cols), dtype=torch.float32, device="cuda"), active=True)
+            for i, m in enumerate(wl.matrices)]
+        M.moara_step(st, Wd, Gd, lr=c.lr)
+        if t == 0:
+            torch.cuda.synchronize()
+            for i in range(n):
+                Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+                _, V = O.decompose(G[i], c.block_size)
+                angles.append(O.max_principal_angle(Pg, O.truncated_svd(V, c.ranks[i], O.projection_side(*G[i].shape))))
+    torch.cuda.synchronize()
+    ocfg = [oracle_cfg(c, i) for i in range(n)]
+    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[i]) for i in range(n)]
+    Wo = [to_np(w) for w in Wd]
+    for i in range(n):
+        ost[i].P = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+        ost[i].exp_avg = M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG).astype(np.float64)
+        ost[i].exp_avg_sq = M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG_SQ).astype(np.float64)
+        ost[i].mag_avg = M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG).astype(np.float64)
+        ost[i].mag_avg_sq = M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG_SQ).astype(np.float64)
+        ost[i].t = M.moara_get_tensor(st, i, M.MOARA_T_STEP)
+        assert ost[i].t == 199
+    report = {}
+    for t in (199, 200, 201):
+        Gs = [WL.grad_np(wl, i, t) for i in range(n)]
+        print(f"[history] llama_300m layer 11, step {t} (library and oracle)", flush=True)
+        M.moara_step(st, Wd, [to_dev(g, "f32") for g in Gs], lr=c.lr)
+        torch.cuda.synchronize()
+        for i in range(n):
+            if ost[i].t % 200 == 0:   # the library refreshed inside this step
+                Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+                _, V = O.decompose(Gs[i], c.block_size)
+                angles.append(O.max_principal_angle(Pg, O.truncated_svd(V, c.ranks[i], ost[i].side)))
+                ost[i].P = Pg   # moments are kept
+            Wo[i] = O.step(Wo[i], Gs[i], ost[i], ocfg[i], c.lr)
+            compare(f"W[{i}]", to_np(Wd[i]), Wo[i], TOL_BF16, report)
+            for name, k, ref in (("exp_avg", M.MOARA_T_EXP_AVG, ost[i].exp_avg),
+                                 ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ, ost[i].exp_avg_sq),
+                                 ("mag_avg", M.MOARA_T_MAG_AVG, ost[i].mag_avg),
+                                 ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ, ost[i].mag_avg_sq)):
+                compare(f"{name}[{i}]", M.moara_get_tensor(st, i, k), ref, TOL_BF16, report)
+            assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == t + 1
+    assert len(angles) == 2 * n and max(angles) <= 1e-3, angles
+    print(f"[history] steps 199-201 across the t = 200 refresh: worst floored rel err {max(report.values()):.3e} "
+          f"(tol {TOL_BF16:.0e}); refresh angles at t = 0 and 200 <= {max(angles):.2e}", flush=True)
