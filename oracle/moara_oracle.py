@@ -225,15 +225,19 @@ def max_principal_angle(A: np.ndarray, B: np.ndarray) -> float:
 # ----------------------------------------------------------------------------
 
 def adam(x: np.ndarray, exp_avg: np.ndarray, exp_avg_sq: np.ndarray, t: int,
-         beta1: float, beta2: float, eps: float, bias_correction: bool = True):
+         beta1: float, beta2: float, eps: float, bias_correction: bool = True, store=None):
     """One Adam step on input x at step t (t >= 1), Kingma & Ba form, no weight decay.
 
     e <- b1 e + (1 - b1) x ;  q <- b2 q + (1 - b2) x^2 ;
     out = (e / (1 - b1^t)) / (sqrt(q / (1 - b2^t)) + eps).
-    Returns (out, e, q).
+    ``store`` is the number format the two moments are kept in (a rounding function,
+    None = exact); the moments are stored first and ``out`` is formed from the stored
+    values. Returns (out, e, q).
     """
     e = beta1 * exp_avg + (1.0 - beta1) * x
     q = beta2 * exp_avg_sq + (1.0 - beta2) * x * x
+    if store is not None:
+        e, q = store(e), store(q)
     if bias_correction:
         c1 = 1.0 - beta1 ** t
         c2 = 1.0 - beta2 ** t
@@ -261,6 +265,7 @@ class OracleConfig:
     decompose: bool = True
     weight_dtype: str = "f32"       # "f32" | "bf16"
     operand_dtype: str = "f32"      # "f32" | "bf16": bf16 rounding of V, P and N before the GEMMs
+    moment_dtype: str = "f32"       # "f32" | "bf16": storage of Optimizer_V's moments (Appendix G's b_V)
     side: Optional[str] = None      # None = projection_side(m, n)
 
 
@@ -315,6 +320,11 @@ def step(W: np.ndarray, G: np.ndarray, st: OracleState, cfg: OracleConfig, lr: f
     ``scale`` is GaLore's scale (0.25 in Appendix D; 1 is Algorithm 1 as
     printed). With bf16 weights the recomposed, scaled update is cast to bf16
     first and the subtraction result is rounded to bf16 (Appendix D).
+
+    With moment_dtype "bf16" the direction moments are 2-byte states (b_V = 2 in
+    Appendix G's memory formulas; with b_M = 4 they reproduce its optimizer-state
+    table exactly): each is rounded to bf16 when stored and N is formed from the
+    stored values. The magnitude branch's states stay exact (fp32 in Appendix D).
     """
     W = np.asarray(W, dtype=np.float64)
     G = np.asarray(G, dtype=np.float64)
@@ -332,7 +342,8 @@ def step(W: np.ndarray, G: np.ndarray, st: OracleState, cfg: OracleConfig, lr: f
     Rt = P.T @ Vo if st.side == LEFT else Vo @ P                      # projected direction
     st.t += 1
     N, st.exp_avg, st.exp_avg_sq = adam(Rt, st.exp_avg, st.exp_avg_sq, st.t,
-                                        cfg.beta1, cfg.beta2, cfg.adam_eps, cfg.bias_correction)
+                                        cfg.beta1, cfg.beta2, cfg.adam_eps, cfg.bias_correction,
+                                        store=round_bf16 if cfg.moment_dtype == "bf16" else None)
     No = _operand(N, cfg)
     dV = P @ No if st.side == LEFT else No @ P.T                       # back-projection
     if cfg.decompose:

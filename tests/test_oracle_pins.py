@@ -423,6 +423,54 @@ def test_bf16_operand_step_hand_derived(side, weights):
         np.testing.assert_array_equal(W1, ref)
 
 
+def test_bf16_direction_moments_two_steps_hand_derived():
+    """Two steps with 2-byte direction moments (b_V = 2, Appendix G) and fp32 magnitude
+    states (Appendix D). m = 1, so P = [[1]] and R = V exactly; betas 1/2 and 3/4 are
+    exact in binary, so every rounding below is a bf16 rounding of a stored moment.
+
+    G1 = [255, 32 | 5, 12] (B = 2): M = (257, 13), V = x1 = (255/257, 32/257, 5/13, 12/13).
+    Step 1 stores e = x1/2 and q = x1^2/4 rounded to nearest-even bf16 (8 significant
+    bits): 255/514 = 254.007 * 2^-9 -> 127/256; 16/257 = 255.004 * 2^-12 -> 255/4096;
+    5/26 = 196.92 * 2^-10 -> 197/1024 (truncation would give 196); 6/13 = 236.31 * 2^-9
+    -> 59/128; 65025/264196 = 252.03 * 2^-10 -> 63/256; 256/66049 = 254.02 * 2^-16 ->
+    127/32768; 25/676 = 151.48 * 2^-12 -> 151/4096; 36/169 = 218.13 * 2^-10 -> 109/512.
+    Step 2 (G2 = [32, 255 | 12, 5]) starts from those stored values; its last e and its
+    third q round differently when step 1 is taken unrounded (27/64 and 123/512 here).
+    The magnitude states stay exact: e_M = M/2 = (128.5, 6.5), where bf16 would give 128.
+    """
+    from fractions import Fraction as Fr
+    cfg = O.OracleConfig(block_size=2, rank=1, beta1=0.5, beta2=0.75, adam_eps=0.25, decomp_eps=0.0,
+                         scale=0.25, refresh_interval=200, moment_dtype="bf16")
+    st = O.init_state(1, 4, cfg)
+    W0 = np.zeros((1, 4))
+    W1 = O.step(W0, np.array([[255.0, 32.0, 5.0, 12.0]]), st, cfg, lr=1.0)
+    assert np.array_equal(st.P, [[1.0]])
+    e1 = [Fr(127, 256), Fr(255, 4096), Fr(197, 1024), Fr(59, 128)]
+    q1 = [Fr(63, 256), Fr(127, 32768), Fr(151, 4096), Fr(109, 512)]
+    np.testing.assert_array_equal(st.exp_avg.ravel(), [float(v) for v in e1])
+    np.testing.assert_array_equal(st.exp_avg_sq.ravel(), [float(v) for v in q1])
+    np.testing.assert_array_equal(st.mag_avg.ravel(), [128.5, 6.5])
+
+    def expect_update(e, q, mag_e, mag_q, t):
+        # N and dM from the stored moments at step t; U = scale * Rep_B(dM) * N
+        c1, c2 = 1 - 0.5 ** t, 1 - 0.75 ** t
+        N = [float(a) / c1 / (math.sqrt(float(b) / c2) + 0.25) for a, b in zip(e, q)]
+        dM = [a / c1 / (math.sqrt(b / c2) + 0.25) for a, b in zip(mag_e, mag_q)]
+        return np.array([0.25 * dM[j // 2] * N[j] for j in range(4)])
+
+    np.testing.assert_allclose(W0 - W1, [expect_update(e1, q1, [128.5, 6.5], [16512.25, 42.25], 1)],
+                               rtol=1e-13, atol=0)
+    W2 = O.step(W1, np.array([[32.0, 255.0, 12.0, 5.0]]), st, cfg, lr=1.0)
+    e2 = [Fr(159, 512), Fr(135, 256), Fr(143, 256), Fr(27, 64)]
+    q2 = [Fr(193, 1024), Fr(255, 1024), Fr(123, 512), Fr(201, 1024)]
+    np.testing.assert_array_equal(st.exp_avg.ravel(), [float(v) for v in e2])
+    np.testing.assert_array_equal(st.exp_avg_sq.ravel(), [float(v) for v in q2])
+    mag_e = [0.5 * 128.5 + 0.5 * 257, 0.5 * 6.5 + 0.5 * 13]
+    mag_q = [0.75 * 16512.25 + 0.25 * 257 ** 2, 0.75 * 42.25 + 0.25 * 13 ** 2]
+    np.testing.assert_array_equal(st.mag_avg.ravel(), mag_e)
+    np.testing.assert_allclose(W1 - W2, [expect_update(e2, q2, mag_e, mag_q, 2)], rtol=1e-13, atol=0)
+
+
 def test_floored_metric():
     b = np.array([1.0, 0.0, -2.0])
     assert O.floored_rel_err(b, b) == 0.0
