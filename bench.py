@@ -42,6 +42,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="llama2_7b")
     ap.add_argument("--operand", default=None, help="GEMM operand dtype override: bf16 | f32")
+    ap.add_argument("--moments", default=None, help="direction-moment storage override: f32 | bf16")
     ap.add_argument("--refresh-reps", type=int, default=3, help="refreshes timed; the median is reported")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-sample-layers", type=int, default=None,
@@ -74,7 +75,7 @@ def v_path(wl, m, operand: str) -> bool:
     return k <= 512 and m.cols % 32 == 0
 
 
-def algorithmic_cost(wl, operand: str, weight_bytes: int, mask=None):
+def algorithmic_cost(wl, operand: str, weight_bytes: int, mask=None, moment_bytes: int = 4):
     """Per-step algorithmic bytes and flops per kernel (what each kernel of this split must
     move or compute, given its inputs and outputs), over the matrices in `mask` (all if None)."""
     ob = 2 if operand == "bf16" else 4
@@ -90,8 +91,10 @@ def algorithmic_cost(wl, operand: str, weight_bytes: int, mask=None):
         # decompose + Optimizer_M: read G; write inv and dM; read+write two magnitude moments;
         # write V in bf16 on the large-tile path
         cost["decompose"][0] += 4 * M * N + 4 * M * k * 6 + (2 * M * N if vp else 0)
-        # projection + Optimizer_V: read V (or G and inv), read P, read+write two fp32 moments, write N
-        cost["project"][0] += (2 * M * N if vp else 4 * M * N + 4 * M * k) + ob * s * r + 16 * L * r + ob * L * r
+        # projection + Optimizer_V: read V (or G and inv), read P, read+write the two direction
+        # moments (fp32 or bf16), write N
+        cost["project"][0] += ((2 * M * N if vp else 4 * M * N + 4 * M * k) + ob * s * r + 4 * moment_bytes * L * r
+                               + ob * L * r)
         cost["project"][1] += 2 * M * N * r
         # back-projection + update: read N and P, read dM, read+write W
         cost["backproject"][0] += ob * L * r + ob * s * r + 4 * M * k + 2 * weight_bytes * M * N
@@ -124,7 +127,7 @@ def measured_traffic(kernel: str, workload: str):
     return val if rec == h.hexdigest() else None
 
 
-def method_cost(wl, operand_bytes: int, weight_bytes: int, mask=None):
+def method_cost(wl, operand_bytes: int, weight_bytes: int, mask=None, moment_bytes: int = 4):
     """What the method itself must move and compute per step, whatever the kernel split:
     read G, read+write W, read+write the two direction moments, read+write the two
     magnitude moments, read P; two GEMMs of 2mnr flops each (matrices in `mask`, all if None)."""
@@ -136,7 +139,7 @@ def method_cost(wl, operand_bytes: int, weight_bytes: int, mask=None):
         M, N = m.rows, m.cols
         s, L = min(M, N), max(M, N)
         k = -(-N // wl.block_size)
-        by += 4 * M * N + 2 * weight_bytes * M * N + 16 * r * L + 16 * M * k + operand_bytes * s * r
+        by += 4 * M * N + 2 * weight_bytes * M * N + 4 * moment_bytes * r * L + 16 * M * k + operand_bytes * s * r
         fl += 4 * M * N * r
     return by, fl
 
@@ -167,7 +170,7 @@ def refresh_cost(wl, p_over: int, q: int, bf16_early: bool):
     return {"bf16_flops": f16, "f32_flops": f32, "f64_flops": f64, "roofline_ms": t * 1e3}
 
 
-def cpu_baseline(wl, layers, one_thread: bool = False):
+def cpu_baseline(wl, layers, one_thread: bool = False, moments: str = "f32"):
     """The oracle (as it stands) on a bounded sample: the first `layers` layers' matrices
     (None: the whole stack if it has at most 0.5 G parameters, else two layers), with their
     projectors already set (steps only), timed on the host cores; optionally again with
@@ -195,7 +198,8 @@ def cpu_baseline(wl, layers, one_thread: bool = False):
         G = WL.grad_np(sub, i, 0)
         W = WL.weight_np(sub, i).astype(np.float64)
         cfg = O.OracleConfig(block_size=sub.block_size, rank=sub.rank_of(m), adam_eps=sub.adam_eps, scale=sub.scale,
-                             refresh_interval=0, weight_dtype=sub.weight_dtype, operand_dtype=sub.operand_dtype)
+                             refresh_interval=0, weight_dtype=sub.weight_dtype, operand_dtype=sub.operand_dtype,
+                             moment_dtype=moments)
         st = O.init_state(m.rows, m.cols, cfg)
         s = min(m.rows, m.cols)
         st.P = np.linalg.qr(np.random.default_rng(i).standard_normal((s, cfg.rank)))[0]
@@ -242,12 +246,14 @@ def main():
     if a.layers:
         wl = WL.subset(wl, list(range(a.layers)))
     operand = a.operand or wl.operand_dtype
+    moments = a.moments or wl.moment_dtype
     ob = 2 if operand == "bf16" else 4
+    mob = 2 if moments == "bf16" else 4
     wb = 2 if wl.weight_dtype == "bf16" else 4
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     n = len(wl.matrices)
-    log(f"[bench] {wl.name}: {n} matrices, {wl.n_params / 1e9:.3f}G params, operand {operand}")
+    log(f"[bench] {wl.name}: {n} matrices, {wl.n_params / 1e9:.3f}G params, operand {operand}, moments {moments}")
 
     # ---- inputs resident in HBM
     wdt = torch.bfloat16 if wl.weight_dtype == "bf16" else torch.float32
@@ -267,6 +273,7 @@ def main():
         adam_eps=wl.adam_eps, scale=wl.scale, refresh_interval=0,
         weight_dtype=M.MOARA_BF16 if wl.weight_dtype == "bf16" else M.MOARA_F32,
         operand_dtype=M.MOARA_BF16 if operand == "bf16" else M.MOARA_F32,
+        moment_dtype=M.MOARA_BF16 if moments == "bf16" else M.MOARA_F32,
         refresh_oversample=wl.refresh_oversample,
         refresh_iters=a.refresh_iters if a.refresh_iters else wl.refresh_iters)
     descs = M.make_descs([(m.rows, m.cols, m.module) for m in wl.matrices])
@@ -337,12 +344,12 @@ def main():
     if moe:   # per-step average over the timed steps' active sets
         cost = {kk: [0.0, 0.0] for kk in ("decompose", "project", "backproject")}
         for k in range(a.steps):
-            ck = algorithmic_cost(wl, operand, wb, masks[a.warmup + k])
+            ck = algorithmic_cost(wl, operand, wb, masks[a.warmup + k], moment_bytes=mob)
             for kk in cost:
                 cost[kk][0] += ck[kk][0] / a.steps
                 cost[kk][1] += ck[kk][1] / a.steps
     else:
-        cost = algorithmic_cost(wl, operand, wb)
+        cost = algorithmic_cost(wl, operand, wb, moment_bytes=mob)
     peak_mfma = PEAK_BF16 if operand == "bf16" else PEAK_F32
     for name, (bytes_, flops) in cost.items():
         t = kern[name]["ms_per_step"] / 1e3
@@ -385,10 +392,10 @@ def main():
     log(f"[bench] alignment diagnostic: {align_ms:.1f} ms")
 
     if moe:
-        mb = sum(method_cost(wl, ob, wb, masks[a.warmup + k])[0] for k in range(a.steps)) / a.steps
-        mf = sum(method_cost(wl, ob, wb, masks[a.warmup + k])[1] for k in range(a.steps)) / a.steps
+        mb = sum(method_cost(wl, ob, wb, masks[a.warmup + k], mob)[0] for k in range(a.steps)) / a.steps
+        mf = sum(method_cost(wl, ob, wb, masks[a.warmup + k], mob)[1] for k in range(a.steps)) / a.steps
     else:
-        mb, mf = method_cost(wl, ob, wb)
+        mb, mf = method_cost(wl, ob, wb, moment_bytes=mob)
     step_roof_ms = max(mb / PEAK_HBM, mf / peak_mfma) * 1e3
     q_used = a.refresh_iters if a.refresh_iters else wl.refresh_iters
     rc = refresh_cost(wl, wl.refresh_oversample, q_used, operand == "bf16")
@@ -404,7 +411,7 @@ def main():
         "dtype": operand, "data": "synthetic",
         "config": {"workload": wl.name, "layers": wl.n_layers, "matrices": n, "params": wl.n_params,
                    "rank_table": list(wl.rank_table[:7] if wl.moe_routed == 0 else wl.rank_table),
-                   "block_size": wl.block_size, "weights": wl.weight_dtype, "grads": "f32", "moments": "f32",
+                   "block_size": wl.block_size, "weights": wl.weight_dtype, "grads": "f32", "moments": moments,
                    "gemm_operands": operand, "refresh": {"oversample": wl.refresh_oversample,
                                                          "iters": q_used}},
         "ms_per_refresh": ref_med,
@@ -440,7 +447,7 @@ def main():
         }
     if not a.no_cpu_baseline:
         log("[bench] cpu baseline (oracle) ...")
-        cb = cpu_baseline(wl, a.cpu_sample_layers, a.cpu_one_thread)
+        cb = cpu_baseline(wl, a.cpu_sample_layers, a.cpu_one_thread, moments)
         out["cpu_baseline"] = {k: cb[k] for k in ("value", "unit", "cores", "kind", "sample", "one_thread",
                                                   "extrapolated_full_stack_s")}
     else:

@@ -83,7 +83,8 @@ enum { MOARA_SIDE_AUTO = 0, MOARA_SIDE_LEFT = 1, MOARA_SIDE_RIGHT = 2 };
 enum { MOARA_F32 = 0, MOARA_BF16 = 1 };
 
 /* Tensor ids for moara_get_tensor / moara_set_tensor. Layouts are the paper's
- * orientation, row-major, fp32 (host side):
+ * orientation, row-major, fp32 on the host side whatever moment_dtype stores on the
+ * device (bf16 moments are widened exactly on get and rounded to nearest-even on set):
  *   MOARA_T_P          : the projector, s x r with s = m (LEFT) or n (RIGHT).
  *   MOARA_T_EXP_AVG    : first moment of Optimizer_V, r x n (LEFT) / m x r (RIGHT).
  *   MOARA_T_EXP_AVG_SQ : second moment of Optimizer_V, same shape.
@@ -128,13 +129,17 @@ typedef struct {
                                             0: skip them (no state change, t not advanced);
                                             1: step them with G = 0 (grads[i] is not read; W moves by
                                                the decayed moments, t advances) */
-  int32_t reserved;                      /* must be 0 */
+  int32_t moment_dtype;                  /* storage of Optimizer_V's two moments: MOARA_F32, or MOARA_BF16
+                                            (the 2-byte direction states of Appendix D / Table 11; each
+                                            update is computed in fp32 from the stored values and
+                                            rounded to nearest-even on store). Optimizer_M's states
+                                            stay fp32 (Appendix D). */
 } moara_config;
 
 /* Fill *out with the paper's defaults (Appendix D): B=128, beta=(0.9,0.999),
  * adam_eps=1e-6, decomp_eps=1e-12, scale=0.25, weight_decay=0, T_SVD=200,
  * bias correction on, decomposition on, bf16 weights, fp32 gradients, bf16
- * GEMM operands, p=-1 (p=r), q=20, seed 0, rank_table all 0 (the caller sets
+ * GEMM operands, p=-1 (p=r), q=20, seed 0, fp32 moments, rank_table all 0 (the caller sets
  * it, e.g. with moara_allocate_ranks). Errors: MOARA_E_ARG if out is NULL. */
 int moara_default_config(moara_config* out);
 

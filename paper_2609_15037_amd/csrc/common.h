@@ -39,6 +39,8 @@ struct MatDev {
   bf16* Vb;            // bf16 direction tensor V written by the decomposition (nullptr: none)
   int32_t n_bf16;      // zero-gradient step: N is bf16 (else fp32) ...
   int32_t n_kp;        // ... in the blocked layout kp_index(l, j, L)
+  int32_t mom_bf16;    // zero-gradient step: exp1 / exp2 hold bf16 values
+  int32_t pad_;
 };
 
 struct StepParams {
@@ -98,6 +100,17 @@ __device__ __forceinline__ float adam_out(float x, float& e, float& q, float b1,
   e = b1 * e + (1.0f - b1) * x;
   q = b2 * q + (1.0f - b2) * x * x;
   return (e / bc1) / (sqrtf(q / bc2) + eps);
+}
+
+// The same step with the moments stored in bf16: the updated moments are rounded to bf16
+// (nearest even) for storage and the output is formed from the stored values.
+__device__ __forceinline__ float adam_out_bf16(float x, bf16& e, bf16& q, float b1, float b2, float eps,
+                                               float bc1, float bc2) {
+  const float e1 = bf2f(f2bf(b1 * bf2f(e) + (1.0f - b1) * x));
+  const float q1 = bf2f(f2bf(b2 * bf2f(q) + (1.0f - b2) * x * x));
+  e = f2bf(e1);
+  q = f2bf(q1);
+  return (e1 / bc1) / (sqrtf(q1 / bc2) + eps);
 }
 
 // ---------------------------------------------------------------- launchers

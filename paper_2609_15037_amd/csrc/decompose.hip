@@ -291,10 +291,20 @@ __global__ __launch_bounds__(256) void k_zero_grad(const MatDev* __restrict__ ma
       d.dM[e] = out;
     } else {
       const int64_t x = e - mk;   // (l, j) of the L x r moments, row-major
-      float a = d.exp1[x], q = d.exp2[x];
-      const float out = adam_out(0.f, a, q, p.beta1, p.beta2, p.adam_eps, d.bc1, d.bc2);
-      d.exp1[x] = a;
-      d.exp2[x] = q;
+      float out;
+      if (d.mom_bf16) {
+        bf16* E1 = reinterpret_cast<bf16*>(d.exp1);
+        bf16* E2 = reinterpret_cast<bf16*>(d.exp2);
+        bf16 a = E1[x], q = E2[x];
+        out = adam_out_bf16(0.f, a, q, p.beta1, p.beta2, p.adam_eps, d.bc1, d.bc2);
+        E1[x] = a;
+        E2[x] = q;
+      } else {
+        float a = d.exp1[x], q = d.exp2[x];
+        out = adam_out(0.f, a, q, p.beta1, p.beta2, p.adam_eps, d.bc1, d.bc2);
+        d.exp1[x] = a;
+        d.exp2[x] = q;
+      }
       if (d.n_bf16) {
         const int64_t l = x / d.r, j = x % d.r;
         ((bf16*)d.N)[d.n_kp ? kp_index(l, j, d.L) : x] = f2bf(out);

@@ -20,13 +20,15 @@ enum { A_G_ROW = 0, A_G_TRANS = 1, A_KC = 2 };
 enum { B_KC = 0, B_NC = 1 };
 // Epilogues:
 //   EP_ADAM   : Optimizer_V on the projected tile; moments e1/e2 and output c are [M][N]
+//               (e1/e2 hold bf16 values when GemmUniform::moment_bf16 is set)
 //   EP_UPDATE : W[i][j] -= lr * scale * dM[i][j/B] * C[i][j] (bf16 or fp32 W in c)
 //   EP_STORE  : c[i*ldc + j] = C[i][j] (fp32)
 //   EP_STORE_BF16: c[i*ldc + j] = bf16(C[i][j])   (large-tile path only)
 //   EP_ALIGN  : alignment sums (fp32 kind): with R[i][j] = M[i][j/B] * C[i][j], M = 1 / inv - eps
 //               (inv = nullptr: M = 1) and G[i][j] = c[i*ldc + j] (read only), adds
 //               sum G R, sum R^2 and sum G^2 of the tile to red[0..2] (fp64 atomics)
-enum { EP_ADAM = 0, EP_UPDATE = 1, EP_STORE = 2, EP_STORE_BF16 = 3, EP_ALIGN = 4 };
+enum { EP_ADAM = 0, EP_UPDATE = 1, EP_STORE = 2, EP_STORE_BF16 = 3, EP_ALIGN = 4,
+       EP_ADAM_B16 = 5 };   // large-tile kernel only: EP_ADAM with bf16 moments (GemmUniform::moment_bf16)
 
 struct GemmProb {
   int64_t M, N, K;
@@ -63,6 +65,8 @@ struct GemmUniform {
   float decomp_eps;     // EP_ALIGN
   float beta1, beta2, adam_eps;
   float lr, scale;
+  int32_t moment_bf16;  // EP_ADAM: the moments are stored in bf16
+  int32_t pad_;
 };
 
 template <int KIND> struct GemmTile;

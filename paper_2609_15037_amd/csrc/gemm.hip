@@ -420,6 +420,20 @@ __device__ __forceinline__ void epilogue(const GemmProb& P, const GemmUniform& U
             s_gg += g * g;
           }
         } else if constexpr (EP == EP_ADAM) {
+          if (U.moment_bf16) {   // moments stored in bf16: element by element (fallback shapes only)
+            bf16* E1 = reinterpret_cast<bf16*>(P.e1);
+            bf16* E2 = reinterpret_cast<bf16*>(P.e2);
+            for (int q = 0; q < 4; ++q) {
+              if (col + q >= P.N) continue;
+              bf16 a = E1[idx + q], b = E2[idx + q];
+              const float o = adam_out_bf16(v[q], a, b, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2);
+              E1[idx + q] = a;
+              E2[idx + q] = b;
+              if constexpr (KIND == KIND_BF16) ((bf16*)P.c)[(P.kp & 4) ? kp_index(row, col + q, P.M) : idx + q] = f2bf(o);
+              else ((float*)P.c)[idx + q] = o;
+            }
+            continue;
+          }
           float e[4], s2[4], o[4];
           const bool fm = (col + 4 <= P.N) && ((idx & 3) == 0);   // moments are library memory (aligned)
           if (fm) {

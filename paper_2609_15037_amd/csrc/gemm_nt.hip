@@ -23,7 +23,8 @@
 // of the wave's sub-tile. The epilogues stage each 32-row slab of the wave's
 // accumulators through LDS and then walk it row-contiguously, so that moments,
 // N and W move as full 128-byte row segments.
-//   EP_ADAM  : Optimizer_V on the projected tile (moments e1/e2, output N bf16).
+//   EP_ADAM  : Optimizer_V on the projected tile (moments e1/e2, output N bf16);
+//              EP_ADAM_B16 the same with the moments stored in bf16 (half the moment traffic).
 //   EP_UPDATE: W[i][j] -= lr * bf16(scale * dM[i][j/B] * C[i][j]) (bf16 or fp32 W).
 //   EP_STORE / EP_STORE_BF16: C stored as fp32 / bf16 (the refresh's subspace products).
 #include "gemm.h"
@@ -33,6 +34,9 @@
 #endif
 #ifndef EPA_ROWS
 #define EPA_ROWS 4
+#endif
+#ifndef EPDB_ADAM16
+#define EPDB_ADAM16 4
 #endif
 #ifndef EPDB_UPD
 #define EPDB_UPD 1
@@ -274,6 +278,59 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
         }
       }
     }
+  } else if constexpr (EP == EP_ADAM_B16) {
+    // as EP_ADAM below, with bf16 moments (8 bytes per 4-column group instead of 16)
+    constexpr int LPR = WTN / 4, RPP = 64 / LPR;
+    constexpr int PR = EPA_ROWS, NPC = 32 / PR, HPP = PR / RPP, NPT = MB * NPC, DB = EPDB_ADAM16;
+    static_assert(PR % RPP == 0 && 32 % PR == 0 && DB >= 1, "epilogue pieces");
+    const int cc = 4 * (lane % LPR);
+    const int64_t col = wcol0 + cc;
+    const bf16* E1 = reinterpret_cast<const bf16*>(P.e1);
+    const bf16* E2 = reinterpret_cast<const bf16*>(P.e2);
+    bf16x4 ev[DB][HPP], qv[DB][HPP];
+    auto load_piece = [&](int h) {
+#pragma unroll
+      for (int p = 0; p < HPP; ++p) {
+        const int64_t row = wrow0 + PR * h + RPP * p + lane / LPR;
+        if (row < P.M && col < P.N) {
+          const int64_t idx = row * P.ldc + col;
+          ev[h % DB][p] = *reinterpret_cast<const bf16x4*>(E1 + idx);
+          qv[h % DB][p] = *reinterpret_cast<const bf16x4*>(E2 + idx);
+        }
+      }
+    };
+    auto compute_piece = [&](int h) {
+#pragma unroll
+      for (int p = 0; p < HPP; ++p) {
+        const int rr = PR * (h % NPC) + RPP * p + lane / LPR;
+        const int64_t row = wrow0 + PR * h + RPP * p + lane / LPR;
+        if (row < P.M && col < P.N) {
+          const float4 v = *reinterpret_cast<const float4*>(slab + rr * EPLD + cc);
+          const float vv[4] = {v.x, v.y, v.z, v.w};
+          const int64_t idx = row * P.ldc + col;
+          bf16x4 e = ev[h % DB][p], q = qv[h % DB][p], o;
+#pragma unroll
+          for (int c = 0; c < 4; ++c) {
+            bf16 ec = e[c], qc = q[c];
+            o[c] = f2bf(adam_out_bf16(vv[c], ec, qc, U.beta1, U.beta2, U.adam_eps, P.bc1, P.bc2));
+            e[c] = ec;
+            q[c] = qc;
+          }
+          *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(P.e1) + idx) = e;
+          *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(P.e2) + idx) = q;
+          *reinterpret_cast<bf16x4*>((bf16*)P.c + ((P.kp & 4) ? kp_index(row, col, P.M) : idx)) = o;
+        }
+      }
+    };
+#pragma unroll
+    for (int h = 0; h < DB - 1; ++h)
+      if (h < NPT) load_piece(h);
+#pragma unroll
+    for (int h = 0; h < NPT; ++h) {
+      if (h + DB - 1 < NPT) load_piece(h + DB - 1);
+      if (h % NPC == 0) stage_slab(h / NPC);
+      compute_piece(h);
+    }
   } else if constexpr (EP == EP_ADAM) {
     // LPR lanes x 4 columns per row, RPP rows per pass. The moments move in pieces of PR
     // rows through a ring of DB register buffers: while one piece is computed, the loads
@@ -483,7 +540,9 @@ namespace {
 template <int NWM, int NWN, int WTN, int NS, int NSU, int OCC>
 hipError_t launch_nt(int ep, const GemmProb* probs_dev, uint32_t total_tiles, const GemmUniform& u, hipStream_t st) {
   const dim3 grid(total_tiles), block(64 * NWM * NWN);
-  if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
+  if (ep == EP_ADAM && u.moment_bf16)
+    hipLaunchKernelGGL((k_gemm_nt<EP_ADAM_B16, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWM, NWN, WTN, NSU, OCC>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_STORE) hipLaunchKernelGGL((k_gemm_nt<EP_STORE, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_STORE_BF16) hipLaunchKernelGGL((k_gemm_nt<EP_STORE_BF16, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);

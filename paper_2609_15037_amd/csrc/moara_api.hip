@@ -81,7 +81,8 @@ struct MatHost {
   bool hasP = false;
   bool refreshed = false;   // the library's refresh has written this matrix's record
   float *inv = nullptr, *dM = nullptr, *mag1 = nullptr, *mag2 = nullptr;
-  float *exp1 = nullptr, *exp2 = nullptr, *P32 = nullptr;
+  void *exp1 = nullptr, *exp2 = nullptr;   // Optimizer_V moments, L x r, fp32 or bf16 (moment_dtype)
+  float* P32 = nullptr;
   void *N = nullptr, *Pop = nullptr, *Ptop = nullptr;
   bool vpath = false;    // the decomposition writes V in bf16 for the large-tile projection
   void* V = nullptr;     // L x s bf16 direction workspace, blocked layout (kp_index, K = s)
@@ -136,6 +137,22 @@ namespace {
 
 int elem_bytes(int dtype) { return dtype == MOARA_BF16 ? 2 : 4; }
 
+// bf16 <-> fp32 on the host for the state-access calls: widening is exact; narrowing
+// rounds to nearest, ties to even, and keeps NaN a quiet NaN
+float host_bf16_to_f32(uint16_t b) {
+  const uint32_t u = (uint32_t)b << 16;
+  float f;
+  memcpy(&f, &u, 4);
+  return f;
+}
+uint16_t host_f32_to_bf16(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  if ((u & 0x7F800000u) == 0x7F800000u && (u & 0x007FFFFFu)) return (uint16_t)((u >> 16) | 0x0040u);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+
 int validate_config(const moara_config* c) {
   if (!c) return fail(MOARA_E_ARG, "config is NULL");
   if (c->block_size < 1) return fail(MOARA_E_ARG, "block_size must be >= 1 (got %d)", c->block_size);
@@ -154,7 +171,7 @@ int validate_config(const moara_config* c) {
   if (c->refresh_oversample < -1) return fail(MOARA_E_ARG, "refresh_oversample must be >= -1");
   if (c->refresh_iters < 1 || c->refresh_iters > 1000) return fail(MOARA_E_ARG, "refresh_iters must be in [1, 1000]");
   if (c->zero_grad_mode != 0 && c->zero_grad_mode != 1) return fail(MOARA_E_ARG, "bad zero_grad_mode");
-  if (c->reserved != 0) return fail(MOARA_E_ARG, "reserved must be 0");
+  if (c->moment_dtype != MOARA_F32 && c->moment_dtype != MOARA_BF16) return fail(MOARA_E_ARG, "bad moment_dtype");
   return MOARA_OK;
 }
 
@@ -211,7 +228,7 @@ size_t mat_state_bytes(const moara_config& c, int64_t m, int64_t n, int side, in
   size_t b = 0;
   if (vpath_shape_ok(c, m, n, side, r)) b += align_up(2 * (size_t)m * n);   // V workspace
   b += align_up(4 * m * k) * 4;          // inv, dM, mag1, mag2
-  b += align_up(4 * L * r) * 2;          // exp1, exp2
+  b += align_up((size_t)elem_bytes(c.moment_dtype) * L * r) * 2;   // exp1, exp2
   b += align_up((size_t)ob * L * r);     // N
   b += align_up(4 * s * r);              // P32
   b += align_up((size_t)ob * s * r) * 2; // Pop, Ptop
@@ -383,6 +400,7 @@ GemmUniform make_uniform(const moara_state* st, float lr) {
   GemmUniform u{};
   u.B = st->cfg.block_size;
   u.weight_bf16 = st->cfg.weight_dtype == MOARA_BF16;
+  u.moment_bf16 = st->cfg.moment_dtype == MOARA_BF16;
   u.beta1 = st->cfg.beta1;
   u.beta2 = st->cfg.beta2;
   u.adam_eps = st->cfg.adam_eps;
@@ -470,7 +488,7 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
       g.b = h.Ptop; g.ldb = h.s;
       g.c = h.N; g.ldc = h.r;
       g.kp = 1 | (h.kp ? 2 | 4 : 0);
-      g.e1 = h.exp1; g.e2 = h.exp2;
+      g.e1 = (float*)h.exp1; g.e2 = (float*)h.exp2;
       g.bc1 = bc1; g.bc2 = bc2;
       g.a_bytes = (uint32_t)(2 * (size_t)h.L * h.s);
       g.b_bytes = (uint32_t)(2 * (size_t)h.r * h.s);
@@ -523,7 +541,7 @@ int run_project_back(moara_state* st, const std::vector<int>& idx, void* const* 
     g.b = h.Ptop; g.ldb = h.s;
     g.c = h.N; g.ldc = h.r;
     g.kp = h.kp ? 2 | 4 : 0;
-    g.e1 = h.exp1; g.e2 = h.exp2;
+    g.e1 = (float*)h.exp1; g.e2 = (float*)h.exp2;
     g.bc1 = bc1;
     g.bc2 = bc2;
     g.tiles_n = gemm_tiles_n(kind, g.N);
@@ -588,7 +606,8 @@ int run_zero_grad(moara_state* st, const std::vector<int>& zidx, hipStream_t str
     MatDev d{};
     d.m = h.m; d.n = h.n; d.k = h.k; d.r = h.r; d.side = h.side; d.L = (int32_t)h.L; d.s = (int32_t)h.s;
     d.dM = h.dM; d.mag1 = h.mag1; d.mag2 = h.mag2;
-    d.exp1 = h.exp1; d.exp2 = h.exp2; d.N = h.N;
+    d.exp1 = (float*)h.exp1; d.exp2 = (float*)h.exp2; d.N = h.N;
+    d.mom_bf16 = st->cfg.moment_dtype == MOARA_BF16;
     d.n_bf16 = obf; d.n_kp = h.kp ? 1 : 0;
     const double t1 = (double)(h.t + 1);
     d.bc1 = st->cfg.bias_correction ? (float)(1.0 - pow((double)st->cfg.beta1, t1)) : 1.f;
@@ -1147,6 +1166,7 @@ int moara_default_config(moara_config* out) {
   out->refresh_iters = 20;
   out->refresh_seed = 0;
   out->zero_grad_mode = 0;
+  out->moment_dtype = MOARA_F32;
   return MOARA_OK;
 }
 
@@ -1277,8 +1297,8 @@ int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, 
     h.dM = (float*)take(4 * h.m * h.k);
     h.mag1 = (float*)take(4 * h.m * h.k);
     h.mag2 = (float*)take(4 * h.m * h.k);
-    h.exp1 = (float*)take(4 * h.L * h.r);
-    h.exp2 = (float*)take(4 * h.L * h.r);
+    h.exp1 = take((size_t)elem_bytes(cfg->moment_dtype) * h.L * h.r);
+    h.exp2 = take((size_t)elem_bytes(cfg->moment_dtype) * h.L * h.r);
     h.N = take((size_t)ob * h.L * h.r);
     h.P32 = (float*)take(4 * h.s * h.r);
     h.Pop = take((size_t)ob * h.s * h.r);
@@ -1529,18 +1549,33 @@ int moara_get_tensor(moara_state* st, int32_t mat, int32_t which, void* host_dst
                   : which == MOARA_T_EXP_AVG ? (const void*)h.exp1
                   : which == MOARA_T_EXP_AVG_SQ ? (const void*)h.exp2
                   : which == MOARA_T_MAG_AVG ? (const void*)h.mag1 : (const void*)h.mag2;
-  const bool transpose = (which == MOARA_T_EXP_AVG || which == MOARA_T_EXP_AVG_SQ) && h.side == MOARA_SIDE_LEFT;
+  const bool moment = which == MOARA_T_EXP_AVG || which == MOARA_T_EXP_AVG_SQ;
+  const bool transpose = moment && h.side == MOARA_SIDE_LEFT;
+  const bool narrow = moment && st->cfg.moment_dtype == MOARA_BF16;
   ORDER_ON(st, hs);
   HIP_TRY(hipStreamSynchronize(hs));
-  if (!transpose) {
+  if (!transpose && !narrow) {
     HIP_TRY(hipMemcpyAsync(host_dst, src, need, hipMemcpyDeviceToHost, hs));
     HIP_TRY(hipStreamSynchronize(hs));
     return MOARA_OK;
   }
-  std::vector<float> tmp((size_t)h.L * h.r);
-  HIP_TRY(hipMemcpyAsync(tmp.data(), src, need, hipMemcpyDeviceToHost, hs));
-  HIP_TRY(hipStreamSynchronize(hs));
-  float* o = (float*)host_dst;   // paper orientation r x n from the stored n x r
+  const size_t cnt = (size_t)h.L * h.r;
+  std::vector<float> tmp(cnt);
+  if (narrow) {
+    std::vector<uint16_t> raw(cnt);
+    HIP_TRY(hipMemcpyAsync(raw.data(), src, 2 * cnt, hipMemcpyDeviceToHost, hs));
+    HIP_TRY(hipStreamSynchronize(hs));
+    for (size_t i = 0; i < cnt; ++i) tmp[i] = host_bf16_to_f32(raw[i]);
+  } else {
+    HIP_TRY(hipMemcpyAsync(tmp.data(), src, need, hipMemcpyDeviceToHost, hs));
+    HIP_TRY(hipStreamSynchronize(hs));
+  }
+  float* o = (float*)host_dst;
+  if (!transpose) {
+    memcpy(o, tmp.data(), need);
+    return MOARA_OK;
+  }
+  // paper orientation r x n from the stored n x r
   for (int64_t l = 0; l < h.L; ++l)
     for (int64_t j = 0; j < h.r; ++j) o[j * h.L + l] = tmp[l * h.r + j];
   return MOARA_OK;
@@ -1565,9 +1600,13 @@ int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* ho
             : which == MOARA_T_EXP_AVG ? (void*)h.exp1
             : which == MOARA_T_EXP_AVG_SQ ? (void*)h.exp2
             : which == MOARA_T_MAG_AVG ? (void*)h.mag1 : (void*)h.mag2;
-  const bool transpose = (which == MOARA_T_EXP_AVG || which == MOARA_T_EXP_AVG_SQ) && h.side == MOARA_SIDE_LEFT;
+  const bool moment = which == MOARA_T_EXP_AVG || which == MOARA_T_EXP_AVG_SQ;
+  const bool transpose = moment && h.side == MOARA_SIDE_LEFT;
+  const bool narrow = moment && st->cfg.moment_dtype == MOARA_BF16;
   std::vector<float> tmp;
+  std::vector<uint16_t> raw;
   const void* src = host_src;
+  size_t dev_bytes = need;
   if (transpose) {
     tmp.resize((size_t)h.L * h.r);
     const float* in = (const float*)host_src;
@@ -1575,9 +1614,17 @@ int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* ho
       for (int64_t j = 0; j < h.r; ++j) tmp[l * h.r + j] = in[j * h.L + l];
     src = tmp.data();
   }
+  if (narrow) {
+    const size_t cnt = (size_t)h.L * h.r;
+    const float* in = (const float*)src;
+    raw.resize(cnt);
+    for (size_t i = 0; i < cnt; ++i) raw[i] = host_f32_to_bf16(in[i]);
+    src = raw.data();
+    dev_bytes = 2 * cnt;
+  }
   ORDER_ON(st, hs);
   HIP_TRY(hipStreamSynchronize(hs));
-  HIP_TRY(hipMemcpyAsync(dst, src, need, hipMemcpyHostToDevice, hs));
+  HIP_TRY(hipMemcpyAsync(dst, src, dev_bytes, hipMemcpyHostToDevice, hs));
   if (which == MOARA_T_P) {
     HIP_TRY(launch_convert_projector(h.P32, h.Pop, h.Ptop, h.s, h.r, st->cfg.operand_dtype == MOARA_BF16, h.kp ? 1 : 0,
                                      hs));

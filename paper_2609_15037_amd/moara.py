@@ -57,7 +57,7 @@ class moara_config(ctypes.Structure):
         ("grad_dtype", ctypes.c_int32), ("operand_dtype", ctypes.c_int32),
         ("refresh_oversample", ctypes.c_int32), ("refresh_iters", ctypes.c_int32),
         ("refresh_seed", ctypes.c_uint64),
-        ("zero_grad_mode", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("zero_grad_mode", ctypes.c_int32), ("moment_dtype", ctypes.c_int32),
     ]
 
 

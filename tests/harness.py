@@ -30,6 +30,7 @@ class Case:
     block_size: int
     weight_dtype: str = "f32"
     operand_dtype: str = "f32"
+    moment_dtype: str = "f32"      # storage of the direction moments: "f32" or "bf16"
     decompose: bool = True
     beta1: float = 0.9
     beta2: float = 0.999
@@ -50,6 +51,7 @@ def case_from_workload(wl: WL.Workload, operand_dtype: Optional[str] = None) -> 
     return Case(shapes=[(m.rows, m.cols, m.module) for m in wl.matrices],
                 ranks=[wl.rank_of(m) for m in wl.matrices], block_size=wl.block_size,
                 weight_dtype=wl.weight_dtype, operand_dtype=operand_dtype or wl.operand_dtype,
+                moment_dtype=wl.moment_dtype,
                 adam_eps=wl.adam_eps, beta1=wl.beta1, beta2=wl.beta2, scale=wl.scale, lr=wl.lr,
                 weight_std=wl.weight_std, grad_std=wl.grad_std,
                 refresh_oversample=wl.refresh_oversample, refresh_iters=wl.refresh_iters)
@@ -58,7 +60,8 @@ def case_from_workload(wl: WL.Workload, operand_dtype: Optional[str] = None) -> 
 def oracle_cfg(c: Case, i: int, refresh_interval: int = 0) -> O.OracleConfig:
     return O.OracleConfig(block_size=c.block_size, rank=c.ranks[i], beta1=c.beta1, beta2=c.beta2,
                           adam_eps=c.adam_eps, scale=c.scale, refresh_interval=refresh_interval,
-                          decompose=c.decompose, weight_dtype=c.weight_dtype, operand_dtype=c.operand_dtype)
+                          decompose=c.decompose, weight_dtype=c.weight_dtype, operand_dtype=c.operand_dtype,
+                          moment_dtype=c.moment_dtype)
 
 
 def gpu_state(c: Case, refresh_interval: int = 0, refresh_iters=None, oversample=None, seed: int = 0, **extra):
@@ -70,6 +73,7 @@ def gpu_state(c: Case, refresh_interval: int = 0, refresh_iters=None, oversample
         refresh_interval=refresh_interval, decompose=1 if c.decompose else 0,
         weight_dtype=M.MOARA_BF16 if c.weight_dtype == "bf16" else M.MOARA_F32,
         operand_dtype=M.MOARA_BF16 if c.operand_dtype == "bf16" else M.MOARA_F32,
+        moment_dtype=M.MOARA_BF16 if c.moment_dtype == "bf16" else M.MOARA_F32,
         refresh_iters=refresh_iters, refresh_oversample=oversample, refresh_seed=seed, **extra)
     descs = M.make_descs([(m, n, mod, r) for (m, n, mod), r in zip(c.shapes, c.ranks)])
     return M.moara_create_state(cfg, descs)
@@ -95,7 +99,8 @@ def to_np(t) -> np.ndarray:
 
 
 def oracle_projector(G: np.ndarray, c: Case, i: int) -> np.ndarray:
-    """Top-r projector of the first step's direction tensor, rounded to fp32 (fed to both sides)."""
+    """The oracle's top-r projector of G's direction tensor (its truncated SVD), rounded to
+    fp32: fed to both sides."""
     _, V = O.decompose(G, c.block_size) if c.decompose else (None, G.astype(np.float64))
     side = O.projection_side(*G.shape)
     return O.round_f32(O.truncated_svd(V, c.ranks[i], side))
@@ -201,3 +206,46 @@ def seeded_history(c: Case, i: int, R_scale: float, M_scale: np.ndarray, seed: i
     a1 = M_scale * 10.0 ** g.uniform(-0.3, 0.3, (m, k))
     a2 = (a1 ** 2) * 10.0 ** g.uniform(0.0, 1.5, (m, k))
     return [O.round_f32(x) for x in (e1, e2, a1, a2)]
+
+
+# ------------------------------------------------------------------ the library's in-step refresh
+# After a refresh, the steps depend on the projector's basis, which is unique only up to
+# rotations inside clusters of (nearly) equal singular values. Parity with the oracle is
+# therefore taken on a state that receives the oracle's own projector (moara_set_tensor);
+# the library's own refresh inside moara_step is checked by principal angle against the
+# oracle's SVD, and, library against library, bit for bit against an explicit
+# moara_refresh_projector before the step whose projector is read back and set again
+# (so that the operand copies the refresh wrote equal those moara_set_tensor derives).
+
+STATE_TENSORS = ("P", "exp_avg", "exp_avg_sq", "mag_avg", "mag_avg_sq")
+
+
+def explicit_refresh(M, st, Gd, mask):
+    """moara_refresh_projector on the matrices in `mask`, then each new projector read back
+    and set again through moara_set_tensor."""
+    import torch
+    if not any(mask):
+        return
+    M.moara_refresh_projector(st, [g if k else None for g, k in zip(Gd, mask)],
+                              active=np.asarray(mask, dtype=np.uint8))
+    torch.cuda.synchronize()
+    for i, k in enumerate(mask):
+        if k:
+            M.moara_set_tensor(st, i, M.MOARA_T_P, M.moara_get_tensor(st, i, M.MOARA_T_P))
+
+
+def assert_same_state(M, sa, sb, Wa, Wb, idx, what=""):
+    """W, projector, all four moments and the counter bit-identical in two library states."""
+    import torch
+    ids = {"P": M.MOARA_T_P, "exp_avg": M.MOARA_T_EXP_AVG, "exp_avg_sq": M.MOARA_T_EXP_AVG_SQ,
+           "mag_avg": M.MOARA_T_MAG_AVG, "mag_avg_sq": M.MOARA_T_MAG_AVG_SQ}
+    for i in idx:
+        assert torch.equal(Wa[i], Wb[i]), f"{what} matrix {i}: W differs"
+        ta, tb = M.moara_get_tensor(sa, i, M.MOARA_T_STEP), M.moara_get_tensor(sb, i, M.MOARA_T_STEP)
+        assert ta == tb, f"{what} matrix {i}: counter {ta} vs {tb}"
+        for name in STATE_TENSORS:
+            if name == "P" and ta == 0:
+                continue
+            a, b = M.moara_get_tensor(sa, i, ids[name]), M.moara_get_tensor(sb, i, ids[name])
+            assert np.array_equal(a, b), f"{what} matrix {i}: {name} differs"
+

@@ -99,7 +99,7 @@ def test_resolve_matrix_errors():
 @pytest.mark.parametrize("field,value,code", [
     ("block_size", 0, -1), ("beta1", 1.0, -1), ("beta2", -0.1, -1), ("adam_eps", 0.0, -1),
     ("weight_decay", 0.01, -4), ("grad_dtype", 1, -4), ("operand_dtype", 7, -1), ("refresh_iters", 0, -1),
-    ("refresh_interval", -1, -1), ("zero_grad_mode", 2, -1), ("decompose", 2, -1), ("reserved", 3, -1),
+    ("refresh_interval", -1, -1), ("zero_grad_mode", 2, -1), ("decompose", 2, -1), ("moment_dtype", 3, -1),
 ])
 def test_create_state_validates_before_touching_the_gpu(field, value, code):
     _lib()
@@ -157,6 +157,17 @@ def test_state_bytes_counts_fp32_moments_projector_copies_and_v_workspace():
         exp32 += 4 * al(4 * m * k) + 2 * al(4 * L * r) + al(4 * L * r) + al(4 * s * r) + 2 * al(4 * s * r)
     exp32 += al(16 * len(shapes))
     assert sb32 == exp32
+    # bf16 direction moments (2-byte states) halve exp_avg / exp_avg_sq and nothing else
+    cfgm = M.moara_default_config(rank_table=[64] * 10, block_size=64, operand_dtype=M.MOARA_BF16,
+                                  moment_dtype=M.MOARA_BF16)
+    sbm, rbm = M.moara_state_bytes(cfgm, descs)
+    assert rbm == rb
+    assert sbm == sb - sum(2 * al(4 * max(m, n) * 64) - 2 * al(2 * max(m, n) * 64) for m, n in shapes)
+
+
+def test_default_config_keeps_fp32_direction_moments():
+    _lib()
+    assert M.moara_default_config().moment_dtype == M.MOARA_F32
 
 
 def test_alignment_rejects_bad_arguments_before_any_gpu_work():

@@ -13,7 +13,9 @@
   refresh on an expert's first active step.
 
 Step parity uses a seeded random orthonormal projector on both sides (the step
-is defined for any P); refresh parity uses the oracle's SVD.
+is defined for any P), or, across a refresh, the oracle's own SVD projector set
+into the parity state; the library's refresh is checked by principal angles against
+the oracle's SVD and, library against library, bit for bit against an explicit refresh.
 """
 import dataclasses
 
@@ -22,8 +24,8 @@ import pytest
 
 import workloads as WL
 from oracle import moara_oracle as O
-from tests.harness import (TOL_BF16, Case, adam_sensitivity, case_from_workload, compare, gpu_state, have_gpu,
-                           oracle_cfg, rng, slices_of, to_dev, to_np)
+from tests.harness import (TOL_BF16, Case, adam_sensitivity, assert_same_state, case_from_workload, compare,
+                           explicit_refresh, gpu_state, have_gpu, oracle_cfg, rng, slices_of, to_dev, to_np)
 
 pytestmark = [pytest.mark.gpu, pytest.mark.skipif(not have_gpu(), reason="needs an MI355X GPU")]
 
@@ -166,12 +168,50 @@ def test_qwen2_7b_attention_refresh():
         assert ang <= 1e-3
 
 
+def _routed_parity(M, c, ost, Wo, Gs, act, C, WC, parity_idx, lr):
+    """One step of the parity state C (interval 0) and of the oracle on the matrices in
+    parity_idx (C's index j holds matrix parity_idx[j]): on a matrix's first active step
+    the oracle refreshes from its own SVD and C receives that projector first."""
+    due = []
+    for j, i in enumerate(parity_idx):
+        if act[i] and ost[j].t == 0:
+            ost[j].P = O.round_f32(O.truncated_svd(O.decompose(Gs[i], c.block_size)[1], c.ranks[i], ost[j].side))
+            M.moara_set_tensor(C, j, M.MOARA_T_P, ost[j].P)
+            due.append(i)
+    actc = np.array([act[i] for i in parity_idx], dtype=np.uint8)
+    M.moara_step(C, WC, [to_dev(Gs[i], "f32") if act[i] else None for i in parity_idx], lr=lr, active=actc)
+    for j, i in enumerate(parity_idx):
+        if act[i]:
+            Wo[j] = O.step(Wo[j], Gs[i], ost[j], oracle_cfg(c, i), lr)
+    return due
+
+
+def _check_routed(M, c, names, ost, Wo, W0, C, WC, report):
+    stepped = 0
+    for j in range(len(ost)):
+        assert M.moara_get_tensor(C, j, M.MOARA_T_STEP) == ost[j].t
+        Wg = to_np(WC[j])
+        if ost[j].t == 0:
+            assert np.array_equal(Wg, W0[j]), f"{names[j]}: idle expert changed"
+            continue
+        stepped += 1
+        compare(f"W[{j}]", Wg, Wo[j], TOL_BF16, report)
+        for name, k, ref in (("exp_avg", M.MOARA_T_EXP_AVG, ost[j].exp_avg),
+                             ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ, ost[j].exp_avg_sq),
+                             ("mag_avg", M.MOARA_T_MAG_AVG, ost[j].mag_avg),
+                             ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ, ost[j].mag_avg_sq)):
+            compare(f"{name}[{j}]", M.moara_get_tensor(C, j, k), ref, TOL_BF16, report)
+    return stepped
+
+
 def test_deepseek_moe_layer_routed_experts():
     """8 routed experts (of the layer's 64; routing keeps its 6-of-64 draw, so some
     of them are idle on a step) + 2 shared + attention, per-expert refresh (T=200:
-    a matrix refreshes on its first active step), three steps. The refresh is checked
-    by principal angles against the oracle's SVD; the oracle's step then uses the
-    GPU's projector so that the updates compare element by element."""
+    a matrix refreshes on its first active step), three steps. State A runs that
+    schedule; state B (interval 0) is refreshed explicitly on the same steps and must
+    stay bit-identical to A; A's projectors lie within 1e-3 rad of the oracle's SVD; the
+    parity state C takes the oracle's projector on a matrix's first active step and is
+    compared with the oracle element by element; idle experts stay bit-identical."""
     import torch
     M = _M()
     full = WL.subset(WL.WORKLOADS["deepseek_moe"], [0])
@@ -180,45 +220,38 @@ def test_deepseek_moe_layer_routed_experts():
     wl = dataclasses.replace(full, matrices=tuple(full.matrices[i] for i in keep))
     c = case_from_workload(wl)
     n = len(wl.matrices)
-    st = gpu_state(c, refresh_interval=200)
-    Wd = [WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
-          for i, m in enumerate(wl.matrices)]
-    W0 = [to_np(w) for w in Wd]
+    A, B, C = gpu_state(c, refresh_interval=200), gpu_state(c), gpu_state(c)
+    WA, WB, WC = [[WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
+                   for i, m in enumerate(wl.matrices)] for _ in range(3)]
+    W0 = [to_np(w) for w in WC]
     Wo = [w.copy() for w in W0]
-    ocfg = [oracle_cfg(c, i) for i in range(n)]          # refresh handled here, with the GPU's P
-    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[i]) for i in range(n)]
+    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], oracle_cfg(c, i)) for i in range(n)]
     report, refreshed, worst_angle = {}, 0, 0.0
     for t in range(3):
         act = np.array([act_all[t][k] for k in keep], dtype=np.uint8)
         Gs = [WL.grad_np(full, k, t, active=bool(a)) for k, a in zip(keep, act)]
+        Gd = [to_dev(g, "f32") if a else None for g, a in zip(Gs, act)]
         print(f"[fullsize] deepseek_moe step {t}: {int(act.sum())} of {n} matrices active", flush=True)
-        M.moara_step(st, Wd, [to_dev(g, "f32") if a else None for g, a in zip(Gs, act)], lr=c.lr, active=act)
+        first = [bool(act[i]) and M.moara_get_tensor(B, i, M.MOARA_T_STEP) == 0 for i in range(n)]
+        explicit_refresh(M, B, Gd, first)
+        M.moara_step(A, WA, Gd, lr=c.lr, active=act)
+        M.moara_step(B, WB, Gd, lr=c.lr, active=act)
+        due = _routed_parity(M, c, ost, Wo, Gs, act, C, WC, list(range(n)), c.lr)
         torch.cuda.synchronize()
-        for i in range(n):
-            if not act[i]:
-                continue
-            if ost[i].t == 0:   # first active step: the GPU refreshed this matrix's projector
-                Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
-                _, V = O.decompose(Gs[i], c.block_size)
-                ref = O.truncated_svd(V, c.ranks[i], O.projection_side(*Gs[i].shape))
-                ang = O.max_principal_angle(Pg, ref)
-                worst_angle = max(worst_angle, ang)
-                assert ang <= 1e-3, f"{wl.matrices[i].name}: refresh principal angle {ang:.2e}"
-                ost[i].P = O.round_f32(Pg)
-                refreshed += 1
-            Wo[i] = O.step(Wo[i], Gs[i], ost[i], ocfg[i], c.lr)
+        assert due == [i for i in range(n) if first[i]]
+        assert_same_state(M, A, B, WA, WB, range(n), f"step {t}:")
+        for i in due:
+            ang = O.max_principal_angle(M.moara_get_tensor(A, i, M.MOARA_T_P).astype(np.float64), ost[i].P)
+            worst_angle = max(worst_angle, ang)
+            assert ang <= 1e-3, f"{wl.matrices[i].name}: refresh principal angle {ang:.2e}"
+            refreshed += 1
+    stepped = _check_routed(M, c, [m.name for m in wl.matrices], ost, Wo, W0, C, WC, report)
     for i in range(n):
-        t_gpu = M.moara_get_tensor(st, i, M.MOARA_T_STEP)
-        assert t_gpu == ost[i].t, f"{wl.matrices[i].name}: counter {t_gpu} vs {ost[i].t}"
-        Wg = to_np(Wd[i])
         if ost[i].t == 0:
-            assert np.array_equal(Wg, W0[i]), f"{wl.matrices[i].name}: idle expert changed"
-            continue
-        compare(f"W[{i}]", Wg, Wo[i], TOL_BF16, report)
-        compare(f"exp_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_EXP_AVG), ost[i].exp_avg, TOL_BF16, report)
-        compare(f"mag_avg[{i}]", M.moara_get_tensor(st, i, M.MOARA_T_MAG_AVG), ost[i].mag_avg, TOL_BF16, report)
-    print(f"[fullsize] deepseek_moe: {sum(o.t > 0 for o in ost)} of {n} matrices stepped, {refreshed} refreshes "
-          f"(worst angle {worst_angle:.2e}), worst floored rel err {max(report.values()):.3e}", flush=True)
+            assert torch.equal(WA[i], WC[i]), f"{wl.matrices[i].name}: idle expert changed in A"
+    print(f"[fullsize] deepseek_moe: {stepped} of {n} matrices stepped, {refreshed} refreshes "
+          f"(worst angle {worst_angle:.2e}, A = B bit for bit), worst floored rel err {max(report.values()):.3e}",
+          flush=True)
 
 
 def test_qwen2_7b_mlp_refresh():
@@ -255,11 +288,14 @@ def test_qwen2_7b_mlp_refresh():
 
 def test_deepseek_moe_full_state_one_layer_checked():
     """All 5,656 matrices of the DeepSeek-MoE batch (28 layers: attention, 2 shared and 64
-    routed experts) in one state, stepped with the router's active set (6 of 64 routed
+    routed experts) in one state A, stepped with the router's active set (6 of 64 routed
     experts per layer and step) exactly as the benchmark runs them; per-expert refresh on
-    an expert's first active step (T = 200). The oracle follows every matrix of the last
-    layer: refreshes by principal angle, then the step with the library's projector; idle
-    experts must stay bit-identical."""
+    an expert's first active step (T = 200). The last layer is followed three ways: a
+    second full state B (interval 0, same matrix order, only that layer active, refreshed
+    explicitly) must match A bit for bit there; A's new projectors lie within 1e-3 rad of
+    the oracle's SVD; a parity state C holding only that layer takes the oracle's
+    projectors and is compared with the oracle element by element. Idle experts stay
+    bit-identical in A."""
     import torch
     M = _M()
     wl = WL.WORKLOADS["deepseek_moe"]
@@ -267,13 +303,18 @@ def test_deepseek_moe_full_state_one_layer_checked():
     c = case_from_workload(wl)
     L = max(m.layer for m in wl.matrices)
     idx = [i for i, m in enumerate(wl.matrices) if m.layer == L]
-    st = gpu_state(c, refresh_interval=200)
-    Wd = [WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
+    A, B = gpu_state(c, refresh_interval=200), gpu_state(c)
+    cl = dataclasses.replace(c, shapes=[c.shapes[i] for i in idx], ranks=[c.ranks[i] for i in idx])
+    C = gpu_state(cl)
+    WA = [WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
           for i, m in enumerate(wl.matrices)]
-    W0 = {i: to_np(Wd[i]) for i in idx}
-    Wo = dict(W0)
-    ocfg = {i: oracle_cfg(c, i) for i in idx}
-    ost = {i: O.init_state(c.shapes[i][0], c.shapes[i][1], ocfg[i]) for i in idx}
+    WB = [WL.weight_device(wl, i, torch.empty((m.rows, m.cols), dtype=torch.bfloat16, device="cuda"))
+          if i in set(idx) else None for i, m in enumerate(wl.matrices)]
+    WC = [WL.weight_device(wl, i, torch.empty((wl.matrices[i].rows, wl.matrices[i].cols), dtype=torch.bfloat16,
+                                              device="cuda")) for i in idx]
+    W0 = [to_np(w) for w in WC]
+    Wo = [w.copy() for w in W0]
+    ost = [O.init_state(c.shapes[i][0], c.shapes[i][1], oracle_cfg(c, i)) for i in idx]
     report, refreshed, worst_angle = {}, 0, 0.0
     for t in range(3):
         act = np.asarray(WL.active_set(wl, t), dtype=np.uint8)
@@ -283,43 +324,36 @@ def test_deepseek_moe_full_state_one_layer_checked():
                 Gd.append(None)
                 continue
             g = torch.empty((m.rows, m.cols), dtype=torch.float32, device="cuda")
-            if i in ost:
+            if m.layer == L:
                 Gs[i] = WL.grad_np(wl, i, t, active=True)
                 g.copy_(torch.from_numpy(Gs[i]))
             else:
                 WL.grad_device(wl, i, t, g, active=True)
             Gd.append(g)
         torch.cuda.synchronize()
-        print(f"[fullsize] deepseek_moe full state: step {t}, {int(act.sum())} of {n} matrices active, oracle on "
-              f"layer {L}", flush=True)
-        M.moara_step(st, Wd, Gd, lr=c.lr, active=act)
+        print(f"[fullsize] deepseek_moe full state: step {t}, {int(act.sum())} of {n} matrices active, layer {L} "
+              f"followed", flush=True)
+        actL = np.array([a if wl.matrices[i].layer == L else 0 for i, a in enumerate(act)], dtype=np.uint8)
+        first = [bool(actL[i]) and M.moara_get_tensor(B, i, M.MOARA_T_STEP) == 0 for i in range(n)]
+        explicit_refresh(M, B, [g if actL[i] else None for i, g in enumerate(Gd)], first)
+        M.moara_step(A, WA, Gd, lr=c.lr, active=act)
+        M.moara_step(B, WB, [g if actL[i] else None for i, g in enumerate(Gd)], lr=c.lr, active=actL)
+        due = _routed_parity(M, c, ost, Wo, Gs, act, C, WC, idx, c.lr)
         torch.cuda.synchronize()
         del Gd
-        for i in idx:
-            if not act[i]:
-                continue
-            if ost[i].t == 0:   # the library refreshed this matrix on its first active step
-                Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
-                _, V = O.decompose(Gs[i], c.block_size)
-                ang = O.max_principal_angle(Pg, O.truncated_svd(V, c.ranks[i], ost[i].side))
+        assert due == [i for i in range(n) if first[i]]
+        assert_same_state(M, A, B, WA, WB, idx, f"full state, step {t}:")
+        for j, i in enumerate(idx):
+            if i in due:
+                ang = O.max_principal_angle(M.moara_get_tensor(A, i, M.MOARA_T_P).astype(np.float64), ost[j].P)
                 worst_angle = max(worst_angle, ang)
                 assert ang <= 1e-3, f"{wl.matrices[i].name}: refresh principal angle {ang:.2e}"
-                ost[i].P = O.round_f32(Pg)
                 refreshed += 1
-            Wo[i] = O.step(Wo[i], Gs[i], ost[i], ocfg[i], c.lr)
-    stepped = 0
-    for i in idx:
-        assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == ost[i].t
-        Wg = to_np(Wd[i])
-        if ost[i].t == 0:
-            assert np.array_equal(Wg, W0[i]), f"{wl.matrices[i].name}: idle expert changed"
-            continue
-        stepped += 1
-        compare(f"W[{i}]", Wg, Wo[i], TOL_BF16, report)
-        for name, k, ref in (("exp_avg", M.MOARA_T_EXP_AVG, ost[i].exp_avg),
-                             ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ, ost[i].exp_avg_sq),
-                             ("mag_avg", M.MOARA_T_MAG_AVG, ost[i].mag_avg),
-                             ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ, ost[i].mag_avg_sq)):
-            compare(f"{name}[{i}]", M.moara_get_tensor(st, i, k), ref, TOL_BF16, report)
+    stepped = _check_routed(M, c, [wl.matrices[i].name for i in idx], ost, Wo, W0, C, WC, report)
+    for j, i in enumerate(idx):
+        assert M.moara_get_tensor(A, i, M.MOARA_T_STEP) == ost[j].t
+        if ost[j].t == 0:
+            assert torch.equal(WA[i], WC[j]), f"{wl.matrices[i].name}: idle expert changed in A"
     print(f"[fullsize] deepseek_moe full state: {stepped} of {len(idx)} layer-{L} matrices stepped, {refreshed} "
-          f"refreshes (worst angle {worst_angle:.2e}), worst floored rel err {max(report.values()):.3e}", flush=True)
+          f"refreshes (worst angle {worst_angle:.2e}, A = B bit for bit), worst floored rel err "
+          f"{max(report.values()):.3e}", flush=True)

@@ -38,10 +38,9 @@ def _weights(c: Case, seed):
 def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=False, misalign: bool = False,
                 refresh_misaligned: bool = False, max_masked: float = 0.1):
     """Steps on the GPU and in the oracle from the same inputs, from zero moments. The
-    projector comes from the oracle's SVD (set into the library), or, with
-    refresh_misaligned, from the library's own refresh of the first gradients placed at
-    unaligned addresses (all-fp32 refresh path); the oracle then uses the library's P, so
-    the steps test the projector copies that the refresh wrote.
+    projector comes from the oracle's SVD (set into the library). With refresh_misaligned
+    the library first refreshes from the first gradients placed at unaligned addresses;
+    its projector must lie within 1e-3 rad of the oracle's, which then replaces it.
 
     At the fp32 bar, elements fed by first-step Adam outputs whose fp32 forward error
     estimate is large (adam_sensitivity) are held to TOL_MASKED instead; at most
@@ -69,8 +68,11 @@ def step_parity(c: Case, steps: int, seed: int = 0, grad_fn=None, check_every=Fa
             M.moara_refresh_projector(st, [to_dev(g, "f32", offset=1) for g in Gs])
             torch.cuda.synchronize()
             for i in range(n):
-                ost[i].P = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
-        elif t == 0:
+                Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+                np.testing.assert_allclose(Pg.T @ Pg, np.eye(Pg.shape[1]), atol=2e-5)
+                ang = O.max_principal_angle(Pg, oracle_projector(Gs[i], c, i))
+                assert ang <= 1e-3, f"matrix {i}: refresh from unaligned buffers: principal angle {ang:.2e}"
+        if t == 0:
             for i in range(n):
                 P = oracle_projector(Gs[i], c, i)
                 M.moara_set_tensor(st, i, M.MOARA_T_P, P)
@@ -153,12 +155,12 @@ def test_llama300m_layer_misaligned_caller_buffers():
     step_parity(c, 3, grad_fn=lambda t, i: WL.grad_np(wl, i, t), misalign=True)
 
 
-def test_llama300m_layer_refresh_then_steps():
-    # the step reads the operand copies of P that the refresh's output kernel wrote
-    # (blocked layout); the oracle steps with the same P (the library's fp32 master)
+def test_llama300m_layer_refresh_from_unaligned_buffers_then_steps():
+    # the refresh and the steps read gradients at unaligned addresses (the paths for caller
+    # buffers the large-tile kernels cannot take)
     wl = WL.subset(WL.WORKLOADS["llama_300m"], [7])
     c = case_from_workload(wl)
-    step_parity(c, 2, grad_fn=lambda t, i: WL.grad_np(wl, i, t), refresh_misaligned=True)
+    step_parity(c, 2, grad_fn=lambda t, i: WL.grad_np(wl, i, t), refresh_misaligned=True, misalign=True)
 
 
 @pytest.mark.parametrize("B", [1, 16, 32, 64, 128, 512, 1024, 48, 20, 256, 1000])   # the block sizes of Fig. 3, then odd ones
@@ -369,8 +371,8 @@ def test_inactive_matrices_are_untouched():
     assert not np.any(M.moara_get_tensor(st, 1, M.MOARA_T_EXP_AVG))
 
 
-@pytest.mark.parametrize("op,wdt", [("f32", "f32"), ("bf16", "bf16")])
-def test_zero_grad_mode_steps_inactive_matrices_with_zero_gradient(op, wdt):
+@pytest.mark.parametrize("op,wdt,mom", [("f32", "f32", "f32"), ("bf16", "bf16", "f32"), ("bf16", "bf16", "bf16")])
+def test_zero_grad_mode_steps_inactive_matrices_with_zero_gradient(op, wdt, mom):
     """zero_grad_mode 1: an inactive matrix takes the step of G = 0 (Algorithm 1 with a zero
     gradient: M = V = 0, both Adam branches decay their moments, W moves by
     Rep_B(dM) (.) P N). Against the oracle's step(W, 0) with the same projector, and bit for
@@ -378,7 +380,8 @@ def test_zero_grad_mode_steps_inactive_matrices_with_zero_gradient(op, wdt):
     import torch
     M = _M()
     c = Case(shapes=[(128, 192, WL.EXP_GATE), (128, 192, WL.EXP_UP), (192, 128, WL.EXP_DOWN)], ranks=[16] * 3,
-             block_size=64, operand_dtype=op, weight_dtype=wdt, weight_std=0.02 if wdt == "bf16" else 1e-3)
+             block_size=64, operand_dtype=op, weight_dtype=wdt, weight_std=0.02 if wdt == "bf16" else 1e-3,
+             moment_dtype=mom)
     tol = TOL_F32 if op == "f32" else TOL_BF16
     n = 3
     masks = [[1, 1, 1], [1, 0, 1], [0, 0, 1], [1, 1, 0], [0, 1, 0]]
@@ -397,7 +400,7 @@ def test_zero_grad_mode_steps_inactive_matrices_with_zero_gradient(op, wdt):
         ost[i].P = P
     zero = [torch.zeros(c.shapes[i][:2], device="cuda") for i in range(n)]
     for t, mask in enumerate(masks):
-        print(f"[zero-grad] step {t} active {mask} op={op} w={wdt}", flush=True)
+        print(f"[zero-grad] step {t} active {mask} op={op} w={wdt} moments={mom}", flush=True)
         act = np.array(mask, dtype=np.uint8)
         M.moara_step(st, Wd, [to_dev(grads[t][i], "f32") if mask[i] else None for i in range(n)], lr=c.lr,
                      active=act)
@@ -476,11 +479,12 @@ def test_state_used_from_two_streams_keeps_call_order():
         assert np.array_equal(a, b)
 
 
-def test_checkpoint_roundtrip_is_bit_identical():
+@pytest.mark.parametrize("mom", ["f32", "bf16"])
+def test_checkpoint_roundtrip_is_bit_identical(mom):
     import torch
     M = _M()
     c = Case(shapes=[(160, 224, WL.Q), (224, 160, WL.UP)], ranks=[24, 32], block_size=32, weight_dtype="bf16",
-             operand_dtype="bf16", weight_std=0.02)
+             operand_dtype="bf16", weight_std=0.02, moment_dtype=mom)
     grads = [[to_dev(_grad(c, 9, t, i), "f32") for i in range(2)] for t in range(6)]
     st = gpu_state(c, refresh_interval=4)
     Wa = [to_dev(w, "bf16") for w in _weights(c, 0)]
@@ -502,6 +506,28 @@ def test_checkpoint_roundtrip_is_bit_identical():
     torch.cuda.synchronize()
     for i in range(2):
         assert torch.equal(Wa[i], Wb[i])
+
+
+def test_bf16_moments_are_stored_rounded_to_nearest_even():
+    """With bf16 direction moments, moara_set_tensor rounds the fp32 values it is given to
+    nearest-even bf16 and moara_get_tensor widens them back exactly, in the paper's
+    orientation on both sides (LEFT r x n, RIGHT m x r): equal to the oracle's rounding,
+    bit for bit, including ties, subnormals and overflow to infinity."""
+    M = _M()
+    c = Case(shapes=[(48, 80, WL.Q), (80, 48, WL.UP)], ranks=[8, 8], block_size=16, moment_dtype="bf16")
+    st = gpu_state(c)
+    special = np.array([1.0 + 2.0 ** -8, 1.0 + 3 * 2.0 ** -8, -(1.0 + 2.0 ** -8), 2.0 ** -130, 3.0 * 2.0 ** -134,
+                        3.3e38, -3.4e38, 0.0, -0.0, 1e-45], dtype=np.float32)
+    for i, (m, n) in enumerate([(48, 80), (80, 48)]):
+        shp = (8, n) if m <= n else (m, 8)
+        for k, seed in ((M.MOARA_T_EXP_AVG, 1), (M.MOARA_T_EXP_AVG_SQ, 2)):
+            v = (rng(seed, i).standard_normal(shp) * 10.0 ** rng(seed, i, 1).uniform(-6, 3, shp)).astype(np.float32)
+            v.ravel()[:special.size] = special
+            M.moara_set_tensor(st, i, k, v)
+            got = M.moara_get_tensor(st, i, k)
+            ref = O.round_bf16(v.astype(np.float64))
+            assert np.array_equal(got.astype(np.float64), ref), f"matrix {i} tensor {k}"
+            assert np.array_equal(np.signbit(got), np.signbit(ref))
 
 
 def test_runs_are_deterministic():
@@ -550,10 +576,14 @@ def test_alignment_matches_oracle(decompose, op):
     print(f"[alignment] decompose={decompose} operands={op}", flush=True)
     M.moara_refresh_projector(st, Gd)
     steps0 = [M.moara_get_tensor(st, i, M.MOARA_T_STEP) for i in range(len(Gs))]
+    # S depends on the projector's span only; both sides take the oracle's (the first r
+    # canonical vectors for the all-zero gradient, as after the library's refresh of it)
+    Ps = [oracle_projector(G, c, i) if i != 4 else np.eye(3, 2) for i, G in enumerate(Gs)]
+    for i, P in enumerate(Ps):
+        M.moara_set_tensor(st, i, M.MOARA_T_P, P)
     S = M.moara_alignment(st, Gd)
     for i, G in enumerate(Gs):
-        P = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
-        ref = O.alignment(G, P, c.block_size, decompose_on=decompose)
+        ref = O.alignment(G, Ps[i], c.block_size, decompose_on=decompose)
         assert abs(S[i] - ref) <= 1e-5, (i, S[i], ref)
         assert M.moara_get_tensor(st, i, M.MOARA_T_STEP) == steps0[i]
     assert S[4] == 0.0 and all(0.0 < S[i] < 1.0 for i in range(4))
@@ -586,20 +616,23 @@ def test_profiling_run_gives_the_oracles_module_scores():
     M = _M()
     c = Case(shapes=[(96, 160, WL.Q), (96, 160, WL.K), (160, 96, WL.GATE), (96, 200, WL.DOWN), (96, 160, WL.Q)],
              ranks=[16, 16, 16, 16, 16], block_size=32)
-    st = gpu_state(c, refresh_interval=4)
+    st = gpu_state(c)
     W = [to_dev(w, c.weight_dtype) for w in _weights(c, 8)]
     prof = PR.AlignmentProfile([sh[2] for sh in c.shapes], stride=2, n_p=6)
-    samples = []
+    samples, Ps = [], None
     for t in range(1, 8):
         Gs = [_grad(c, 9, t, i) for i in range(len(c.shapes))]
         Gd = [to_dev(g, "f32") for g in Gs]
-        M.moara_step(st, W, Gd, lr=1e-3)   # refreshes on steps 1 and 5 (counter 0 and 4)
+        if t in (1, 5):   # the T = 4 schedule (counter 0 and 4), with the oracle's projectors
+            Ps = [oracle_projector(G, c, i) for i, G in enumerate(Gs)]
+            for i, P in enumerate(Ps):
+                M.moara_set_tensor(st, i, M.MOARA_T_P, P)
+        M.moara_step(st, W, Gd, lr=1e-3)
         torch.cuda.synchronize()
         if prof.due(t):
             S = prof.record(st, Gd, t=t)
             for i, G in enumerate(Gs):
-                P = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
-                ref = O.alignment(G, P, c.block_size)
+                ref = O.alignment(G, Ps[i], c.block_size)
                 assert abs(S[i] - ref) <= 1e-5, (t, i, S[i], ref)
                 samples.append((c.shapes[i][2], ref))
     assert prof.steps == [2, 4, 6]

@@ -22,7 +22,8 @@ def _opt(model, **kw):
     from paper_2609_15037_amd.optim import MoARa, moara_targets
     targets, others = moara_targets(model)
     ranks = M.moara_allocate_ranks(64, range(7), [M.MOARA_Q, M.MOARA_K], [M.MOARA_DOWN], 32)
-    return MoARa(targets, others, lr=kw.pop("lr", 1e-2), rank_table=ranks, block_size=64, refresh_interval=20, **kw)
+    return MoARa(targets, others, lr=kw.pop("lr", 1e-2), rank_table=ranks, block_size=64,
+                 refresh_interval=kw.pop("refresh_interval", 20), **kw)
 
 
 def _batch(seed, step):
@@ -127,16 +128,17 @@ def test_experts_without_gradient_are_skipped():
 def test_moara_steps_of_a_bf16_model_match_the_oracle():
     """The optimizer wrapper end to end on a bf16 model: three MoARa.step calls under a
     warmup schedule (the lr is read from param_groups), bf16 gradients copied to fp32 by
-    the wrapper, the projector refreshed inside the first step. The oracle repeats each
-    step on every target weight from the same fp32 gradient values, the same lr and the
-    library's projector (whose refresh is checked by principal angle elsewhere), with the
-    bf16 operand and weight roundings; weights agree to the bf16 bar and in bf16 ulps."""
+    the wrapper. Before the first step every target's projector is set to the oracle's SVD
+    of its first gradient through load_state_dict (the library's own refresh is checked
+    against the oracle elsewhere). The oracle repeats each step on every target weight from
+    the same fp32 gradient values, the same lr and that projector, with the bf16 operand
+    and weight roundings; weights agree to the bf16 bar and in bf16 ulps."""
     from oracle import moara_oracle as O
     from paper_2609_15037_amd import moara as M
     from paper_2609_15037_amd.optim import warmup_cosine
     from tests.harness import TOL_BF16, bf16_ulp, compare
     model = _model(5).to(torch.bfloat16)
-    opt = _opt(model)
+    opt = _opt(model, refresh_interval=0)
     sched = torch.optim.lr_scheduler.LambdaLR(opt, warmup_cosine(20, warmup_frac=0.2))   # 4 warmup steps
     targets = list(opt.param_groups[0]["params"])
     cfg = opt._cfg
@@ -156,14 +158,18 @@ def test_moara_steps_of_a_bf16_model_match_the_oracle():
         grads = [p.grad.detach().float().cpu().numpy().reshape(M.flatten_shape(p.shape)) for p in targets]
         lr = float(opt.param_groups[0]["lr"])
         lrs.append(lr)
+        if step == 0:
+            for i in range(len(targets)):
+                ost[i].P = O.round_f32(O.truncated_svd(O.decompose(grads[i], cfg.block_size)[1], ocfg[i].rank,
+                                                       ost[i].side))
+            opt.load_state_dict({"moara": [{"step": 0, "P": torch.from_numpy(o.P.astype(np.float32))} for o in ost],
+                                 "adamw": None, "lr": [g["lr"] for g in opt.param_groups]})
         print(f"[wrapper] step {step}, lr {lr:.3e}", flush=True)
         opt.step()
         sched.step()
         opt.zero_grad()
         torch.cuda.synchronize()
         for i in range(len(targets)):
-            if step == 0:
-                ost[i].P = M.moara_get_tensor(opt.moara_state, i, M.MOARA_T_P).astype(np.float64)
             Wo[i] = O.step(Wo[i], grads[i], ost[i], ocfg[i], lr)
     assert len(set(lrs)) == 3   # the warmup changed the lr every step
     beyond, exact = 0, 1.0

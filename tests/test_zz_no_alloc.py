@@ -78,9 +78,10 @@ def test_step_noalloc_matches_step_on_two_calls_in_a_row():
 
 
 def test_step_noalloc_zero_grad_mode_and_inactive_matrices():
+    """zero_grad_mode 1 with bf16 direction moments (the zero-gradient kernel's 2-byte path)."""
     M = _M()
     c = Case(shapes=[(128, 192, WL.EXP_GATE), (128, 192, WL.EXP_UP), (192, 128, WL.EXP_DOWN)], ranks=[16] * 3,
-             block_size=64, operand_dtype="bf16", weight_dtype="bf16", weight_std=0.02)
+             block_size=64, operand_dtype="bf16", weight_dtype="bf16", weight_std=0.02, moment_dtype="bf16")
     W, G = _inputs(c, 8, 4)
     sa = gpu_state(c, refresh_interval=2, zero_grad_mode=1)
     sb = gpu_state(c, refresh_interval=2, zero_grad_mode=1)

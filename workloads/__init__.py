@@ -56,6 +56,8 @@ class Workload:
     block_size: int
     weight_dtype: str                      # "f32" | "bf16"
     operand_dtype: str                     # GEMM operand dtype used for this workload's headline run
+    moment_dtype: str = "f32"              # storage of the direction moments: "f32" | "bf16" (2-byte
+                                           # states, the paper's training setting)
     lr: float = 1e-3
     beta1: float = 0.9
     beta2: float = 0.999
@@ -159,28 +161,28 @@ def build_workloads() -> dict:
         description="Llama-300M-shaped stack: 24 layers d=1024 ffn=2736, bf16 weights, rank-64 1/i gradients",
         matrices=_stack(24, _dense_layer, 1024, 2736),
         rank_table=_ranks(q=128, k=128, v=256, o=256, gate=192, up=192, down=192),
-        block_size=64, weight_dtype="bf16", operand_dtype="bf16",
+        block_size=64, weight_dtype="bf16", operand_dtype="bf16", moment_dtype="bf16",
         lowrank_rank=64, lowrank_power=1.0, noise_std=1e-4, steps=400, n_layers=24)
     w["llama2_7b"] = Workload(
         name="llama2_7b",
         description="Llama-2-7B-shaped stack: 32 layers d=4096 ffn=11008, bf16 weights, rank-256 i^-0.8 gradients",
         matrices=_stack(32, _dense_layer, 4096, 11008),
         rank_table=_ranks(q=512, k=512, v=1024, o=1024, gate=768, up=768, down=768),
-        block_size=128, weight_dtype="bf16", operand_dtype="bf16",
+        block_size=128, weight_dtype="bf16", operand_dtype="bf16", moment_dtype="bf16",
         lowrank_rank=256, lowrank_power=0.8, noise_std=1e-4, steps=200, n_layers=32)
     w["qwen2_7b"] = Workload(
         name="qwen2_7b",
         description="Qwen2-7B-shaped GQA stack: 28 layers d=3584, k/v 512x3584, ffn=18944, bf16 weights",
         matrices=_stack(28, _dense_layer, 3584, 18944, 512),
         rank_table=_ranks(q=512, k=128, v=128, o=512, gate=1024, up=1024, down=1024),
-        block_size=128, weight_dtype="bf16", operand_dtype="bf16",
+        block_size=128, weight_dtype="bf16", operand_dtype="bf16", moment_dtype="bf16",
         lowrank_rank=256, lowrank_power=0.8, noise_std=1e-4, steps=200, n_layers=28)
     w["deepseek_moe"] = Workload(
         name="deepseek_moe",
         description="DeepSeek-MoE-shaped stack: 28 layers d=2048, 64 routed (6 active) + 2 shared experts of ffn 1408",
         matrices=_stack(28, _moe_layer, 2048, 1408, 64, 2),
         rank_table=_ranks(q=512, k=512, v=512, o=512, exp_gate=128, exp_up=128, exp_down=128),
-        block_size=128, weight_dtype="bf16", operand_dtype="bf16",
+        block_size=128, weight_dtype="bf16", operand_dtype="bf16", moment_dtype="bf16",
         lowrank_rank=256, lowrank_power=0.8, noise_std=1e-4, steps=200, n_layers=28,
         moe_routed=64, moe_active=6)
     # model-family comparison at 350M scale (Appendix D model table): d = 1024, 24 layers,
@@ -192,14 +194,14 @@ def build_workloads() -> dict:
         w[name] = Workload(
             name=name, description=f"{desc}: 24 layers d=1024, k/v 256x1024 (4 kv heads), ffn={ffn}, bf16 weights",
             matrices=_stack(24, _dense_layer, 1024, ffn, 256), rank_table=r350,
-            block_size=32, weight_dtype="bf16", operand_dtype="bf16",
+            block_size=32, weight_dtype="bf16", operand_dtype="bf16", moment_dtype="bf16",
             lowrank_rank=64, lowrank_power=1.0, noise_std=1e-4, steps=200, n_layers=24)
     w["deepseek_v2_350m"] = Workload(
         name="deepseek_v2_350m",
         description="DeepSeek-V2-350M-shaped MLA stack: 24 layers d=1024, q_lora 768, kv_lora 256, "
                     "head dims 64/32/64, 16 heads, dense ffn=2736, bf16 weights",
         matrices=_stack(24, _mla_layer, 1024, 2736, 16, 768, 256, 64, 32, 64), rank_table=r350,
-        block_size=32, weight_dtype="bf16", operand_dtype="bf16",
+        block_size=32, weight_dtype="bf16", operand_dtype="bf16", moment_dtype="bf16",
         lowrank_rank=64, lowrank_power=1.0, noise_std=1e-4, steps=200, n_layers=24)
     return w
 
