@@ -241,7 +241,7 @@ int moara_step(moara_state* st, void* const* weights, const void* const* grads,
  * bookkeeping uses ordinary heap memory; a refresh chunk's descriptors are copied from
  * it synchronously (the call then waits for that copy). Errors: as moara_step, plus
  * MOARA_E_UNSUPPORTED for the limits above. */
-#define MOARA_NOALLOC_SCRATCH_BYTES (512ull << 20)
+#define MOARA_NOALLOC_SCRATCH_BYTES (1024ull << 20)
 int moara_step_noalloc(moara_state* st, void* const* weights, const void* const* grads,
                        const uint8_t* active, float lr, void* stream);
 

@@ -56,6 +56,15 @@ struct GemmProb {
   uint32_t tri_b;     // fp32 kind: 1 = B[j][k] is zero for k > j (upper triangular right factor),
                       // so a tile's K loop stops after its last column
   double* red;        // EP_ALIGN accumulators (three per problem)
+  // Large-tile path, split operands: the K loop runs nseg (1 .. 6) segments of K each,
+  // segment 0 on (a, b), segment i > 0 on (seg_a[i-1], seg_b[i-1]), all with the layouts
+  // and extents of a and b; with the operands split into bf16 parts (x = x_h + x_m + x_l)
+  // this forms a product near fp32 accuracy from bf16 MFMA work. nseg 0 means 1.
+  const void* seg_a[5];
+  const void* seg_b[5];
+  int32_t nseg;
+  int32_t pad2_;
+  void* c_lo;         // EP_STORE_BF16: also store the residual bf16(C - bf16(C)) here (nullable)
 };
 
 struct GemmUniform {

@@ -241,7 +241,7 @@ size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w, int32_t r, bool bf) {
   const int64_t wpad = (w + 63) / 64 * 64;
   size_t b = 0;
   b += align_up(4 * (size_t)s * r) + align_up(4 * (size_t)r * w);   // Pw, Bt
-  if (bf) b += align_up(2 * (size_t)s * L) + align_up(2 * (size_t)w * s) + align_up(2 * (size_t)w * L);
+  if (bf) b += 5 * align_up(2 * (size_t)s * L) + 2 * align_up(2 * (size_t)w * s) + 3 * align_up(2 * (size_t)w * L);
   b += align_up(4 * s * w) * 2;            // Z, Z2
   b += align_up(4 * L * w) * 2;            // Y, Y2
   b += align_up(8 * (size_t)w * w) * 2;    // C, X
@@ -633,8 +633,10 @@ int run_zero_grad(moara_state* st, const std::vector<int>& zidx, hipStream_t str
 // ------------------------------------------------------------------ refresh driver
 struct RefMat {
   int idx;
-  bool bf;               // early iterations on the bf16 V (large-tile GEMMs)
+  bool bf;               // iterations on the bf16 V (large-tile GEMMs; the last ones split)
   void *XL, *Zt, *Yt;    // bf16: V as s x L; iterates Z^T (w x s) and Y^T (w x L)
+  void *VKm, *VKl, *XLm, *XLl;   // split products: V's further bf16 parts (as L x s and s x L) ...
+  void *Ztlo, *Ytlo, *Ytl2;      // ... and the iterates' bf16 parts (Y^T in three for the last product)
   float *Pw, *Bt;        // Ritz vectors before signs (s x r), (R J)_top^T (r x w)
   int64_t s, L;
   int32_t w, wpad;
@@ -676,7 +678,14 @@ constexpr int MAX_SWEEPS = 14;
 //   last  : Y <- X Z ; Y2 <- orth(Y) ; Z2 <- X^T Y2 ; Jacobi on Z2 ; P <- top r
 // usev (indexed by matrix, may be null): the bf16 V of that matrix was written by this
 // step's decomposition, so its early subspace iterations can run on bf16 MFMA.
-constexpr int REFRESH_F32_ITERS = 3;   // the last iterations always run in fp32 on G and inv
+// The last iterations run at fp32 accuracy: fp32 products on G and inv, or, for matrices
+// with a bf16 V, split bf16 products (operand + residual, three MFMA products per GEMM).
+constexpr int REFRESH_F32_ITERS = 3;
+// of which the last ones use the five-product split (the others three products)
+#ifndef MOARA_SPLIT5_ITERS
+#define MOARA_SPLIT5_ITERS 2
+#endif
+constexpr int REFRESH_SPLIT5_ITERS = MOARA_SPLIT5_ITERS;
 
 int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream,
                   const std::vector<char>* usev) {
@@ -691,7 +700,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.wpad = (x.w + 63) / 64 * 64;
     x.bf = usev && (*usev)[i] && c.refresh_iters > REFRESH_F32_ITERS && x.w % 8 == 0 &&
            gemm_nt_eligible(EP_STORE_BF16, x.w, h.L, h.s, h.s, h.s, h.L, h.V, h.V, h.V, 0) &&
-           gemm_nt_eligible(EP_STORE, h.s, x.w, h.L, h.L, h.L, x.w, h.V, h.V, h.V, 0);
+           gemm_nt_eligible(EP_STORE, h.s, x.w, h.L, h.L, h.L, x.w, h.V, h.V, h.V, 0) &&
+           gemm_nt_eligible(EP_STORE, h.L, x.w, h.s, h.s, h.s, x.w, h.V, h.V, h.V, 0);
     need += mat_refresh_bytes(h.s, h.L, x.w, h.r, x.bf);
     rm.push_back(x);
   }
@@ -705,6 +715,13 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       x.XL = take(2 * (size_t)x.s * x.L);
       x.Zt = take(2 * (size_t)x.w * x.s);
       x.Yt = take(2 * (size_t)x.w * x.L);
+      x.VKm = take(2 * (size_t)x.s * x.L);
+      x.VKl = take(2 * (size_t)x.s * x.L);
+      x.XLm = take(2 * (size_t)x.s * x.L);
+      x.XLl = take(2 * (size_t)x.s * x.L);
+      x.Ztlo = take(2 * (size_t)x.w * x.s);
+      x.Ytlo = take(2 * (size_t)x.w * x.L);
+      x.Ytl2 = take(2 * (size_t)x.w * x.L);
     }
     x.Z = (float*)take(4 * x.s * x.w);
     x.Z2 = (float*)take(4 * x.s * x.w);
@@ -846,14 +863,13 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   }
   auto gZ2 = gram_list(false), gY = gram_list(true);
   auto aZ = apply_list(false), aY = apply_list(true);
-  auto xzR = big_list(MOARA_SIDE_RIGHT, false, false), xzL = big_list(MOARA_SIDE_LEFT, false, false);
-  auto xtR = big_list(MOARA_SIDE_RIGHT, true, false), xtL = big_list(MOARA_SIDE_LEFT, true, false);
-  auto xt2R = big_list(MOARA_SIDE_RIGHT, true, true), xt2L = big_list(MOARA_SIDE_LEFT, true, true);
-  // early (bf16) iterations: the fp32 products of the matrices without a bf16 V ...
-  auto fxzR = big_list(MOARA_SIDE_RIGHT, false, false, true), fxzL = big_list(MOARA_SIDE_LEFT, false, false, true);
-  auto fxtR = big_list(MOARA_SIDE_RIGHT, true, false, true), fxtL = big_list(MOARA_SIDE_LEFT, true, false, true);
+  // fp32 products on G and inv: the matrices without a bf16 V (every iteration) ...
+  auto xzR = big_list(MOARA_SIDE_RIGHT, false, false, true), xzL = big_list(MOARA_SIDE_LEFT, false, false, true);
+  auto xtR = big_list(MOARA_SIDE_RIGHT, true, false, true), xtL = big_list(MOARA_SIDE_LEFT, true, false, true);
+  auto xt2R = big_list(MOARA_SIDE_RIGHT, true, true, true), xt2L = big_list(MOARA_SIDE_LEFT, true, true, true);
   // ... and, for the others, Z^T (bf16) = transpose(Z), Y^T = Z^T X_K^T, Z2 = X_L Y  (X_K: L x s = the
-  // step's V workspace, X_L: s x L = its transpose)
+  // step's V workspace, X_L: s x L = its transpose); in the last REFRESH_F32_ITERS iterations
+  // every operand is split into bf16 + bf16 residual (three products per GEMM, near fp32)
   // Ritz vectors: Pw = Q Bt^T (M = s, N = r, K = w)
   std::vector<GemmProb> pwl;
   uint32_t tpw = 0;
@@ -870,9 +886,10 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     tpw += gemm_tiles_m(kind, gp.M) * gp.tiles_n;
     pwl.push_back(gp);
   }
-  std::vector<TransProb> tZ, tX;
-  std::vector<GemmProb> nY, nZ;
-  uint32_t ttz = 0, ttx = 0, tny = 0, tnz = 0;
+  std::vector<TransProb> tZ, tX, tZs, tY2;
+  std::vector<GemmProb> nY, nZ, nYs, nZs, nYf, nYs3, nZs3, nZf;
+  std::vector<SplitProb> vlo;
+  uint32_t ttz = 0, ttx = 0, tny = 0, tnz = 0, tvlo = 0, tnyf = 0, tty2 = 0;
   for (int q = 0; q < nm; ++q) {
     const RefMat& x = rm[q];
     if (!x.bf) continue;
@@ -900,6 +917,71 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     z.a_bytes = (uint32_t)(2 * (size_t)x.s * x.L); z.b_bytes = (uint32_t)(2 * (size_t)x.w * x.L);
     z.tiles_n = gemm_nt_tiles_n(z.N); z.tile_start = tnz; tnz += gemm_nt_tiles_m(z.M) * z.tiles_n;
     nZ.push_back(z);
+    // split iterations: V's bf16 parts v_m, v_l (both orientations), the iterates' residuals.
+    // The operator V is kept to about 2^-24 (v_h + v_m + v_l), the iterates Z^T and Y^T to
+    // 2^-17 (a perturbation of the iterate, which later iterations damp, not of the
+    // operator): five products, h.h + l.h + h.m + l.m + h.l (iterate.operator); the
+    // three-product form drops the last two (operator kept to 2^-17 only).
+    SplitProb sp{};
+    sp.g = (const float*)grads[x.idx]; sp.inv = c.decompose ? h.inv : nullptr; sp.inv_ld = h.k;
+    sp.B = c.block_size; sp.m = h.m; sp.n = h.n;
+    const bool rgt = h.side == MOARA_SIDE_RIGHT;   // m x n is X_K (RIGHT) or X_L (LEFT)
+    sp.out_n[0] = rgt ? x.VKm : x.XLm; sp.out_n[1] = rgt ? x.VKl : x.XLl;
+    sp.out_t[0] = rgt ? x.XLm : x.VKm; sp.out_t[1] = rgt ? x.XLl : x.VKl;
+    sp.tiles_c = (int32_t)((h.n + 63) / 64); sp.tile_start = tvlo; tvlo += split_lo_tiles(h.m, h.n);
+    vlo.push_back(sp);
+    a.out_lo = x.Ztlo;   // same tiles as tZ
+    tZs.push_back(a);
+    auto segs = [](GemmProb& g, int terms, const void* it_h, const void* it_l, const void* op_h, const void* op_m,
+                   const void* op_l, bool it_is_a) {
+      const void* it[5] = {it_h, it_l, it_h, it_l, it_h};
+      const void* op[5] = {op_h, op_h, op_m, op_m, op_l};
+      g.nseg = terms;
+      for (int j = 0; j < 5; ++j) {
+        const void* pa = it_is_a ? it[j] : op[j];
+        const void* pb = it_is_a ? op[j] : it[j];
+        if (j == 0) { g.a = pa; g.b = pb; } else if (j < terms) { g.seg_a[j - 1] = pa; g.seg_b[j - 1] = pb; }
+      }
+    };
+    GemmProb y3 = y;   // Y^T = Z^T X_K^T: iterate Zt (A), operator X_K (B); Yt split on output
+    segs(y, 5, x.Zt, x.Ztlo, h.V, x.VKm, x.VKl, true);
+    segs(y3, 3, x.Zt, x.Ztlo, h.V, x.VKm, x.VKl, true);
+    y.c_lo = y3.c_lo = x.Ytlo;
+    nYs.push_back(y);
+    nYs3.push_back(y3);
+    GemmProb z3 = z;   // Z2 = X_L Y: operator X_L (A), iterate Yt (B)
+    segs(z, 5, x.Yt, x.Ytlo, x.XL, x.XLm, x.XLl, false);
+    segs(z3, 3, x.Yt, x.Ytlo, x.XL, x.XLm, x.XLl, false);
+    nZs.push_back(z);
+    nZs3.push_back(z3);
+    // last iteration: Y (L x w, fp32 for its CholeskyQR) = X_K Z, split
+    GemmProb f{};
+    f.M = x.L; f.N = x.w; f.K = x.s;
+    f.lda = x.s; f.ldb = x.s;
+    segs(f, 5, x.Zt, x.Ztlo, h.V, x.VKm, x.VKl, false);
+    f.c = x.Y; f.ldc = x.w;
+    f.kp = 1 | 2;
+    f.a_bytes = (uint32_t)(2 * (size_t)x.L * x.s); f.b_bytes = (uint32_t)(2 * (size_t)x.w * x.s);
+    f.tiles_n = gemm_nt_tiles_n(f.N); f.tile_start = tnyf; tnyf += gemm_nt_tiles_m(f.M) * f.tiles_n;
+    nYf.push_back(f);
+    // ... and its orthonormalised Y2 split into three bf16 parts of Y^T (w x L, blocked, K = L)
+    // for the last product Z2 = X_L Y2, where a perturbation of the iterate is no longer
+    // damped (it moves span(Z2) by about its size times sigma_1 / sigma_r): six products,
+    // operator . iterate h.h + h.m + m.h + h.l + m.m + l.h (both kept to about 2^-24)
+    GemmProb zf = z;
+    {
+      const void* op[6] = {x.XL, x.XL, x.XLm, x.XL, x.XLm, x.XLl};
+      const void* it[6] = {x.Yt, x.Ytlo, x.Yt, x.Ytl2, x.Ytlo, x.Yt};
+      zf.a = op[0]; zf.b = it[0]; zf.nseg = 6;
+      for (int j = 1; j < 6; ++j) { zf.seg_a[j - 1] = op[j]; zf.seg_b[j - 1] = it[j]; }
+    }
+    nZf.push_back(zf);
+    TransProb q2{};
+    q2.in = x.Y2; q2.out = x.Yt; q2.out_lo = x.Ytlo; q2.out_lo2 = x.Ytl2;
+    q2.rows = x.L; q2.cols = x.w; q2.ldi = x.w; q2.ldo = x.L;
+    q2.in_f32 = 1; q2.out_kp = 1;
+    q2.tiles_c = (int32_t)((x.w + 63) / 64); q2.tile_start = tty2; tty2 += transpose_tiles(x.L, x.w);
+    tY2.push_back(q2);
   }
 
   struct Part { const void* p; size_t b; };
@@ -918,15 +1000,20 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       {pan_pref.data(), sizeof(uint32_t) * pan_pref.size()},          // 11
       {upd_pref.data(), sizeof(uint32_t) * upd_pref.size()},          // 12
       {inv_pref.data(), sizeof(uint32_t) * inv_pref.size()},          // 13
-      {fxzR.first.data(), sizeof(GemmProb) * fxzR.first.size()},     // 14
-      {fxzL.first.data(), sizeof(GemmProb) * fxzL.first.size()},     // 15
-      {fxtR.first.data(), sizeof(GemmProb) * fxtR.first.size()},     // 16
-      {fxtL.first.data(), sizeof(GemmProb) * fxtL.first.size()},     // 17
+      {vlo.data(), sizeof(SplitProb) * vlo.size()},                   // 14
+      {tZs.data(), sizeof(TransProb) * tZs.size()},                   // 15
+      {nYs.data(), sizeof(GemmProb) * nYs.size()},                    // 16
+      {nZs.data(), sizeof(GemmProb) * nZs.size()},                    // 17
       {tZ.data(), sizeof(TransProb) * tZ.size()},                     // 18
       {tX.data(), sizeof(TransProb) * tX.size()},                     // 19
       {nY.data(), sizeof(GemmProb) * nY.size()},                      // 20
       {nZ.data(), sizeof(GemmProb) * nZ.size()},                      // 21
       {pwl.data(), sizeof(GemmProb) * pwl.size()},                    // 22
+      {nYf.data(), sizeof(GemmProb) * nYf.size()},                    // 23
+      {tY2.data(), sizeof(TransProb) * tY2.size()},                   // 24
+      {nYs3.data(), sizeof(GemmProb) * nYs3.size()},                  // 25
+      {nZs3.data(), sizeof(GemmProb) * nZs3.size()},                  // 26
+      {nZf.data(), sizeof(GemmProb) * nZf.size()},                    // 27
   };
   size_t total = 0;
   std::vector<size_t> offs;
@@ -992,33 +1079,50 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   if (orth0) HIP_TRY(orth_Z());
   const int q_iters = c.refresh_iters;
   const int q_bf = q_iters > REFRESH_F32_ITERS ? q_iters - REFRESH_F32_ITERS : 0;
-  if (!nY.empty() && q_bf > 0) HIP_TRY(launch_transpose((const TransProb*)D(19), (int)tX.size(), ttx, stream));
+  if (!nY.empty()) {
+    HIP_TRY(launch_transpose((const TransProb*)D(19), (int)tX.size(), ttx, stream));
+    HIP_TRY(launch_split_lo((const SplitProb*)D(14), (int)vlo.size(), tvlo, stream));
+  }
   for (int it = 0; it < q_iters; ++it) {
-    if (it < q_bf && !nY.empty()) {
-      // early iteration: bf16 MFMA products for the matrices with a bf16 V, fp32 for the rest
-      HIP_TRY(gemm(A_G_ROW, 14, fxzR));
-      HIP_TRY(gemm(A_G_TRANS, 15, fxzL));
-      HIP_TRY(gemm(A_G_TRANS, 16, fxtR));
-      HIP_TRY(gemm(A_G_ROW, 17, fxtL));
-      HIP_TRY(launch_transpose((const TransProb*)D(18), (int)tZ.size(), ttz, stream));
-      HIP_TRY(launch_gemm_nt(EP_STORE_BF16, (const GemmProb*)D(20), (int)nY.size(), tny, u, stream));
-      HIP_TRY(launch_gemm_nt(EP_STORE, (const GemmProb*)D(21), (int)nZ.size(), tnz, u, stream));
-      HIP_TRY(orth_Z());
-      continue;
-    }
-    // Y = X Z : RIGHT X = V -> rows of G ; LEFT X = V^T -> columns of G
+    const bool last = it + 1 == q_iters;
+    // fp32 products for the matrices without a bf16 V. Y = X Z : RIGHT X = V -> rows of G ;
+    // LEFT X = V^T -> columns of G
     HIP_TRY(gemm(A_G_ROW, 5, xzR));
     HIP_TRY(gemm(A_G_TRANS, 6, xzL));
-    if (it + 1 < q_iters) {
+    if (!last) {
       HIP_TRY(gemm(A_G_TRANS, 7, xtR));
       HIP_TRY(gemm(A_G_ROW, 8, xtL));
+    }
+    // bf16 MFMA products for the others: plain in the early iterations, split (operands
+    // and their residuals) in the last ones
+    if (!nY.empty()) {
+      if (it < q_bf) {
+        HIP_TRY(launch_transpose((const TransProb*)D(18), (int)tZ.size(), ttz, stream));
+        HIP_TRY(launch_gemm_nt(EP_STORE_BF16, (const GemmProb*)D(20), (int)nY.size(), tny, u, stream));
+        HIP_TRY(launch_gemm_nt(EP_STORE, (const GemmProb*)D(21), (int)nZ.size(), tnz, u, stream));
+      } else {
+        HIP_TRY(launch_transpose((const TransProb*)D(15), (int)tZs.size(), ttz, stream));
+        if (!last) {
+          const bool five = it + REFRESH_SPLIT5_ITERS >= q_iters;
+          HIP_TRY(launch_gemm_nt(EP_STORE_BF16, (const GemmProb*)D(five ? 16 : 25), (int)nYs.size(), tny, u, stream));
+          HIP_TRY(launch_gemm_nt(EP_STORE, (const GemmProb*)D(five ? 17 : 26), (int)nZs.size(), tnz, u, stream));
+        } else {
+          HIP_TRY(launch_gemm_nt(EP_STORE, (const GemmProb*)D(23), (int)nYf.size(), tnyf, u, stream));
+        }
+      }
+    }
+    if (!last) {
       HIP_TRY(orth_Z());
-    } else {
+    } else {   // Y2 = orth(Y) ; Z2 = X^T Y2
       HIP_TRY(launch_gram((const GramProb*)D(2), nm, gY.second, stream));
       HIP_TRY(chol_inv());
       HIP_TRY(gemm(A_KC, 4, aY));
       HIP_TRY(gemm(A_G_TRANS, 9, xt2R));
       HIP_TRY(gemm(A_G_ROW, 10, xt2L));
+      if (!nY.empty()) {
+        HIP_TRY(launch_transpose((const TransProb*)D(24), (int)tY2.size(), tty2, stream));
+        HIP_TRY(launch_gemm_nt(EP_STORE, (const GemmProb*)D(27), (int)nZf.size(), tnz, u, stream));
+      }
     }
   }
   // Rayleigh-Ritz: Z2 = Q R (CholeskyQR), SVD of the w x w factor R by one-sided Jacobi
@@ -1040,9 +1144,11 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
 
 // Device bytes per refresh chunk. One chunk per refresh is fastest (the latency-bound
 // Cholesky chains and Jacobi rounds then cover every matrix in one launch sequence):
-// a Llama-2-7B-shaped stack needs about 70 GB, a third of one MI355X's 288 GB.
+// a Llama-2-7B-shaped stack needs about 131 GB (the split operands of the last
+// iterations are 52 GB of it), under half of one MI355X's 288 GB. Callers short of
+// memory cap it with MOARA_REFRESH_CHUNK_MIB (the projectors do not depend on the chunks).
 #ifndef MOARA_REFRESH_BUDGET_GIB
-#define MOARA_REFRESH_BUDGET_GIB 96
+#define MOARA_REFRESH_BUDGET_GIB 128
 #endif
 constexpr size_t REFRESH_BUDGET = (size_t)MOARA_REFRESH_BUDGET_GIB << 30;
 
@@ -1064,8 +1170,8 @@ size_t refresh_budget() {
 // inverse prefix arrays, each part aligned).
 size_t ref_desc_bound(size_t nm, int nbmax) {
   const int nlev = std::max(1, trtri_levels(nbmax));
-  return 24 * ALIGN + nm * (sizeof(RefDev) + 2 * sizeof(GramProb) + 10 * sizeof(GemmProb) + 2 * sizeof(TransProb) +
-                            4 * (2 * (size_t)nbmax + (size_t)nlev));
+  return 29 * ALIGN + nm * (sizeof(RefDev) + 2 * sizeof(GramProb) + 14 * sizeof(GemmProb) + 4 * sizeof(TransProb) +
+                            sizeof(SplitProb) + 4 * (2 * (size_t)nbmax + (size_t)nlev));
 }
 
 // Refresh the matrices idx in order, in chunks whose workspace stays within the budget

@@ -67,9 +67,29 @@ struct TransProb {
   int32_t in_kp;             // 1: bf16 input in the blocked layout (kp_index(r, c, rows))
   int32_t out_kp;            // 1: output in the blocked layout (kp_index(c, r, cols))
   int32_t pad_;
+  void* out_lo;              // fp32 input: also x_m = bf16(x - x_h), x_h = bf16(x), same layout (nullable)
+  void* out_lo2;             // ... and x_l = bf16(x - x_h - x_m) (nullable; needs out_lo)
 };
 uint32_t transpose_tiles(int64_t rows, int64_t cols);
 hipError_t launch_transpose(const TransProb* t, int n, uint32_t total, hipStream_t st);
+
+// The bf16 parts of the direction tensor beyond its bf16 value v_h = bf16(v), for the split
+// products of the last subspace iterations: v_m = bf16(v - v_h) and v_l = bf16(v - v_h - v_m)
+// (v = v_h + v_m + v_l to about 2^-24 relative), with v = G * inv in fp32 as the
+// decomposition and the fp32 products form V (inv = nullptr: v = G); each stored in the
+// blocked layout both as the m x n operand (K = n) and as the n x m one (K = m).
+struct SplitProb {
+  const float* g;       // m x n, row stride n
+  const float* inv;     // m x k, row stride inv_ld (nullable)
+  void* out_n[2];       // v_m, v_l as m x n
+  void* out_t[2];       // v_m, v_l as n x m
+  int64_t m, n;
+  int32_t inv_ld, B;
+  int32_t tiles_c;      // 64-wide tiles along n
+  uint32_t tile_start;
+};
+uint32_t split_lo_tiles(int64_t m, int64_t n);
+hipError_t launch_split_lo(const SplitProb* p, int n, uint32_t total, hipStream_t st);
 
 hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st);
 hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st);

@@ -460,8 +460,58 @@ __global__ __launch_bounds__(256) void k_transpose(const TransProb* __restrict__
   __syncthreads();
   for (int e = threadIdx.x; e < 64 * 64; e += 256) {
     const int c = e >> 6, r = e & 63;
-    if (r0 + r < P.rows && c0 + c < P.cols)
-      ((bf16*)P.out)[P.out_kp ? kp_index(c0 + c, r0 + r, P.cols) : (c0 + c) * P.ldo + r0 + r] = (bf16)T[r][c];
+    if (r0 + r < P.rows && c0 + c < P.cols) {
+      const int64_t o = P.out_kp ? kp_index(c0 + c, r0 + r, P.cols) : (c0 + c) * P.ldo + r0 + r;
+      const bf16 h = f2bf(T[r][c]);
+      ((bf16*)P.out)[o] = h;
+      if (P.out_lo) {
+        const float d = T[r][c] - bf2f(h);   // exact
+        const bf16 m = f2bf(d);
+        ((bf16*)P.out_lo)[o] = m;
+        if (P.out_lo2) ((bf16*)P.out_lo2)[o] = f2bf(d - bf2f(m));
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------------ bf16 parts of V
+// One workgroup per 64 x 64 tile of G: read along rows (coalesced), form v and its parts
+// v_m, v_l (each difference is exact in fp32), store them straight (blocked, rows m) and,
+// through LDS, transposed (blocked, rows n); both stores run along the K index of their
+// layout.
+__global__ __launch_bounds__(256) void k_split_lo(const SplitProb* __restrict__ ps, int np) {
+  __shared__ float T[2][64][65];
+  const uint32_t t = blockIdx.x;
+  int lo = 0, hi = np - 1;
+  while (lo < hi) { int mid = (lo + hi + 1) >> 1; if (ps[mid].tile_start <= t) lo = mid; else hi = mid - 1; }
+  const SplitProb& P = ps[lo];
+  const int rel = (int)(t - P.tile_start);
+  const int64_t r0 = (int64_t)(rel / P.tiles_c) * 64, c0 = (int64_t)(rel % P.tiles_c) * 64;
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int r = e >> 6, c = e & 63;
+    float xm = 0.f, xl = 0.f;
+    if (r0 + r < P.m && c0 + c < P.n) {
+      const float g = P.g[(r0 + r) * P.n + c0 + c];
+      const float v = P.inv ? g * P.inv[(r0 + r) * P.inv_ld + (c0 + c) / P.B] : g;
+      const float d = v - bf2f(f2bf(v));
+      const bf16 m = f2bf(d);
+      xm = bf2f(m);
+      xl = d - xm;
+      const int64_t o = kp_index(r0 + r, c0 + c, P.m);
+      ((bf16*)P.out_n[0])[o] = m;
+      ((bf16*)P.out_n[1])[o] = f2bf(xl);
+    }
+    T[0][r][c] = xm;
+    T[1][r][c] = xl;
+  }
+  __syncthreads();
+  for (int e = threadIdx.x; e < 64 * 64; e += 256) {
+    const int c = e >> 6, r = e & 63;
+    if (r0 + r < P.m && c0 + c < P.n) {
+      const int64_t o = kp_index(c0 + c, r0 + r, P.n);
+      ((bf16*)P.out_t[0])[o] = f2bf(T[0][r][c]);
+      ((bf16*)P.out_t[1])[o] = f2bf(T[1][r][c]);
+    }
   }
 }
 
@@ -900,6 +950,12 @@ uint32_t transpose_tiles(int64_t rows, int64_t cols) { return (uint32_t)(((rows 
 hipError_t launch_transpose(const TransProb* t, int n, uint32_t total, hipStream_t st) {
   if (!n || !total) return hipSuccess;
   hipLaunchKernelGGL(k_transpose, dim3(total), dim3(256), 0, st, t, n);
+  return hipGetLastError();
+}
+uint32_t split_lo_tiles(int64_t m, int64_t n) { return (uint32_t)(((m + 63) / 64) * ((n + 63) / 64)); }
+hipError_t launch_split_lo(const SplitProb* p, int n, uint32_t total, hipStream_t st) {
+  if (!total) return hipSuccess;
+  hipLaunchKernelGGL(k_split_lo, dim3(total), dim3(256), 0, st, p, n);
   return hipGetLastError();
 }
 uint32_t r_colmajor_tiles(int32_t w, int32_t wpad) { return (uint32_t)(((w + 31) / 32) * ((wpad + 31) / 32)); }

@@ -286,7 +286,7 @@ def moara_active_mask(st: State, active):
     return _active_array(st, active)
 
 
-MOARA_NOALLOC_SCRATCH_BYTES = 512 << 20
+MOARA_NOALLOC_SCRATCH_BYTES = 1024 << 20
 
 
 def moara_step(st: State, weights, grads, lr: float, active=None, stream=None, args: StepArgs = None,
