@@ -114,7 +114,6 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)P.b, (short)0, (int)P.b_bytes, 0x00020000);
   // K segments (split operands): the refresh's plain-store products only
   constexpr bool SEGS = EP == EP_STORE || EP == EP_STORE_BF16;
-  const int nseg = SEGS && P.nseg > 1 ? P.nseg : 1;
   const int nk1 = (int)(P.K / TBK);          // K steps of one segment
   static_assert(SA <= 4 && SB <= 4, "DMA slot arrays");
   // blocked operands: one K step of the tile's rows is a contiguous 64-byte-per-row run,
@@ -139,23 +138,30 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
   }
   auto issue = [&](int kt, int slot) {
     char* base = smem + slot * STAGEB;
-    int seg = 0, kk = kt;   // uniform
-    if constexpr (SEGS)
+    if constexpr (!SEGS) {
+      const int soa = (int)(kt * sta), sob = (int)(kt * stb);
+#pragma unroll
+      for (int j = 0; j < SA; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(ra, (lds_void*)(base + (SA * wave + j) * 1024), 16, va[j], soa, 0, 0);
+#pragma unroll
+      for (int j = 0; j < SB; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rb, (lds_void*)(base + TILEA + (SB * wave + j) * 1024), 16, vb[j], sob, 0, 0);
+    } else {
+      int seg = 0, kk = kt;   // uniform
       while (kk >= nk1) { kk -= nk1; ++seg; }
-    const int soa = (int)(kk * sta), sob = (int)(kk * stb);
-    __amdgpu_buffer_rsrc_t rsa = ra, rsb = rb;
-    if constexpr (SEGS) {
+      const int soa = (int)(kk * sta), sob = (int)(kk * stb);
+      __amdgpu_buffer_rsrc_t rsa = ra, rsb = rb;
       if (seg > 0) {
         rsa = __builtin_amdgcn_make_buffer_rsrc((void*)P.seg_a[seg - 1], (short)0, (int)P.a_bytes, 0x00020000);
         rsb = __builtin_amdgcn_make_buffer_rsrc((void*)P.seg_b[seg - 1], (short)0, (int)P.b_bytes, 0x00020000);
       }
+#pragma unroll
+      for (int j = 0; j < SA; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_void*)(base + (SA * wave + j) * 1024), 16, va[j], soa, 0, 0);
+#pragma unroll
+      for (int j = 0; j < SB; ++j)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_void*)(base + TILEA + (SB * wave + j) * 1024), 16, vb[j], sob, 0, 0);
     }
-#pragma unroll
-    for (int j = 0; j < SA; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsa, (lds_void*)(base + (SA * wave + j) * 1024), 16, va[j], soa, 0, 0);
-#pragma unroll
-    for (int j = 0; j < SB; ++j)
-      __builtin_amdgcn_raw_ptr_buffer_load_lds(rsb, (lds_void*)(base + TILEA + (SB * wave + j) * 1024), 16, vb[j], sob, 0, 0);
   };
 
   f32x16 acc[MB][NB];
@@ -193,7 +199,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
   // A slot is refilled only after every wave has passed the barrier that follows
   // its last MFMA on that slot's data, and each wave waits (vmcnt) for its own DMA
   // loads of a stage before the barrier that publishes it.
-  const int nk = nseg * nk1;
+  const int nk = SEGS && P.nseg > 1 ? P.nseg * nk1 : nk1;
   bf16x8 fa0[4], fb0[4], fa1[4], fb1[4];
   auto read_frags = [&](int stage, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
     const char* st = smem + stage * STAGEB;
