@@ -1145,8 +1145,10 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
 // Device bytes per refresh chunk. One chunk per refresh is fastest (the latency-bound
 // Cholesky chains and Jacobi rounds then cover every matrix in one launch sequence):
 // a Llama-2-7B-shaped stack needs about 131 GB (the split operands of the last
-// iterations are 52 GB of it), under half of one MI355X's 288 GB. Callers short of
-// memory cap it with MOARA_REFRESH_CHUNK_MIB (the projectors do not depend on the chunks).
+// iterations are 52 GB of it), under half of one MI355X's 288 GB. A refresh never plans
+// a chunk larger than the device's free memory (plus the workspace it already holds),
+// and callers cap it with MOARA_REFRESH_CHUNK_MIB (the projectors do not depend on the
+// chunks).
 #ifndef MOARA_REFRESH_BUDGET_GIB
 #define MOARA_REFRESH_BUDGET_GIB 128
 #endif
@@ -1181,7 +1183,18 @@ size_t ref_desc_bound(size_t nm, int nbmax) {
 int refresh_in_chunks(moara_state* st, const std::vector<int>& idx, const void* const* grads, hipStream_t stream,
                       const std::vector<char>& usev) {
   const bool na = st->noalloc;
-  const size_t budget = na ? st->ref_ws_bytes : refresh_budget();
+  size_t budget = na ? st->ref_ws_bytes : refresh_budget();
+  if (!na) {
+    // never plan chunks larger than the device can hold now: the free memory plus the
+    // workspace this state already owns (which a larger chunk would replace), less 1 GiB
+    // for the caller (the projectors do not depend on how the matrices are chunked)
+    size_t free_b = 0, total_b = 0;
+    if (hipMemGetInfo(&free_b, &total_b) == hipSuccess) {
+      const size_t usable = free_b + st->ref_ws_bytes;
+      const size_t margin = (size_t)1 << 30;
+      budget = std::min(budget, usable > margin ? usable - margin : (size_t)0);
+    }
+  }
   std::vector<int> chunk;
   size_t bytes = 0;
   int nbm = 1;
