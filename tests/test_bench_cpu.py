@@ -49,3 +49,20 @@ def test_more_than_one_gpu_is_refused():
                        text=True, timeout=120)
     assert r.returncode == 2
     assert "exactly one GPU" in r.stdout
+
+
+@pytest.mark.parametrize("operand", ["bf16", "f32"])
+def test_step_accounting_prices_the_direction_moments_by_their_storage(operand):
+    # Optimizer_V reads and writes two L x r moments: 16 L r bytes in fp32, 8 L r in bf16;
+    # nothing else in the projection's or the method's bytes depends on the moment dtype
+    wl = _one_matrix(64, 160, 32)
+    L, r = 160, 32
+    c4 = bench.algorithmic_cost(wl, operand, 2, moment_bytes=4)
+    c2 = bench.algorithmic_cost(wl, operand, 2, moment_bytes=2)
+    assert c4["project"][0] - c2["project"][0] == 8 * L * r
+    assert c4["project"][1] == c2["project"][1]
+    assert c4["decompose"] == c2["decompose"] and c4["backproject"] == c2["backproject"]
+    ob = 2 if operand == "bf16" else 4
+    m4, f4 = bench.method_cost(wl, ob, 2, moment_bytes=4)
+    m2, f2 = bench.method_cost(wl, ob, 2, moment_bytes=2)
+    assert m4 - m2 == 8 * r * L and f4 == f2
