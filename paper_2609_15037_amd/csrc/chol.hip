@@ -1,9 +1,11 @@
 // Blocked Cholesky factorisation and triangular inverse of the fp64 Gram
 // matrices of a refresh batch (CholeskyQR: Z = Q R with R^T R = Z^T Z, then
 // Q = Z R^{-1}). 64 x 64 blocks; every launch covers all matrices of the batch:
-//   for each block row k:  row(k)    C_kc -= sum_{j<k} R_jk^T R_jc for c >= k  (one WG per block, k >= 1)
-//                          diag(k)   factor C_kk = R_kk^T R_kk and invert R_kk (one WG per matrix)
-//                          panel(k)  R_kc = R_kk^{-T} C_kc for c > k           (one WG per block)
+//   block row 0:   diag      factor C_00 = R_00^T R_00 and invert R_00 (one wave per matrix)
+//   block row k:   row(k)    C_kc -= sum_{j<k} R_jk^T R_jc for c >= k (one WG per block, k >= 1);
+//                            the WG of the diagonal block then factors C_kk and inverts
+//                            R_kk while the launch's other WGs still run
+//                  panel(k)  R_kc = R_kk^{-T} C_kc for c > k           (one WG per block)
 //   then X = R^{-1} by recursive doubling over the blocks (k_trtri).
 // A pivot not above 1e-13 * max(diag C) marks a numerically dependent column (a
 // rank-deficient iterate): its row of R and its row and column of X = R^{-1} are set to
@@ -63,72 +65,93 @@ __device__ __forceinline__ void mfma_blk(const double (*A)[LDB], const double (*
 __device__ __forceinline__ int mfma_row(int r) { return 16 * (threadIdx.x >> 6) + 4 * r + ((threadIdx.x & 63) >> 4); }
 __device__ __forceinline__ int mfma_col(int jt) { return 16 * jt + (threadIdx.x & 15); }
 
-__global__ __launch_bounds__(256) void k_chol_diag(const RefDev* __restrict__ ds, int k) {
+// One wave factors a 64 x 64 diagonal block held in LDS (D_ic at Dl[i * LD + c]) and
+// inverts its factor; it writes R_kk, X_kk = R_kk^{-1} and its fp32 copy. Lane c keeps
+// column c in registers (col[i] = D_ic); row j of R, which every column's update needs,
+// goes through LDS (over the block's own rows, which are in registers by then), where
+// all lanes read one address at a time (a broadcast). The LDS operations of one wave
+// take effect in program order, so no step needs a workgroup barrier. A ragged block is
+// padded with the identity, which factors and inverts to itself; take = 0 (an all-zero
+// Gram) gives R_kk = X_kk = I.
+//   factor, right-looking, column j = 0 .. kb-1:
+//     R_jj = sqrt(D_jj) (0 for a dependent column), R_jc = D_jc / R_jj (c > j),
+//     D_ac -= R_ja R_jc for a > j (lane c; for a > c this is the lower triangle,
+//     which follows the symmetric Schur complement and is not read);
+//   invert from the last row up, lane c: a_ic = sum_{t > i} R_it X_tc accumulated as
+//     the rows of X below i are finished (X_tc = 0 for t > c),
+//     X_cc = 1 / R_cc, X_ic = -a_ic / R_ii (i < c); a zero R_ii gives a zero row of X.
+// Each step's updates are kept inside the step (a wave-uniform branch per step ends its
+// basic block): left free, the compiler defers them into long chains that spill.
+template <int LD>
+__device__ __forceinline__ void diag_factor(double* Dl, int kb, bool take, double floor_piv, const RefDev& d,
+                                            int r0) {
+  const int w = d.w;
+  const int lane = threadIdx.x & 63;
+  const bool live = lane < kb;
+  double col[NB];
+#pragma unroll
+  for (int i = 0; i < NB; ++i) {
+    const double c = Dl[i * LD + lane];
+    col[i] = (take && live && i < kb) ? c : (i == lane ? 1.0 : 0.0);
+  }
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    if (j >= kb) continue;
+    const double v = __shfl(col[j], j, 64);
+    const double rjj = v > floor_piv ? sqrt(v) : 0.0;   // 0: dependent column
+    const double q = col[j] / (rjj > 0.0 ? rjj : 1.0);
+    const double rjc = lane == j ? rjj : (lane > j && rjj > 0.0 ? q : 0.0);
+    col[j] = rjc;
+    Dl[j * LD + lane] = rjc;
+#pragma unroll
+    for (int a = j + 1; a < NB; ++a) col[a] -= Dl[j * LD + a] * rjc;
+  }
+  if (live) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      if (i < kb) d.C[(int64_t)(r0 + i) * w + r0 + lane] = col[i];
+  }
+  double* acc = col;   // a_ic, accumulated from the bottom row up
+#pragma unroll
+  for (int i = 0; i < NB; ++i) acc[i] = 0.0;
+#pragma unroll
+  for (int t = NB - 1; t >= 0; --t) {
+    if (t >= kb) continue;
+    const double rtt = Dl[t * LD + t];
+    const double num = lane == t ? 1.0 : -acc[t];
+    const double q = num / (rtt > 0.0 ? rtt : 1.0);
+    const double x = (lane >= t && rtt > 0.0) ? q : 0.0;
+    acc[t] = x;
+#pragma unroll
+    for (int i = 0; i < t; ++i) acc[i] += Dl[i * LD + t] * x;
+  }
+  if (live) {
+#pragma unroll
+    for (int i = 0; i < NB; ++i)
+      if (i < kb) {
+        const int64_t g = (int64_t)(r0 + i) * w + r0 + lane;
+        d.X[g] = acc[i];
+        d.Rinv[g] = (float)acc[i];
+      }
+  }
+}
+
+// Block 0 (no update before it): one wave per matrix; also records the pivot floor's
+// reference, the largest diagonal entry of the untouched Gram.
+__global__ __launch_bounds__(64) void k_chol_diag(const RefDev* __restrict__ ds) {
+  __shared__ double Dl[NB][NB];
   const RefDev& d = ds[blockIdx.x];
   const int w = d.w;
-  if (k >= nblk(w)) return;
-  __shared__ double D[NB][LDB];
-  __shared__ double Xi[NB][LDB];
-  __shared__ double red[256];
-  const int tid = threadIdx.x;
-  if (k == 0) {   // pivot floor from the diagonal of the untouched Gram
-    double mx = 0.0;
-    for (int i = tid; i < w; i += 256) mx = fmax(mx, d.C[(int64_t)i * w + i]);
-    red[tid] = mx;
-    __syncthreads();
-    for (int o = 128; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
-    if (tid == 0) d.cmax[0] = red[0];
-    __syncthreads();
-  }
-  const double cmax = (k == 0) ? red[0] : d.cmax[0];
-  const bool zero = !(cmax > 0.0);
-  const double floor_piv = cmax * 1e-13;
-  const int kb = bsz(w, k);
-  load_blk(D, d.C, w, k, k);
-  __syncthreads();
-  if (zero) {
-    for (int e = tid; e < NB * NB; e += 256) { const int i = e >> 6, j = e & 63; D[i][j] = (i == j) ? 1.0 : 0.0; }
-    __syncthreads();
-  } else {
-    // right-looking, one column per step; the trailing update maps lane -> column and
-    // the four waves stride over the rows (no integer division in the inner loop)
-    const int cx = tid & 63, ry = tid >> 6;
-    for (int j = 0; j < kb; ++j) {
-      if (tid == 0) {
-        const double v = D[j][j];
-        D[j][j] = (v > floor_piv) ? sqrt(v) : 0.0;   // 0: dependent column
-      }
-      __syncthreads();
-      if (tid > j && tid < kb) D[j][tid] = D[j][j] > 0.0 ? D[j][tid] / D[j][j] : 0.0;
-      __syncthreads();
-      if (cx > j && cx < kb) {
-        const double djc = D[j][cx];
-        for (int a = j + 1 + ry; a <= cx; a += 4) D[a][cx] -= D[j][a] * djc;
-      }
-      __syncthreads();
-    }
-  }
-  // inverse of the upper triangular D (back substitution, one thread per column)
-  if (tid < kb) {
-    const int j = tid;
-    for (int i = NB - 1; i >= 0; --i) Xi[i][j] = 0.0;
-    Xi[j][j] = D[j][j] > 0.0 ? 1.0 / D[j][j] : 0.0;
-    for (int i = j - 1; i >= 0; --i) {
-      double v = 0.0;
-      for (int t = i + 1; t <= j; ++t) v += D[i][t] * Xi[t][j];
-      Xi[i][j] = D[i][i] > 0.0 ? -v / D[i][i] : 0.0;
-    }
-  }
-  __syncthreads();
-  const int r0 = k * NB;
-  for (int e = tid; e < kb * kb; e += 256) {
-    const int i = e / kb, j = e % kb;
-    const int64_t g = (int64_t)(r0 + i) * w + r0 + j;
-    const bool up = j >= i;
-    d.C[g] = up ? D[i][j] : 0.0;
-    d.X[g] = up ? Xi[i][j] : 0.0;
-    d.Rinv[g] = up ? (float)Xi[i][j] : 0.f;
-  }
+  const int lane = threadIdx.x;
+  double mx = 0.0;
+  for (int i = lane; i < w; i += 64) mx = fmax(mx, d.C[(int64_t)i * w + i]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o, 64));
+  if (lane == 0) d.cmax[0] = mx;
+  const int kb = bsz(w, 0);
+  const int lc = min(lane, kb - 1);   // clamped: every lane loads in bounds
+  for (int i = 0; i < NB; ++i) Dl[i][lane] = d.C[(int64_t)min(i, kb - 1) * w + lc];
+  diag_factor<NB>(&Dl[0][0], kb, mx > 0.0, mx * 1e-13, d, 0);
 }
 
 __global__ __launch_bounds__(256, 4) void k_chol_panel(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
@@ -183,11 +206,15 @@ __global__ __launch_bounds__(256, 4) void k_chol_panel(const RefDev* __restrict_
 // panel; the factored rows R_j. are shared by all workgroups of a matrix (L2 hits).
 __global__ __launch_bounds__(256, 2) void k_chol_row(const RefDev* __restrict__ ds, const uint32_t* __restrict__ pref,
                                                      int n, int k) {
+  // workgroups 0 .. n-1: the diagonal block of matrix t (updated, then factored here);
+  // the rest: the blocks c > k, matrices by prefix
   const uint32_t t = blockIdx.x;
-  const int mi = find_pref(pref, n, t);
+  const bool diag = t < (uint32_t)n;
+  const int mi = diag ? (int)t : find_pref(pref, n, t - n);
   const RefDev& d = ds[mi];
   const int w = d.w;
-  const int c = k + (int)(t - pref[mi]);
+  if (diag && k >= nblk(w)) return;
+  const int c = diag ? k : k + 1 + (int)(t - n - pref[mi]);
   __shared__ double Rb[NB][LDB];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   double av[NB / 4], an[NB / 4], pb[16];
@@ -235,13 +262,28 @@ __global__ __launch_bounds__(256, 2) void k_chol_row(const RefDev* __restrict__ 
       __syncthreads();
     }
   }
+  if (!diag) {
+#pragma unroll
+    for (int jt = 0; jt < 4; ++jt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = k * NB + mfma_row(r), col = c * NB + mfma_col(jt);
+        if (row < w && col < w) d.C[(int64_t)row * w + col] -= acc[jt][r];
+      }
+    return;
+  }
+  // diagonal block: the updated C_kk goes to LDS (Rb is free: the K loop ended with a
+  // barrier) and wave 0 factors it while the other workgroups of the launch run on
+  const double cmax = d.cmax[0];
 #pragma unroll
   for (int jt = 0; jt < 4; ++jt)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int row = k * NB + mfma_row(r), col = c * NB + mfma_col(jt);
-      if (row < w && col < w) d.C[(int64_t)row * w + col] -= acc[jt][r];
+      const int i = mfma_row(r), j = mfma_col(jt), row = k * NB + i, col = k * NB + j;
+      Rb[i][j] = (row < w && col < w) ? d.C[(int64_t)row * w + col] - acc[jt][r] : 0.0;
     }
+  __syncthreads();
+  if (wave == 0) diag_factor<LDB>(&Rb[0][0], bsz(w, k), cmax > 0.0, cmax * 1e-13, d, k * NB);
 }
 
 // Triangular inverse X = R^{-1} by recursive doubling over the 64 x 64 blocks. Level l
@@ -341,9 +383,9 @@ __global__ __launch_bounds__(256, 2) void k_trtri(const RefDev* __restrict__ ds,
 
 int chol_blocks(int32_t w) { return (w + NB - 1) / NB; }
 
-hipError_t launch_chol_diag(const RefDev* d, int n, int k, hipStream_t st) {
+hipError_t launch_chol_diag(const RefDev* d, int n, hipStream_t st) {
   if (!n) return hipSuccess;
-  hipLaunchKernelGGL(k_chol_diag, dim3(n), dim3(256), 0, st, d, k);
+  hipLaunchKernelGGL(k_chol_diag, dim3(n), dim3(64), 0, st, d);
   return hipGetLastError();
 }
 hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st) {
@@ -352,7 +394,7 @@ hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint3
   return hipGetLastError();
 }
 hipError_t launch_chol_row(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st) {
-  if (!total || k < 1) return hipSuccess;
+  if (!n || k < 1 || total < (uint32_t)n) return hipSuccess;
   hipLaunchKernelGGL(k_chol_row, dim3(total), dim3(256), 0, st, d, pref, n, k);
   return hipGetLastError();
 }

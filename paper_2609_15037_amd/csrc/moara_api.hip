@@ -849,9 +849,11 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       const int nb = chol_blocks(rm[q].w);
       const int T = std::max(0, nb - k - 1);
       pan_pref[(size_t)k * nm + q] = tp; tp += (uint32_t)T;
-      upd_pref[(size_t)k * nm + q] = tu; tu += (uint32_t)(k >= 1 && k < nb ? nb - k : 0);   // row(k): c = k .. nb-1
+      // row(k), k >= 1: one workgroup per matrix for the diagonal block (numbered first),
+      // then the blocks c = k+1 .. nb-1 by prefix
+      upd_pref[(size_t)k * nm + q] = tu; tu += (uint32_t)(k >= 1 && k < nb ? nb - k - 1 : 0);
     }
-    pan_tot[k] = tp; upd_tot[k] = tu;
+    pan_tot[k] = tp; upd_tot[k] = k >= 1 ? (uint32_t)nm + tu : 0;
   }
   for (int l = 1; l <= nlev; ++l) {   // recursive-doubling levels of the triangular inverse
     uint32_t ti = 0;
@@ -1057,8 +1059,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   auto chol_inv = [&]() -> hipError_t {      // C -> R (in place), X = R^{-1}, Rinv = fp32(X)
     hipError_t e = hipSuccess;
     for (int k = 0; k < nbmax && e == hipSuccess; ++k) {
-      e = launch_chol_row(RD, UPD + (size_t)k * nm, nm, upd_tot[k], k, stream);
-      if (e == hipSuccess) e = launch_chol_diag(RD, nm, k, stream);
+      e = k == 0 ? launch_chol_diag(RD, nm, stream) : launch_chol_row(RD, UPD + (size_t)k * nm, nm, upd_tot[k], k, stream);
       if (e == hipSuccess) e = launch_chol_panel(RD, PAN + (size_t)k * nm, nm, pan_tot[k], k, stream);
     }
     for (int l = 1; l <= nlev && e == hipSuccess; ++l)

@@ -94,9 +94,10 @@ hipError_t launch_split_lo(const SplitProb* p, int n, uint32_t total, hipStream_
 hipError_t launch_gauss(const RefDev* d, int n, uint32_t total, hipStream_t st);
 hipError_t launch_gram(const GramProb* g, int n, uint32_t total, hipStream_t st);
 int chol_blocks(int32_t w);
-hipError_t launch_chol_diag(const RefDev* d, int n, int k, hipStream_t st);
+hipError_t launch_chol_diag(const RefDev* d, int n, hipStream_t st);   // block 0
 hipError_t launch_chol_panel(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
-hipError_t launch_chol_row(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k, hipStream_t st);
+hipError_t launch_chol_row(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int k,
+                           hipStream_t st);   // k >= 1, factors block k too
 int trtri_levels(int32_t nbmax);
 uint32_t trtri_tiles(int32_t w, int l);
 hipError_t launch_trtri(const RefDev* d, const uint32_t* pref, int n, uint32_t total, int l, int phase, hipStream_t st);
