@@ -285,7 +285,7 @@ int moara_set_tensor(moara_state* st, int32_t mat, int32_t which, const void* ho
 /* Record of the matrix's last refresh by the library (moara_refresh_projector or a
  * refresh inside moara_step), for callers that check how TruncatedSVD (Algorithm 1)
  * went. The refresh finishes with a Rayleigh-Ritz step whose w x w SVD is computed by
- * one-sided Jacobi sweeps; they stop when every column pair's cosine is below 1e-8 or
+ * one-sided Jacobi sweeps; they stop when every column pair's cosine is below 1e-7 or
  * after a fixed number of sweeps (14).
  *   out_sweeps:    Jacobi sweeps run;
  *   out_converged: 1 if the sweeps met the tolerance, 0 if they stopped at the limit

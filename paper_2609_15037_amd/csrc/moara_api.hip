@@ -249,6 +249,7 @@ size_t mat_refresh_bytes(int64_t s, int64_t L, int32_t w, int32_t r, bool bf) {
   b += align_up(4 * (size_t)w * w);        // Rinv
   b += align_up(8 * (size_t)wpad * w);     // Zc (R, column-major)
   b += align_up(4 * 64);                   // off
+  b += 2 * align_up(4 * (size_t)(wpad / 32 - 1) * (wpad / 64)) + align_up(4 * (size_t)(wpad / 32));   // Jacobi records
   b += align_up(4 * wpad) + align_up(8 * wpad);
   b += align_up(8 * 64 * (size_t)s) + align_up(8 * 64 * (size_t)r) + align_up(8 * (size_t)s) + align_up(4 * (size_t)r);  // completion
   return b;
@@ -644,6 +645,8 @@ struct RefMat {
   double *C, *X, *cmax, *Zc, *norms;
   uint32_t* off;
   int32_t* order;
+  uint32_t *jconv, *jmod;   // Jacobi pair and block records
+  float* jmx;
   double* cw;            // basis completion workspace (s x 64, r x 64, s)
   int32_t* sidx;         // basis completion indices (r)
 };
@@ -735,6 +738,12 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.Pw = (float*)take(4 * (size_t)x.s * h_r_of(x));
     x.Bt = (float*)take(4 * (size_t)h_r_of(x) * x.w);
     x.off = (uint32_t*)take(4 * 64);
+    {
+      const size_t nbj = (size_t)x.wpad / JB, npr = (nbj - 1) * (nbj / 2);
+      x.jconv = (uint32_t*)take(4 * npr);
+      x.jmx = (float*)take(4 * npr);
+      x.jmod = (uint32_t*)take(4 * nbj);
+    }
     x.order = (int32_t*)take(4 * x.wpad);
     x.norms = (double*)take(8 * x.wpad);
     x.cw = (double*)take(8 * 64 * (size_t)x.s + 8 * 64 * h_r_of(x) + 8 * (size_t)x.s);
@@ -766,6 +775,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     d.jl = x.w; d.Q = x.Z; d.Pw = x.Pw; d.Bt = x.Bt;
     d.P32 = h.P32; d.Pop = h.Pop; d.Ptop = h.Ptop; d.kp = h.kp ? 1 : 0;
     d.off = x.off; d.order = x.order; d.norms = x.norms;
+    d.jconv = x.jconv; d.jmx = x.jmx; d.jmod = x.jmod;
     d.tile_gauss = tg; tg += gauss_tiles(x.s, x.w);
     d.tile_jac = tj; tj += jacobi_tiles(x.wpad);
     d.tile_cm = tc; tc += r_colmajor_tiles(x.w, x.wpad);

@@ -39,6 +39,13 @@ struct RefDev {
                       // [3] largest pair cosine of the last sweep measured (float bits)
   double* cw;         // basis completion workspace: s x 64 block, r x 64 coefficients, s row norms
   int32_t* sidx;      // basis completion: the r canonical indices, by increasing row norm
+  // Jacobi pair records: for the pair visited in round rr at position p (index
+  // rr * nb / 2 + p, nb = wpad / JB blocks) the sweep + 1 of its last visit that measured
+  // it converged (0: rotated), and that measurement; per block, 1 + the global round
+  // index (sweep * (nb - 1) + round) of its last rotation (0: none yet)
+  uint32_t* jconv;
+  float* jmx;
+  uint32_t* jmod;
 };
 
 // Ritz directions whose value is not above this fraction of the largest one are

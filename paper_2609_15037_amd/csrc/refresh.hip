@@ -164,7 +164,7 @@ constexpr int PW = 2 * JB;   // 64 columns per pair
 // iteration itself resolves) and below fp32 rounding for gaps above 0.1. A tolerance
 // of 1e-10 cost about 5 % more sweep time for digits the fp32 projector does not keep.
 #ifndef MOARA_JAC_TOL
-#define MOARA_JAC_TOL 1e-8
+#define MOARA_JAC_TOL 1e-7
 #endif
 constexpr double JAC_TOL = MOARA_JAC_TOL;
 // Inner Jacobi sweeps per pair visit. The pair's Gram need not be diagonalised
@@ -217,6 +217,24 @@ __global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restric
   if (sweep > 0 && __uint_as_float(d.off[sweep - 1]) < (float)JAC_TOL) return;   // converged
   const int ba = circle(pair, round, nb), bb = circle(nb - 1 - pair, round, nb);
   const int tid = threadIdx.x;
+  // The circle schedule brings this pair back at the same round of every sweep. If its
+  // last visit measured it converged and neither block was rotated since, its columns,
+  // hence its Gram and measure, are what they were: record that measure again and skip
+  // the visit (the sweeps' results are exactly those of visiting it).
+  const uint32_t pidx = (uint32_t)round * (uint32_t)(nb / 2) + (uint32_t)pair;
+  const uint32_t gnow = (uint32_t)sweep * (uint32_t)(nb - 1) + (uint32_t)round;
+  if (sweep == 0) {
+    if (round == 0 && tid == 0) { d.jmod[ba] = 0; d.jmod[bb] = 0; }   // round 0 covers every block
+  } else {
+    const uint32_t gprev = gnow - (uint32_t)(nb - 1);
+    if (d.jconv[pidx] == (uint32_t)sweep && d.jmod[ba] <= gprev && d.jmod[bb] <= gprev) {
+      if (tid == 0) {
+        atomicMax(&d.off[sweep], __float_as_uint(d.jmx[pidx]));
+        d.jconv[pidx] = (uint32_t)sweep + 1;
+      }
+      return;
+    }
+  }
   const int64_t s = d.jl;   // column length
   auto colp = [&](int x) -> double* { return d.Zc + (int64_t)((x < JB) ? ba * JB + x : bb * JB + (x - JB)) * s; };
   const int lane = tid & 63, wave = tid >> 6;
@@ -322,8 +340,14 @@ __global__ __launch_bounds__(JNT, 2) void k_jacobi_round(const RefDev* __restric
     __syncthreads();
     for (int o = JNT / 2; o > 0; o >>= 1) { if (tid < o) red[tid] = fmax(red[tid], red[tid + o]); __syncthreads(); }
     const double mx = red[0];
-    if (tid == 0) atomicMax(&d.off[sweep], __float_as_uint((float)mx));
-    if (mx < JAC_TOL) return;   // already orthogonal: nothing to rotate (uniform branch)
+    const bool conv = mx < JAC_TOL;
+    if (tid == 0) {
+      atomicMax(&d.off[sweep], __float_as_uint((float)mx));
+      d.jconv[pidx] = conv ? (uint32_t)sweep + 1 : 0u;
+      d.jmx[pidx] = (float)mx;
+      if (!conv) { d.jmod[ba] = gnow + 1; d.jmod[bb] = gnow + 1; }
+    }
+    if (conv) return;   // already orthogonal: nothing to rotate (uniform branch)
     __syncthreads();            // red[0] is read by every thread before J overwrites it
   }
   for (int e = tid; e < PW * PW; e += JNT) Jm[e / PW][e % PW] = (e / PW == e % PW) ? 1.0 : 0.0;

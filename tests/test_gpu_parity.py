@@ -219,7 +219,7 @@ def test_refresh_layer_d256_principal_angles():
     print(f"[refresh] worst principal angle {worst:.2e}", flush=True)
     for i in range(len(Gs)):   # the Jacobi sweeps met their tolerance and kept all r directions
         info = M.moara_refresh_info(st, i)
-        assert info["converged"] and info["rank"] == c.ranks[i] and info["offdiag"] < 1e-8, (i, info)
+        assert info["converged"] and info["rank"] == c.ranks[i] and info["offdiag"] < 1e-7, (i, info)
 
 
 def test_refresh_lowrank_llama300m_layer():
