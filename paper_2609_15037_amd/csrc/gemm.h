@@ -54,7 +54,8 @@ struct GemmProb {
   uint32_t b_bytes;   // extent of the B array
   uint32_t inv_bytes; // extent of the inv array
   uint32_t tri_b;     // fp32 kind: 1 = B[j][k] is zero for k > j (upper triangular right factor),
-                      // so a tile's K loop stops after its last column
+                      // so a tile's K loop stops after its last column; large-tile plain-store
+                      // path: 2 = A[i][k] is zero for k > i, so it stops after the tile's last row
   double* red;        // EP_ALIGN accumulators (three per problem)
   // Large-tile path, split operands: the K loop runs nseg (1 .. 6) segments of K each,
   // segment 0 on (a, b), segment i > 0 on (seg_a[i-1], seg_b[i-1]), all with the layouts
@@ -65,6 +66,9 @@ struct GemmProb {
   int32_t nseg;
   int32_t pad2_;
   void* c_lo;         // EP_STORE_BF16: also store the residual bf16(C - bf16(C)) here (nullable)
+  void* c_parts;      // EP_STORE (large-tile path): also store C's three bf16 parts
+                      // c_h = bf16(C), c_m = bf16(C - c_h), c_l = bf16(C - c_h - c_m) as three
+                      // consecutive M x N arrays in the blocked layout (rows M, K = N) (nullable)
 };
 
 struct GemmUniform {

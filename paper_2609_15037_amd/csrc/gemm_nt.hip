@@ -114,7 +114,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
   const __amdgpu_buffer_rsrc_t rb = __builtin_amdgcn_make_buffer_rsrc((void*)P.b, (short)0, (int)P.b_bytes, 0x00020000);
   // K segments (split operands): the refresh's plain-store products only
   constexpr bool SEGS = EP == EP_STORE || EP == EP_STORE_BF16;
-  const int nk1 = (int)(P.K / TBK);          // K steps of one segment
+  // K steps of one segment; a left factor that is zero above its diagonal ends the K
+  // loop of a tile at the tile's last row
+  const int nk1 = (SEGS && P.tri_b == 2) ? min((int)(P.K / TBK), (int)((row0 + TBM) / TBK)) : (int)(P.K / TBK);
   static_assert(SA <= 4 && SB <= 4, "DMA slot arrays");
   // blocked operands: one K step of the tile's rows is a contiguous 64-byte-per-row run,
   // the next K step starts rows * 64 bytes further; row-major: the next 64 bytes of each row
@@ -290,6 +292,22 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
           const int64_t idx = row * P.ldc + col;
           if constexpr (EP == EP_STORE) {
             *reinterpret_cast<float4*>((float*)P.c + idx) = v;
+            if (P.c_parts) {   // v = h + m + l exactly (three 8-bit slices of the 24-bit significand)
+              const float x[4] = {v.x, v.y, v.z, v.w};
+              bf16x4 ph, pm, pl;
+#pragma unroll
+              for (int q = 0; q < 4; ++q) {
+                ph[q] = f2bf(x[q]);
+                const float d = x[q] - bf2f(ph[q]);
+                pm[q] = f2bf(d);
+                pl[q] = f2bf(d - bf2f(pm[q]));
+              }
+              bf16* pp = (bf16*)P.c_parts + kp_index(row, col, P.M);
+              const int64_t plane = P.M * P.N;
+              *reinterpret_cast<bf16x4*>(pp) = ph;
+              *reinterpret_cast<bf16x4*>(pp + plane) = pm;
+              *reinterpret_cast<bf16x4*>(pp + 2 * plane) = pl;
+            }
           } else {
             bf16x4 o;
             o[0] = f2bf(v.x); o[1] = f2bf(v.y); o[2] = f2bf(v.z); o[3] = f2bf(v.w);

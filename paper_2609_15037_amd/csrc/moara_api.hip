@@ -647,6 +647,11 @@ struct RefMat {
   int32_t* order;
   uint32_t *jconv, *jmod;   // Jacobi pair and block records
   float* jmx;
+  // bf16 path, early orthonormalisations: the parts of Z2 (three s x w bf16 arrays, blocked,
+  // K = w) and of R^{-1} transposed (three w x w, blocked): they live in Y..Y2 and in X,
+  // which hold nothing between the first and the last iteration (Y, Y2: last iteration
+  // only; X: read inside the factorisation only)
+  void *Z2p, *Rtp;
   double* cw;            // basis completion workspace (s x 64, r x 64, s)
   int32_t* sidx;         // basis completion indices (r)
 };
@@ -748,6 +753,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.norms = (double*)take(8 * x.wpad);
     x.cw = (double*)take(8 * 64 * (size_t)x.s + 8 * 64 * h_r_of(x) + 8 * (size_t)x.s);
     x.sidx = (int32_t*)take(4 * h_r_of(x));
+    x.Z2p = x.Y;    // 6 s w bytes <= the 8 L w of Y and Y2 (taken one after the other; L >= s)
+    x.Rtp = x.X;    // 6 w^2 bytes <= 8 w^2
   }
   const int nm = (int)rm.size();
   const int kind = KIND_F32;
@@ -802,12 +809,14 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     }
     return std::make_pair(g, t);
   };
-  auto apply_list = [&](bool onY) {   // Z = Z2 Rinv  or  Y2 = Y Rinv
-    std::vector<GemmProb> g(nm);
+  auto apply_list = [&](bool onY, bool only_f32 = false) {   // Z = Z2 Rinv  or  Y2 = Y Rinv
+    std::vector<GemmProb> g;
     uint32_t t = 0;
     for (int q = 0; q < nm; ++q) {
       const RefMat& x = rm[q];
-      GemmProb& gp = g[q];
+      if (only_f32 && x.bf) continue;
+      g.emplace_back();
+      GemmProb& gp = g.back();
       gp.M = onY ? x.L : x.s; gp.N = x.w; gp.K = x.w;
       gp.a = onY ? (const void*)x.Y : (const void*)x.Z2;
       gp.lda = x.w;
@@ -874,7 +883,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     inv_tot[l - 1] = ti;
   }
   auto gZ2 = gram_list(false), gY = gram_list(true);
-  auto aZ = apply_list(false), aY = apply_list(true);
+  auto aZ = apply_list(false), aY = apply_list(true), aZf = apply_list(false, true);
   // fp32 products on G and inv: the matrices without a bf16 V (every iteration) ...
   auto xzR = big_list(MOARA_SIDE_RIGHT, false, false, true), xzL = big_list(MOARA_SIDE_LEFT, false, false, true);
   auto xtR = big_list(MOARA_SIDE_RIGHT, true, false, true), xtL = big_list(MOARA_SIDE_LEFT, true, false, true);
@@ -898,10 +907,21 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     tpw += gemm_tiles_m(kind, gp.M) * gp.tiles_n;
     pwl.push_back(gp);
   }
-  std::vector<TransProb> tZ, tX, tZs, tY2;
-  std::vector<GemmProb> nY, nZ, nYs, nZs, nYf, nYs3, nZs3, nZf;
+  std::vector<TransProb> tZ, tX, tZs, tY2, tR;
+  std::vector<GemmProb> nY, nZ, nYs, nZs, nYf, nYs3, nZs3, nZf, qZ, qZs;
   std::vector<SplitProb> vlo;
-  uint32_t ttz = 0, ttx = 0, tny = 0, tnz = 0, tvlo = 0, tnyf = 0, tty2 = 0;
+  uint32_t ttz = 0, ttx = 0, tny = 0, tnz = 0, tvlo = 0, tnyf = 0, tty2 = 0, ttr = 0, tqz = 0;
+  // The early orthonormalisations of the bf16-path matrices form the next iterate's bf16
+  // copy Z^T (w x s, blocked) straight from split bf16 products, Z^T = (R^{-1})^T Z2^T with
+  // both factors in three parts (about fp32 accuracy, as the fp32 GEMM it replaces), instead
+  // of an fp32 GEMM followed by a transpose. Needs K = w in 32-steps for every such matrix.
+  bool use_qz = false;
+  for (const RefMat& x : rm) {
+    if (!x.bf) continue;
+    const MatHost& h = st->mats[x.idx];
+    use_qz = x.w % 32 == 0 && gemm_nt_eligible(EP_STORE_BF16, x.w, h.s, x.w, x.w, x.w, h.s, h.V, h.V, h.V, 0);
+    if (!use_qz) break;
+  }
   for (int q = 0; q < nm; ++q) {
     const RefMat& x = rm[q];
     if (!x.bf) continue;
@@ -928,6 +948,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     z.kp = 1 | 2;       // XL and Yt blocked (K = L)
     z.a_bytes = (uint32_t)(2 * (size_t)x.s * x.L); z.b_bytes = (uint32_t)(2 * (size_t)x.w * x.L);
     z.tiles_n = gemm_nt_tiles_n(z.N); z.tile_start = tnz; tnz += gemm_nt_tiles_m(z.M) * z.tiles_n;
+    if (use_qz) z.c_parts = x.Z2p;   // every Z2 but the last one feeds an early orthonormalisation
     nZ.push_back(z);
     // split iterations: V's bf16 parts v_m, v_l (both orientations), the iterates' residuals.
     // The operator V is kept to about 2^-24 (v_h + v_m + v_l), the iterates Z^T and Y^T to
@@ -981,6 +1002,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     // damped (it moves span(Z2) by about its size times sigma_1 / sigma_r): six products,
     // operator . iterate h.h + h.m + m.h + h.l + m.m + l.h (both kept to about 2^-24)
     GemmProb zf = z;
+    zf.c_parts = nullptr;
     {
       const void* op[6] = {x.XL, x.XL, x.XLm, x.XL, x.XLm, x.XLl};
       const void* it[6] = {x.Yt, x.Ytlo, x.Yt, x.Ytl2, x.Ytlo, x.Yt};
@@ -993,6 +1015,35 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     q2.rows = x.L; q2.cols = x.w; q2.ldi = x.w; q2.ldo = x.L;
     q2.in_f32 = 1; q2.out_kp = 1;
     q2.tiles_c = (int32_t)((x.w + 63) / 64); q2.tile_start = tty2; tty2 += transpose_tiles(x.L, x.w);
+    if (use_qz) {
+      // (R^{-1})^T in three bf16 parts, blocked (rows w, K = w): A of the product below
+      TransProb tr{};
+      const size_t ww = (size_t)x.w * x.w;
+      tr.in = x.Rinv; tr.out = x.Rtp; tr.out_lo = (bf16*)x.Rtp + ww; tr.out_lo2 = (bf16*)x.Rtp + 2 * ww;
+      tr.rows = x.w; tr.cols = x.w; tr.ldi = x.w; tr.ldo = x.w; tr.in_f32 = 1; tr.out_kp = 1;
+      tr.tiles_c = (int32_t)((x.w + 63) / 64); tr.tile_start = ttr; ttr += transpose_tiles(x.w, x.w);
+      tR.push_back(tr);
+      // Z^T = (R^{-1})^T Z2^T: A = (R^{-1})^T (zero above... below its diagonal: A[n][k] = 0
+      // for k > n, so a tile's K loop ends at its last row), B = Z2 (rows s, K = w); six
+      // part products h.h + h.m + m.h + h.l + l.h + m.m; output Z^T in bf16, blocked (K = s)
+      GemmProb g{};
+      g.M = x.w; g.N = x.s; g.K = x.w;
+      g.lda = x.w; g.ldb = x.w; g.c = x.Zt; g.ldc = x.s;
+      g.kp = 1 | 2 | 4;
+      g.tri_b = 2;
+      g.a_bytes = (uint32_t)(2 * ww); g.b_bytes = (uint32_t)(2 * (size_t)x.s * x.w);
+      const bf16* ra = (const bf16*)x.Rtp;
+      const bf16* zb = (const bf16*)x.Z2p;
+      const size_t sw = (size_t)x.s * x.w;
+      const void* pa[6] = {ra, ra, ra + ww, ra, ra + 2 * ww, ra + ww};
+      const void* pb[6] = {zb, zb + sw, zb, zb + 2 * sw, zb, zb + sw};
+      g.a = pa[0]; g.b = pb[0]; g.nseg = 6;
+      for (int j = 1; j < 6; ++j) { g.seg_a[j - 1] = pa[j]; g.seg_b[j - 1] = pb[j]; }
+      g.tiles_n = gemm_nt_tiles_n(g.N); g.tile_start = tqz; tqz += gemm_nt_tiles_m(g.M) * g.tiles_n;
+      qZ.push_back(g);
+      g.c_lo = x.Ztlo;   // before a split iteration: also the residual part of Z^T
+      qZs.push_back(g);
+    }
     tY2.push_back(q2);
   }
 
@@ -1026,6 +1077,10 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       {nYs3.data(), sizeof(GemmProb) * nYs3.size()},                  // 25
       {nZs3.data(), sizeof(GemmProb) * nZs3.size()},                  // 26
       {nZf.data(), sizeof(GemmProb) * nZf.size()},                    // 27
+      {tR.data(), sizeof(TransProb) * tR.size()},                     // 28
+      {qZ.data(), sizeof(GemmProb) * qZ.size()},                      // 29
+      {qZs.data(), sizeof(GemmProb) * qZs.size()},                    // 30
+      {aZf.first.data(), sizeof(GemmProb) * aZf.first.size()},       // 31
   };
   size_t total = 0;
   std::vector<size_t> offs;
@@ -1077,19 +1132,28 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
         e = launch_trtri(RD, INV + (size_t)(l - 1) * nm, nm, inv_tot[l - 1], l, ph, stream);
     return e;
   };
-  auto orth_Z = [&]() -> hipError_t {        // Z <- orth(Z2)
+  // Z <- orth(Z2). An early one (more iterations follow) forms the bf16-path matrices'
+  // next Z^T (and its residual part before a split iteration) directly; the fp32 Z
+  // is then formed for the other matrices only.
+  bool zt_ready = false;
+  auto orth_Z = [&](bool early, bool next_split) -> hipError_t {
     hipError_t e = launch_gram((const GramProb*)D(1), nm, gZ2.second, stream);
     if (e == hipSuccess) e = chol_inv();
-    if (e == hipSuccess) e = gemm(A_KC, 3, aZ);
+    zt_ready = early && use_qz;
+    if (!zt_ready) return e == hipSuccess ? gemm(A_KC, 3, aZ) : e;
+    if (e == hipSuccess) e = gemm(A_KC, 31, aZf);
+    if (e == hipSuccess) e = launch_transpose((const TransProb*)D(28), (int)tR.size(), ttr, stream);
+    if (e == hipSuccess)
+      e = launch_gemm_nt(EP_STORE_BF16, (const GemmProb*)D(next_split ? 30 : 29), (int)qZ.size(), tqz, u, stream);
     return e;
   };
   TimerScope ts(st, MOARA_KERN_REFRESH, stream);
   // blocks below the diagonal of Rinv are never written by the factorisation kernels
   for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.Rinv, 0, 4 * (size_t)x.w * x.w, stream));
   HIP_TRY(launch_gauss(RD, nm, tg, stream));
-  if (orth0) HIP_TRY(orth_Z());
   const int q_iters = c.refresh_iters;
   const int q_bf = q_iters > REFRESH_F32_ITERS ? q_iters - REFRESH_F32_ITERS : 0;
+  if (orth0) HIP_TRY(orth_Z(false, false));   // the Gaussian block has no bf16 parts
   if (!nY.empty()) {
     HIP_TRY(launch_transpose((const TransProb*)D(19), (int)tX.size(), ttx, stream));
     HIP_TRY(launch_split_lo((const SplitProb*)D(14), (int)vlo.size(), tvlo, stream));
@@ -1108,11 +1172,11 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     // and their residuals) in the last ones
     if (!nY.empty()) {
       if (it < q_bf) {
-        HIP_TRY(launch_transpose((const TransProb*)D(18), (int)tZ.size(), ttz, stream));
+        if (!zt_ready) HIP_TRY(launch_transpose((const TransProb*)D(18), (int)tZ.size(), ttz, stream));
         HIP_TRY(launch_gemm_nt(EP_STORE_BF16, (const GemmProb*)D(20), (int)nY.size(), tny, u, stream));
         HIP_TRY(launch_gemm_nt(EP_STORE, (const GemmProb*)D(21), (int)nZ.size(), tnz, u, stream));
       } else {
-        HIP_TRY(launch_transpose((const TransProb*)D(15), (int)tZs.size(), ttz, stream));
+        if (!zt_ready) HIP_TRY(launch_transpose((const TransProb*)D(15), (int)tZs.size(), ttz, stream));
         if (!last) {
           const bool five = it + REFRESH_SPLIT5_ITERS >= q_iters;
           HIP_TRY(launch_gemm_nt(EP_STORE_BF16, (const GemmProb*)D(five ? 16 : 25), (int)nYs.size(), tny, u, stream));
@@ -1123,7 +1187,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       }
     }
     if (!last) {
-      HIP_TRY(orth_Z());
+      HIP_TRY(orth_Z(true, it + 1 >= q_bf));
     } else {   // Y2 = orth(Y) ; Z2 = X^T Y2
       HIP_TRY(launch_gram((const GramProb*)D(2), nm, gY.second, stream));
       HIP_TRY(chol_inv());
@@ -1138,7 +1202,7 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   }
   // Rayleigh-Ritz: Z2 = Q R (CholeskyQR), SVD of the w x w factor R by one-sided Jacobi
   // (R J has orthogonal columns, norms = Ritz values), Ritz vectors Q (R J) / norm
-  HIP_TRY(orth_Z());
+  HIP_TRY(orth_Z(false, false));
   HIP_TRY(launch_r_colmajor(RD, nm, tc, stream));
   for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.off, 0, 4 * 64, stream));
   for (int sw = 0; sw < MAX_SWEEPS; ++sw)
@@ -1179,11 +1243,11 @@ size_t refresh_budget() {
 }
 
 // Upper bound of one refresh chunk's descriptor bytes (refresh_chunk's parts: RefDev,
-// two Gram lists, at most ten GEMM lists, two transpose lists and the Cholesky and
-// inverse prefix arrays, each part aligned).
+// two Gram lists, the GEMM, transpose and split lists and the Cholesky and inverse
+// prefix arrays, each part aligned).
 size_t ref_desc_bound(size_t nm, int nbmax) {
   const int nlev = std::max(1, trtri_levels(nbmax));
-  return 29 * ALIGN + nm * (sizeof(RefDev) + 2 * sizeof(GramProb) + 14 * sizeof(GemmProb) + 4 * sizeof(TransProb) +
+  return 33 * ALIGN + nm * (sizeof(RefDev) + 2 * sizeof(GramProb) + 17 * sizeof(GemmProb) + 5 * sizeof(TransProb) +
                             sizeof(SplitProb) + 4 * (2 * (size_t)nbmax + (size_t)nlev));
 }
 
