@@ -1148,8 +1148,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     return e;
   };
   TimerScope ts(st, MOARA_KERN_REFRESH, stream);
-  // blocks below the diagonal of Rinv are never written by the factorisation kernels
-  for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.Rinv, 0, 4 * (size_t)x.w * x.w, stream));
+  // the Gaussian start block; the same launch zeroes Rinv (its blocks below the diagonal
+  // are never written by the factorisation kernels) and the per-sweep Jacobi measures
   HIP_TRY(launch_gauss(RD, nm, tg, stream));
   const int q_iters = c.refresh_iters;
   const int q_bf = q_iters > REFRESH_F32_ITERS ? q_iters - REFRESH_F32_ITERS : 0;
@@ -1204,7 +1204,6 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   // (R J has orthogonal columns, norms = Ritz values), Ritz vectors Q (R J) / norm
   HIP_TRY(orth_Z(false, false));
   HIP_TRY(launch_r_colmajor(RD, nm, tc, stream));
-  for (auto& x : rm) HIP_TRY(hipMemsetAsync(x.off, 0, 4 * 64, stream));
   for (int sw = 0; sw < MAX_SWEEPS; ++sw)
     for (int rr = 0; rr < nb_max - 1; ++rr) HIP_TRY(launch_jacobi_round(RD, nm, tj, rr, sw, stream));
   HIP_TRY(launch_finalize_order(RD, nm, tnorm, stream));

@@ -46,6 +46,7 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
   const RefDev& d = ds[lo];
   const int64_t total = d.s * d.w;
   const int64_t e0 = ((int64_t)(t - d.tile_gauss) * GAUSS_PER_WG) + threadIdx.x * 4;
+  if (t == d.tile_gauss && threadIdx.x < 64) d.off[threadIdx.x] = 0u;   // per-sweep Jacobi measures
   if (e0 >= total) return;
   uint32_t c[4] = {(uint32_t)(e0 >> 2), (uint32_t)(e0 >> 34), 0x4D6F4152u, 0x52656672u};
   philox4x32_10(c, d.seed);
@@ -53,6 +54,13 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
   const float a0 = 6.283185307179586f * u01(c[1]), a1 = 6.283185307179586f * u01(c[3]);
   float v[4] = {r0 * cosf(a0), r0 * sinf(a0), r1 * cosf(a1), r1 * sinf(a1)};
   for (int q = 0; q < 4 && e0 + q < total; ++q) d.Z0[e0 + q] = v[q];
+  // the same launch clears what later kernels expect at zero (a fill kernel rather than a
+  // memset node, so that a captured refresh replays correctly): the measures above and
+  // the blocks of the fp32 R^{-1} below its diagonal, which the factorisation never
+  // writes (w^2 <= s w)
+  const int64_t ww = (int64_t)d.w * d.w;
+  for (int q = 0; q < 4; ++q)
+    if (e0 + q < ww) d.Rinv[e0 + q] = 0.f;
 }
 
 // ------------------------------------------------------------------ fp64 Gram C = A^T A
