@@ -240,6 +240,31 @@ def test_refresh_lowrank_llama300m_layer():
         assert info["converged"] and info["rank"] == c.ranks[i], (i, info)
 
 
+def test_refresh_bf16_path_with_fp32_orthonormalisation():
+    """A bf16-path matrix whose subspace width is not a multiple of 32 (r = 40, w = 80) keeps
+    the early orthonormalisations of its refresh chunk on the fp32 product and the transpose
+    (the split bf16 form needs K = w in 32-steps): that path must still match the oracle."""
+    import dataclasses
+    import torch
+    M = _M()
+    wl = WL.subset(WL.WORKLOADS["llama_300m"], [0])
+    rt = list(wl.rank_table)
+    rt[WL.Q] = 40
+    wl = dataclasses.replace(wl, rank_table=tuple(rt))
+    c = case_from_workload(wl)
+    st = gpu_state(c)
+    Gs = [WL.grad_np(wl, i, 0) for i in range(len(wl.matrices))]
+    print("[refresh] llama_300m layer 0, q at r = 40", flush=True)
+    M.moara_refresh_projector(st, [to_dev(g, "f32") for g in Gs])
+    torch.cuda.synchronize()
+    Ps = [M.moara_get_tensor(st, i, M.MOARA_T_P) for i in range(len(Gs))]
+    worst = _angles_vs_oracle(c, Gs, Ps)
+    print(f"[refresh] worst principal angle {worst:.2e}", flush=True)
+    for i in range(len(Gs)):
+        info = M.moara_refresh_info(st, i)
+        assert info["converged"] and info["rank"] == c.ranks[i], (i, info)
+
+
 def test_refresh_in_several_chunks_is_bit_identical(monkeypatch):
     """A refresh split into chunks (workspace budget below one layer's need) gives the
     same projectors, bit for bit, as one chunk: every matrix is computed on its own."""
