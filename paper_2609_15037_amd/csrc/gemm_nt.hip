@@ -46,6 +46,8 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -339,8 +341,10 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
         const int64_t row = wrow0 + PR * h + RPP * p + lane / LPR;
         if (row < P.M && col < P.N) {
           const int64_t idx = row * P.ldc + col;
-          ev[h % DB][p] = *reinterpret_cast<const bf16x4*>(E1 + idx);
-          qv[h % DB][p] = *reinterpret_cast<const bf16x4*>(E2 + idx);
+          // the moments are read and written once per step: non-temporal accesses keep them
+          // from displacing the operand panels and the next kernels' data in the caches
+          ev[h % DB][p] = __builtin_bit_cast(bf16x4, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(E1 + idx)));
+          qv[h % DB][p] = __builtin_bit_cast(bf16x4, __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(E2 + idx)));
         }
       }
     };
@@ -361,8 +365,8 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
             e[c] = ec;
             q[c] = qc;
           }
-          *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(P.e1) + idx) = e;
-          *reinterpret_cast<bf16x4*>(reinterpret_cast<bf16*>(P.e2) + idx) = q;
+          __builtin_nontemporal_store(__builtin_bit_cast(u32x2, e), reinterpret_cast<u32x2*>(reinterpret_cast<bf16*>(P.e1) + idx));
+          __builtin_nontemporal_store(__builtin_bit_cast(u32x2, q), reinterpret_cast<u32x2*>(reinterpret_cast<bf16*>(P.e2) + idx));
           *reinterpret_cast<bf16x4*>((bf16*)P.c + ((P.kp & 4) ? kp_index(row, col, P.M) : idx)) = o;
         }
       }
@@ -443,7 +447,9 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
           const int64_t row = wrow0 + 32 * mb + RPP * p + lane / LPR;
           mg[mb % DB][p] = 1.f;
           if (row < P.M && col < P.N) {
-            wv[mb % DB][p] = *reinterpret_cast<const bf16x8*>((const bf16*)P.c + row * P.ldc + col);
+            // W is read and written once per step: non-temporal, as the moments above
+            wv[mb % DB][p] = __builtin_bit_cast(
+                bf16x8, __builtin_nontemporal_load(reinterpret_cast<const u32x4*>((const bf16*)P.c + row * P.ldc + col)));
             if (P.dM) mg[mb % DB][p] = P.dM[row * P.dM_ld + col / U.B];
           }
         }
@@ -465,7 +471,7 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
             bf16x8 o;
 #pragma unroll
             for (int q = 0; q < 8; ++q) o[q] = f2bf(bf2f(wv[mb % DB][p][q]) - U.lr * bf2f(f2bf(U.scale * (m * v[q]))));
-            *reinterpret_cast<bf16x8*>((bf16*)P.c + row * P.ldc + col) = o;
+            __builtin_nontemporal_store(__builtin_bit_cast(u32x4, o), reinterpret_cast<u32x4*>((bf16*)P.c + row * P.ldc + col));
           }
         }
         if (mb + DB < MB) load_w(mb + DB);
