@@ -91,11 +91,11 @@ template <> struct GemmTile<KIND_F32> { static constexpr int BM = 128, BN = 128,
 // the GM A tile-rows stay resident too.
 constexpr int GM = 8;
 __device__ __forceinline__ void tile_coords(uint32_t lt, uint32_t tiles_m, uint32_t tiles_n, uint32_t& tm,
-                                            uint32_t& tn) {
-  const uint32_t per_group = GM * tiles_n;
+                                            uint32_t& tn, uint32_t gm = GM) {
+  const uint32_t per_group = gm * tiles_n;
   const uint32_t group = lt / per_group;
-  const uint32_t first = group * GM;
-  const uint32_t gsz = (tiles_m - first < (uint32_t)GM) ? tiles_m - first : (uint32_t)GM;
+  const uint32_t first = group * gm;
+  const uint32_t gsz = (tiles_m - first < gm) ? tiles_m - first : gm;
   const uint32_t idx = lt - group * per_group;
   tm = first + idx % gsz;
   tn = idx / gsz;
