@@ -1023,9 +1023,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
       tr.rows = x.w; tr.cols = x.w; tr.ldi = x.w; tr.ldo = x.w; tr.in_f32 = 1; tr.out_kp = 1;
       tr.tiles_c = (int32_t)((x.w + 63) / 64); tr.tile_start = ttr; ttr += transpose_tiles(x.w, x.w);
       tR.push_back(tr);
-      // Z^T = (R^{-1})^T Z2^T: A = (R^{-1})^T (zero above... below its diagonal: A[n][k] = 0
-      // for k > n, so a tile's K loop ends at its last row), B = Z2 (rows s, K = w); six
-      // part products h.h + h.m + m.h + h.l + l.h + m.m; output Z^T in bf16, blocked (K = s)
+      // Z^T = (R^{-1})^T Z2^T: A = (R^{-1})^T, lower triangular (A[n][k] = 0 for k > n, so a
+      // tile's K loop ends at its last row), B = Z2 (rows s, K = w); six part products
+      // h.h + h.m + m.h + h.l + l.h + m.m; output Z^T in bf16, blocked (K = s)
       GemmProb g{};
       g.M = x.w; g.N = x.s; g.K = x.w;
       g.lda = x.w; g.ldb = x.w; g.c = x.Zt; g.ldc = x.s;
