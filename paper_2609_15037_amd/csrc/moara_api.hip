@@ -755,6 +755,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.sidx = (int32_t*)take(4 * h_r_of(x));
     x.Z2p = x.Y;    // 6 s w bytes <= the 8 L w of Y and Y2 (taken one after the other; L >= s)
     x.Rtp = x.X;    // 6 w^2 bytes <= 8 w^2
+    if (x.s > x.L)  // the projected side is the shorter one by construction
+      return fail(MOARA_E_STATE, "refresh of matrix %d: s = %lld exceeds L = %lld", x.idx, (long long)x.s,
+                  (long long)x.L);
   }
   const int nm = (int)rm.size();
   const int kind = KIND_F32;
