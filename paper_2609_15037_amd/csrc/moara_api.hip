@@ -753,11 +753,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
     x.norms = (double*)take(8 * x.wpad);
     x.cw = (double*)take(8 * 64 * (size_t)x.s + 8 * 64 * h_r_of(x) + 8 * (size_t)x.s);
     x.sidx = (int32_t*)take(4 * h_r_of(x));
-    x.Z2p = x.Y;    // 6 s w bytes <= the 8 L w of Y and Y2 (taken one after the other; L >= s)
+    x.Z2p = x.Y;    // 6 s w bytes <= the 8 L w of Y and Y2 (taken one after the other) when 3 s <= 4 L
     x.Rtp = x.X;    // 6 w^2 bytes <= 8 w^2
-    if (x.s > x.L)  // the projected side is the shorter one by construction
-      return fail(MOARA_E_STATE, "refresh of matrix %d: s = %lld exceeds L = %lld", x.idx, (long long)x.s,
-                  (long long)x.L);
   }
   const int nm = (int)rm.size();
   const int kind = KIND_F32;
@@ -922,7 +919,9 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
   for (const RefMat& x : rm) {
     if (!x.bf) continue;
     const MatHost& h = st->mats[x.idx];
-    use_qz = x.w % 32 == 0 && gemm_nt_eligible(EP_STORE_BF16, x.w, h.s, x.w, x.w, x.w, h.s, h.V, h.V, h.V, 0);
+    // (Z2's parts live in Y..Y2: 3 s <= 4 L, which the automatic side choice, s <= L, meets)
+    use_qz = x.w % 32 == 0 && 3 * x.s <= 4 * x.L &&
+             gemm_nt_eligible(EP_STORE_BF16, x.w, h.s, x.w, x.w, x.w, h.s, h.V, h.V, h.V, 0);
     if (!use_qz) break;
   }
   for (int q = 0; q < nm; ++q) {

@@ -265,6 +265,40 @@ def test_refresh_bf16_path_with_fp32_orthonormalisation():
         assert info["converged"] and info["rank"] == c.ranks[i], (i, info)
 
 
+def test_refresh_forced_side_on_the_longer_dimension():
+    """A projector forced onto the longer side (LEFT on a 384 x 256 matrix: s = 384 > L = 256)
+    is still the top-r left singular subspace of V; such a refresh keeps the fp32
+    orthonormalisation (the split one keeps Z2's parts in buffers sized for s <= 4 L / 3).
+    Checked next to an automatic-side matrix of the same state against the oracle."""
+    import torch
+    M = _M()
+    B, rk = 32, 32
+    shapes = [(384, 256, WL.Q, rk, M.MOARA_SIDE_LEFT), (256, 384, WL.K, rk, M.MOARA_SIDE_AUTO)]
+    cfg = M.moara_default_config(block_size=B, refresh_interval=0, weight_dtype=M.MOARA_BF16,
+                                 operand_dtype=M.MOARA_BF16, refresh_oversample=rk, refresh_iters=20)
+    st = M.moara_create_state(cfg, M.make_descs(shapes))
+    rng = np.random.default_rng(7)
+    Gs = []
+    for (m, n, *_rest) in shapes:   # low rank plus noise, a decaying spectrum
+        U = np.linalg.qr(rng.standard_normal((m, 48)))[0]
+        Y = np.linalg.qr(rng.standard_normal((n, 48)))[0]
+        Gs.append(((U * np.arange(1, 49) ** -1.0) @ Y.T + 1e-3 * rng.standard_normal((m, n))).astype(np.float32))
+    print("[refresh] forced LEFT on 384 x 256", flush=True)
+    M.moara_refresh_projector(st, [to_dev(g, "f32") for g in Gs])
+    torch.cuda.synchronize()
+    for i, G in enumerate(Gs):
+        Pg = M.moara_get_tensor(st, i, M.MOARA_T_P).astype(np.float64)
+        _, V = O.decompose(G, B)
+        ref = O.truncated_svd(V, rk, O.LEFT)   # both matrices project on the left
+        assert Pg.shape == ref.shape == (G.shape[0], rk)
+        np.testing.assert_allclose(Pg.T @ Pg, np.eye(rk), atol=2e-5)
+        ang = O.max_principal_angle(Pg, ref)
+        print(f"[refresh] matrix {i}: principal angle {ang:.2e}", flush=True)
+        assert ang <= 1e-3
+        info = M.moara_refresh_info(st, i)
+        assert info["converged"] and info["rank"] == rk, (i, info)
+
+
 def test_refresh_in_several_chunks_is_bit_identical(monkeypatch):
     """A refresh split into chunks (workspace budget below one layer's need) gives the
     same projectors, bit for bit, as one chunk: every matrix is computed on its own."""
