@@ -7,8 +7,8 @@
 // Default configuration: workgroup tile 256 x 256, sixteen waves (4 along M x 4 along
 // N), each wave a 64 x 64 sub-tile of 2 x 2 v_mfma_f32_32x32x16_bf16 blocks (64 fp32
 // accumulators per lane), one workgroup per CU. K advances in steps of 32 through a
-// ring of LDS stages (32 KB each: four for the projection, five for the back-projection
-// whose K loop is short) filled by direct global->LDS buffer loads (no register
+// ring of LDS stages (32 KB each: four for the step's products, five for the refresh's
+// plain-store products) filled by direct global->LDS buffer loads (no register
 // staging), the stages ahead of the one being multiplied in flight, one barrier per
 // step. Operands may be row-major or in the blocked K-panel layout (kp_index), where
 // one K step of the tile's rows is a contiguous run and the DMA loads move whole lines.
@@ -542,9 +542,11 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 //   4: 256 x 128 tiles, eight waves of 64 x 64, three stages, two workgroups per CU
 //      (3.61 / 3.89);
 //   5: 256 x 256 tiles, sixteen waves of 64 x 64, four stages, one workgroup per CU
-//      (3.28 / 3.88) -- the default; its back-projection (K = r, 16 to 32 steps) now
-//      runs five stages, which hides the pipeline fill of the short K loop better
-//      than the cache warm-up did (-4 % on that kernel).
+//      (3.28 / 3.88) -- the default. Its back-projection (K = r, 16 to 32 steps) ran
+//      five stages while the epilogue's W accesses went through the caches (-4 %
+//      against four then); with non-temporal W accesses four are faster again (full
+//      7B stack: 13.05 -> 12.38 ms). The plain-store products of the projector refresh
+//      run five (7B refresh -1.3 %).
 // Re-measured with blocked operands and barrier-free epilogues (stand-alone copy of the
 // kernel on 8 layers' worth of problems, projection / back-projection ms): variant 5
 // 2.64 / 2.95, variant 4 3.04 / 3.11, variant 1 2.87 / 3.52.
@@ -555,15 +557,15 @@ __global__ __launch_bounds__(64 * NWM * NWN, (OCC * NWM * NWN + 3) / 4) void k_g
 #define GEMM_NT_VARIANT 5
 #endif
 #if GEMM_NT_VARIANT == 1
-constexpr int V_NWM = 2, V_NWN = 4, V_WTN = 64, V_NS = 4, V_NSU = 4, V_OCC = 1;
+constexpr int V_NWM = 2, V_NWN = 4, V_WTN = 64, V_NS = 4, V_NSU = 4, V_NSS = 4, V_OCC = 1;
 #elif GEMM_NT_VARIANT == 2
-constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 128, V_NS = 4, V_NSU = 4, V_OCC = 1;
+constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 128, V_NS = 4, V_NSU = 4, V_NSS = 4, V_OCC = 1;
 #elif GEMM_NT_VARIANT == 3
-constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 64, V_NS = 3, V_NSU = 3, V_OCC = 2;
+constexpr int V_NWM = 2, V_NWN = 2, V_WTN = 64, V_NS = 3, V_NSU = 3, V_NSS = 3, V_OCC = 2;
 #elif GEMM_NT_VARIANT == 4
-constexpr int V_NWM = 4, V_NWN = 2, V_WTN = 64, V_NS = 3, V_NSU = 3, V_OCC = 2;
+constexpr int V_NWM = 4, V_NWN = 2, V_WTN = 64, V_NS = 3, V_NSU = 3, V_NSS = 3, V_OCC = 2;
 #else
-constexpr int V_NWM = 4, V_NWN = 4, V_WTN = 64, V_NS = 4, V_NSU = 5, V_OCC = 1;
+constexpr int V_NWM = 4, V_NWN = 4, V_WTN = 64, V_NS = 4, V_NSU = 4, V_NSS = 5, V_OCC = 1;
 #endif
 constexpr int GEMM_NT_BN = V_NWN * V_WTN;
 uint32_t gemm_nt_tiles_m(int64_t M) { return (uint32_t)((M + TBM - 1) / TBM); }
@@ -591,15 +593,15 @@ bool gemm_nt_eligible(int ep, int64_t M, int64_t N, int64_t K, int64_t lda, int6
 }
 
 namespace {
-template <int NWM, int NWN, int WTN, int NS, int NSU, int OCC>
+template <int NWM, int NWN, int WTN, int NS, int NSU, int NSS, int OCC>
 hipError_t launch_nt(int ep, const GemmProb* probs_dev, uint32_t total_tiles, const GemmUniform& u, hipStream_t st) {
   const dim3 grid(total_tiles), block(64 * NWM * NWN);
   if (ep == EP_ADAM && u.moment_bf16)
     hipLaunchKernelGGL((k_gemm_nt<EP_ADAM_B16, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_ADAM) hipLaunchKernelGGL((k_gemm_nt<EP_ADAM, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
   else if (ep == EP_UPDATE) hipLaunchKernelGGL((k_gemm_nt<EP_UPDATE, NWM, NWN, WTN, NSU, OCC>), grid, block, 0, st, probs_dev, u);
-  else if (ep == EP_STORE) hipLaunchKernelGGL((k_gemm_nt<EP_STORE, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
-  else if (ep == EP_STORE_BF16) hipLaunchKernelGGL((k_gemm_nt<EP_STORE_BF16, NWM, NWN, WTN, NS, OCC>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_STORE) hipLaunchKernelGGL((k_gemm_nt<EP_STORE, NWM, NWN, WTN, NSS, OCC>), grid, block, 0, st, probs_dev, u);
+  else if (ep == EP_STORE_BF16) hipLaunchKernelGGL((k_gemm_nt<EP_STORE_BF16, NWM, NWN, WTN, NSS, OCC>), grid, block, 0, st, probs_dev, u);
   else return hipErrorInvalidValue;
   return hipGetLastError();
 }
@@ -610,5 +612,5 @@ hipError_t launch_gemm_nt(int ep, const GemmProb* probs_dev, int nprob, uint32_t
   if (total_tiles == 0 || nprob == 0) return hipSuccess;
   GemmUniform u = u0;
   u.nprob = nprob;
-  return launch_nt<V_NWM, V_NWN, V_WTN, V_NS, V_NSU, V_OCC>(ep, probs_dev, total_tiles, u, st);
+  return launch_nt<V_NWM, V_NWN, V_WTN, V_NS, V_NSU, V_NSS, V_OCC>(ep, probs_dev, total_tiles, u, st);
 }
