@@ -344,6 +344,31 @@ def test_right_side_uses_state_m_by_r():
     np.testing.assert_allclose(-W1, O.rep_b(M / (M + 1e-8), 2, n) * (N1 @ Q.T), rtol=1e-12, atol=1e-15)
 
 
+def test_square_matrix_takes_the_printed_left_form():
+    """Algorithm 1 is written in the left form (R = P^T V, dV = P N, P the top-r left
+    singular vectors); with m = n neither side keeps a smaller state, and the printed
+    form is the one taken. The singular vectors come from the hand-written Jacobi SVD."""
+    g = np.random.default_rng(12)
+    n, r = 6, 2
+    cfg = O.OracleConfig(block_size=2, rank=r, scale=1.0)
+    st = O.init_state(n, n, cfg)
+    assert st.side == O.LEFT and st.exp_avg.shape == (r, n)
+    G = g.standard_normal((n, n)) * np.linspace(3.0, 0.3, n)
+    W1 = O.step(np.zeros((n, n)), G, st, cfg, lr=1.0)
+    M, V = O.decompose(G, 2)
+    Uj, sj, Vj = _jacobi_svd(V)
+    assert sj[r - 1] - sj[r] > 1e-3 * sj[0]          # the top-r subspace is separated
+    mag = O.rep_b(M / (M + 1e-8), 2, n)
+    P = Uj[:, :r]
+    R = P.T @ V
+    left = mag * (P @ (R / (np.abs(R) + cfg.adam_eps)))
+    np.testing.assert_allclose(-W1, left, rtol=1e-10, atol=1e-14)
+    Q = Vj[:, :r]                                     # the right form moves W differently here
+    Rq = V @ Q
+    right = mag * ((Rq / (np.abs(Rq) + cfg.adam_eps)) @ Q.T)
+    assert np.max(np.abs(right - left)) > 1e-2
+
+
 def test_refresh_schedule_and_moment_continuity():
     g = np.random.default_rng(11)
     cfg = O.OracleConfig(block_size=4, rank=2, refresh_interval=3)
@@ -542,8 +567,9 @@ def test_alignment_depends_on_the_subspace_only():
 
 
 def test_module_alignment_is_the_mean_per_type():
-    got = O.module_alignment([(0, 0.2), (3, 1.0), (0, 0.4), (6, -0.5)])
-    assert got == pytest.approx({0: 0.3, 3: 1.0, 6: -0.5})
+    # three samples of type 0, skewed so that the mean (0.4) is not the median (0.2)
+    got = O.module_alignment([(0, 0.2), (3, 1.0), (0, 0.9), (6, -0.5), (0, 0.1)])
+    assert got == pytest.approx({0: 0.4, 3: 1.0, 6: -0.5})
 
 
 def test_flatten_keeps_axis_zero_and_blocks_run_over_the_flattened_columns():
