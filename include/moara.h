@@ -1,7 +1,7 @@
 /*
  * moara.h -- C ABI of the MI355X (gfx950) MoARa optimizer library.
  *
- * MoARa ("module-aware rank allocation" with block-wise magnitude/direction
+ * MoARa (module-aware rank allocation, with block-wise magnitude/direction
  * decomposition) is a GaLore-style low-rank optimizer. For every target weight
  * W (m x n, stored out x in, row-major) and every training step it computes,
  * following the training phase of Algorithm 1:
@@ -23,7 +23,7 @@
  *   7. W <- W - lr * scale * (Rep_B(dM) (.) dV), scale = GaLore scale (0.25 in
  *      Appendix D). With bf16 weights the scaled update is rounded to bf16
  *      (round to nearest even) before it is applied, and the result is rounded
- *      to bf16 (Appendix D: "the recomposed update is cast to bf16").
+ *      to bf16 (Appendix D).
  *
  * The per-module rank r_tau comes from a rank table, usually produced by the
  * budget-preserving reallocation of Algorithm 1, Phase 3 (moara_allocate_ranks).
@@ -143,7 +143,7 @@ typedef struct {
  * it, e.g. with moara_allocate_ranks). Errors: MOARA_E_ARG if out is NULL. */
 int moara_default_config(moara_config* out);
 
-/* Algorithm 1, Phase 3 ("Static budget-preserving reallocation", Section 3.2):
+/* Algorithm 1, Phase 3 (the static budget-preserving reallocation of Section 3.2):
  * r_tau = r_base - delta_r for tau in D, r_base + delta_r*|D|/|R| for tau in R,
  * r_base otherwise, for the module types in `types_mask`. Masks are bit sets
  * over module ids (bit i = module i). Entries of out_rank_table for modules not
@@ -185,7 +185,7 @@ int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, i
 int moara_create_state(const moara_config* cfg, const moara_matrix_desc* descs, int32_t n,
                        void* stream, moara_state** out);
 
-/* Algorithm 1, "P_tau <- TruncatedSVD(V, r_tau)", run now for the selected
+/* Algorithm 1's TruncatedSVD step (P_tau from V at rank r_tau), run now for the selected
  * matrices from their current gradients: V is formed from G exactly as in the
  * step, and P is computed by fp32 subspace iteration (q sweeps of V and V^T
  * with re-orthonormalisation, p oversampling columns) followed by a

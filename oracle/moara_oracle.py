@@ -12,7 +12,7 @@ It is a plain, slow, float64 NumPy transcription of what the paper defines:
 * Section 3.1 and Appendix B.1: block-wise magnitude/direction decomposition
   along the column (in-feature) axis, right zero padding of the last block,
   epsilon in the denominator only, cropping after recomposition.
-* Algorithm 1 Phase 3 (Section 3.2, "Static budget-preserving reallocation"):
+* Algorithm 1 Phase 3 (Section 3.2, the static budget-preserving reallocation):
   the integer rank table.
 * Appendix D: Adam with beta=(0.9, 0.999), bias correction, zero weight decay,
   GaLore scale 0.25, magnitude branch in fp32, recomposed update cast to bf16.
