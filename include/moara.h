@@ -41,6 +41,9 @@
  *     moara_step and moara_refresh_projector only enqueue work on it and return
  *     without synchronising; the caller must keep W and G alive and unmodified
  *     until that work has run.
+ *   - A state lives on the HIP device that is current when moara_create_state is
+ *     called; every later call that enqueues work on it must be made with that
+ *     device current (MOARA_E_STATE otherwise, before anything is enqueued).
  *   - A state is not thread-safe: do not use one state from two threads at once.
  *     It may be used from several streams: every call that enqueues work on a
  *     state first makes its stream wait for the work the previous call on that

@@ -296,6 +296,16 @@ int end_stage(moara_state* st, Stager& sg, hipStream_t stream) {
 // previous call enqueued (on whatever stream), and records the event again when it
 // returns: calls on one state run in call order even across streams, so the shared
 // descriptor arenas, workspaces and state tensors are never used by two streams at once.
+// The state's memory and its GPU's scratch live on the device that was current when the
+// state was created; a call enqueues on `stream`, which belongs to the current device.
+static int check_device(const moara_state* st) {
+  int cur = -1;
+  if (hipGetDevice(&cur) != hipSuccess) return fail(MOARA_E_HIP, "hipGetDevice failed");
+  if (cur != st->device)
+    return fail(MOARA_E_STATE, "the current HIP device is %d but the state lives on device %d", cur, st->device);
+  return MOARA_OK;
+}
+
 struct StreamOrder {
   moara_state* st;
   hipStream_t stream;
@@ -308,6 +318,7 @@ struct StreamOrder {
   }
 };
 #define ORDER_ON(st_, stream_)                                                               \
+  if (const int dev_rc_ = check_device(st_)) return dev_rc_;                                \
   StreamOrder order_guard_((st_), (stream_));                                               \
   if (order_guard_.err != hipSuccess)                                                       \
     return fail(MOARA_E_HIP, "hipStreamWaitEvent: %s", hipGetErrorString(order_guard_.err))
@@ -332,15 +343,20 @@ struct TimerScope {
   TimerScope(moara_state* s, int k, hipStream_t str) : st(s), kind(k), stream(str) {
     if (st->timing) {
       a = get_event(st);
-      if (a) hipEventRecord(a, stream);
+      if (a && hipEventRecord(a, stream) != hipSuccess) {   // no bracket: this launch goes untimed
+        st->ev_pool.push_back(a);
+        a = nullptr;
+      }
     }
   }
   ~TimerScope() {
     if (st->timing && a) {
       hipEvent_t b = get_event(st);
-      if (b) {
-        hipEventRecord(b, stream);
+      if (b && hipEventRecord(b, stream) == hipSuccess) {
         st->pending.push_back({kind, a, b});
+      } else {
+        st->ev_pool.push_back(a);
+        if (b) st->ev_pool.push_back(b);
       }
     }
   }
@@ -663,7 +679,7 @@ int ensure_ref_ws(moara_state* st, size_t bytes) {
                 st->ref_ws_bytes);
   if (st->ref_ws) {
     HIP_TRY(hipDeviceSynchronize());
-    hipFree(st->ref_ws);
+    (void)hipFree(st->ref_ws);
     st->ref_ws = nullptr;
     st->ref_ws_bytes = 0;
   }
@@ -1092,8 +1108,8 @@ int refresh_chunk(moara_state* st, const std::vector<int>& idx, const void* cons
                 st->ref_arena_bytes);
   if (total > st->ref_arena_bytes) {
     HIP_TRY(hipStreamSynchronize(stream));
-    if (st->ref_arena) hipFree(st->ref_arena);
-    if (st->ref_host) hipHostFree(st->ref_host);
+    if (st->ref_arena) (void)hipFree(st->ref_arena);
+    if (st->ref_host) (void)hipHostFree(st->ref_host);
     st->ref_arena = nullptr; st->ref_host = nullptr; st->ref_arena_bytes = 0;
     if (hipMalloc(&st->ref_arena, total) != hipSuccess) return fail(MOARA_E_OOM, "refresh descriptor arena");
     if (hipHostMalloc(&st->ref_host, total) != hipSuccess) return fail(MOARA_E_OOM, "refresh pinned arena");
@@ -1443,17 +1459,18 @@ int moara_state_bytes(const moara_config* cfg, const moara_matrix_desc* descs, i
 
 static void free_state(moara_state* st) {
   if (!st) return;
-  if (st->block) hipFree(st->block);
-  if (st->dev_arena) hipFree(st->dev_arena);
-  if (st->host_ring) hipHostFree(st->host_ring);
-  if (st->ref_ws) hipFree(st->ref_ws);
-  if (st->ref_arena) hipFree(st->ref_arena);
-  if (st->ref_host) hipHostFree(st->ref_host);
+  // teardown: a failure to release one resource does not stop the release of the others
+  if (st->block) (void)hipFree(st->block);
+  if (st->dev_arena) (void)hipFree(st->dev_arena);
+  if (st->host_ring) (void)hipHostFree(st->host_ring);
+  if (st->ref_ws) (void)hipFree(st->ref_ws);
+  if (st->ref_arena) (void)hipFree(st->ref_arena);
+  if (st->ref_host) (void)hipHostFree(st->ref_host);
   for (auto& e : st->slot_ev)
-    if (e) hipEventDestroy(e);
-  if (st->order_ev) hipEventDestroy(st->order_ev);
-  for (auto& tl : st->pending) { hipEventDestroy(tl.a); hipEventDestroy(tl.b); }
-  for (auto e : st->ev_pool) hipEventDestroy(e);
+    if (e) (void)hipEventDestroy(e);
+  if (st->order_ev) (void)hipEventDestroy(st->order_ev);
+  for (auto& tl : st->pending) { (void)hipEventDestroy(tl.a); (void)hipEventDestroy(tl.b); }
+  for (auto e : st->ev_pool) (void)hipEventDestroy(e);
   delete st;
 }
 
@@ -1885,7 +1902,9 @@ int moara_matrix_info(const moara_state* st, int32_t mat, int64_t* rows, int64_t
 
 void moara_destroy_state(moara_state* st) {
   if (!st) return;
-  hipDeviceSynchronize();
+  // every call that enqueued work on the state recorded order_ev last: waiting for it
+  // waits for all of the state's work, on whichever streams it ran
+  if (st->order_valid) (void)hipEventSynchronize(st->order_ev);
   free_state(st);
 }
 
