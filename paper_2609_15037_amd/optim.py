@@ -115,6 +115,11 @@ class MoARa(torch.optim.Optimizer):
         self._g32: List[Optional[torch.Tensor]] = [None] * len(targets)
         self._adamw = torch.optim.AdamW(others, lr=lr, betas=tuple(betas), eps=eps, weight_decay=0.0) if others else None
 
+    def _device(self):
+        """The target weights' GPU as the current device: the library's calls act on the
+        current device, and the state lives on the one that was current at its creation."""
+        return torch.cuda.device(self.param_groups[0]["params"][0].device)
+
     @property
     def moara_state(self) -> Optional[M.State]:
         """The library state (created at the first step), e.g. for moara_alignment."""
@@ -144,13 +149,14 @@ class MoARa(torch.optim.Optimizer):
             with torch.enable_grad():
                 loss = closure()
         tg = self.param_groups[0]
-        if self._st is None:
-            self._st = M.moara_create_state(self._cfg, self._descs)
-        grads = self._grads()
-        active = [g is not None for g in grads]
-        if any(active):
-            M.moara_step(self._st, list(tg["params"]), grads, lr=float(tg["lr"]),
-                         active=None if all(active) else active)
+        with self._device():
+            if self._st is None:
+                self._st = M.moara_create_state(self._cfg, self._descs)
+            grads = self._grads()
+            active = [g is not None for g in grads]
+            if any(active):
+                M.moara_step(self._st, list(tg["params"]), grads, lr=float(tg["lr"]),
+                             active=None if all(active) else active)
         if self._adamw is not None:
             og = self.param_groups[1]
             for g in self._adamw.param_groups:   # the schedule drives both groups
@@ -163,16 +169,19 @@ class MoARa(torch.optim.Optimizer):
         tensors, plus the AdamW state of the other parameters and the group settings."""
         lib = None
         if self._st is not None:
-            lib = []
-            for i in range(len(self._modules)):
-                d = {"step": int(M.moara_get_tensor(self._st, i, M.MOARA_T_STEP))}
-                for name, which in (("P", M.MOARA_T_P), ("exp_avg", M.MOARA_T_EXP_AVG),
-                                    ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ), ("mag_avg", M.MOARA_T_MAG_AVG),
-                                    ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ)):
-                    if which == M.MOARA_T_P and d["step"] == 0:
-                        continue   # no projector before the first refresh
-                    d[name] = torch.from_numpy(np.array(M.moara_get_tensor(self._st, i, which)))
-                lib.append(d)
+            with self._device():
+                lib = []
+                for i in range(len(self._modules)):
+                    d = {"step": int(M.moara_get_tensor(self._st, i, M.MOARA_T_STEP))}
+                    for name, which in (("P", M.MOARA_T_P), ("exp_avg", M.MOARA_T_EXP_AVG),
+                                        ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ), ("mag_avg", M.MOARA_T_MAG_AVG),
+                                        ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ)):
+                        try:
+                            d[name] = torch.from_numpy(np.array(M.moara_get_tensor(self._st, i, which)))
+                        except M.MoaraError as e:   # no projector yet: nothing to save for P
+                            if which != M.MOARA_T_P or e.status != M.MOARA_E_STATE:
+                                raise
+                    lib.append(d)
         # the AdamW part is copied: torch's state_dict hands out the live moment tensors, and
         # loading those into another optimizer would alias the two
         return {"moara": lib, "adamw": copy.deepcopy(self._adamw.state_dict()) if self._adamw else None,
@@ -185,12 +194,13 @@ class MoARa(torch.optim.Optimizer):
             self._adamw.load_state_dict(sd["adamw"])
         if sd["moara"] is None:
             return
-        if self._st is None:
-            self._st = M.moara_create_state(self._cfg, self._descs)
-        for i, d in enumerate(sd["moara"]):
-            for name, which in (("P", M.MOARA_T_P), ("exp_avg", M.MOARA_T_EXP_AVG),
-                                ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ), ("mag_avg", M.MOARA_T_MAG_AVG),
-                                ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ)):
-                if name in d:
-                    M.moara_set_tensor(self._st, i, which, d[name].numpy())
-            M.moara_set_tensor(self._st, i, M.MOARA_T_STEP, np.int64(d["step"]))
+        with self._device():
+            if self._st is None:
+                self._st = M.moara_create_state(self._cfg, self._descs)
+            for i, d in enumerate(sd["moara"]):
+                for name, which in (("P", M.MOARA_T_P), ("exp_avg", M.MOARA_T_EXP_AVG),
+                                    ("exp_avg_sq", M.MOARA_T_EXP_AVG_SQ), ("mag_avg", M.MOARA_T_MAG_AVG),
+                                    ("mag_avg_sq", M.MOARA_T_MAG_AVG_SQ)):
+                    if name in d:
+                        M.moara_set_tensor(self._st, i, which, d[name].numpy())
+                M.moara_set_tensor(self._st, i, M.MOARA_T_STEP, np.int64(d["step"]))

@@ -45,7 +45,7 @@ def test_small_llama_trains_with_moara():
         opt.step()
         sched.step()
         opt.zero_grad()
-        losses.append(float(loss))
+        losses.append(float(loss.detach()))
         if step % 10 == 0:
             print(f"[train] step {step} loss {losses[-1]:.4f} lr {sched.get_last_lr()[0]:.2e}", flush=True)
     assert np.isfinite(losses).all()
@@ -164,6 +164,9 @@ def test_moara_steps_of_a_bf16_model_match_the_oracle():
                                                        ost[i].side))
             opt.load_state_dict({"moara": [{"step": 0, "P": torch.from_numpy(o.P.astype(np.float32))} for o in ost],
                                  "adamw": None, "lr": [g["lr"] for g in opt.param_groups]})
+            sd0 = opt.state_dict()   # a projector set before the first step is saved too
+            for o, d in zip(ost, sd0["moara"]):
+                assert d["step"] == 0 and np.array_equal(d["P"].numpy(), o.P.astype(np.float32))
         print(f"[wrapper] step {step}, lr {lr:.3e}", flush=True)
         opt.step()
         sched.step()
