@@ -169,8 +169,8 @@ int moara_resolve_matrix(const moara_config* cfg, const moara_matrix_desc* desc,
 /* Device bytes a state for these n matrices would hold (persistent state plus
  * the per-step workspace; the refresh workspace is reported separately because
  * it is sized per refresh batch: a refresh works through its matrices in chunks
- * of at most 96 GiB of workspace, so the figure is the smaller of the whole
- * batch's need and that bound plus one matrix's share). The environment
+ * of at most 128 GiB of workspace, so the figure is the smaller of the whole
+ * batch's need and that bound plus the average matrix's share). The environment
  * variable MOARA_REFRESH_CHUNK_MIB, when set to a positive integer, replaces the
  * bound (in MiB) for this call and for later refreshes. Errors as
  * moara_create_state's validation. */

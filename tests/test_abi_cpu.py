@@ -129,6 +129,23 @@ def test_refresh_workspace_follows_the_chunk_budget(monkeypatch):
         assert M.moara_state_bytes(cfg, descs)[1] == whole
 
 
+def test_default_chunk_budget_is_128_gib(monkeypatch):
+    """A Llama-2-7B-shaped stack (224 matrices, ranks 512 / 1024 / 2048, p = r) needs more
+    refresh workspace than one chunk holds: the default bound is 128 GiB."""
+    _lib()
+    ranks = M.moara_allocate_ranks(1024, range(7), [M.MOARA_Q, M.MOARA_K], [M.MOARA_DOWN], 512)
+    cfg = M.moara_default_config(rank_table=ranks, block_size=128)
+    d, f = 4096, 11008
+    descs = M.make_descs([((d, d), 0), ((d, d), 1), ((d, d), 2), ((d, d), 3),
+                          ((f, d), 4), ((f, d), 5), ((d, f), 6)] * 32)
+    monkeypatch.setenv("MOARA_REFRESH_CHUNK_MIB", str(1 << 30))   # 1 PiB: no bound
+    _, whole = M.moara_state_bytes(cfg, descs)
+    monkeypatch.delenv("MOARA_REFRESH_CHUNK_MIB")
+    _, capped = M.moara_state_bytes(cfg, descs)
+    assert whole > (128 << 30)
+    assert capped == (128 << 30) + whole // 224
+
+
 def test_state_bytes_counts_fp32_moments_projector_copies_and_v_workspace():
     _lib()
     cfg = M.moara_default_config(rank_table=[64] * 10, block_size=64, operand_dtype=M.MOARA_BF16)
