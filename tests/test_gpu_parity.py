@@ -605,6 +605,33 @@ def test_runs_are_deterministic():
         assert torch.equal(a, b)
 
 
+def test_kernel_timing_counts_each_launch_and_resets():
+    """Per-kernel timing (the measurement path): with timing on, every step adds one launch of
+    each step kernel with a positive duration, a refresh adds to the refresh entry, a reset
+    zeroes them, and with timing off nothing is recorded; results are those of an untimed run."""
+    import torch
+    M = _M()
+    c = Case(shapes=[(256, 384, WL.Q), (384, 256, WL.GATE)], ranks=[32, 48], block_size=64)
+    outs = []
+    for timed in (True, False):
+        st = gpu_state(c, refresh_interval=2)
+        M.moara_set_timing(st, timed)
+        Wd = [to_dev(w, "f32") for w in _weights(c, 0)]
+        for t in range(3):   # refreshes at t = 0 and t = 2
+            M.moara_step(st, Wd, [to_dev(_grad(c, 4, t, i), "f32") for i in range(2)], lr=1e-3)
+        torch.cuda.synchronize()
+        outs.append([w.clone() for w in Wd])
+        for kid in (M.MOARA_KERN_DECOMPOSE, M.MOARA_KERN_PROJECT, M.MOARA_KERN_BACKPROJ, M.MOARA_KERN_REFRESH):
+            n, ms = M.moara_kernel_stats(st, kid)
+            want = (2 if kid == M.MOARA_KERN_REFRESH else 3) if timed else 0
+            assert n == want, (kid, n)
+            assert (ms > 0.0) == timed, (kid, ms)
+        M.moara_reset_kernel_stats(st)
+        assert M.moara_kernel_stats(st, M.MOARA_KERN_PROJECT) == (0, 0.0)
+    for a, b in zip(*outs):
+        assert torch.equal(a, b)
+
+
 def test_step_without_projector_is_rejected_before_launch():
     import torch
     M = _M()
