@@ -203,3 +203,9 @@ def test_nd_shapes_flatten_into_descriptors():
     assert (d[2].rows, d[2].cols, d[2].rank_override) == (10, 7, 5)
     with pytest.raises(ValueError):
         M.flatten_shape((5,))
+
+
+def test_version_names_the_target():
+    _lib()
+    v = M.moara_version()
+    assert re.fullmatch(r"moara-mi355x \d+\.\d+ \(gfx950\)", v), v

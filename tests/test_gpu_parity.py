@@ -632,6 +632,26 @@ def test_kernel_timing_counts_each_launch_and_resets():
         assert torch.equal(a, b)
 
 
+def test_matrix_info_matches_the_host_resolver():
+    """The state's per-matrix layout (moara_matrix_info) equals what moara_resolve_matrix
+    gives for the same descriptor: rank (table, override), side (auto, forced) and the
+    number of magnitude blocks ceil(n / B)."""
+    M = _M()
+    cfg = M.moara_default_config(rank_table=[16, 24, 32, 8, 40, 48, 12, 4, 4, 4], block_size=48,
+                                 operand_dtype=M.MOARA_F32, weight_dtype=M.MOARA_F32, refresh_interval=0)
+    entries = [(96, 200, M.MOARA_Q), (200, 96, M.MOARA_GATE), (128, 128, M.MOARA_K),
+               (150, 97, M.MOARA_DOWN, 20), (64, 300, M.MOARA_UP, 0, M.MOARA_SIDE_RIGHT),
+               (300, 64, M.MOARA_V, 10, M.MOARA_SIDE_LEFT)]
+    descs = M.make_descs(entries)
+    st = M.moara_create_state(cfg, descs)
+    for i, d in enumerate(descs):
+        r, side = M.moara_resolve_matrix(cfg, d)
+        assert M.moara_matrix_info(st, i) == (d.rows, d.cols, r, side, -(-d.cols // 48)), i
+    assert [M.moara_matrix_info(st, i)[2] for i in range(len(entries))] == [16, 40, 24, 20, 48, 10]
+    with pytest.raises(M.MoaraError):
+        M.moara_matrix_info(st, len(entries))
+
+
 def test_step_without_projector_is_rejected_before_launch():
     import torch
     M = _M()
