@@ -222,8 +222,11 @@ int moara_refresh_projector(moara_state* st, const void* const* grads, const uin
 int moara_step(moara_state* st, void* const* weights, const void* const* grads,
                const uint8_t* active, float lr, void* stream);
 
-/* moara_step for callers that cannot allocate device memory (code under HIP graph
- * capture, allocation-free serving or training loops, harnesses that forbid hipMalloc).
+/* moara_step for callers that cannot allocate device memory (allocation-free serving or
+ * training loops, harnesses that forbid hipMalloc). It allocates nothing, but it is not
+ * made for stream capture: like moara_step it stages each launch's descriptors through
+ * the state's pinned host ring (a host-to-device copy on `stream`, and a host wait before
+ * a ring slot is reused), so a graph captured from it would not replay correctly.
  * Same arguments, semantics and results as moara_step, bit for bit, but it calls no
  * hipMalloc, hipFree, hipHostMalloc or other device/pinned allocator: the step's
  * descriptors, and when a refresh falls due its descriptors and workspace, live in one
