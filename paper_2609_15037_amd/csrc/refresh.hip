@@ -54,10 +54,9 @@ __global__ __launch_bounds__(256) void k_gauss(const RefDev* __restrict__ ds, in
   const float a0 = 6.283185307179586f * u01(c[1]), a1 = 6.283185307179586f * u01(c[3]);
   float v[4] = {r0 * cosf(a0), r0 * sinf(a0), r1 * cosf(a1), r1 * sinf(a1)};
   for (int q = 0; q < 4 && e0 + q < total; ++q) d.Z0[e0 + q] = v[q];
-  // the same launch clears what later kernels expect at zero (a fill kernel rather than a
-  // memset node, so that a captured refresh replays correctly): the measures above and
-  // the blocks of the fp32 R^{-1} below its diagonal, which the factorisation never
-  // writes (w^2 <= s w)
+  // the same launch clears what later kernels expect at zero, saving separate memsets:
+  // the measures above and the blocks of the fp32 R^{-1} below its diagonal, which the
+  // factorisation never writes (w^2 <= s w)
   const int64_t ww = (int64_t)d.w * d.w;
   for (int q = 0; q < 4; ++q)
     if (e0 + q < ww) d.Rinv[e0 + q] = 0.f;
