@@ -202,6 +202,8 @@ class State:
         self.n = len(descs)
         self.shapes = [(int(d.rows), int(d.cols)) for d in descs]
         self.info = [moara_matrix_info(self, i) for i in range(self.n)]
+        import torch
+        self.device = torch.cuda.current_device()   # the library creates the state on the current device
 
     def __del__(self):
         if getattr(self, "handle", None):
@@ -242,6 +244,8 @@ def _ptr_array(st: State, tensors, what: str, dtype_name: str, active):
             raise ValueError(f"{what}[{i}]: need a contiguous {dtype_name} CUDA tensor of shape {st.shapes[i]} "
                              f"(or with that flattened shape), got {tuple(t.shape)} {t.dtype} cuda={t.is_cuda} "
                              f"contiguous={t.is_contiguous()}")
+        if t.device.index != st.device:   # the kernels would read another GPU's memory
+            raise ValueError(f"{what}[{i}] is on {t.device}, the state lives on cuda:{st.device}")
         arr[i] = t.data_ptr()
     return arr
 
