@@ -66,3 +66,23 @@ def test_step_accounting_prices_the_direction_moments_by_their_storage(operand):
     m4, f4 = bench.method_cost(wl, ob, 2, moment_bytes=4)
     m2, f2 = bench.method_cost(wl, ob, 2, moment_bytes=2)
     assert m4 - m2 == 8 * r * L and f4 == f2
+
+
+def test_measured_traffic_only_for_the_profiled_sources_and_workload(tmp_path, monkeypatch):
+    """The roofline's measured HBM traffic comes from the committed counter summary only
+    while the kernel sources hash to the value recorded there and the workload is the
+    profiled one; otherwise it is reported as null."""
+    import hashlib
+    h = hashlib.sha256()
+    for src in bench.TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    prof = tmp_path / "traffic.txt"
+    prof.write_text(f"sources-sha256 {h.hexdigest()}\ntraffic-bytes-per-launch backproject 123.0\n")
+    monkeypatch.setattr(bench, "TRAFFIC_FILE", str(prof))
+    assert bench.measured_traffic("backproject", "llama2_7b") == 123.0
+    assert bench.measured_traffic("project", "llama2_7b") is None          # kernel not in the summary
+    assert bench.measured_traffic("backproject", "qwen2_7b") is None       # another workload
+    prof.write_text("sources-sha256 " + "0" * 64 + "\ntraffic-bytes-per-launch backproject 123.0\n")
+    assert bench.measured_traffic("backproject", "llama2_7b") is None      # sources changed since
+
