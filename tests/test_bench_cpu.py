@@ -1,5 +1,7 @@
 """Host-side accounting of bench.py (no GPU): the refresh roofline counts the flops of the
-iteration as described (per precision), and the --gpus guard refuses more than one GPU."""
+iteration as described (per precision), the step accounting prices the moments by their
+storage, the measured traffic is used only while it fits the sources, and the --gpus guard
+refuses more than one GPU."""
 import dataclasses
 import subprocess
 import sys
