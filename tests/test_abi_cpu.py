@@ -209,3 +209,38 @@ def test_version_names_the_target():
     _lib()
     v = M.moara_version()
     assert re.fullmatch(r"moara-mi355x \d+\.\d+ \(gfx950\)", v), v
+
+
+def test_last_error_is_per_thread():
+    """moara_last_error is thread-local: an error raised in one thread does not replace the
+    message another thread reads for its own last error."""
+    import threading
+    _lib()
+    cfg = M.moara_default_config(rank_table=[8] * 10)
+    gate, out = threading.Barrier(2), {}
+
+    def bad_shape():
+        try:
+            M.moara_resolve_matrix(cfg, M.make_descs([(0, 5, 0)])[0])
+        except M.MoaraError:
+            pass
+        gate.wait()   # the other thread fails while this one still holds its message
+        gate.wait()
+        out["shape"] = M.moara_last_error()
+
+    def bad_rank():
+        gate.wait()
+        try:
+            M.moara_allocate_ranks(256, range(7), [0, 1, 2], [5, 6], 1)
+        except M.MoaraError:
+            pass
+        out["rank"] = M.moara_last_error()
+        gate.wait()
+
+    ts = [threading.Thread(target=bad_shape), threading.Thread(target=bad_rank)]
+    for t in ts:
+        t.start()
+    for t in ts:
+        t.join(timeout=30)
+    assert "shape" in out["shape"] and "receiver share" not in out["shape"], out
+    assert "receiver share" in out["rank"], out
