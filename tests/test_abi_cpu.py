@@ -244,3 +244,16 @@ def test_last_error_is_per_thread():
         t.join(timeout=30)
     assert "shape" in out["shape"] and "receiver share" not in out["shape"], out
     assert "receiver share" in out["rank"], out
+
+
+def test_failed_calls_leave_outputs_as_documented():
+    """On error moara_allocate_ranks leaves the caller's table unchanged and
+    moara_create_state sets *out to NULL (both before any GPU work)."""
+    L = _lib()
+    tab = (ctypes.c_int32 * M.MOARA_NUM_MODULES)(*range(100, 110))
+    rc = L.moara_allocate_ranks(256, 0x7F, 0x7, 0x60, 1, tab)    # share 1 * 3 / 2 is not an integer
+    assert rc == M.MOARA_E_RANK and list(tab) == list(range(100, 110))
+    cfg = M.moara_default_config(rank_table=[8] * 10, weight_decay=0.5)
+    h = ctypes.c_void_p(0x1234)
+    rc = L.moara_create_state(ctypes.byref(cfg), M.make_descs([(64, 64, 0)]), 1, None, ctypes.byref(h))
+    assert rc == M.MOARA_E_UNSUPPORTED and not h.value
